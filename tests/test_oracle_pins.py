@@ -1,0 +1,306 @@
+"""Pins of the CPU oracle against facts fixed by the paper and by mathematics.
+
+None of these tests recompute the oracle's own formulas: each compares it with
+something independent — the paper's worked uniquification example, closed
+forms derived by hand, a textbook hard k-means, central finite differences,
+exact symmetries, or a library routine.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import dense, table
+from paper_2309_00964_amd import inputs
+from golden_io import read_uniquify_example
+
+
+def rel(a, b):
+    a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+    return np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300)
+
+
+# --------------------------------------------------------------------------- keys
+
+def test_fp16_decode_matches_ieee_library():
+    """The oracle's bit-level binary16 decode equals numpy's float16 for all 2^16 patterns."""
+    keys = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    mine = dense.decode_fp16(keys)
+    lib = keys.view(np.float16).astype(np.float64)
+    both_nan = np.isnan(mine) & np.isnan(lib)
+    assert np.all(both_nan | (mine == lib))
+    assert np.array_equal(np.isnan(mine), np.isnan(lib))
+    # signed zeros are distinct keys with equal value
+    assert dense.fp16_value(0x0000) == 0.0 and dense.fp16_value(0x8000) == 0.0
+    assert math.copysign(1.0, dense.fp16_value(0x8000)) == -1.0
+    # smallest and largest subnormals
+    assert dense.fp16_value(0x0001) == 2.0 ** -24
+    assert dense.fp16_value(0x03FF) == 1023 * 2.0 ** -24
+
+
+def test_worked_uniquification_example():
+    """Sec. 2.2 / Fig. mem_dkm:flow: BA45, CB1F, BA45 -> two table rows, shared attention."""
+    keys, counts, values = read_uniquify_example()
+    k16 = np.array(keys, dtype=np.uint16)
+    h = table.histogram(k16)
+    assert int(h.sum()) == len(keys)
+    for key, c in counts.items():
+        assert int(h[key]) == c
+    assert int(np.count_nonzero(h)) == len(counts)
+    for key, val in values.items():
+        assert dense.fp16_value(key) == val
+    # the index list is the bit pattern itself; compacted, it is the rank of the key
+    u, inv = table.unique_keys(k16)
+    assert list(u) == sorted(counts)
+    assert list(u[inv]) == keys
+    # equal patterns give bitwise-equal attention rows
+    c0 = np.array([-10.0, -1.0, 0.5])
+    f = dense.forward(k16, c0, tau=0.5, max_iter=3, want_attn=True)
+    assert np.array_equal(f["attn"][0], f["attn"][2])
+    assert not np.array_equal(f["attn"][0], f["attn"][1])
+    assert f["w_tilde"][0] == f["w_tilde"][2]
+
+
+def test_histogram_totals():
+    """<= 2^16 table rows; histogram total equals N (paper Sec. 2.2)."""
+    keys = inputs.fp16_weights(200_000, seed=7, outliers=True)
+    h = table.histogram(keys)
+    assert h.size == 1 << 16
+    assert int(h.sum()) == keys.size
+    assert np.array_equal(h, np.bincount(keys.astype(np.int64), minlength=1 << 16))
+
+
+# --------------------------------------------------------------------------- forward
+
+def test_attention_rows_sum_to_one():
+    keys = inputs.fp16_weights(4096, seed=3)
+    c0 = inputs.quantile_init(keys, 8)
+    f = dense.forward(keys, c0, 2e-3, 5, want_attn=True)
+    assert np.max(np.abs(f["attn"].sum(axis=1) - 1.0)) <= 8 * 2.3e-16
+    assert np.all(f["attn"] >= 0)
+
+
+def test_k1_closed_form():
+    """k = 1: every centroid update is the mean; W~_i = mean(w)."""
+    keys = inputs.fp16_weights(5000, seed=11)
+    v = keys.view(np.float16).astype(np.float64)
+    f = dense.forward(keys, [0.3], 2e-3, 4)
+    assert f["T"] == 4
+    assert np.allclose(f["c_hist"][1:], v.mean(), rtol=1e-13, atol=0)
+    assert np.allclose(f["w_tilde"], v.mean(), rtol=1e-13, atol=0)
+    g = inputs.upstream_grad(keys.size, 12).astype(np.float64)
+    gw, gc = dense.backward(keys, f, g)
+    assert np.allclose(gw, g.sum() / keys.size, rtol=1e-12, atol=1e-15)
+    assert abs(gc[0]) <= 1e-12 * np.abs(g).sum()
+
+
+def _two_point(x, c0, tau, T):
+    c = [c0]
+    for _ in range(T):
+        c.append(x * math.tanh(min(x, c[-1]) / tau))
+    return c, c[T] * math.tanh(min(x, c[T - 1]) / tau)
+
+
+@pytest.mark.parametrize("x,c0,tau,T", [(0.01, 0.004, 2e-3, 5), (0.01, 0.02, 5e-3, 3),
+                                        (0.3, 0.1, 0.2, 6)])
+def test_two_point_closed_form(x, c0, tau, T):
+    """w in {+x, -x} with equal counts, C^(0) = (-c0, +c0):
+    c_t = x tanh(min(x, c_{t-1}) / tau) and W~(+x) = c_T tanh(min(x, c_{T-1}) / tau).
+    This also fixes that W~ uses A^(T) (built from C^(T-1)) and C^(T)."""
+    v = np.array([x, -x] * 7)
+    f = dense.forward(v, [-c0, c0], tau, T)
+    cs, wt = _two_point(x, c0, tau, T)
+    for t in range(T + 1):
+        assert abs(f["c_hist"][t][1] - cs[t]) <= 1e-15 * x + 1e-15
+        assert abs(f["c_hist"][t][0] + cs[t]) <= 1e-15 * x + 1e-15
+    assert abs(f["w_tilde"][0] - wt) <= 2e-15 * x
+    assert abs(f["w_tilde"][1] + wt) <= 2e-15 * x
+
+
+def test_two_point_fp16_keys():
+    """The same closed form through the fp16 key path (x exactly representable)."""
+    x = float(np.float16(0.01))
+    keys = np.array([x, -x] * 64, dtype=np.float16).view(np.uint16)
+    f = dense.forward(keys, [-0.004, 0.004], 2e-3, 5)
+    cs, wt = _two_point(x, 0.004, 2e-3, 5)
+    assert abs(f["c_out"][1] - cs[5]) <= 1e-15
+    assert abs(f["w_tilde"][0] - wt) <= 1e-15
+
+
+def _lloyd(v, c0, T):
+    """Textbook hard k-means: argmin assignment (lowest index on ties), cluster means,
+    an empty cluster keeps its centroid."""
+    c = np.array(c0, np.float64)
+    hist = [c.copy()]
+    for _ in range(T):
+        assign = np.argmin(np.abs(v[:, None] - c[None, :]), axis=1)
+        nc = c.copy()
+        for j in range(c.size):
+            sel = v[assign == j]
+            if sel.size:
+                nc[j] = sel.mean()
+        c = nc
+        hist.append(c.copy())
+    assign = np.argmin(np.abs(v[:, None] - hist[T - 1][None, :]), axis=1)
+    return hist, hist[T][assign]
+
+
+def test_tau_to_zero_is_hard_lloyd():
+    rng = np.random.default_rng(5)
+    v = rng.normal(0, 0.05, 300)
+    c0 = np.array([-0.08, -0.01, 0.02, 0.09])
+    T = 4
+    hist, wt = _lloyd(v, c0, T)
+    # no weight is (nearly) equidistant from two centroids at any step
+    for c in hist:
+        d = np.sort(np.abs(v[:, None] - c[None, :]), axis=1)
+        assert np.min(d[:, 1] - d[:, 0]) > 1e-7
+    f = dense.forward(v, c0, 1e-12, T)
+    assert rel(f["c_hist"], np.array(hist)) <= 1e-14
+    assert rel(f["w_tilde"], wt) <= 1e-14
+
+
+def test_scale_by_two_is_exact():
+    """w, C and tau times 2: C and W~ double exactly, gradients unchanged bitwise."""
+    rng = np.random.default_rng(9)
+    v = rng.normal(0, 0.02, 2000)
+    c0 = np.quantile(v, [0.1, 0.3, 0.5, 0.7, 0.9])
+    g = rng.normal(0, 1, v.size)
+    f1 = dense.forward(v, c0, 2e-3, 5)
+    f2 = dense.forward(2 * v, 2 * c0, 4e-3, 5)
+    assert np.array_equal(f2["c_hist"], 2 * f1["c_hist"])
+    assert np.array_equal(f2["w_tilde"], 2 * f1["w_tilde"])
+    gw1, gc1 = dense.backward(v, f1, g)
+    gw2, gc2 = dense.backward(2 * v, f2, g)
+    assert np.array_equal(gw1, gw2)
+    assert np.array_equal(gc1, gc2)
+
+
+def test_negation_symmetry():
+    """w, C -> -w, -C: C and W~ negate; dL/dw and dL/dC^(0) unchanged."""
+    rng = np.random.default_rng(10)
+    v = rng.normal(0, 0.02, 1500)
+    c0 = np.quantile(v, [0.1, 0.4, 0.6, 0.95])
+    g = rng.normal(0, 1, v.size)
+    f1 = dense.forward(v, c0, 2e-3, 5)
+    f2 = dense.forward(-v, -c0, 2e-3, 5)
+    assert np.array_equal(f2["c_hist"], -f1["c_hist"])
+    assert np.array_equal(f2["w_tilde"], -f1["w_tilde"])
+    gw1, gc1 = dense.backward(v, f1, g)
+    gw2, gc2 = dense.backward(-v, f2, g)
+    assert np.array_equal(gw1, gw2)
+    assert np.array_equal(gc1, gc2)
+
+
+def test_empty_cluster_keeps_centroid():
+    """A centroid whose attention underflows for every weight keeps its value, and
+    the rest of the clustering equals the run without it."""
+    keys = inputs.fp16_weights(3000, seed=21)
+    c0 = inputs.quantile_init(keys, 4).astype(np.float64)
+    g = inputs.upstream_grad(keys.size, 22).astype(np.float64)
+    far = np.append(c0, 2.0)   # 2.0 / 2e-3 = 1000 > 745: exp underflows in fp64
+    f = dense.forward(keys, far, 2e-3, 5)
+    f0 = dense.forward(keys, c0, 2e-3, 5)
+    assert np.all(f["c_hist"][:, 4] == 2.0)
+    assert np.all(f["s_hist"][1:, 4] == 0.0)
+    assert np.array_equal(f["c_hist"][:, :4], f0["c_hist"])
+    assert np.array_equal(f["w_tilde"], f0["w_tilde"])
+    gw, gc = dense.backward(keys, f, g)
+    gw0, gc0 = dense.backward(keys, f0, g)
+    assert rel(gw, gw0) <= 1e-14
+    assert rel(gc[:4], gc0) <= 1e-14
+    assert gc[4] == 0.0
+
+
+def test_early_stop_criterion():
+    """eps > 0 stops at the first t with max_j |C^(t) - C^(t-1)| <= eps (L-inf)."""
+    keys = inputs.fp16_weights(20000, seed=31)
+    c0 = inputs.quantile_init(keys, 8)
+    full = dense.forward(keys, c0, 2e-3, 12)
+    steps = np.max(np.abs(np.diff(full["c_hist"], axis=0)), axis=1)
+    eps = float(np.sort(steps)[len(steps) // 2])
+    expect = int(np.argmax(steps <= eps)) + 1
+    f = dense.forward(keys, c0, 2e-3, 12, eps=eps)
+    assert f["T"] == expect
+    assert np.array_equal(f["c_hist"][: expect + 1], full["c_hist"][: expect + 1])
+    assert dense.forward(keys, c0, 2e-3, 12, eps=1.0)["T"] == 1
+
+
+# --------------------------------------------------------------------------- backward
+
+def _loss(v, c0, g, tau, T):
+    return float(np.dot(g, dense.forward(v, c0, tau, T)["w_tilde"]))
+
+
+@pytest.mark.parametrize("seed,k,T", [(1, 3, 3), (2, 4, 2), (3, 2, 5)])
+def test_backward_matches_central_differences(seed, k, T):
+    rng = np.random.default_rng(seed)
+    v = rng.normal(0, 0.05, 24)
+    c0 = np.sort(rng.normal(0, 0.05, k)) + 1e-3
+    g = rng.normal(0, 1, v.size)
+    tau = 0.01
+    f = dense.forward(v, c0, tau, T)
+    h = 1e-7
+    # stay away from the kinks of |v - c|: every |v_i - C^(t)_j| is far above the step
+    assert np.min(np.abs(v[:, None, None] - f["c_hist"][None, :T, :])) > 100 * h
+    gw, gc = dense.backward(v, f, g)
+    fd_w = np.array([(_loss(v + h * e, c0, g, tau, T) - _loss(v - h * e, c0, g, tau, T)) / (2 * h)
+                     for e in np.eye(v.size)])
+    fd_c = np.array([(_loss(v, c0 + h * e, g, tau, T) - _loss(v, c0 - h * e, g, tau, T)) / (2 * h)
+                     for e in np.eye(k)])
+    assert rel(gw, fd_w) <= 1e-6
+    assert rel(gc, fd_c) <= 1e-6
+
+
+def test_backward_is_linear_in_upstream_per_key():
+    """dL/dw_i = g_i H(key) + R(key): weights sharing a key differ only through g."""
+    keys = np.array([0x2000, 0x2000, 0x2000, 0xA400, 0x1800, 0x2000], dtype=np.uint16)
+    c0 = [-0.01, 0.004, 0.01]
+    f = dense.forward(keys, c0, 2e-3, 4)
+    g = np.array([0.5, -1.5, 2.0, 1.0, -0.3, 0.5])
+    gw, _ = dense.backward(keys, f, g)
+    # weights 0 and 5 share key and g; 0,1,2 share key: gw is affine in g on that key
+    assert gw[0] == gw[5]
+    slope = (gw[1] - gw[0]) / (g[1] - g[0])
+    assert abs(gw[2] - (gw[0] + slope * (g[2] - g[0]))) <= 1e-12 * max(1.0, abs(gw[2]))
+
+
+# --------------------------------------------------------------------------- second oracle
+
+@pytest.mark.parametrize("bits,outliers,eps", [(3, False, 0.0), (2, False, 0.0), (4, True, 0.0),
+                                                (3, True, 1e-6)])
+def test_table_oracle_equals_dense(bits, outliers, eps):
+    """Uniquification is exact (Sec. 2.2): the table form equals the dense map."""
+    keys = inputs.fp16_weights(65536, seed=inputs.weight_seed(1, bits), outliers=outliers)
+    k = 1 << bits
+    c0 = inputs.quantile_init(keys, k)
+    g = inputs.upstream_grad(keys.size, inputs.grad_seed(1, bits)).astype(np.float64)
+    fd = dense.forward(keys, c0, 2e-3, 5, eps=eps)
+    ft = table.forward(keys, c0, 2e-3, 5, eps=eps)
+    assert fd["T"] == ft["T"]
+    assert rel(ft["c_hist"][: fd["T"] + 1], fd["c_hist"][: fd["T"] + 1]) <= 1e-12
+    assert rel(ft["w_tilde"], fd["w_tilde"]) <= 1e-12
+    gwd, gcd = dense.backward(keys, fd, g)
+    gwt, gct, _ = table.backward(keys, ft, g)
+    # the unrolled backward sums cancelling terms over all weights five times, so two
+    # fp64 summation orders differ by up to ~2e-11 there; 1e-10 is still 1e7 below the
+    # GPU gradient tolerance, while a dropped or misplaced term shows up at >= 1e-4
+    assert rel(gwt, gwd) <= 1e-10
+    assert rel(gct, gcd) <= 1e-10
+
+
+# --------------------------------------------------------------------------- inputs
+
+def test_inputs_are_seeded_and_shaped():
+    a = inputs.fp16_weights(100_000, 5)
+    b = inputs.fp16_weights(100_000, 5)
+    assert a.dtype == np.uint16 and np.array_equal(a, b)
+    v = a.view(np.float16).astype(np.float64)
+    assert abs(v.std() - inputs.SIGMA) < 0.01 * inputs.SIGMA
+    o = inputs.fp16_weights(1_000_000, 6, outliers=True).view(np.float16).astype(np.float64)
+    assert np.mean(np.abs(o) > 0.12) > 5e-4        # outliers beyond 6 sigma exist
+    c = inputs.quantile_init(a, 8)
+    assert c.dtype == np.float32 and np.all(np.diff(c) > 0)
+    assert np.all(np.isin(c.astype(np.float16).view(np.uint16), a))
+    gr = inputs.upstream_grad(1000, 1)
+    assert gr.dtype == np.float32
