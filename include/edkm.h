@@ -1,0 +1,192 @@
+/*
+ * edkm.h — C ABI of the MI355X (gfx950) eDKM hot path: DKM weight clustering,
+ * forward and backward, computed on the 16-bit uniquified attention table.
+ *
+ * The method (paper: "eDKM: An Efficient and Accurate Train-time Weight
+ * Clustering for Large Language Models", Sec. 2 and 2.2):
+ *
+ *   DKM (Sec. 2) clusters a weight tensor W against k = 2^b centroids C through
+ *   an attention map A_ij = softmax_j(-|w_i - c_j| / tau), iterates
+ *   C_j = sum_i A_ij w_i / sum_i A_ij, and outputs W~ = A C; training needs
+ *   the backward of W~ with respect to W and C.  The map is O(|W||C|).
+ *
+ *   Uniquification (Sec. 2.2, Fig. "mem_dkm:flow"): a 16-bit weight has at most
+ *   65,536 distinct bit patterns and equal patterns have equal attention rows,
+ *   so the map becomes an attention table with one row per pattern plus an
+ *   index list whose entry is the weight's own pattern.  Here every sum over
+ *   weights becomes a sum over table rows weighted by per-pattern counts, and
+ *   the N-sized work reduces to a histogram, a keyed gradient sum and two
+ *   gathers.
+ *
+ * Conventions for every entry point:
+ *   - Weights are fp16 passed as their raw bit patterns (uint16_t), flat, any
+ *     shape (all operations are elementwise in the weight index).  A pattern
+ *     is a table key; +0 and -0 are distinct keys of equal value.
+ *   - Device pointers are HIP device memory owned by the caller.  The library
+ *     allocates nothing and keeps no global state; all calls are asynchronous
+ *     on the given stream except where noted.  Pointers need only natural
+ *     alignment (2 bytes for keys, 4 for floats); 16-byte-aligned buffers take
+ *     the vectorised path.
+ *   - Per-matrix state lives in two caller-owned places: an edkm_plan (host
+ *     memory, filled by edkm_plan_init) and a device workspace of
+ *     edkm_workspace_bytes() bytes.  Calls on one plan must be issued in the
+ *     order init_unique -> forward -> backward (or forward_dense ->
+ *     backward_dense) on one stream, with the same key buffer and unchanged
+ *     keys; a call out of order returns EDKM_ERR_STATE before touching the
+ *     GPU.  Distinct plans with distinct workspaces may be used concurrently.
+ *   - Errors are returned, never thrown; argument errors are detected on the
+ *     host before any HIP call and leave the plan unchanged.
+ */
+#ifndef EDKM_H
+#define EDKM_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define EDKM_NKEYS 65536        /* table rows: every 16-bit pattern */
+#define EDKM_MAX_BITS 4         /* k = 2^bits <= 16 centroids */
+#define EDKM_MAX_ITER 1024
+#define EDKM_MAX_N 4294967295ull /* per matrix; counts are uint32 */
+
+typedef int edkm_status;
+enum {
+    EDKM_OK = 0,
+    EDKM_ERR_ARG = -1,        /* invalid argument (null pointer, size, bits, tau, ...) */
+    EDKM_ERR_NONFINITE = -2,  /* a weight is Inf or NaN (only reported when checked) */
+    EDKM_ERR_WORKSPACE = -3,  /* workspace null, too small, or misaligned (256 B) */
+    EDKM_ERR_STATE = -4,      /* call out of order for this plan, or different keys */
+    EDKM_ERR_HIP = -5         /* a HIP runtime call failed */
+};
+
+/* Host-side per-matrix record.  Opaque; the caller owns the memory (stack or
+ * heap) and must not copy it between calls. */
+typedef struct edkm_plan {
+    uint64_t opaque[24];
+} edkm_plan;
+
+/* Device workspace size for one matrix of n weights with k = 2^bits
+ * centroids and up to max_iter DKM iterations; 0 if the arguments are invalid.
+ * It is about 40 MiB and does not grow with n. */
+size_t edkm_workspace_bytes(uint64_t n, int bits, int max_iter);
+
+/* Set up a plan for n (1..EDKM_MAX_N) weights, bits in 1..4, max_iter in
+ * 1..EDKM_MAX_ITER, with ws a device buffer of ws_bytes >= the size above,
+ * 256-byte aligned, used only by this plan.  Host only; no HIP call. */
+edkm_status edkm_plan_init(edkm_plan* plan, uint64_t n, int bits, int max_iter,
+                           void* ws, size_t ws_bytes);
+
+/* Uniquification (Sec. 2.2): counts[u] = #{i : w_bits[i] = u} for all 65,536
+ * patterns, kept in the workspace for forward/backward.
+ *   w_bits         device, n patterns
+ *   counts_out     nullable, device uint32[65536]: copy of the counts
+ *   num_unique_out nullable, device uint32[1]: number of occupied patterns
+ *   check_finite   1: synchronise the stream and return EDKM_ERR_NONFINITE if
+ *                  any weight is Inf/NaN; 0: no sync, and non-finite weights are
+ *                  left out of the clustering (their outputs are NaN).
+ * The counts are exact (integer).  Cost: one read of the keys. */
+edkm_status edkm_init_unique(edkm_plan* plan, const uint16_t* w_bits,
+                             uint32_t* counts_out, uint32_t* num_unique_out,
+                             int check_finite, hipStream_t stream);
+
+/* DKM forward on the table (Sec. 2, Sec. 2.2).  For t = 1..T:
+ *   a_uj = softmax_j(-|v_u - C^(t-1)_j| / tau) for each occupied pattern u
+ *   (v_u its fp16 value), S_j = sum_u n_u a_uj, P_j = sum_u n_u a_uj v_u,
+ *   C^(t)_j = P_j / S_j (a centroid with S_j = 0 keeps its value).
+ * T = max_iter, or the first t with max_j |C^(t)_j - C^(t-1)_j| <= eps when
+ * eps > 0.  Output W~_i = sum_j a^(T)_{w_i, j} C^(T)_j, i.e. a gather of the
+ * table row of w_i's pattern.
+ *   w_bits     device, n patterns; must be the buffer given to init_unique
+ *   tau        > 0, finite;  eps >= 0 (0: exactly max_iter iterations)
+ *   c_in       device float[k]: C^(0)
+ *   c_out      device float[k]: C^(T)
+ *   w_tilde    device, n outputs: float, or fp16 bits (uint16) if out_fp16 = 1
+ *              (round to nearest even)
+ *   iters_out  nullable, device int32[1]: T
+ * Arithmetic is fp32 with fixed-order reductions: results are bitwise
+ * repeatable.  Saves C^(0..T), S^(1..T) and the table in the workspace. */
+edkm_status edkm_forward(edkm_plan* plan, const uint16_t* w_bits, float tau, float eps,
+                         const float* c_in, float* c_out, void* w_tilde, int out_fp16,
+                         int32_t* iters_out, hipStream_t stream);
+
+/* DKM backward (the gradient that autograd of the dense map gives, Sec. 2.2),
+ * for L with dL/dW~ = grad_w_tilde, through all T iterations:
+ *   G_u = sum_{i: w_bits[i] = u} grad_w_tilde[i]   (keyed reduction)
+ *   dL/dw_i = grad_w_tilde[i] * H[w_bits[i]] + R[w_bits[i]]
+ * with H, R and dL/dC^(0) from the analytic softmax Jacobian on the table.
+ *   grad_w_tilde  device float[n]
+ *   grad_w        device float[n]
+ *   grad_c        device float[k]: dL/dC^(0)
+ * d|x|/dx at x = 0 is 0.  The keyed reduction uses float atomics, so results
+ * vary in the last bits between runs. */
+edkm_status edkm_backward(edkm_plan* plan, const uint16_t* w_bits, const float* grad_w_tilde,
+                          float* grad_w, float* grad_c, hipStream_t stream);
+
+/* Batched forms: `count` independent matrices (own plan, keys and outputs;
+ * same tau and eps) processed together, with one launch per step for the
+ * whole batch.  Arrays are host arrays of `count` entries; entries of the
+ * nullable output arrays may be NULL, and the arrays themselves may be NULL.
+ * Equivalent to calling the single-matrix form on each. */
+edkm_status edkm_init_unique_batch(int count, edkm_plan* const* plans,
+                                   const uint16_t* const* w_bits,
+                                   uint32_t* const* counts_out,
+                                   uint32_t* const* num_unique_out,
+                                   int check_finite, hipStream_t stream);
+edkm_status edkm_forward_batch(int count, edkm_plan* const* plans,
+                               const uint16_t* const* w_bits, float tau, float eps,
+                               const float* const* c_in, float* const* c_out,
+                               void* const* w_tilde, int out_fp16,
+                               int32_t* const* iters_out, hipStream_t stream);
+edkm_status edkm_backward_batch(int count, edkm_plan* const* plans,
+                                const uint16_t* const* w_bits,
+                                const float* const* grad_w_tilde,
+                                float* const* grad_w, float* const* grad_c,
+                                hipStream_t stream);
+
+/* Dense (non-uniquified) DKM for comparison (Sec. 2: the O(|W||C|) map):
+ * the same mathematics evaluated per weight over the N x k map, recomputing
+ * the map row of every weight in every pass.  Same arguments and outputs as
+ * edkm_forward; needs no init_unique.  attn_out (nullable, device
+ * float[n * k], row-major) receives the final map A^(T). */
+edkm_status edkm_forward_dense(edkm_plan* plan, const uint16_t* w_bits, float tau, float eps,
+                               const float* c_in, float* c_out, void* w_tilde, int out_fp16,
+                               int32_t* iters_out, float* attn_out, hipStream_t stream);
+
+/* Backward of edkm_forward_dense, same contract as edkm_backward
+ * (deterministic: no atomics). */
+edkm_status edkm_backward_dense(edkm_plan* plan, const uint16_t* w_bits,
+                                const float* grad_w_tilde, float* grad_w, float* grad_c,
+                                hipStream_t stream);
+
+/* Timing hook (diagnostics).  The N-sized passes, one kernel launch each per
+ * call (per launch group in the batched forms): */
+enum {
+    EDKM_PASS_HIST = 0,         /* init_unique: pattern histogram, reads 2 B/weight */
+    EDKM_PASS_GATHER_WT = 1,    /* forward: W~ gather, 2 B + 4 B (fp16 out: 2 B) */
+    EDKM_PASS_KEYED_GRAD = 2,   /* backward: keyed sum of dL/dW~, 2 B + 4 B */
+    EDKM_PASS_GATHER_GRAD = 3   /* backward: dL/dw gather, 2 B + 4 B + 4 B */
+};
+/* When set (non-NULL), later calls on this plan record `start` on the stream
+ * right before that pass's launch and `stop` right after it; in a batched call
+ * the events of the first plan of each launch group are used.  The caller owns
+ * the events (created with timing enabled) and reads them with
+ * hipEventElapsedTime.  NULL events switch the hook off.  Host only. */
+edkm_status edkm_plan_set_pass_events(edkm_plan* plan, int pass, hipEvent_t start, hipEvent_t stop);
+
+/* Diagnostics for the last EDKM_ERR_HIP returned on this plan: the HIP error
+ * code (0 if none), the launch or runtime call that failed, and the HIP
+ * runtime's description.  The strings are static.  Any output may be NULL. */
+edkm_status edkm_plan_hip_error(const edkm_plan* plan, int* code, const char** step,
+                                const char** message);
+
+/* Static string for a status code. */
+const char* edkm_status_str(edkm_status status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* EDKM_H */

@@ -1,0 +1,477 @@
+// C ABI of the eDKM hot path: argument checks, per-plan call order, workspace
+// layout, and the split of each batch into launches.  Every check runs on the
+// host before any HIP call; kernels never see an argument this layer rejected.
+
+#include "../../include/edkm.h"
+#include "edkm_internal.h"
+
+#include <cmath>
+#include <cstring>
+
+namespace edkm {
+
+namespace {
+
+constexpr uint64_t PLAN_MAGIC = 0x65444B4D706C616EULL;   // "eDKMplan"
+enum Stage : int32_t { PLANNED = 1, COUNTED = 2, FORWARD = 3, DENSE_FORWARD = 4 };
+
+struct PlanImpl {
+    uint64_t magic;
+    uint64_t n;
+    int32_t bits, k, max_iter, stage;
+    void* ws;
+    size_t ws_bytes;
+    const uint16_t* keys;   // key buffer of the current sequence
+    float tau;
+    float eps;
+    int32_t hip_code;        // last HIP failure on this plan (0 if none)
+    const char* hip_step;    // the launch or runtime call that failed
+    PassEvents ev;           // caller's timing events (diagnostics), null when unset
+};
+static_assert(sizeof(PlanImpl) <= sizeof(edkm_plan), "edkm_plan too small");
+static_assert(EDKM_PASS_HIST == PASS_HIST && EDKM_PASS_GATHER_WT == PASS_GATHER_WT &&
+                  EDKM_PASS_KEYED_GRAD == PASS_KEYED_GRAD && EDKM_PASS_GATHER_GRAD == PASS_GATHER_GRAD,
+              "pass ids");
+
+inline PlanImpl* impl(edkm_plan* p) { return reinterpret_cast<PlanImpl*>(p); }
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct Layout {
+    size_t counts, tab, H, R, HR, G, chist, shist, ghist, ehist, tpart, bpart, dpart, span, part, st,
+        total;
+};
+
+Layout layout(int max_iter) {
+    Layout L{};
+    size_t o = 0;
+    auto take = [&](size_t bytes) { size_t at = o; o = align256(o + bytes); return at; };
+    const size_t hist = (size_t)(max_iter + 1) * KMAX * sizeof(float);
+    const size_t tp = (size_t)(max_iter + 1) * T_WG * PSTRIDE * sizeof(float);
+    L.st = take(sizeof(DevState));
+    L.counts = take(NKEYS * sizeof(uint32_t));
+    L.tab = take(NKEYS * sizeof(float));
+    L.H = take(NKEYS * sizeof(float));
+    L.R = take(NKEYS * sizeof(float));
+    L.HR = take(NKEYS * sizeof(float2));
+    L.G = take(NKEYS * sizeof(float));
+    L.chist = take(hist);
+    L.shist = take(hist);
+    L.ghist = take(hist);
+    L.ehist = take(KMAX * sizeof(float));
+    L.tpart = take(tp);
+    L.bpart = take(tp);
+    L.dpart = take((size_t)D_WG * PSTRIDE * sizeof(float));
+    L.span = take(NP_MAX_WG * sizeof(int2));
+    L.part = take((size_t)NP_MAX_WG * ROW4 * sizeof(uint32_t));
+    L.total = o;
+    return L;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+bool plan_ok(const edkm_plan* p) {
+    return p && reinterpret_cast<const PlanImpl*>(p)->magic == PLAN_MAGIC;
+}
+
+// Split the N-sized passes of a group over workgroups: about NP_MAX_WG in
+// total, shared in proportion to matrix size, at least one and at most
+// NP_MAX_WG per matrix, each slice a multiple of 8 weights.
+uint32_t partition(BatchArgs& b) {
+    uint64_t total = 0;
+    for (int i = 0; i < b.count; ++i) total += b.m[i].n;
+    uint32_t wg = 0;
+    for (int i = 0; i < b.count; ++i) {
+        MatArgs& M = b.m[i];
+        uint64_t want = (uint64_t)std::llround((double)NP_MAX_WG * (double)M.n / (double)total);
+        const uint64_t cap = (M.n + NP_MIN_CHUNK - 1) / NP_MIN_CHUNK;
+        if (want > cap) want = cap;
+        if (want > (uint64_t)NP_MAX_WG) want = NP_MAX_WG;
+        if (want < 1) want = 1;
+        uint64_t chunk = (M.n + want - 1) / want;
+        chunk = (chunk + 7) & ~7ull;
+        M.chunk = chunk;
+        M.wg_count = (uint32_t)((M.n + chunk - 1) / chunk);
+        M.wg_begin = wg;
+        wg += M.wg_count;
+    }
+    return wg;
+}
+
+float tau_s2(float tau) { return (float)(1.4426950408889634 / (double)tau); }
+
+// Record a HIP failure on plans[first .. first+cnt) and return EDKM_ERR_HIP.
+edkm_status hip_fail(edkm_plan* const* plans, int first, int cnt, hipError_t e, const char* step) {
+    for (int i = 0; i < cnt; ++i) {
+        reinterpret_cast<PlanImpl*>(plans[first + i])->hip_code = (int32_t)e;
+        reinterpret_cast<PlanImpl*>(plans[first + i])->hip_step = step;
+    }
+    return EDKM_ERR_HIP;
+}
+
+}  // namespace
+
+size_t workspace_bytes(int max_iter) { return layout(max_iter).total; }
+
+Ws carve_workspace(void* base, int max_iter) {
+    const Layout L = layout(max_iter);
+    char* c = static_cast<char*>(base);
+    Ws w;
+    w.st = reinterpret_cast<DevState*>(c + L.st);
+    w.counts = reinterpret_cast<uint32_t*>(c + L.counts);
+    w.tab = reinterpret_cast<float*>(c + L.tab);
+    w.H = reinterpret_cast<float*>(c + L.H);
+    w.R = reinterpret_cast<float*>(c + L.R);
+    w.HR = reinterpret_cast<float2*>(c + L.HR);
+    w.G = reinterpret_cast<float*>(c + L.G);
+    w.chist = reinterpret_cast<float*>(c + L.chist);
+    w.shist = reinterpret_cast<float*>(c + L.shist);
+    w.ghist = reinterpret_cast<float*>(c + L.ghist);
+    w.ehist = reinterpret_cast<float*>(c + L.ehist);
+    w.tpart = reinterpret_cast<float*>(c + L.tpart);
+    w.bpart = reinterpret_cast<float*>(c + L.bpart);
+    w.dpart = reinterpret_cast<float*>(c + L.dpart);
+    w.span = reinterpret_cast<int2*>(c + L.span);
+    w.part = reinterpret_cast<uint32_t*>(c + L.part);
+    return w;
+}
+
+namespace {
+
+void fill_mat(MatArgs& M, const PlanImpl* P, const uint16_t* keys) {
+    std::memset(&M, 0, sizeof(M));
+    M.keys = keys;
+    M.n = P->n;
+    M.k = P->k;
+    M.max_iter = P->max_iter;
+    M.ws = carve_workspace(P->ws, P->max_iter);
+}
+
+// Common checks of a batch: plans valid and distinct, key buffers non-null.
+edkm_status check_batch(int count, edkm_plan* const* plans, const uint16_t* const* keys) {
+    if (count < 1 || !plans || !keys) return EDKM_ERR_ARG;
+    for (int i = 0; i < count; ++i) {
+        if (!plan_ok(plans[i]) || !keys[i]) return EDKM_ERR_ARG;
+        for (int j = 0; j < i; ++j)
+            if (plans[j] == plans[i] || impl(plans[j])->ws == impl(plans[i])->ws) return EDKM_ERR_ARG;
+    }
+    return EDKM_OK;
+}
+
+bool tau_ok(float tau) { return std::isfinite(tau) && tau > 0.f && std::isfinite(1.0f / tau); }
+bool eps_ok(float eps) { return std::isfinite(eps) && eps >= 0.f; }
+
+// Launch groups: consecutive matrices with the same k, at most MAXB each.
+template <class Fn>
+edkm_status for_groups(int count, edkm_plan* const* plans, Fn fn) {
+    int i = 0;
+    while (i < count) {
+        int j = i + 1;
+        while (j < count && j - i < MAXB && impl(plans[j])->k == impl(plans[i])->k) ++j;
+        edkm_status st = fn(i, j - i);
+        if (st != EDKM_OK) return st;
+        i = j;
+    }
+    return EDKM_OK;
+}
+
+}  // namespace
+}  // namespace edkm
+
+using namespace edkm;
+
+extern "C" {
+
+size_t edkm_workspace_bytes(uint64_t n, int bits, int max_iter) {
+    if (n < 1 || n > EDKM_MAX_N || bits < 1 || bits > EDKM_MAX_BITS || max_iter < 1 ||
+        max_iter > EDKM_MAX_ITER)
+        return 0;
+    return workspace_bytes(max_iter);
+}
+
+edkm_status edkm_plan_init(edkm_plan* plan, uint64_t n, int bits, int max_iter, void* ws,
+                           size_t ws_bytes) {
+    if (!plan) return EDKM_ERR_ARG;
+    const size_t need = edkm_workspace_bytes(n, bits, max_iter);
+    if (need == 0) return EDKM_ERR_ARG;
+    if (!ws || ws_bytes < need || ((uintptr_t)ws & 255u)) return EDKM_ERR_WORKSPACE;
+    std::memset(plan, 0, sizeof(*plan));
+    PlanImpl* P = impl(plan);
+    P->n = n;
+    P->bits = bits;
+    P->k = 1 << bits;
+    P->max_iter = max_iter;
+    P->ws = ws;
+    P->ws_bytes = ws_bytes;
+    P->stage = PLANNED;
+    P->magic = PLAN_MAGIC;
+    return EDKM_OK;
+}
+
+edkm_status edkm_init_unique_batch(int count, edkm_plan* const* plans,
+                                   const uint16_t* const* w_bits, uint32_t* const* counts_out,
+                                   uint32_t* const* num_unique_out, int check_finite,
+                                   hipStream_t stream) {
+    edkm_status st = check_batch(count, plans, w_bits);
+    if (st != EDKM_OK) return st;
+    if (check_finite != 0 && check_finite != 1) return EDKM_ERR_ARG;
+    st = for_groups(count, plans, [&](int first, int cnt) -> edkm_status {
+        BatchArgs b;
+        std::memset(&b, 0, sizeof(b));
+        b.count = cnt;
+        bool vec = true;
+        for (int i = 0; i < cnt; ++i) {
+            const PlanImpl* P = impl(plans[first + i]);
+            fill_mat(b.m[i], P, w_bits[first + i]);
+            b.m[i].nuniq_out = num_unique_out ? num_unique_out[first + i] : nullptr;
+            vec = vec && aligned16(w_bits[first + i]);
+        }
+        for (int i = 0; i < cnt; ++i) b.m[i].vec = vec;
+        const uint32_t grid = partition(b);
+        const char* where = "";
+        const hipError_t e = launch_init_unique(b, grid, stream, &where, &impl(plans[first])->ev);
+        if (e != hipSuccess) return hip_fail(plans, first, cnt, e, where);
+        return EDKM_OK;
+    });
+    if (st != EDKM_OK) return st;
+    for (int i = 0; i < count; ++i) {
+        if (counts_out && counts_out[i]) {
+            Ws w = carve_workspace(impl(plans[i])->ws, impl(plans[i])->max_iter);
+            const hipError_t e = hipMemcpyAsync(counts_out[i], w.counts, NKEYS * sizeof(uint32_t),
+                                                hipMemcpyDeviceToDevice, stream);
+            if (e != hipSuccess) return hip_fail(plans, i, 1, e, "hipMemcpyAsync(counts)");
+        }
+    }
+    bool bad = false;
+    if (check_finite) {
+        for (int i = 0; i < count; ++i) {
+            Ws w = carve_workspace(impl(plans[i])->ws, impl(plans[i])->max_iter);
+            uint32_t flag = 0;
+            hipError_t e = hipMemcpyAsync(&flag, &w.st->nonfinite, sizeof(flag),
+                                          hipMemcpyDeviceToHost, stream);
+            if (e == hipSuccess) e = hipStreamSynchronize(stream);
+            if (e != hipSuccess) return hip_fail(plans, i, 1, e, "non-finite check");
+            bad = bad || flag != 0;
+        }
+    }
+    for (int i = 0; i < count; ++i) {
+        PlanImpl* P = impl(plans[i]);
+        P->stage = bad ? PLANNED : COUNTED;
+        P->keys = bad ? nullptr : w_bits[i];
+    }
+    return bad ? EDKM_ERR_NONFINITE : EDKM_OK;
+}
+
+edkm_status edkm_init_unique(edkm_plan* plan, const uint16_t* w_bits, uint32_t* counts_out,
+                             uint32_t* num_unique_out, int check_finite, hipStream_t stream) {
+    return edkm_init_unique_batch(1, &plan, &w_bits, &counts_out, &num_unique_out, check_finite,
+                                  stream);
+}
+
+edkm_status edkm_forward_batch(int count, edkm_plan* const* plans, const uint16_t* const* w_bits,
+                               float tau, float eps, const float* const* c_in,
+                               float* const* c_out, void* const* w_tilde, int out_fp16,
+                               int32_t* const* iters_out, hipStream_t stream) {
+    edkm_status st = check_batch(count, plans, w_bits);
+    if (st != EDKM_OK) return st;
+    if (!tau_ok(tau) || !eps_ok(eps) || !c_in || !c_out || !w_tilde ||
+        (out_fp16 != 0 && out_fp16 != 1))
+        return EDKM_ERR_ARG;
+    for (int i = 0; i < count; ++i)
+        if (!c_in[i] || !c_out[i] || !w_tilde[i]) return EDKM_ERR_ARG;
+    for (int i = 0; i < count; ++i) {
+        const PlanImpl* P = impl(plans[i]);
+        if (P->stage < COUNTED || P->stage == DENSE_FORWARD || P->keys != w_bits[i])
+            return EDKM_ERR_STATE;
+    }
+    st = for_groups(count, plans, [&](int first, int cnt) -> edkm_status {
+        BatchArgs b;
+        std::memset(&b, 0, sizeof(b));
+        b.count = cnt;
+        b.out_fp16 = out_fp16;
+        b.s2 = tau_s2(tau);
+        b.inv_tau = 1.0f / tau;
+        b.eps = eps;
+        bool vec = true;
+        int max_t = 0;
+        for (int i = 0; i < cnt; ++i) {
+            const int q = first + i;
+            const PlanImpl* P = impl(plans[q]);
+            MatArgs& M = b.m[i];
+            fill_mat(M, P, w_bits[q]);
+            M.c_in = c_in[q];
+            M.c_out = c_out[q];
+            M.wt = w_tilde[q];
+            M.iters_out = iters_out ? iters_out[q] : nullptr;
+            vec = vec && aligned16(w_bits[q]) && aligned16(w_tilde[q]);
+            if (P->max_iter > max_t) max_t = P->max_iter;
+        }
+        for (int i = 0; i < cnt; ++i) b.m[i].vec = vec;
+        const uint32_t grid = partition(b);
+        const char* where = "";
+        const hipError_t e = launch_forward(b, grid, max_t, stream, &where, &impl(plans[first])->ev);
+        if (e != hipSuccess) return hip_fail(plans, first, cnt, e, where);
+        return EDKM_OK;
+    });
+    if (st != EDKM_OK) return st;
+    for (int i = 0; i < count; ++i) {
+        PlanImpl* P = impl(plans[i]);
+        P->stage = FORWARD;
+        P->tau = tau;
+        P->eps = eps;
+    }
+    return EDKM_OK;
+}
+
+edkm_status edkm_forward(edkm_plan* plan, const uint16_t* w_bits, float tau, float eps,
+                         const float* c_in, float* c_out, void* w_tilde, int out_fp16,
+                         int32_t* iters_out, hipStream_t stream) {
+    return edkm_forward_batch(1, &plan, &w_bits, tau, eps, &c_in, &c_out, &w_tilde, out_fp16,
+                              &iters_out, stream);
+}
+
+edkm_status edkm_backward_batch(int count, edkm_plan* const* plans, const uint16_t* const* w_bits,
+                                const float* const* grad_w_tilde, float* const* grad_w,
+                                float* const* grad_c, hipStream_t stream) {
+    edkm_status st = check_batch(count, plans, w_bits);
+    if (st != EDKM_OK) return st;
+    if (!grad_w_tilde || !grad_w || !grad_c) return EDKM_ERR_ARG;
+    for (int i = 0; i < count; ++i)
+        if (!grad_w_tilde[i] || !grad_w[i] || !grad_c[i]) return EDKM_ERR_ARG;
+    for (int i = 0; i < count; ++i) {
+        const PlanImpl* P = impl(plans[i]);
+        if (P->stage != FORWARD || P->keys != w_bits[i]) return EDKM_ERR_STATE;
+    }
+    // one tau per launch group: split groups where tau differs
+    st = for_groups(count, plans, [&](int first, int cnt) -> edkm_status {
+        int i0 = 0;
+        while (i0 < cnt) {
+            int i1 = i0 + 1;
+            while (i1 < cnt && impl(plans[first + i1])->tau == impl(plans[first + i0])->tau) ++i1;
+            BatchArgs b;
+            std::memset(&b, 0, sizeof(b));
+            b.count = i1 - i0;
+            const float tau = impl(plans[first + i0])->tau;
+            b.s2 = tau_s2(tau);
+            b.inv_tau = 1.0f / tau;
+            bool vec = true;
+            int max_t = 0;
+            for (int i = 0; i < b.count; ++i) {
+                const int q = first + i0 + i;
+                const PlanImpl* P = impl(plans[q]);
+                MatArgs& M = b.m[i];
+                fill_mat(M, P, w_bits[q]);
+                M.g = grad_w_tilde[q];
+                M.gw = grad_w[q];
+                M.gc = grad_c[q];
+                vec = vec && aligned16(w_bits[q]) && aligned16(grad_w_tilde[q]) &&
+                      aligned16(grad_w[q]);
+                if (P->max_iter > max_t) max_t = P->max_iter;
+            }
+            for (int i = 0; i < b.count; ++i) b.m[i].vec = vec;
+            const uint32_t grid = partition(b);
+            const char* where = "";
+            const hipError_t e =
+                launch_backward(b, grid, max_t, stream, &where, &impl(plans[first + i0])->ev);
+            if (e != hipSuccess) return hip_fail(plans, first + i0, b.count, e, where);
+            i0 = i1;
+        }
+        return EDKM_OK;
+    });
+    return st;
+}
+
+edkm_status edkm_backward(edkm_plan* plan, const uint16_t* w_bits, const float* grad_w_tilde,
+                          float* grad_w, float* grad_c, hipStream_t stream) {
+    return edkm_backward_batch(1, &plan, &w_bits, &grad_w_tilde, &grad_w, &grad_c, stream);
+}
+
+edkm_status edkm_forward_dense(edkm_plan* plan, const uint16_t* w_bits, float tau, float eps,
+                               const float* c_in, float* c_out, void* w_tilde, int out_fp16,
+                               int32_t* iters_out, float* attn_out, hipStream_t stream) {
+    if (!plan_ok(plan) || !w_bits || !tau_ok(tau) || !eps_ok(eps) || !c_in || !c_out ||
+        !w_tilde || (out_fp16 != 0 && out_fp16 != 1))
+        return EDKM_ERR_ARG;
+    PlanImpl* P = impl(plan);
+    BatchArgs b;
+    std::memset(&b, 0, sizeof(b));
+    b.count = 1;
+    b.out_fp16 = out_fp16;
+    b.s2 = tau_s2(tau);
+    b.inv_tau = 1.0f / tau;
+    b.eps = eps;
+    MatArgs& M = b.m[0];
+    fill_mat(M, P, w_bits);
+    M.c_in = c_in;
+    M.c_out = c_out;
+    M.wt = w_tilde;
+    M.iters_out = iters_out;
+    M.attn = attn_out;
+    uint64_t nwg = (P->n + 4095) / 4096;
+    if (nwg > (uint64_t)D_WG) nwg = D_WG;
+    M.chunk = (P->n + nwg - 1) / nwg;
+    const char* where = "";
+    const hipError_t e = launch_forward_dense(b, (uint32_t)nwg, stream, &where);
+    if (e != hipSuccess) return hip_fail(&plan, 0, 1, e, where);
+    P->stage = DENSE_FORWARD;
+    P->keys = w_bits;
+    P->tau = tau;
+    P->eps = eps;
+    return EDKM_OK;
+}
+
+edkm_status edkm_backward_dense(edkm_plan* plan, const uint16_t* w_bits, const float* grad_w_tilde,
+                                float* grad_w, float* grad_c, hipStream_t stream) {
+    if (!plan_ok(plan) || !w_bits || !grad_w_tilde || !grad_w || !grad_c) return EDKM_ERR_ARG;
+    PlanImpl* P = impl(plan);
+    if (P->stage != DENSE_FORWARD || P->keys != w_bits) return EDKM_ERR_STATE;
+    BatchArgs b;
+    std::memset(&b, 0, sizeof(b));
+    b.count = 1;
+    b.s2 = tau_s2(P->tau);
+    b.inv_tau = 1.0f / P->tau;
+    MatArgs& M = b.m[0];
+    fill_mat(M, P, w_bits);
+    M.g = grad_w_tilde;
+    M.gw = grad_w;
+    M.gc = grad_c;
+    uint64_t nwg = (P->n + 4095) / 4096;
+    if (nwg > (uint64_t)D_WG) nwg = D_WG;
+    M.chunk = (P->n + nwg - 1) / nwg;
+    const char* where = "";
+    const hipError_t e = launch_backward_dense(b, (uint32_t)nwg, stream, &where);
+    if (e != hipSuccess) return hip_fail(&plan, 0, 1, e, where);
+    return EDKM_OK;
+}
+
+edkm_status edkm_plan_set_pass_events(edkm_plan* plan, int pass, hipEvent_t start, hipEvent_t stop) {
+    if (!plan_ok(plan) || pass < 0 || pass >= NPASS) return EDKM_ERR_ARG;
+    PlanImpl* P = impl(plan);
+    P->ev.start[pass] = start;
+    P->ev.stop[pass] = stop;
+    return EDKM_OK;
+}
+
+edkm_status edkm_plan_hip_error(const edkm_plan* plan, int* code, const char** step,
+                                const char** message) {
+    if (!plan_ok(plan)) return EDKM_ERR_ARG;
+    const PlanImpl* P = reinterpret_cast<const PlanImpl*>(plan);
+    if (code) *code = P->hip_code;
+    if (step) *step = P->hip_step ? P->hip_step : "";
+    if (message) *message = P->hip_code ? hipGetErrorString((hipError_t)P->hip_code) : "";
+    return EDKM_OK;
+}
+
+const char* edkm_status_str(edkm_status s) {
+    switch (s) {
+    case EDKM_OK: return "ok";
+    case EDKM_ERR_ARG: return "invalid argument";
+    case EDKM_ERR_NONFINITE: return "non-finite weight (Inf or NaN)";
+    case EDKM_ERR_WORKSPACE: return "workspace null, too small or not 256-byte aligned";
+    case EDKM_ERR_STATE: return "call out of order for this plan, or a different key buffer";
+    case EDKM_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+    }
+}
+
+}  // extern "C"

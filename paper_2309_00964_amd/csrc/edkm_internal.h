@@ -1,0 +1,109 @@
+// Internal declarations shared by the eDKM kernels and the C-ABI layer.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace edkm {
+
+constexpr int NKEYS = 65536;          // every 16-bit pattern
+constexpr int FIN_MAGS = 0x7C00;      // magnitudes (low 15 bits) of finite fp16 values
+constexpr int W4 = 19456;             // magnitudes per sign in a 4-byte LDS window (152 KiB)
+constexpr int W8 = 10240;             // magnitudes per sign in the 8-byte LDS window (160 KiB)
+constexpr int NP_THREADS = 1024;      // N-pass workgroup size
+constexpr int NP_MAX_WG = 256;        // N-pass workgroups per matrix (one per CU)
+constexpr int NP_MIN_CHUNK = 16384;   // smallest slice of a matrix given to one workgroup
+constexpr int ROW4 = 2 * W4;          // 32-bit words per N-pass partial row
+constexpr int T_WG = 64;              // table-phase workgroups per matrix (= wave size)
+constexpr int T_THREADS = 256;
+constexpr int KMAX = 16;
+constexpr int PSTRIDE = 32;           // floats per table-phase partial row (2 * KMAX)
+constexpr int MAXB = 8;               // matrices per launch
+constexpr int D_WG = 1024;            // dense path: max workgroups
+constexpr int D_THREADS = 256;
+
+// Device-side per-matrix state (in the workspace).
+struct DevState {
+    int teff;            // iterations executed by the last forward
+    int conv;            // 1 once the eps criterion stopped the iteration
+    uint32_t nonfinite;  // 1 if any weight is Inf/NaN
+    uint32_t num_unique; // occupied patterns
+    int lo4, w4;         // 4-byte table window: magnitudes [lo4, lo4 + w4), both signs
+    int lo8, w8;         // 8-byte table window
+    int mlo, mhi;        // occupied finite magnitude range
+    int pad[6];
+};
+
+// Device pointers into one plan's workspace.
+struct Ws {
+    uint32_t* counts;   // [NKEYS]
+    float* tab;         // [NKEYS]  W~ value per pattern
+    float* H;           // [NKEYS]  dW~/dw per pattern (through the final softmax)
+    float* R;           // [NKEYS]  accumulated R during the backward
+    float2* HR;         // [NKEYS]  (H, R) for the gradient gather
+    float* G;           // [NKEYS]  keyed gradient sums outside the LDS window
+    float* chist;       // [(max_iter+1) * KMAX]  C^(t)
+    float* shist;       // [(max_iter+1) * KMAX]  S^(t)
+    float* ghist;       // [(max_iter+1) * KMAX]  dL/dC^(t)
+    float* ehist;       // [KMAX]  direct-use term of the dense backward
+    float* tpart;       // [(max_iter+1) * T_WG * PSTRIDE]  forward table partials
+    float* bpart;       // [(max_iter+1) * T_WG * PSTRIDE]  backward table partials
+    float* dpart;       // [D_WG * PSTRIDE]  dense-path partials
+    int2* span;         // [NP_MAX_WG]  histogram partial spans
+    uint32_t* part;     // [NP_MAX_WG * ROW4]  N-pass partial rows
+    DevState* st;
+};
+
+// Everything a kernel needs about one matrix.
+struct MatArgs {
+    const uint16_t* keys;
+    uint64_t n;
+    const float* c_in;
+    float* c_out;
+    void* wt;                 // W~ output (float or fp16 bits)
+    int32_t* iters_out;
+    uint32_t* nuniq_out;
+    const float* g;           // dL/dW~
+    float* gw;                // dL/dw
+    float* gc;                // dL/dC^(0)
+    float* attn;              // dense map output (nullable)
+    Ws ws;
+    int k;
+    int max_iter;
+    uint32_t wg_begin;        // first N-pass workgroup of this matrix
+    uint32_t wg_count;        // N-pass workgroups (= partial rows)
+    uint64_t chunk;           // weights per N-pass workgroup (multiple of 8)
+    int vec;                  // all N-sized buffers 16-byte aligned
+};
+
+struct BatchArgs {
+    int count;
+    int t;                    // iteration index of a per-iteration launch
+    int out_fp16;
+    float s2;                 // log2(e) / tau
+    float inv_tau;
+    float eps;
+    MatArgs m[MAXB];
+};
+
+// Optional timing events recorded around the N-sized passes (diagnostics).
+enum Pass { PASS_HIST = 0, PASS_GATHER_WT = 1, PASS_KEYED_GRAD = 2, PASS_GATHER_GRAD = 3, NPASS = 4 };
+struct PassEvents {
+    hipEvent_t start[NPASS];
+    hipEvent_t stop[NPASS];
+};
+
+size_t workspace_bytes(int max_iter);
+Ws carve_workspace(void* base, int max_iter);
+
+// Launch sequences (all asynchronous on `s`).  Each returns the first HIP error.
+// On failure *where names the launch that failed.
+hipError_t launch_init_unique(BatchArgs& b, uint32_t grid_np, hipStream_t s, const char** where,
+                              const PassEvents* ev = nullptr);
+hipError_t launch_forward(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_t s, const char** where,
+                              const PassEvents* ev = nullptr);
+hipError_t launch_backward(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_t s, const char** where,
+                              const PassEvents* ev = nullptr);
+hipError_t launch_forward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where);
+hipError_t launch_backward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where);
+
+}  // namespace edkm

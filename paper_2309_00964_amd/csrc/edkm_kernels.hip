@@ -1,0 +1,1150 @@
+// eDKM hot-path kernels for gfx950 (MI355X).
+//
+// Uniquified DKM (paper Sec. 2.2): the attention map of N fp16 weights against
+// k <= 16 centroids is kept as a 65,536-row table indexed by the weights' own
+// bit patterns.  Work splits into
+//   * N-sized passes, bound by HBM bandwidth: the pattern histogram, the W~
+//     gather, the keyed reduction of dL/dW~ and the dL/dw gather.  They run one
+//     1024-thread workgroup per CU, keep a window of the table in LDS (up to
+//     160 KiB), stream the weights with 16-byte loads and merge per-workgroup
+//     results through dense partial rows instead of global atomics;
+//   * table-sized phases, bound by latency: the T softmax / centroid-update
+//     iterations and the unrolled analytic backward, one launch per iteration,
+//     64 workgroups per matrix, fixed-order tree reductions so the forward is
+//     bitwise repeatable.
+// Every launch carries up to MAXB matrices (blockIdx.y or a workgroup range per
+// matrix), so a whole decoder layer pays each launch latency once.
+//
+// Nothing here uses MFMA: k <= 16 centroids is not a dense contraction.
+
+#include "edkm_internal.h"
+
+#include <hip/hip_fp16.h>
+
+namespace edkm {
+
+// ----------------------------------------------------------------------------
+// small device helpers
+
+// fp16 bit pattern -> fp32, exact for finite values including subnormals
+// (integer decode, independent of the denormal mode).
+__device__ __forceinline__ float key_value(uint32_t h) {
+    const uint32_t e = (h >> 10) & 0x1Fu;
+    const uint32_t m = h & 0x3FFu;
+    float mag = e ? __uint_as_float(((e + 112u) << 23) | (m << 13)) : (float)m * 0x1p-24f;
+    return __uint_as_float(__float_as_uint(mag) | ((h & 0x8000u) << 16));
+}
+
+__device__ __forceinline__ bool key_finite(uint32_t h) { return (h & 0x7C00u) != 0x7C00u; }
+
+__device__ __forceinline__ float sgnf(float x) { return (float)((x > 0.f) - (x < 0.f)); }
+
+// One attention row: a_j = softmax_j(-|v - c_j| / tau), with s2 = log2(e) / tau.
+// Returns m, the nearest centroid.  The exponent -(|v - c_j| - |v - c_m|) / tau
+// is formed without subtracting two distances of size |v|: when v lies on the
+// same side of c_j and c_m the difference is exactly |c_j - c_m|, otherwise v
+// lies between them and both distances are at most |c_j - c_m|.  (Subtracting
+// fp32 distances directly loses every digit once |v| is large against the
+// centroid spacing, e.g. an outlier far from the bulk.)
+template <int K>
+__device__ __forceinline__ int attn_row(float v, const float (&c)[K], float s2, float (&a)[K]) {
+    float t[K];
+    t[0] = v - c[0];
+    float xm = fabsf(t[0]);
+    int m = 0;
+#pragma unroll
+    for (int j = 1; j < K; ++j) {
+        t[j] = v - c[j];
+        if (fabsf(t[j]) < xm) { xm = fabsf(t[j]); m = j; }
+    }
+    float cm = c[0], tm = t[0];
+#pragma unroll
+    for (int j = 1; j < K; ++j)
+        if (j == m) { cm = c[j]; tm = t[j]; }
+    const uint32_t sm = __float_as_uint(tm) >> 31;
+    float sum = 0.f;
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        const bool same = (__float_as_uint(t[j]) >> 31) == sm;
+        const float d = same ? fabsf(c[j] - cm) : fabsf(t[j]) - xm;
+        a[j] = __builtin_amdgcn_exp2f(-d * s2);
+        sum += a[j];
+    }
+    const float r = 1.0f / sum;
+#pragma unroll
+    for (int j = 0; j < K; ++j) a[j] *= r;
+    return m;
+}
+
+// Select c[m] for a run-time index m without indexing a register array.
+template <int K>
+__device__ __forceinline__ float pick(const float (&c)[K], int m) {
+    float r = c[0];
+#pragma unroll
+    for (int j = 1; j < K; ++j)
+        if (j == m) r = c[j];
+    return r;
+}
+
+// Softmax-Jacobian deviations of one table row in the backward:
+//   dev_j = alpha_j - sum_i a_i alpha_i,  alpha_j = gS_j (v - c1_j),
+// written around the reference c1_m as
+//   dev_j = (gS_j - gbar)(v - c1_m) - (gS_j (c1_j - c1_m) - hb),
+//   gbar = sum_i a_i gS_i,  hb = sum_i a_i gS_i (c1_i - c1_m),
+// which never subtracts two terms of size |v|.  Returns gbar.
+template <int K>
+__device__ __forceinline__ float softmax_dev(float v, const float (&a)[K], const float (&gS)[K],
+                                             const float (&c1)[K], int m, float (&dev)[K]) {
+    const float cm = pick<K>(c1, m);
+    float gbar = 0.f, hb = 0.f;
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        const float ag = a[j] * gS[j];
+        gbar += ag;
+        hb = fmaf(ag, c1[j] - cm, hb);
+    }
+    const float w1 = v - cm;
+#pragma unroll
+    for (int j = 0; j < K; ++j) dev[j] = fmaf(gS[j] - gbar, w1, -fmaf(gS[j], c1[j] - cm, -hb));
+    return gbar;
+}
+
+// Butterfly sum over the 64 lanes; lane 0's value is the one used, so the
+// association order is fixed.
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+    return x;
+}
+
+// Sum NV per-thread values over a block of NT threads into out[0..NV) (LDS),
+// in a fixed order.  `scratch` holds NT/64 * NV floats.
+template <int NV, int NT>
+__device__ __forceinline__ void block_sum(const float (&v)[NV], float* scratch, float* out) {
+    constexpr int NW = NT / 64;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        float s = wave_sum(v[j]);
+        if (lane == 0) scratch[wave * NV + j] = s;
+    }
+    __syncthreads();
+    if (threadIdx.x < NV) {
+        float s = 0.f;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) s += scratch[w * NV + threadIdx.x];
+        out[threadIdx.x] = s;
+    }
+    __syncthreads();
+}
+
+// Reduce rows [0, T_WG) of a partial block (T_WG x PSTRIDE floats) for columns
+// [c0, c0 + ncol) into out[0..ncol) (LDS), by wave butterflies.  Called by all
+// threads of a T_THREADS block.
+__device__ __forceinline__ void reduce_tparts(const float* part, int c0, int ncol, float* out) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (int j = wave; j < ncol; j += T_THREADS / 64) {
+        float s = wave_sum(part[lane * PSTRIDE + c0 + j]);
+        if (lane == 0) out[j] = s;
+    }
+    __syncthreads();
+}
+
+// Matrix of an N-pass workgroup, and its slice [beg, end).
+__device__ __forceinline__ int np_matrix(const BatchArgs& b) {
+    int m = 0;
+    while (m + 1 < b.count && blockIdx.x >= b.m[m + 1].wg_begin) ++m;
+    return m;
+}
+
+// Apply f8(i) to 8-weight groups and f1(i) to single weights covering [beg, end).
+template <class F8, class F1>
+__device__ __forceinline__ void for_slice(uint64_t beg, uint64_t end, bool vec, F8 f8, F1 f1) {
+    if (vec) {
+        const uint64_t vend = beg + ((end - beg) & ~7ull);
+        const uint64_t step = 8ull * NP_THREADS;
+        uint64_t i = beg + 8ull * threadIdx.x;
+        for (; i + step < vend; i += 2 * step) {   // two groups in flight per thread
+            f8(i);
+            f8(i + step);
+        }
+        if (i < vend) f8(i);
+        for (uint64_t j = vend + threadIdx.x; j < end; j += NP_THREADS) f1(j);
+    } else {
+        for (uint64_t j = beg + threadIdx.x; j < end; j += NP_THREADS) f1(j);
+    }
+}
+
+// ----------------------------------------------------------------------------
+// init_unique: zero, histogram, partial merge, window selection
+
+__global__ void __launch_bounds__(T_THREADS) k_init_zero(BatchArgs b) {
+    const MatArgs& M = b.m[blockIdx.y];
+    for (int u = blockIdx.x * T_THREADS + threadIdx.x; u < NKEYS; u += gridDim.x * T_THREADS)
+        M.ws.counts[u] = 0u;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        DevState* st = M.ws.st;
+        st->teff = 0;
+        st->conv = 0;
+        st->nonfinite = 0u;
+        st->num_unique = 0u;
+    }
+}
+
+// Pattern histogram.  Magnitudes [0, W4) of both signs (|w| < 16) count in
+// LDS; anything else goes straight to the global counts with an atomic.
+// Each workgroup then writes the occupied span of its LDS histogram as packed
+// 16-bit counts (two bins per word); a bin that reached 2^16 in this
+// workgroup is added to the global counts instead.
+__global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
+    __shared__ uint32_t h[2 * W4];
+    __shared__ int red[2];
+    const int mi = np_matrix(b);
+    const MatArgs& M = b.m[mi];
+    const uint32_t wl = blockIdx.x - M.wg_begin;
+    const uint64_t beg = (uint64_t)wl * M.chunk;
+    const uint64_t end = min(M.n, beg + M.chunk);
+    for (int i = threadIdx.x; i < 2 * W4; i += NP_THREADS) h[i] = 0u;
+    if (threadIdx.x == 0) { red[0] = W4; red[1] = 0; }
+    __syncthreads();
+    const uint16_t* keys = M.keys;
+    uint32_t* gcounts = M.ws.counts;
+    auto add = [&](uint32_t key) {
+        const uint32_t mag = key & 0x7FFFu;
+        if (mag < (uint32_t)W4) atomicAdd(&h[(key >> 15) * W4 + mag], 1u);
+        else atomicAdd(&gcounts[key], 1u);
+    };
+    for_slice(beg, end, M.vec != 0,
+        [&](uint64_t i) {
+            const uint4 q = *reinterpret_cast<const uint4*>(keys + i);
+            add(q.x & 0xFFFFu); add(q.x >> 16);
+            add(q.y & 0xFFFFu); add(q.y >> 16);
+            add(q.z & 0xFFFFu); add(q.z >> 16);
+            add(q.w & 0xFFFFu); add(q.w >> 16);
+        },
+        [&](uint64_t i) { add(keys[i]); });
+    __syncthreads();
+    // occupied span [lo, hi) over both signs, rounded out to even magnitudes
+    int lo = W4, hi = 0;
+    for (int mag = threadIdx.x; mag < W4; mag += NP_THREADS) {
+        if (h[mag] | h[W4 + mag]) { lo = min(lo, mag); hi = max(hi, mag + 1); }
+    }
+    atomicMin(&red[0], lo);
+    atomicMax(&red[1], hi);
+    __syncthreads();
+    lo = red[0] & ~1;
+    hi = (red[1] + 1) & ~1;
+    if (hi <= lo) { lo = 0; hi = 0; }
+    const int half = (hi - lo) >> 1;
+    uint32_t* row = M.ws.part + (size_t)wl * ROW4;
+    for (int p = threadIdx.x; p < 2 * half; p += NP_THREADS) {
+        const int s = p >= half;
+        const int mag = lo + 2 * (p - s * half);
+        uint32_t c0 = h[s * W4 + mag], c1 = h[s * W4 + mag + 1];
+        if (c0 > 0xFFFFu) { atomicAdd(&gcounts[(s << 15) | mag], c0); c0 = 0u; }
+        if (c1 > 0xFFFFu) { atomicAdd(&gcounts[(s << 15) | (mag + 1)], c1); c1 = 0u; }
+        row[p] = c0 | (c1 << 16);
+    }
+    if (threadIdx.x == 0) M.ws.span[wl] = make_int2(lo, hi);
+}
+
+// Sum the histogram partial rows of each matrix: one thread per pair of bins.
+// Grid (W4 / NP_THREADS, count).
+__global__ void __launch_bounds__(NP_THREADS) k_hist_merge(BatchArgs b) {
+    __shared__ int2 sp[NP_MAX_WG];
+    const MatArgs& M = b.m[blockIdx.y];
+    const int nrow = (int)M.wg_count;
+    for (int r = threadIdx.x; r < nrow; r += NP_THREADS) sp[r] = M.ws.span[r];
+    __syncthreads();
+    const int q = blockIdx.x * NP_THREADS + threadIdx.x;   // < W4
+    const int s = q >= W4 / 2;
+    const int mag = 2 * (q - s * (W4 / 2));
+    uint32_t s0 = 0u, s1 = 0u;
+    const uint32_t* part = M.ws.part;
+    for (int r = 0; r < nrow; ++r) {
+        const int2 lh = sp[r];
+        if (mag >= lh.x && mag < lh.y) {
+            const int half = (lh.y - lh.x) >> 1;
+            const uint32_t x = part[(size_t)r * ROW4 + s * half + ((mag - lh.x) >> 1)];
+            s0 += x & 0xFFFFu;
+            s1 += x >> 16;
+        }
+    }
+    uint32_t* c = M.ws.counts + (s << 15) + mag;
+    c[0] += s0;   // the global counts may already hold this workgroup-overflow share
+    c[1] += s1;
+}
+
+// Block-wide exclusive scan of one uint32 per thread (1024 threads).
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t x, uint32_t* tmp /*16*/) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint32_t inc = x;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        uint32_t y = __shfl_up(inc, o, 64);
+        if (lane >= o) inc += y;
+    }
+    if (lane == 63) tmp[wave] = inc;
+    __syncthreads();
+    uint32_t base = 0;
+    for (int w = 0; w < wave; ++w) base += tmp[w];
+    __syncthreads();
+    return base + inc - x;
+}
+
+// Per matrix, one block: occupied-pattern count, non-finite flag, the
+// occupied finite magnitude range, and the LDS windows of the later passes.
+// A window of width W covers the whole occupied range when it fits, else the
+// W consecutive magnitudes holding the most weights (lowest start on ties).
+__global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
+    __shared__ uint32_t P[FIN_MAGS + 1];
+    __shared__ uint32_t tmp[16];
+    __shared__ int ired[4];
+    __shared__ unsigned long long best[2];
+    const MatArgs& M = b.m[blockIdx.y];
+    const uint32_t* counts = M.ws.counts;
+    const int m0 = threadIdx.x * 32;   // 32 magnitudes per thread; threads >= 992 hold non-finite ones
+    uint32_t local = 0, nuniq = 0, nonfin = 0;
+    int lo = 1 << 30, hi = -1;
+    for (int j = 0; j < 32; ++j) {
+        const int mag = m0 + j;
+        const uint32_t cp = counts[mag], cn = counts[0x8000 | mag];
+        nuniq += (cp != 0u) + (cn != 0u);
+        if (mag < FIN_MAGS) {
+            const uint32_t c = cp + cn;
+            if (c) { lo = min(lo, mag); hi = mag; }
+            local += c;
+        } else {
+            nonfin |= (cp | cn) != 0u;
+        }
+    }
+    if (threadIdx.x == 0) { ired[0] = 1 << 30; ired[1] = -1; ired[2] = 0; ired[3] = 0; P[0] = 0u; }
+    __syncthreads();
+    atomicMin(&ired[0], lo);
+    atomicMax(&ired[1], hi);
+    atomicAdd(&ired[2], (int)nuniq);
+    atomicOr(&ired[3], (int)nonfin);
+    uint32_t run = block_excl_scan(local, tmp);
+    if (m0 < FIN_MAGS) {
+        for (int j = 0; j < 32; ++j) {
+            const int mag = m0 + j;
+            run += counts[mag] + counts[0x8000 | mag];
+            P[mag + 1] = run;                       // P[m] = weights with magnitude < m
+        }
+    }
+    __syncthreads();
+    const int mlo = ired[0], mhi = ired[1];
+    int wl[2], ww[2];
+    const int widths[2] = {W4, W8};
+    for (int w = 0; w < 2; ++w) {
+        const int W = widths[w];
+        if (mhi < 0) { wl[w] = 0; ww[w] = 0; continue; }
+        if (mhi - mlo + 1 <= W) { wl[w] = mlo; ww[w] = mhi - mlo + 1; continue; }
+        if (threadIdx.x == 0) best[w] = 0ull;
+        __syncthreads();
+        unsigned long long mine = 0ull;
+        for (int s = mlo + threadIdx.x; s <= mhi - W + 1; s += NP_THREADS) {
+            const uint32_t cov = P[s + W] - P[s];
+            // larger coverage wins, then the smaller start
+            const unsigned long long key = ((unsigned long long)cov << 32) | (uint32_t)(0x7FFFFFFF - s);
+            mine = key > mine ? key : mine;
+        }
+        atomicMax(&best[w], mine);
+        __syncthreads();
+        wl[w] = 0x7FFFFFFF - (int)(uint32_t)(best[w] & 0xFFFFFFFFull);
+        ww[w] = W;
+    }
+    if (threadIdx.x == 0) {
+        DevState* st = M.ws.st;
+        st->num_unique = (uint32_t)ired[2];
+        st->nonfinite = (uint32_t)ired[3];
+        st->mlo = mlo;
+        st->mhi = mhi;
+        st->lo4 = wl[0]; st->w4 = ww[0];
+        st->lo8 = wl[1]; st->w8 = ww[1];
+        if (M.nuniq_out) *M.nuniq_out = (uint32_t)ired[2];
+    }
+}
+
+// ----------------------------------------------------------------------------
+// forward table phase
+
+// Table keys of block x (T_WG blocks x T_THREADS threads x 4 = 65,536).
+#define FOR_TABLE_KEYS(u) \
+    for (int r_ = 0, u = blockIdx.x * T_THREADS + threadIdx.x; r_ < 4; ++r_, u += T_WG * T_THREADS)
+
+// Iteration t (1..max_iter): C^(t-1) from the partials of iteration t-1 (or
+// c_in), early stop test, then this block's partial S_j = sum n_u a_uj and
+// P_j = sum n_u a_uj v_u.  Grid (T_WG, count).
+template <int K>
+__global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
+    __shared__ float tot[2 * K];
+    __shared__ float scratch[T_THREADS / 64 * 2 * K];
+    __shared__ float csh[K];
+    __shared__ int stop;
+    const MatArgs& M = b.m[blockIdx.y];
+    const int t = b.t;
+    if (t > M.max_iter) return;
+    DevState* st = M.ws.st;
+    const bool lead = blockIdx.x == 0;
+    if (t == 1) {
+        if (threadIdx.x < K) {
+            const float c = M.c_in[threadIdx.x];
+            csh[threadIdx.x] = c;
+            if (lead) { M.ws.chist[threadIdx.x] = c; M.ws.shist[threadIdx.x] = 0.f; }
+        }
+        if (lead && threadIdx.x == 0) { st->conv = 0; st->teff = 0; }
+        __syncthreads();
+    } else {
+        if (st->conv) return;
+        reduce_tparts(M.ws.tpart + (size_t)(t - 1) * T_WG * PSTRIDE, 0, 2 * K, tot);
+        if (threadIdx.x == 0) stop = 0;
+        __syncthreads();
+        if (threadIdx.x < K) {
+            const int j = threadIdx.x;
+            const float S = tot[j], P = tot[K + j];
+            const float cprev = M.ws.chist[(t - 2) * KMAX + j];
+            const float cn = S > 0.f ? P / S : cprev;
+            csh[j] = cn;
+            if (lead) { M.ws.chist[(t - 1) * KMAX + j] = cn; M.ws.shist[(t - 1) * KMAX + j] = S; }
+            if (b.eps > 0.f && !(fabsf(cn - cprev) <= b.eps)) atomicOr(&stop, 1);
+        }
+        __syncthreads();
+        if (b.eps > 0.f && stop == 0) {   // max_j |C^(t-1) - C^(t-2)| <= eps: T = t - 1
+            if (lead && threadIdx.x == 0) { st->teff = t - 1; st->conv = 1; }
+            return;
+        }
+    }
+    float c[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) c[j] = csh[j];
+    float acc[2 * K];
+#pragma unroll
+    for (int j = 0; j < 2 * K; ++j) acc[j] = 0.f;
+    const uint32_t* counts = M.ws.counts;
+    FOR_TABLE_KEYS(u) {
+        const uint32_t n = counts[u];
+        if (n == 0u || !key_finite(u)) continue;
+        const float v = key_value(u);
+        float a[K];
+        attn_row<K>(v, c, b.s2, a);
+        const float nf = (float)n;
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const float w = nf * a[j];
+            acc[j] += w;
+            acc[K + j] = fmaf(w, v, acc[K + j]);
+        }
+    }
+    block_sum<2 * K, T_THREADS>(acc, scratch, tot);
+    if (threadIdx.x < 2 * K)
+        M.ws.tpart[((size_t)t * T_WG + blockIdx.x) * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
+}
+
+// After the last iteration: C^(T), c_out, T; per occupied pattern the W~ value
+// Tab_u = sum_j a^(T)_uj C^(T)_j (a^(T) built from C^(T-1)) and
+// H_u = -(1/tau) sum_j a^(T)_uj (C^(T)_j - Tab_u) sgn(v_u - C^(T-1)_j);
+// clears G.  Grid (T_WG, count).
+template <int K>
+__global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
+    __shared__ float tot[2 * K];
+    __shared__ float cT[K], cP[K];
+    const MatArgs& M = b.m[blockIdx.y];
+    DevState* st = M.ws.st;
+    const bool lead = blockIdx.x == 0;
+    int T;
+    if (st->conv) {
+        T = st->teff;
+        if (threadIdx.x < K) {
+            cT[threadIdx.x] = M.ws.chist[T * KMAX + threadIdx.x];
+            cP[threadIdx.x] = M.ws.chist[(T - 1) * KMAX + threadIdx.x];
+        }
+        __syncthreads();
+    } else {
+        T = M.max_iter;
+        reduce_tparts(M.ws.tpart + (size_t)T * T_WG * PSTRIDE, 0, 2 * K, tot);
+        if (threadIdx.x < K) {
+            const int j = threadIdx.x;
+            const float S = tot[j], P = tot[K + j];
+            const float cprev = M.ws.chist[(T - 1) * KMAX + j];
+            const float cn = S > 0.f ? P / S : cprev;
+            cT[j] = cn;
+            cP[j] = cprev;
+            if (lead) { M.ws.chist[T * KMAX + j] = cn; M.ws.shist[T * KMAX + j] = S; }
+        }
+        if (lead && threadIdx.x == 0) st->teff = T;
+        __syncthreads();
+    }
+    if (lead) {
+        if (threadIdx.x < K) M.c_out[threadIdx.x] = cT[threadIdx.x];
+        if (threadIdx.x == 0 && M.iters_out) *M.iters_out = T;
+    }
+    float c1[K], c0[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) { c1[j] = cT[j]; c0[j] = cP[j]; }
+    const uint32_t* counts = M.ws.counts;
+    FOR_TABLE_KEYS(u) {
+        M.ws.G[u] = 0.f;
+        const uint32_t n = counts[u];
+        if (n == 0u) continue;
+        if (!key_finite(u)) { M.ws.tab[u] = __builtin_nanf(""); M.ws.H[u] = __builtin_nanf(""); continue; }
+        const float v = key_value(u);
+        float a[K];
+        attn_row<K>(v, c0, b.s2, a);
+        float tv = 0.f;
+#pragma unroll
+        for (int j = 0; j < K; ++j) tv = fmaf(a[j], c1[j], tv);
+        float h = 0.f;
+#pragma unroll
+        for (int j = 0; j < K; ++j) h = fmaf(a[j] * (c1[j] - tv), sgnf(v - c0[j]), h);
+        M.ws.tab[u] = tv;
+        M.ws.H[u] = -h * b.inv_tau;
+    }
+}
+
+// ----------------------------------------------------------------------------
+// N-sized gathers and the keyed reduction
+
+// W~_i = Tab[bits_i]; the window [lo4, lo4 + w4) of the table sits in LDS.
+__global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
+    __shared__ float tw[2 * W4];
+    const int mi = np_matrix(b);
+    const MatArgs& M = b.m[mi];
+    const uint32_t wl = blockIdx.x - M.wg_begin;
+    const uint64_t beg = (uint64_t)wl * M.chunk;
+    const uint64_t end = min(M.n, beg + M.chunk);
+    const int lo = M.ws.st->lo4, w = M.ws.st->w4;
+    const float* tab = M.ws.tab;
+    for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) {
+        const int s = i >= w;
+        tw[i] = tab[(s << 15) | (lo + i - s * w)];
+    }
+    __syncthreads();
+    auto look = [&](uint32_t key) -> float {
+        const uint32_t d = (key & 0x7FFFu) - (uint32_t)lo;
+        return d < (uint32_t)w ? tw[(key >> 15) * w + d] : tab[key];
+    };
+    const uint16_t* keys = M.keys;
+    if (b.out_fp16) {
+        __half* out = reinterpret_cast<__half*>(M.wt);
+        for_slice(beg, end, M.vec != 0,
+            [&](uint64_t i) {
+                const uint4 q = *reinterpret_cast<const uint4*>(keys + i);
+                const uint32_t ks[4] = {q.x, q.y, q.z, q.w};
+                uint32_t o[4];
+#pragma unroll
+                for (int p = 0; p < 4; ++p) {
+                    const __half lo_h = __float2half_rn(look(ks[p] & 0xFFFFu));
+                    const __half hi_h = __float2half_rn(look(ks[p] >> 16));
+                    o[p] = (uint32_t)__half_as_ushort(lo_h) | ((uint32_t)__half_as_ushort(hi_h) << 16);
+                }
+                *reinterpret_cast<uint4*>(out + i) = make_uint4(o[0], o[1], o[2], o[3]);
+            },
+            [&](uint64_t i) { out[i] = __float2half_rn(look(keys[i])); });
+    } else {
+        float* out = reinterpret_cast<float*>(M.wt);
+        for_slice(beg, end, M.vec != 0,
+            [&](uint64_t i) {
+                const uint4 q = *reinterpret_cast<const uint4*>(keys + i);
+                float4 a, c;
+                a.x = look(q.x & 0xFFFFu); a.y = look(q.x >> 16);
+                a.z = look(q.y & 0xFFFFu); a.w = look(q.y >> 16);
+                c.x = look(q.z & 0xFFFFu); c.y = look(q.z >> 16);
+                c.z = look(q.w & 0xFFFFu); c.w = look(q.w >> 16);
+                *reinterpret_cast<float4*>(out + i) = a;
+                *reinterpret_cast<float4*>(out + i + 4) = c;
+            },
+            [&](uint64_t i) { out[i] = look(keys[i]); });
+    }
+}
+
+// G_u = sum over weights with pattern u of dL/dW~_i.  Window patterns add in
+// LDS (fp32 atomics), the rest into the global G; each workgroup then writes
+// its window as one partial row.
+__global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
+    __shared__ float acc[2 * W4];
+    const int mi = np_matrix(b);
+    const MatArgs& M = b.m[mi];
+    const uint32_t wl = blockIdx.x - M.wg_begin;
+    const uint64_t beg = (uint64_t)wl * M.chunk;
+    const uint64_t end = min(M.n, beg + M.chunk);
+    const int lo = M.ws.st->lo4, w = M.ws.st->w4;
+    for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) acc[i] = 0.f;
+    __syncthreads();
+    float* G = M.ws.G;
+    auto add = [&](uint32_t key, float g) {
+        const uint32_t d = (key & 0x7FFFu) - (uint32_t)lo;
+        if (d < (uint32_t)w) atomicAdd(&acc[(key >> 15) * w + d], g);
+        else atomicAdd(&G[key], g);
+    };
+    const uint16_t* keys = M.keys;
+    const float* g = M.g;
+    for_slice(beg, end, M.vec != 0,
+        [&](uint64_t i) {
+            const uint4 q = *reinterpret_cast<const uint4*>(keys + i);
+            const float4 ga = *reinterpret_cast<const float4*>(g + i);
+            const float4 gb = *reinterpret_cast<const float4*>(g + i + 4);
+            add(q.x & 0xFFFFu, ga.x); add(q.x >> 16, ga.y);
+            add(q.y & 0xFFFFu, ga.z); add(q.y >> 16, ga.w);
+            add(q.z & 0xFFFFu, gb.x); add(q.z >> 16, gb.y);
+            add(q.w & 0xFFFFu, gb.z); add(q.w >> 16, gb.w);
+        },
+        [&](uint64_t i) { add(keys[i], g[i]); });
+    __syncthreads();
+    float* row = reinterpret_cast<float*>(M.ws.part) + (size_t)wl * ROW4;
+    for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) row[i] = acc[i];
+}
+
+// dL/dw_i = g_i H[bits_i] + R[bits_i]; the window [lo8, lo8 + w8) of (H, R) sits
+// in LDS.  The first workgroup of each matrix also finishes dL/dC^(0); every
+// workgroup clears a slice of G for the next backward.
+__global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
+    __shared__ float2 hw[2 * W8];
+    const int mi = np_matrix(b);
+    const MatArgs& M = b.m[mi];
+    const uint32_t wl = blockIdx.x - M.wg_begin;
+    const uint64_t beg = (uint64_t)wl * M.chunk;
+    const uint64_t end = min(M.n, beg + M.chunk);
+    const DevState* st = M.ws.st;
+    const int lo = st->lo8, w = st->w8;
+    const float2* HR = M.ws.HR;
+    if (wl == 0 && threadIdx.x < 64) {
+        // dL/dC^(0) = (1/tau) sum of the t = 1 partials + the terms that bypass the softmax
+        const int T = st->teff, k = M.k;
+        const float* p1 = M.ws.bpart + (size_t)1 * T_WG * PSTRIDE;
+        const float* p0 = M.ws.bpart;
+        for (int j = 0; j < k; ++j) {
+            const float x = wave_sum(p1[threadIdx.x * PSTRIDE + j]);
+            const float e = wave_sum(p0[threadIdx.x * PSTRIDE + k + j]);
+            if (threadIdx.x == 0) {
+                float gc = x * b.inv_tau;
+                if (T == 1) gc += e * b.inv_tau;
+                if (!(M.ws.shist[KMAX + j] > 0.f)) gc += M.ws.ghist[KMAX + j];
+                M.gc[j] = gc;
+            }
+        }
+    }
+    {
+        const uint32_t per = (NKEYS + M.wg_count - 1) / M.wg_count;
+        const uint32_t u0 = wl * per, u1 = min((uint32_t)NKEYS, u0 + per);
+        for (uint32_t u = u0 + threadIdx.x; u < u1; u += NP_THREADS) M.ws.G[u] = 0.f;
+    }
+    for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) {
+        const int s = i >= w;
+        hw[i] = HR[(s << 15) | (lo + i - s * w)];
+    }
+    __syncthreads();
+    auto look = [&](uint32_t key) -> float2 {
+        const uint32_t d = (key & 0x7FFFu) - (uint32_t)lo;
+        return d < (uint32_t)w ? hw[(key >> 15) * w + d] : HR[key];
+    };
+    const uint16_t* keys = M.keys;
+    const float* g = M.g;
+    float* out = M.gw;
+    for_slice(beg, end, M.vec != 0,
+        [&](uint64_t i) {
+            const uint4 q = *reinterpret_cast<const uint4*>(keys + i);
+            const float4 ga = *reinterpret_cast<const float4*>(g + i);
+            const float4 gb = *reinterpret_cast<const float4*>(g + i + 4);
+            float2 h;
+            float4 oa, ob;
+            h = look(q.x & 0xFFFFu); oa.x = fmaf(ga.x, h.x, h.y);
+            h = look(q.x >> 16);     oa.y = fmaf(ga.y, h.x, h.y);
+            h = look(q.y & 0xFFFFu); oa.z = fmaf(ga.z, h.x, h.y);
+            h = look(q.y >> 16);     oa.w = fmaf(ga.w, h.x, h.y);
+            h = look(q.z & 0xFFFFu); ob.x = fmaf(gb.x, h.x, h.y);
+            h = look(q.z >> 16);     ob.y = fmaf(gb.y, h.x, h.y);
+            h = look(q.w & 0xFFFFu); ob.z = fmaf(gb.z, h.x, h.y);
+            h = look(q.w >> 16);     ob.w = fmaf(gb.w, h.x, h.y);
+            *reinterpret_cast<float4*>(out + i) = oa;
+            *reinterpret_cast<float4*>(out + i + 4) = ob;
+        },
+        [&](uint64_t i) {
+            const float2 h = look(keys[i]);
+            out[i] = fmaf(g[i], h.x, h.y);
+        });
+}
+
+// ----------------------------------------------------------------------------
+// backward table phase
+
+// Direct use of A^(T) and C^(T) by W~: G_u from the keyed-reduction partial
+// rows, then partials of gamma_j = sum_u G_u a^(T)_uj (= dL/dC^(T)_j) and
+// E_j = sum_u G_u a^(T)_uj (C^(T)_j - Tab_u) sgn(v_u - C^(T-1)_j).
+// Grid (T_WG, count).
+template <int K>
+__global__ void __launch_bounds__(T_THREADS) k_bwd_top(BatchArgs b) {
+    __shared__ float tot[2 * K];
+    __shared__ float scratch[T_THREADS / 64 * 2 * K];
+    const MatArgs& M = b.m[blockIdx.y];
+    const DevState* st = M.ws.st;
+    const int T = st->teff;
+    float c1[K], c0[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) { c1[j] = M.ws.chist[T * KMAX + j]; c0[j] = M.ws.chist[(T - 1) * KMAX + j]; }
+    const int lo = st->lo4, w = st->w4;
+    const int nrow = (int)M.wg_count;
+    const float* part = reinterpret_cast<const float*>(M.ws.part);
+    float acc[2 * K];
+#pragma unroll
+    for (int j = 0; j < 2 * K; ++j) acc[j] = 0.f;
+    const uint32_t* counts = M.ws.counts;
+    FOR_TABLE_KEYS(u) {
+        if (counts[u] == 0u || !key_finite(u)) continue;
+        const uint32_t d = (uint32_t)(u & 0x7FFF) - (uint32_t)lo;
+        float G;
+        if (d < (uint32_t)w) {
+            const float* p = part + (u >> 15) * w + d;
+            G = 0.f;
+            for (int r = 0; r < nrow; ++r) G += p[(size_t)r * ROW4];
+        } else {
+            G = M.ws.G[u];
+        }
+        const float v = key_value(u);
+        float a[K];
+        attn_row<K>(v, c0, b.s2, a);
+        const float tv = M.ws.tab[u];
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const float ga = G * a[j];
+            acc[j] += ga;
+            acc[K + j] = fmaf(ga * (c1[j] - tv), sgnf(v - c0[j]), acc[K + j]);
+        }
+    }
+    block_sum<2 * K, T_THREADS>(acc, scratch, tot);
+    if (threadIdx.x < 2 * K)
+        M.ws.bpart[(size_t)blockIdx.x * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
+}
+
+// Iteration t = T..1 of the backward: gamma = dL/dC^(t), then per occupied
+// pattern
+//   alpha_j = gamma_j (v_u - C^(t)_j) / S^(t)_j,  abar = sum_j a_uj alpha_j,
+//   delta_j = a_uj (alpha_j - abar),
+//   R_u    += sum_j a_uj gamma_j / S^(t)_j - (1/tau) sum_j delta_j sgn(v_u - C^(t-1)_j),
+// and partials of sum_u n_u delta_j sgn(v_u - C^(t-1)_j), which (times 1/tau)
+// make dL/dC^(t-1).  Grid (T_WG, count).
+template <int K>
+__global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
+    __shared__ float tot[2 * K];
+    __shared__ float scratch[T_THREADS / 64 * K];
+    __shared__ float gsh[K];
+    const MatArgs& M = b.m[blockIdx.y];
+    const DevState* st = M.ws.st;
+    const int T = st->teff;
+    const int t = b.t;
+    if (t > T) return;
+    const bool lead = blockIdx.x == 0;
+    if (t == T) {
+        reduce_tparts(M.ws.bpart, 0, K, tot);
+        if (threadIdx.x < K) gsh[threadIdx.x] = tot[threadIdx.x];
+    } else {
+        reduce_tparts(M.ws.bpart + (size_t)(t + 1) * T_WG * PSTRIDE, 0, K, tot);
+        reduce_tparts(M.ws.bpart, K, K, tot + K);
+        if (threadIdx.x < K) {
+            const int j = threadIdx.x;
+            float gm = tot[j] * b.inv_tau;
+            if (t + 1 == T) gm += tot[K + j] * b.inv_tau;
+            if (!(M.ws.shist[(t + 1) * KMAX + j] > 0.f)) gm += M.ws.ghist[(t + 1) * KMAX + j];
+            gsh[j] = gm;
+        }
+    }
+    __syncthreads();
+    if (lead && threadIdx.x < K) M.ws.ghist[t * KMAX + threadIdx.x] = gsh[threadIdx.x];
+    float c1[K], c0[K], gS[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        c1[j] = M.ws.chist[t * KMAX + j];
+        c0[j] = M.ws.chist[(t - 1) * KMAX + j];
+        const float S = M.ws.shist[t * KMAX + j];
+        gS[j] = S > 0.f ? gsh[j] / S : 0.f;
+    }
+    float acc[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) acc[j] = 0.f;
+    const uint32_t* counts = M.ws.counts;
+    FOR_TABLE_KEYS(u) {
+        const uint32_t n = counts[u];
+        if (n == 0u) continue;
+        if (!key_finite(u)) {
+            if (t == 1) M.ws.HR[u] = make_float2(__builtin_nanf(""), __builtin_nanf(""));
+            continue;
+        }
+        const float v = key_value(u);
+        float a[K], dev[K];
+        const int m = attn_row<K>(v, c0, b.s2, a);
+        const float direct = softmax_dev<K>(v, a, gS, c1, m, dev);
+        const float nf = (float)n;
+        float r = 0.f;
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const float dl = a[j] * dev[j] * sgnf(v - c0[j]);
+            r += dl;
+            acc[j] = fmaf(nf, dl, acc[j]);
+        }
+        float Ru = fmaf(-r, b.inv_tau, direct);
+        if (t != T) Ru += M.ws.R[u];
+        if (t == 1) M.ws.HR[u] = make_float2(M.ws.H[u], Ru);
+        else M.ws.R[u] = Ru;
+    }
+    block_sum<K, T_THREADS>(acc, scratch, tot);
+    if (threadIdx.x < K)
+        M.ws.bpart[((size_t)t * T_WG + blockIdx.x) * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
+}
+
+// ----------------------------------------------------------------------------
+// dense (non-uniquified) comparison path: one attention row per weight
+
+__device__ __forceinline__ bool dense_range(const MatArgs& M, uint64_t& beg, uint64_t& end) {
+    beg = (uint64_t)blockIdx.x * M.chunk;
+    end = min(M.n, beg + M.chunk);
+    return beg < end;
+}
+
+// Fixed-order sum of the first nrow dense partial rows, columns [c0, c0+ncol),
+// by one block of 1024 threads; result in out[0..ncol) (LDS).
+__device__ __forceinline__ void reduce_dparts(const float* part, int nrow, int c0, int ncol,
+                                              float* scratch /*16*32*/, float* out) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (int j = 0; j < ncol; ++j) {
+        float x = threadIdx.x < nrow ? part[threadIdx.x * PSTRIDE + c0 + j] : 0.f;
+        x = wave_sum(x);
+        if (lane == 0) scratch[wave * PSTRIDE + j] = x;
+    }
+    __syncthreads();
+    if (threadIdx.x < ncol) {
+        float s = 0.f;
+        for (int w = 0; w < 16; ++w) s += scratch[w * PSTRIDE + threadIdx.x];
+        out[threadIdx.x] = s;
+    }
+    __syncthreads();
+}
+
+template <int K>
+__global__ void __launch_bounds__(D_THREADS) k_dense_iter(BatchArgs b) {
+    __shared__ float tot[2 * K];
+    __shared__ float scratch[D_THREADS / 64 * 2 * K];
+    const MatArgs& M = b.m[0];
+    const int t = b.t;
+    if (t > 1 && M.ws.st->conv) return;
+    float c[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) c[j] = t == 1 ? M.c_in[j] : M.ws.chist[(t - 1) * KMAX + j];
+    float acc[2 * K];
+#pragma unroll
+    for (int j = 0; j < 2 * K; ++j) acc[j] = 0.f;
+    uint64_t beg, end;
+    dense_range(M, beg, end);
+    for (uint64_t i = beg + threadIdx.x; i < end; i += D_THREADS) {
+        const uint32_t key = M.keys[i];
+        if (!key_finite(key)) continue;
+        const float v = key_value(key);
+        float a[K];
+        attn_row<K>(v, c, b.s2, a);
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            acc[j] += a[j];
+            acc[K + j] = fmaf(a[j], v, acc[K + j]);
+        }
+    }
+    block_sum<2 * K, D_THREADS>(acc, scratch, tot);
+    if (threadIdx.x < 2 * K) M.ws.dpart[(size_t)blockIdx.x * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
+}
+
+// One block: C^(t) from the dense partials, history, early stop.
+template <int K>
+__global__ void __launch_bounds__(1024) k_dense_fin(BatchArgs b, int nrow) {
+    __shared__ float scratch[16 * PSTRIDE];
+    __shared__ float tot[2 * K];
+    __shared__ int stop;
+    const MatArgs& M = b.m[0];
+    DevState* st = M.ws.st;
+    const int t = b.t;
+    if (t > 1 && st->conv) return;
+    reduce_dparts(M.ws.dpart, nrow, 0, 2 * K, scratch, tot);
+    if (threadIdx.x == 0) stop = 0;
+    __syncthreads();
+    if (threadIdx.x < K) {
+        const int j = threadIdx.x;
+        const float cprev = t == 1 ? M.c_in[j] : M.ws.chist[(t - 1) * KMAX + j];
+        if (t == 1) { M.ws.chist[j] = cprev; M.ws.shist[j] = 0.f; }
+        const float S = tot[j], P = tot[K + j];
+        const float cn = S > 0.f ? P / S : cprev;
+        M.ws.chist[t * KMAX + j] = cn;
+        M.ws.shist[t * KMAX + j] = S;
+        if (!(fabsf(cn - cprev) <= b.eps)) atomicOr(&stop, 1);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        if (b.eps > 0.f && stop == 0) { st->conv = 1; st->teff = t; }
+        else { st->conv = 0; st->teff = t; }
+    }
+}
+
+template <int K>
+__global__ void __launch_bounds__(D_THREADS) k_dense_out(BatchArgs b) {
+    const MatArgs& M = b.m[0];
+    const int T = M.ws.st->teff;
+    float c1[K], c0[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) { c1[j] = M.ws.chist[T * KMAX + j]; c0[j] = M.ws.chist[(T - 1) * KMAX + j]; }
+    if (blockIdx.x == 0) {
+        if (threadIdx.x < K) M.c_out[threadIdx.x] = M.ws.chist[T * KMAX + threadIdx.x];
+        if (threadIdx.x == 0 && M.iters_out) *M.iters_out = T;
+    }
+    uint64_t beg, end;
+    dense_range(M, beg, end);
+    for (uint64_t i = beg + threadIdx.x; i < end; i += D_THREADS) {
+        const uint32_t key = M.keys[i];
+        float wv;
+        float a[K];
+        if (key_finite(key)) {
+            const float v = key_value(key);
+            attn_row<K>(v, c0, b.s2, a);
+            wv = 0.f;
+#pragma unroll
+            for (int j = 0; j < K; ++j) wv = fmaf(a[j], c1[j], wv);
+        } else {
+            wv = __builtin_nanf("");
+#pragma unroll
+            for (int j = 0; j < K; ++j) a[j] = __builtin_nanf("");
+        }
+        if (b.out_fp16) reinterpret_cast<__half*>(M.wt)[i] = __float2half_rn(wv);
+        else reinterpret_cast<float*>(M.wt)[i] = wv;
+        if (M.attn) {
+#pragma unroll
+            for (int j = 0; j < K; ++j) M.attn[i * K + j] = a[j];
+        }
+    }
+}
+
+// Dense backward, direct use of A^(T): dL/dw_i = g_i H_i, and partials of gamma and E.
+template <int K>
+__global__ void __launch_bounds__(D_THREADS) k_dense_btop(BatchArgs b) {
+    __shared__ float tot[2 * K];
+    __shared__ float scratch[D_THREADS / 64 * 2 * K];
+    const MatArgs& M = b.m[0];
+    const int T = M.ws.st->teff;
+    float c1[K], c0[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) { c1[j] = M.ws.chist[T * KMAX + j]; c0[j] = M.ws.chist[(T - 1) * KMAX + j]; }
+    float acc[2 * K];
+#pragma unroll
+    for (int j = 0; j < 2 * K; ++j) acc[j] = 0.f;
+    uint64_t beg, end;
+    dense_range(M, beg, end);
+    for (uint64_t i = beg + threadIdx.x; i < end; i += D_THREADS) {
+        const uint32_t key = M.keys[i];
+        if (!key_finite(key)) { M.gw[i] = __builtin_nanf(""); continue; }
+        const float v = key_value(key);
+        const float g = M.g[i];
+        float a[K];
+        attn_row<K>(v, c0, b.s2, a);
+        float tv = 0.f;
+#pragma unroll
+        for (int j = 0; j < K; ++j) tv = fmaf(a[j], c1[j], tv);
+        float h = 0.f;
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const float q = a[j] * (c1[j] - tv) * sgnf(v - c0[j]);
+            h += q;
+            acc[j] = fmaf(g, a[j], acc[j]);
+            acc[K + j] = fmaf(g, q, acc[K + j]);
+        }
+        M.gw[i] = -g * h * b.inv_tau;
+    }
+    block_sum<2 * K, D_THREADS>(acc, scratch, tot);
+    if (threadIdx.x < 2 * K) M.ws.dpart[(size_t)blockIdx.x * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
+}
+
+// Dense backward iteration t (reads gamma^(t) from ghist).
+template <int K>
+__global__ void __launch_bounds__(D_THREADS) k_dense_biter(BatchArgs b) {
+    __shared__ float tot[K];
+    __shared__ float scratch[D_THREADS / 64 * K];
+    const MatArgs& M = b.m[0];
+    const int T = M.ws.st->teff;
+    const int t = b.t;
+    if (t > T) return;
+    float c1[K], c0[K], gS[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        c1[j] = M.ws.chist[t * KMAX + j];
+        c0[j] = M.ws.chist[(t - 1) * KMAX + j];
+        const float S = M.ws.shist[t * KMAX + j];
+        gS[j] = S > 0.f ? M.ws.ghist[t * KMAX + j] / S : 0.f;
+    }
+    float acc[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) acc[j] = 0.f;
+    uint64_t beg, end;
+    dense_range(M, beg, end);
+    for (uint64_t i = beg + threadIdx.x; i < end; i += D_THREADS) {
+        const uint32_t key = M.keys[i];
+        if (!key_finite(key)) continue;
+        const float v = key_value(key);
+        float a[K], dev[K];
+        const int m = attn_row<K>(v, c0, b.s2, a);
+        const float direct = softmax_dev<K>(v, a, gS, c1, m, dev);
+        float r = 0.f;
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const float dl = a[j] * dev[j] * sgnf(v - c0[j]);
+            r += dl;
+            acc[j] += dl;
+        }
+        M.gw[i] += fmaf(-r, b.inv_tau, direct);
+    }
+    block_sum<K, D_THREADS>(acc, scratch, tot);
+    if (threadIdx.x < K) M.ws.dpart[(size_t)blockIdx.x * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
+}
+
+// One block.  b.t = 0 (after btop): gamma^(T) = dL/dC^(T) and E.  b.t = t in
+// T..1 (after biter t): gamma^(t-1) = dL/dC^(t-1); at t = 1 also dL/dC^(0).
+template <int K>
+__global__ void __launch_bounds__(1024) k_dense_bfin(BatchArgs b, int nrow) {
+    __shared__ float scratch[16 * PSTRIDE];
+    __shared__ float tot[2 * K];
+    const MatArgs& M = b.m[0];
+    const int T = M.ws.st->teff;
+    const int t = b.t;
+    if (t == 0) {
+        reduce_dparts(M.ws.dpart, nrow, 0, 2 * K, scratch, tot);
+        if (threadIdx.x < K) {
+            M.ws.ghist[T * KMAX + threadIdx.x] = tot[threadIdx.x];
+            M.ws.ehist[threadIdx.x] = tot[K + threadIdx.x] * b.inv_tau;
+        }
+        return;
+    }
+    if (t > T) return;
+    reduce_dparts(M.ws.dpart, nrow, 0, K, scratch, tot);
+    if (threadIdx.x < K) {
+        const int j = threadIdx.x;
+        float gm = tot[j] * b.inv_tau;
+        if (t == T) gm += M.ws.ehist[j];
+        if (!(M.ws.shist[t * KMAX + j] > 0.f)) gm += M.ws.ghist[t * KMAX + j];
+        M.ws.ghist[(t - 1) * KMAX + j] = gm;
+        if (t == 1) M.gc[j] = gm;
+    }
+}
+
+// ----------------------------------------------------------------------------
+// launch sequences
+
+// Each launch is followed by a check; the name of a failing launch goes to *where.
+// An N-sized pass, with the caller's timing events recorded around it if set.
+#define EDKM_NPASS(pass, name, kern, grid, block, ...)                                   \
+    do {                                                                                 \
+        if (ev && ev->start[pass]) { hipError_t e0_ = hipEventRecord(ev->start[pass], s); \
+            if (e0_ != hipSuccess) { *where = "hipEventRecord"; return e0_; } }            \
+        EDKM_LAUNCH(name, kern, grid, block, __VA_ARGS__);                               \
+        if (ev && ev->stop[pass]) { hipError_t e1_ = hipEventRecord(ev->stop[pass], s);   \
+            if (e1_ != hipSuccess) { *where = "hipEventRecord"; return e1_; } }            \
+    } while (0)
+
+#define EDKM_LAUNCH(name, kern, grid, block, ...)                       \
+    do {                                                                  \
+        hipLaunchKernelGGL(kern, grid, block, 0, s, __VA_ARGS__);         \
+        hipError_t e_ = hipGetLastError();                                \
+        if (e_ != hipSuccess) { *where = name; return e_; }              \
+    } while (0)
+
+template <int K>
+static hipError_t forward_k(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_t s, const char** where,
+                            const PassEvents* ev) {
+    const dim3 tg(T_WG, b.count);
+    for (int t = 1; t <= max_t; ++t) {
+        b.t = t;
+        EDKM_LAUNCH("k_fwd_iter", k_fwd_iter<K>, tg, dim3(T_THREADS), b);
+    }
+    EDKM_LAUNCH("k_fwd_out", k_fwd_out<K>, tg, dim3(T_THREADS), b);
+    EDKM_NPASS(PASS_GATHER_WT, "k_gather_wt", k_gather_wt, dim3(grid_np), dim3(NP_THREADS), b);
+    return hipSuccess;
+}
+
+template <int K>
+static hipError_t backward_k(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_t s, const char** where,
+                             const PassEvents* ev) {
+    const dim3 tg(T_WG, b.count);
+    EDKM_NPASS(PASS_KEYED_GRAD, "k_keyed_grad", k_keyed_grad, dim3(grid_np), dim3(NP_THREADS), b);
+    EDKM_LAUNCH("k_bwd_top", k_bwd_top<K>, tg, dim3(T_THREADS), b);
+    for (int t = max_t; t >= 1; --t) {
+        b.t = t;
+        EDKM_LAUNCH("k_bwd_iter", k_bwd_iter<K>, tg, dim3(T_THREADS), b);
+    }
+    EDKM_NPASS(PASS_GATHER_GRAD, "k_gather_grad", k_gather_grad, dim3(grid_np), dim3(NP_THREADS), b);
+    return hipSuccess;
+}
+
+template <int K>
+static hipError_t forward_dense_k(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where) {
+    const int max_t = b.m[0].max_iter;
+    for (int t = 1; t <= max_t; ++t) {
+        b.t = t;
+        EDKM_LAUNCH("k_dense_iter", k_dense_iter<K>, dim3(nwg), dim3(D_THREADS), b);
+        EDKM_LAUNCH("k_dense_fin", k_dense_fin<K>, dim3(1), dim3(1024), b, (int)nwg);
+    }
+    EDKM_LAUNCH("k_dense_out", k_dense_out<K>, dim3(nwg), dim3(D_THREADS), b);
+    return hipSuccess;
+}
+
+template <int K>
+static hipError_t backward_dense_k(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where) {
+    const int max_t = b.m[0].max_iter;
+    EDKM_LAUNCH("k_dense_btop", k_dense_btop<K>, dim3(nwg), dim3(D_THREADS), b);
+    b.t = 0;
+    EDKM_LAUNCH("k_dense_bfin", k_dense_bfin<K>, dim3(1), dim3(1024), b, (int)nwg);
+    for (int t = max_t; t >= 1; --t) {
+        b.t = t;
+        EDKM_LAUNCH("k_dense_biter", k_dense_biter<K>, dim3(nwg), dim3(D_THREADS), b);
+        EDKM_LAUNCH("k_dense_bfin", k_dense_bfin<K>, dim3(1), dim3(1024), b, (int)nwg);
+    }
+    return hipSuccess;
+}
+
+#define EDKM_DISPATCH_K(k, fn, ...)            \
+    switch (k) {                               \
+    case 2: return fn<2>(__VA_ARGS__);         \
+    case 4: return fn<4>(__VA_ARGS__);         \
+    case 8: return fn<8>(__VA_ARGS__);         \
+    case 16: return fn<16>(__VA_ARGS__);       \
+    default: return hipErrorInvalidValue;      \
+    }
+
+hipError_t launch_init_unique(BatchArgs& b, uint32_t grid_np, hipStream_t s, const char** where,
+                              const PassEvents* ev) {
+    (void)hipGetLastError();   // an earlier, unrelated failure is not ours to report
+    EDKM_LAUNCH("k_init_zero", k_init_zero, dim3(T_WG, b.count), dim3(T_THREADS), b);
+    EDKM_NPASS(PASS_HIST, "k_hist", k_hist, dim3(grid_np), dim3(NP_THREADS), b);
+    EDKM_LAUNCH("k_hist_merge", k_hist_merge, dim3(W4 / NP_THREADS, b.count), dim3(NP_THREADS), b);
+    EDKM_LAUNCH("k_window", k_window, dim3(1, b.count), dim3(NP_THREADS), b);
+    return hipSuccess;
+}
+
+hipError_t launch_forward(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_t s, const char** where,
+                          const PassEvents* ev) {
+    (void)hipGetLastError();
+    EDKM_DISPATCH_K(b.m[0].k, forward_k, b, grid_np, max_t, s, where, ev);
+}
+
+hipError_t launch_backward(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_t s, const char** where,
+                           const PassEvents* ev) {
+    (void)hipGetLastError();
+    EDKM_DISPATCH_K(b.m[0].k, backward_k, b, grid_np, max_t, s, where, ev);
+}
+
+hipError_t launch_forward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where) {
+    (void)hipGetLastError();
+    EDKM_DISPATCH_K(b.m[0].k, forward_dense_k, b, nwg, s, where);
+}
+
+hipError_t launch_backward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where) {
+    (void)hipGetLastError();
+    EDKM_DISPATCH_K(b.m[0].k, backward_dense_k, b, nwg, s, where);
+}
+
+static_assert(W4 % NP_THREADS == 0, "merge grid covers the window exactly");
+static_assert(NP_THREADS * 32 == 32768, "window scan: 32 magnitudes per thread");
+static_assert(T_WG == 64, "table partial reduction uses one lane per workgroup");
+static_assert(T_WG * T_THREADS * 4 == NKEYS, "table blocks cover every pattern");
+
+}  // namespace edkm

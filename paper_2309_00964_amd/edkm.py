@@ -1,0 +1,255 @@
+"""Python binding of the C-ABI library ``libedkm.so`` (see ``include/edkm.h``).
+
+Argument marshalling only: tensors become device pointers and the current HIP
+stream; every step of the computation runs in the library's HIP kernels.  The
+functions keep the C names without the ``edkm_`` prefix.  Importing this module
+loads the library and raises ``ImportError`` if it has not been built (run
+``__graft_entry__.build()``); there is no fallback.
+
+Weights are passed as fp16 bit patterns: any contiguous 2-byte device tensor
+(``torch.float16`` weights themselves, or ``int16`` / ``uint16`` views).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libedkm.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError("libedkm.so is not built at %s; run __graft_entry__.build()" % LIB_PATH)
+
+# torch brings its own HIP runtime (SONAME libamdhip64.so.7, loaded under the
+# name libamdhip64.so).  It must be in the process before libedkm.so is loaded,
+# so that libedkm.so binds to that same runtime instead of mapping a second one
+# from /opt/rocm, which would not see the device.
+import torch  # noqa: E402,F401
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+
+def _hip_runtimes():
+    try:
+        with open("/proc/self/maps") as f:
+            return sorted({line.split()[-1] for line in f if "libamdhip64" in line})
+    except OSError:
+        return []
+
+
+if len(_hip_runtimes()) > 1:
+    raise ImportError("two HIP runtimes are mapped in this process (%s); import torch before "
+                      "loading libedkm.so" % ", ".join(_hip_runtimes()))
+
+OK = 0
+ERR_ARG = -1
+ERR_NONFINITE = -2
+ERR_WORKSPACE = -3
+ERR_STATE = -4
+ERR_HIP = -5
+NKEYS = 65536
+PASS_HIST, PASS_GATHER_WT, PASS_KEYED_GRAD, PASS_GATHER_GRAD = 0, 1, 2, 3
+
+
+class EdkmError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str = ""):
+        self.status = status
+        super().__init__("%s: %s (%d)%s" % (where, status_str(status), status,
+                                            (" — " + detail) if detail else ""))
+
+
+class edkm_plan(ctypes.Structure):
+    _fields_ = [("opaque", ctypes.c_uint64 * 24)]
+
+
+_P = ctypes.c_void_p
+_PP = ctypes.POINTER(ctypes.c_void_p)
+_i32, _u64, _f32, _sz = ctypes.c_int, ctypes.c_uint64, ctypes.c_float, ctypes.c_size_t
+_PLAN = ctypes.POINTER(edkm_plan)
+
+_SIGS = {
+    "edkm_workspace_bytes": (_sz, [_u64, _i32, _i32]),
+    "edkm_plan_init": (_i32, [_PLAN, _u64, _i32, _i32, _P, _sz]),
+    "edkm_init_unique": (_i32, [_PLAN, _P, _P, _P, _i32, _P]),
+    "edkm_forward": (_i32, [_PLAN, _P, _f32, _f32, _P, _P, _P, _i32, _P, _P]),
+    "edkm_backward": (_i32, [_PLAN, _P, _P, _P, _P, _P]),
+    "edkm_init_unique_batch": (_i32, [_i32, _PP, _PP, _PP, _PP, _i32, _P]),
+    "edkm_forward_batch": (_i32, [_i32, _PP, _PP, _f32, _f32, _PP, _PP, _PP, _i32, _PP, _P]),
+    "edkm_backward_batch": (_i32, [_i32, _PP, _PP, _PP, _PP, _PP, _P]),
+    "edkm_forward_dense": (_i32, [_PLAN, _P, _f32, _f32, _P, _P, _P, _i32, _P, _P, _P]),
+    "edkm_backward_dense": (_i32, [_PLAN, _P, _P, _P, _P, _P]),
+    "edkm_plan_set_pass_events": (_i32, [_PLAN, _i32, _P, _P]),
+    "edkm_plan_hip_error": (_i32, [_PLAN, ctypes.POINTER(_i32), ctypes.POINTER(ctypes.c_char_p),
+                                   ctypes.POINTER(ctypes.c_char_p)]),
+    "edkm_status_str": (ctypes.c_char_p, [_i32]),
+}
+for _name, (_res, _args) in _SIGS.items():
+    _fn = getattr(_lib, _name)
+    _fn.restype = _res
+    _fn.argtypes = _args
+
+EXPORTS = tuple(_SIGS)
+
+
+def status_str(status: int) -> str:
+    return _lib.edkm_status_str(int(status)).decode()
+
+
+def plan_hip_error(plan) -> tuple:
+    """(HIP error code, failing step, HIP description) of the last EDKM_ERR_HIP on a plan."""
+    code = _i32(0)
+    step = ctypes.c_char_p()
+    msg = ctypes.c_char_p()
+    _lib.edkm_plan_hip_error(plan.ref, ctypes.byref(code), ctypes.byref(step), ctypes.byref(msg))
+    return code.value, (step.value or b"").decode(), (msg.value or b"").decode()
+
+
+def _check(status: int, where: str, plans=()) -> None:
+    if status != OK:
+        detail = ""
+        if status == ERR_HIP:
+            for p in plans:
+                code, step, msg = plan_hip_error(p)
+                if code:
+                    detail = "%s failed with hipError %d (%s)" % (step, code, msg)
+                    break
+        raise EdkmError(status, where, detail)
+
+
+def _ptr(t, nbytes_elem=None, name="tensor"):
+    """Device pointer of a contiguous tensor (None -> NULL)."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if nbytes_elem is not None and t.element_size() != nbytes_elem:
+        raise ValueError("%s must have %d-byte elements" % (name, nbytes_elem))
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def workspace_bytes(n: int, bits: int, max_iter: int) -> int:
+    return int(_lib.edkm_workspace_bytes(int(n), int(bits), int(max_iter)))
+
+
+class Plan:
+    """An ``edkm_plan`` plus its device workspace (allocated through torch)."""
+
+    def __init__(self, n: int, bits: int, max_iter: int, device="cuda", workspace=None):
+        import torch
+        self.n, self.bits, self.k, self.max_iter = int(n), int(bits), 1 << int(bits), int(max_iter)
+        nbytes = workspace_bytes(n, bits, max_iter)
+        if nbytes == 0:
+            raise EdkmError(ERR_ARG, "workspace_bytes")
+        if workspace is None:
+            workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        self.workspace = workspace
+        self.plan = edkm_plan()
+        _check(_lib.edkm_plan_init(ctypes.byref(self.plan), self.n, self.bits, self.max_iter,
+                                   _ptr(workspace), workspace.numel() * workspace.element_size()),
+               "plan_init")
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.plan)
+
+
+def plan_set_pass_events(plan: Plan, pass_id: int, start, stop) -> None:
+    """Record raw hipEvent_t handles (ints, or None to clear) around an N-sized pass."""
+    _check(_lib.edkm_plan_set_pass_events(plan.ref, int(pass_id), start, stop), "plan_set_pass_events")
+
+
+def plan_init(n: int, bits: int, max_iter: int, device="cuda") -> Plan:
+    return Plan(n, bits, max_iter, device)
+
+
+def init_unique(plan: Plan, w_bits, counts_out=None, num_unique_out=None, check_finite=False,
+                stream=None) -> None:
+    _check(_lib.edkm_init_unique(plan.ref, _ptr(w_bits, 2, "w_bits"), _ptr(counts_out, 4),
+                                 _ptr(num_unique_out, 4), int(bool(check_finite)), _stream(stream)),
+           "init_unique", (plan,))
+
+
+def forward(plan: Plan, w_bits, tau: float, eps: float, c_in, c_out, w_tilde, out_fp16=False,
+            iters_out=None, stream=None) -> None:
+    _check(_lib.edkm_forward(plan.ref, _ptr(w_bits, 2, "w_bits"), float(tau), float(eps),
+                             _ptr(c_in, 4), _ptr(c_out, 4), _ptr(w_tilde, 2 if out_fp16 else 4),
+                             int(bool(out_fp16)), _ptr(iters_out, 4), _stream(stream)),
+           "forward", (plan,))
+
+
+def backward(plan: Plan, w_bits, grad_w_tilde, grad_w, grad_c, stream=None) -> None:
+    _check(_lib.edkm_backward(plan.ref, _ptr(w_bits, 2, "w_bits"), _ptr(grad_w_tilde, 4),
+                              _ptr(grad_w, 4), _ptr(grad_c, 4), _stream(stream)),
+           "backward", (plan,))
+
+
+def forward_dense(plan: Plan, w_bits, tau: float, eps: float, c_in, c_out, w_tilde,
+                  out_fp16=False, iters_out=None, attn_out=None, stream=None) -> None:
+    _check(_lib.edkm_forward_dense(plan.ref, _ptr(w_bits, 2, "w_bits"), float(tau), float(eps),
+                                   _ptr(c_in, 4), _ptr(c_out, 4),
+                                   _ptr(w_tilde, 2 if out_fp16 else 4), int(bool(out_fp16)),
+                                   _ptr(iters_out, 4), _ptr(attn_out, 4), _stream(stream)),
+           "forward_dense", (plan,))
+
+
+def backward_dense(plan: Plan, w_bits, grad_w_tilde, grad_w, grad_c, stream=None) -> None:
+    _check(_lib.edkm_backward_dense(plan.ref, _ptr(w_bits, 2, "w_bits"), _ptr(grad_w_tilde, 4),
+                                    _ptr(grad_w, 4), _ptr(grad_c, 4), _stream(stream)),
+           "backward_dense", (plan,))
+
+
+def _parr(items, esize=None):
+    arr = (ctypes.c_void_p * len(items))(*[_ptr(t, esize) for t in items])
+    return ctypes.cast(arr, _PP), arr
+
+
+def _plans(plans):
+    arr = (ctypes.c_void_p * len(plans))(*[ctypes.addressof(p.plan) for p in plans])
+    return ctypes.cast(arr, _PP), arr
+
+
+def init_unique_batch(plans, w_bits, counts_out=None, num_unique_out=None, check_finite=False,
+                      stream=None) -> None:
+    n = len(plans)
+    pp, _a = _plans(plans)
+    kk, _b = _parr(w_bits, 2)
+    co, _c = _parr(counts_out, 4) if counts_out is not None else (None, None)
+    nu, _d = _parr(num_unique_out, 4) if num_unique_out is not None else (None, None)
+    _check(_lib.edkm_init_unique_batch(n, pp, kk, co, nu, int(bool(check_finite)), _stream(stream)),
+           "init_unique_batch", plans)
+
+
+def forward_batch(plans, w_bits, tau, eps, c_in, c_out, w_tilde, out_fp16=False, iters_out=None,
+                  stream=None) -> None:
+    n = len(plans)
+    pp, _a = _plans(plans)
+    kk, _b = _parr(w_bits, 2)
+    ci, _c = _parr(c_in, 4)
+    co, _d = _parr(c_out, 4)
+    wt, _e = _parr(w_tilde, 2 if out_fp16 else 4)
+    it, _f = _parr(iters_out, 4) if iters_out is not None else (None, None)
+    _check(_lib.edkm_forward_batch(n, pp, kk, float(tau), float(eps), ci, co, wt,
+                                   int(bool(out_fp16)), it, _stream(stream)),
+           "forward_batch", plans)
+
+
+def backward_batch(plans, w_bits, grad_w_tilde, grad_w, grad_c, stream=None) -> None:
+    n = len(plans)
+    pp, _a = _plans(plans)
+    kk, _b = _parr(w_bits, 2)
+    g, _c = _parr(grad_w_tilde, 4)
+    gw, _d = _parr(grad_w, 4)
+    gc, _e = _parr(grad_c, 4)
+    _check(_lib.edkm_backward_batch(n, pp, kk, g, gw, gc, _stream(stream)), "backward_batch", plans)

@@ -1,0 +1,39 @@
+"""Comparison rules for GPU results against the fp64 oracle.
+
+Floating point: a result x passes against the oracle's ref at tolerance tol when
+  ||x - ref||_2 / ||ref||_2 <= tol   and   max_i |x_i - ref_i| / (|ref_i| + med|ref|) <= tol.
+The floor med|ref| (the median magnitude) keeps entries where ref nearly cancels
+(W~ near 0, g H + R near 0) from dominating, without letting a few huge entries
+(outliers, far clusters) loosen the check on the rest as an rms floor would.  tol is 1e-4 for centroids and W~, 1e-3 for gradients (fp32
+arithmetic against fp64).  fp16 W~ outputs must lie within one fp16 ulp of the
+oracle value rounded to fp16.
+"""
+import numpy as np
+
+TOL_FWD = 1e-4
+TOL_BWD = 1e-3
+
+
+def rel_errors(x, ref):
+    x = np.asarray(x, np.float64).ravel()
+    ref = np.asarray(ref, np.float64).ravel()
+    floor = float(np.median(np.abs(ref))) if ref.size else 0.0
+    den = max(float(np.linalg.norm(ref)), 1e-300)
+    l2 = float(np.linalg.norm(x - ref)) / den
+    worst = float(np.max(np.abs(x - ref) / (np.abs(ref) + floor + 1e-300))) if ref.size else 0.0
+    return l2, worst
+
+
+def assert_close(x, ref, tol, what=""):
+    assert np.all(np.isfinite(np.asarray(x))), "%s has non-finite entries" % what
+    l2, worst = rel_errors(x, ref)
+    assert l2 <= tol and worst <= tol, "%s: rel_l2=%.3e worst=%.3e tol=%.1e" % (what, l2, worst, tol)
+
+
+def assert_fp16_within_ulp(x_bits, ref, what="fp16 W~"):
+    """x_bits: uint16 patterns; ref: fp64 oracle values."""
+    x = np.asarray(x_bits, np.uint16).view(np.float16).astype(np.float64)
+    r16 = np.asarray(ref, np.float64).astype(np.float16)
+    ulp = np.abs(np.spacing(r16).astype(np.float64))
+    bad = np.abs(x - r16.astype(np.float64)) > ulp
+    assert not np.any(bad), "%s: %d entries beyond one ulp" % (what, int(bad.sum()))

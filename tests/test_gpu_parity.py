@@ -1,0 +1,415 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Counts and occupied-pattern numbers are compared bit-exactly; floating point
+uses the rules in parity_util (1e-4 forward, 1e-3 gradients).  Sizes run from
+single weights through several workgroup slices with ragged tails up to the
+full workload shapes (4096x4096, 11008x4096 with outliers at 3 and 4 bits, and
+the seven matrices of a LLaMA-7B decoder layer in one batch, which is the call
+the benchmark times).  The dense oracle checks everything up to a few hundred
+thousand weights; the full shapes use the table-form oracle, itself pinned to
+the dense one in test_oracle_pins.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import dense, table                                  # noqa: E402
+from paper_2309_00964_amd import edkm, inputs                     # noqa: E402
+from paper_2309_00964_amd.runner import run                       # noqa: E402
+from parity_util import (TOL_BWD, TOL_FWD, assert_close,          # noqa: E402
+                         assert_fp16_within_ulp)
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+TAU, ITERS = inputs.TAU, inputs.ITERS
+
+
+def say(*a):
+    print("[gpu-case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def dkeys(keys):
+    return torch.from_numpy(np.ascontiguousarray(keys).view(np.int16)).to(DEV)
+
+
+def gpu(keys, c0, bits, g=None, tau=TAU, iters=ITERS, eps=0.0, **kw):
+    out = run(dkeys(keys), torch.from_numpy(np.asarray(c0, np.float32)), bits, tau, iters, eps,
+              grad=None if g is None else torch.from_numpy(np.asarray(g, np.float32)), **kw)
+    torch.cuda.synchronize()
+    res = {}
+    for k, v in out.items():
+        if isinstance(v, torch.Tensor):
+            res[k] = v.cpu().numpy()
+    return res
+
+
+def oracle(keys, c0, g=None, tau=TAU, iters=ITERS, eps=0.0, form="dense"):
+    mod = dense if form == "dense" else table
+    f = mod.forward(keys, np.asarray(c0, np.float64), tau, iters, eps=eps)
+    if g is not None:
+        r = mod.backward(keys, f, np.asarray(g, np.float64))
+        f["gw"], f["gc"] = r[0], r[1]
+    return f
+
+
+def check(res, ref, g=True, what=""):
+    assert int(res["iters"][0]) == ref["T"], what
+    assert_close(res["c_out"], ref["c_out"], TOL_FWD, what + " c_out")
+    assert_close(res["w_tilde"], ref["w_tilde"], TOL_FWD, what + " w_tilde")
+    if g:
+        assert_close(res["grad_w"], ref["gw"], TOL_BWD, what + " grad_w")
+        assert_close(res["grad_c"], ref["gc"], TOL_BWD, what + " grad_c")
+
+
+def special_keys(n, seed):
+    """Gaussian weights mixed with signed zeros, subnormals, |w| >= 16 and tiny values."""
+    keys = inputs.fp16_weights(n, seed)
+    rng = np.random.default_rng(seed)
+    extra = np.array([0x0000, 0x8000, 0x0001, 0x8001, 0x03FF, 0x83FF, 0x0400, 0x4C00, 0xCC00,
+                      0x7BFF, 0xFBFF, 0x5A00, 0xDA00], dtype=np.uint16)
+    pos = rng.choice(n, size=min(n, 4 * extra.size), replace=False)
+    keys[pos] = np.resize(extra, pos.size)
+    return keys
+
+
+# ------------------------------------------------------------------ histogram
+
+@pytest.mark.parametrize("n,seed,outl,special", [
+    (65536, inputs.weight_seed(1, 0), False, False),
+    (3 * 65536 + 37, 11, True, False),
+    (100003, 12, False, True),
+    (1, 13, False, False),
+    (7, 14, False, True),
+    (9, 15, False, False),
+])
+def test_counts_bit_exact(n, seed, outl, special):
+    keys = special_keys(n, seed) if special else inputs.fp16_weights(n, seed, outliers=outl)
+    c0 = inputs.quantile_init(keys, 8)
+    say("counts", n, seed)
+    res = gpu(keys, c0, 3, want_counts=True)
+    ref = table.histogram(keys)
+    assert np.array_equal(res["counts"].view(np.uint32), ref)
+    assert int(res["num_unique"].view(np.uint32)[0]) == int(np.count_nonzero(ref))
+
+
+def test_counts_single_pattern_overflow_path():
+    """17M copies of one pattern: every workgroup's bin passes 2^16."""
+    n = 17_000_000
+    keys = np.full(n, 0x2000, dtype=np.uint16)
+    c0 = inputs.quantile_init(keys, 8)
+    say("single pattern", n)
+    res = gpu(keys, c0, 3, g=np.ones(n, np.float32), want_counts=True)
+    ref = table.histogram(keys)
+    assert np.array_equal(res["counts"].view(np.uint32), ref)
+    v = float(np.uint16(0x2000).view(np.float16))
+    assert np.allclose(res["c_out"], v, rtol=1e-6)
+    assert np.allclose(res["w_tilde"], v, rtol=1e-6)
+
+
+# ------------------------------------------------------------------ forward / backward
+
+CASES = [
+    # n, bits, outliers, seed
+    (65536, 3, False, inputs.weight_seed(1, 0)),
+    (65536, 1, False, 21),
+    (65536, 2, False, 22),
+    (65536, 4, False, 23),
+    (2 * 65536 + 37, 3, True, 24),
+    (300007, 4, True, 25),
+    (1, 3, False, 26),
+    (7, 2, False, 27),
+    (1000, 3, False, 28),
+]
+
+
+@pytest.mark.parametrize("n,bits,outl,seed", CASES)
+def test_unique_path_matches_oracle(n, bits, outl, seed):
+    keys = inputs.fp16_weights(n, seed, outliers=outl)
+    c0 = inputs.quantile_init(keys, 1 << bits)
+    g = inputs.upstream_grad(n, seed + 500)
+    say("unique", n, bits, outl, seed)
+    res = gpu(keys, c0, bits, g=g)
+    check(res, oracle(keys, c0, g), what="unique n=%d bits=%d" % (n, bits))
+
+
+@pytest.mark.parametrize("n,bits,outl,seed", [c for c in CASES if c[0] <= 300007])
+def test_dense_path_matches_oracle(n, bits, outl, seed):
+    keys = inputs.fp16_weights(n, seed, outliers=outl)
+    c0 = inputs.quantile_init(keys, 1 << bits)
+    g = inputs.upstream_grad(n, seed + 500)
+    say("dense", n, bits, outl, seed)
+    res = gpu(keys, c0, bits, g=g, dense=True, want_attn=n <= 70000)
+    ref = oracle(keys, c0, g)
+    check(res, ref, what="dense n=%d bits=%d" % (n, bits))
+    if "attn" in res:
+        fa = dense.forward(keys, c0.astype(np.float64), TAU, ITERS, want_attn=True)["attn"]
+        assert_close(res["attn"], fa, TOL_FWD, "attention map")
+        assert np.allclose(res["attn"].sum(axis=1), 1.0, atol=1e-5)
+
+
+def test_dense_and_unique_agree_on_gpu():
+    keys = inputs.fp16_weights(200_000, 31, outliers=True)
+    c0 = inputs.quantile_init(keys, 8)
+    g = inputs.upstream_grad(keys.size, 32)
+    say("dense vs unique")
+    u = gpu(keys, c0, 3, g=g)
+    d = gpu(keys, c0, 3, g=g, dense=True)
+    assert_close(u["c_out"], d["c_out"], TOL_FWD, "c_out")
+    assert_close(u["w_tilde"], d["w_tilde"], TOL_FWD, "w_tilde")
+    assert_close(u["grad_w"], d["grad_w"], TOL_BWD, "grad_w")
+    assert_close(u["grad_c"], d["grad_c"], TOL_BWD, "grad_c")
+
+
+@pytest.mark.parametrize("dense_path", [False, True])
+def test_fp16_output_within_one_ulp(dense_path):
+    keys = inputs.fp16_weights(65536 + 5, 41)
+    c0 = inputs.quantile_init(keys, 8)
+    say("fp16 out", dense_path)
+    res = gpu(keys, c0, 3, out_fp16=True, dense=dense_path)
+    ref = oracle(keys, c0)
+    assert_fp16_within_ulp(res["w_tilde"].view(np.uint16), ref["w_tilde"])
+
+
+def test_special_values_and_wide_range():
+    """Signed zeros, subnormals, |w| >= 16 up to 65504: exact decode, global
+    fallbacks outside the LDS windows."""
+    keys = special_keys(100003, 51)
+    c0 = inputs.quantile_init(keys, 16)
+    g = inputs.upstream_grad(keys.size, 52)
+    say("special values")
+    res = gpu(keys, c0, 4, g=g)
+    check(res, oracle(keys, c0, g), what="special")
+
+
+def test_wide_magnitude_span_exceeds_windows():
+    """Occupied magnitudes spanning more than the LDS windows: the densest part
+    is windowed, the rest is read through the global table."""
+    rng = np.random.default_rng(61)
+    n = 150_000
+    logs = rng.uniform(-24, 15.9, n)
+    vals = np.sign(rng.standard_normal(n)) * np.exp2(logs)
+    keys = vals.astype(np.float16).view(np.uint16)
+    keys[: n // 2] = inputs.fp16_weights(n // 2, 62)
+    c0 = inputs.quantile_init(keys, 8)
+    g = inputs.upstream_grad(n, 63)
+    say("wide span")
+    res = gpu(keys, c0, 3, g=g, want_counts=True)
+    assert np.array_equal(res["counts"].view(np.uint32), table.histogram(keys))
+    check(res, oracle(keys, c0, g), what="wide span")
+
+
+def test_nonfinite_weights():
+    keys = inputs.fp16_weights(50_000, 71)
+    bad = keys.copy()
+    bad[[5, 777, 40_000]] = [0x7C00, 0xFC00, 0x7E00]
+    c0 = inputs.quantile_init(keys, 8)
+    say("non-finite checked")
+    with pytest.raises(edkm.EdkmError) as e:
+        gpu(bad, c0, 3, check_finite=True)
+    assert e.value.status == edkm.ERR_NONFINITE
+    say("non-finite unchecked")
+    g = inputs.upstream_grad(bad.size, 72)
+    res = gpu(bad, c0, 3, g=g)
+    finite = np.ones(bad.size, bool)
+    finite[[5, 777, 40_000]] = False
+    ref = oracle(bad[finite], c0, g[finite])
+    assert np.all(np.isnan(res["w_tilde"][~finite]))
+    assert np.all(np.isnan(res["grad_w"][~finite]))
+    assert_close(res["c_out"], ref["c_out"], TOL_FWD, "c_out")
+    assert_close(res["w_tilde"][finite], ref["w_tilde"], TOL_FWD, "w_tilde")
+    assert_close(res["grad_w"][finite], ref["gw"], TOL_BWD, "grad_w")
+    assert_close(res["grad_c"], ref["gc"], TOL_BWD, "grad_c")
+
+
+def test_unit_upstream_gradient_identity():
+    """With dL/dW~ = 1 the loss is sum_i w_i whatever the centroids (sum_i W~_i =
+    sum_j S_j C_j = sum_j P_j), so dL/dw_i = 1 and dL/dC^(0) = 0."""
+    keys = inputs.fp16_weights(200_003, 75, outliers=True)
+    c0 = inputs.quantile_init(keys, 8)
+    say("unit gradient")
+    res = gpu(keys, c0, 3, g=np.ones(keys.size, np.float32))
+    assert np.max(np.abs(res["grad_w"] - 1.0)) <= 1e-3
+    rnd = gpu(keys, c0, 3, g=inputs.upstream_grad(keys.size, 76))
+    assert np.max(np.abs(res["grad_c"])) <= 1e-3 * np.max(np.abs(rnd["grad_c"]))
+
+
+def test_early_stop_matches_oracle():
+    keys = inputs.fp16_weights(65536, 81)
+    c0 = inputs.quantile_init(keys, 8)
+    g = inputs.upstream_grad(keys.size, 82)
+    full = dense.forward(keys, c0.astype(np.float64), TAU, 12)
+    steps = np.max(np.abs(np.diff(full["c_hist"], axis=0)), axis=1)
+    s = np.sort(steps)
+    # an eps between two step sizes that differ by >= 10%, far from fp32 rounding
+    i = next(i for i in range(len(s) // 3, len(s) - 1) if s[i + 1] > 1.1 * s[i])
+    eps = float(np.sqrt(s[i] * s[i + 1]))
+    say("early stop", eps)
+    for dense_path in (False, True):
+        res = gpu(keys, c0, 3, g=g, iters=12, eps=eps, dense=dense_path)
+        check(res, oracle(keys, c0, g, iters=12, eps=eps), what="eps dense=%s" % dense_path)
+
+
+def test_empty_cluster_keeps_centroid():
+    keys = inputs.fp16_weights(30_000, 91)
+    c0 = np.append(inputs.quantile_init(keys, 7), np.float32(2.0))   # fp64 underflows too
+    g = inputs.upstream_grad(keys.size, 92)
+    say("empty cluster")
+    for dense_path in (False, True):
+        res = gpu(keys, c0, 3, g=g, dense=dense_path)
+        ref = oracle(keys, c0, g)
+        assert res["c_out"][7] == np.float32(2.0)
+        check(res, ref, what="empty cluster dense=%s" % dense_path)
+
+
+def test_forward_repeatable_and_exact_scaling():
+    """Forward results are bitwise repeatable.  Scaling w, C^(0) and tau by 2 scales
+    C and W~ by 2: bitwise on the dense path (same reduction order), and to
+    rounding on the table path, where doubling moves every pattern to another
+    table row (key + 0x400) and so reorders the fixed-order sums."""
+    keys = inputs.fp16_weights(65536 * 2 + 3, 101)
+    c0 = inputs.quantile_init(keys, 8)
+    k2 = (keys.view(np.float16) * np.float16(2)).view(np.uint16)
+    assert np.array_equal(k2.view(np.float16).astype(np.float64), 2 * keys.view(np.float16).astype(np.float64))
+    say("repeat/scale")
+    for dense_path in (False, True):
+        a = gpu(keys, c0, 3, dense=dense_path)
+        b = gpu(keys, c0, 3, dense=dense_path)
+        assert np.array_equal(a["c_out"], b["c_out"]) and np.array_equal(a["w_tilde"], b["w_tilde"])
+        s = gpu(k2, 2 * c0, 3, tau=2 * TAU, dense=dense_path)
+        if dense_path:
+            assert np.array_equal(s["c_out"], 2 * a["c_out"])
+            assert np.array_equal(s["w_tilde"], 2 * a["w_tilde"])
+        else:
+            assert_close(s["c_out"], 2 * a["c_out"].astype(np.float64), 1e-6, "scaled c_out")
+            assert_close(s["w_tilde"], 2 * a["w_tilde"].astype(np.float64), 1e-6, "scaled w_tilde")
+
+
+def test_misaligned_buffers_take_the_scalar_path():
+    n = 65536 + 11
+    keys = inputs.fp16_weights(n + 1, 111)
+    c0 = inputs.quantile_init(keys[1:], 8)
+    g = inputs.upstream_grad(n + 1, 112)
+    say("misaligned")
+    kd = dkeys(keys)[1:]
+    gd = torch.from_numpy(g).to(DEV)[1:]
+    plan = edkm.Plan(n, 3, ITERS)
+    c_in = torch.from_numpy(c0).to(DEV)
+    c_out = torch.empty(8, device=DEV)
+    wt = torch.empty(n + 1, device=DEV)[1:]
+    gw = torch.empty(n + 1, device=DEV)[1:]
+    gc = torch.empty(8, device=DEV)
+    it = torch.zeros(1, dtype=torch.int32, device=DEV)
+    edkm.init_unique(plan, kd)
+    edkm.forward(plan, kd, TAU, 0.0, c_in, c_out, wt, False, it)
+    edkm.backward(plan, kd, gd, gw, gc)
+    torch.cuda.synchronize()
+    res = dict(iters=it.cpu().numpy(), c_out=c_out.cpu().numpy(), w_tilde=wt.cpu().numpy(),
+               grad_w=gw.cpu().numpy(), grad_c=gc.cpu().numpy())
+    check(res, oracle(keys[1:], c0, g[1:]), what="misaligned")
+
+
+def test_batch_equals_single_calls():
+    sizes = [65536, 100003, 7, 300000]
+    bits = 3
+    ks = [inputs.fp16_weights(n, 120 + i, outliers=(i == 3)) for i, n in enumerate(sizes)]
+    c0s = [inputs.quantile_init(k, 8) for k in ks]
+    gs = [inputs.upstream_grad(n, 130 + i) for i, n in enumerate(sizes)]
+    say("batch")
+    plans = [edkm.Plan(n, bits, ITERS) for n in sizes]
+    kd = [dkeys(k) for k in ks]
+    ci = [torch.from_numpy(c).to(DEV) for c in c0s]
+    co = [torch.empty(8, device=DEV) for _ in sizes]
+    wt = [torch.empty(n, device=DEV) for n in sizes]
+    it = [torch.zeros(1, dtype=torch.int32, device=DEV) for _ in sizes]
+    gd = [torch.from_numpy(g).to(DEV) for g in gs]
+    gw = [torch.empty(n, device=DEV) for n in sizes]
+    gc = [torch.empty(8, device=DEV) for _ in sizes]
+    edkm.init_unique_batch(plans, kd)
+    edkm.forward_batch(plans, kd, TAU, 0.0, ci, co, wt, False, it)
+    edkm.backward_batch(plans, kd, gd, gw, gc)
+    torch.cuda.synchronize()
+    for i, n in enumerate(sizes):
+        single = gpu(ks[i], c0s[i], bits, g=gs[i])
+        assert np.array_equal(co[i].cpu().numpy(), single["c_out"])
+        assert np.array_equal(wt[i].cpu().numpy(), single["w_tilde"])
+        assert_close(gw[i].cpu().numpy(), single["grad_w"], 1e-5, "batch grad_w")
+        res = dict(iters=it[i].cpu().numpy(), c_out=co[i].cpu().numpy(), w_tilde=wt[i].cpu().numpy(),
+                   grad_w=gw[i].cpu().numpy(), grad_c=gc[i].cpu().numpy())
+        check(res, oracle(ks[i], c0s[i], gs[i]), what="batch %d" % i)
+
+
+def test_call_order_and_key_buffer_checks():
+    keys = inputs.fp16_weights(4096, 141)
+    c0 = torch.from_numpy(inputs.quantile_init(keys, 8)).to(DEV)
+    kd = dkeys(keys)
+    other = kd.clone()
+    plan = edkm.Plan(keys.size, 3, ITERS)
+    c_out = torch.empty(8, device=DEV)
+    wt = torch.empty(keys.size, device=DEV)
+    g = torch.ones(keys.size, device=DEV)
+    gw, gc = torch.empty_like(wt), torch.empty(8, device=DEV)
+    with pytest.raises(edkm.EdkmError):
+        edkm.forward(plan, kd, TAU, 0.0, c0, c_out, wt)
+    edkm.init_unique(plan, kd)
+    with pytest.raises(edkm.EdkmError) as e:
+        edkm.forward(plan, other, TAU, 0.0, c0, c_out, wt)
+    assert e.value.status == edkm.ERR_STATE
+    with pytest.raises(edkm.EdkmError):
+        edkm.backward(plan, kd, g, gw, gc)
+    edkm.forward(plan, kd, TAU, 0.0, c0, c_out, wt)
+    edkm.backward(plan, kd, g, gw, gc)
+    first = gw.clone()
+    edkm.backward(plan, kd, g, gw, gc)       # a second backward reuses the forward state
+    torch.cuda.synchronize()
+    assert_close(gw.cpu().numpy(), first.cpu().numpy(), 1e-6, "repeat backward")
+
+
+# ------------------------------------------------------------------ full workload shapes
+
+@pytest.mark.parametrize("cfg,bits", [(2, 3), (3, 3), (3, 4)])
+def test_full_size_matrix(cfg, bits):
+    w = inputs.WORKLOADS[cfg]
+    _, r, c = w["mats"][0]
+    n = r * c
+    keys = inputs.fp16_weights(n, inputs.weight_seed(cfg, 0), outliers=w["outliers"])
+    c0 = inputs.quantile_init(keys, 1 << bits)
+    g = inputs.upstream_grad(n, inputs.grad_seed(cfg, 0))
+    say("full", cfg, bits, n)
+    res = gpu(keys, c0, bits, g=g, want_counts=True)
+    assert np.array_equal(res["counts"].view(np.uint32), table.histogram(keys))
+    check(res, oracle(keys, c0, g, form="table"), what="cfg%d bits=%d" % (cfg, bits))
+
+
+def test_decoder_layer_batch_full_size():
+    """The seven matrices of one LLaMA-7B decoder layer in one batch (the call the
+    benchmark times), each against the table-form oracle."""
+    w = inputs.WORKLOADS[4]
+    say("decoder layer")
+    plans, kd, ci, co, wt, it, gd, gw, gc, host = [], [], [], [], [], [], [], [], [], []
+    for i, (name, r, c) in enumerate(w["mats"]):
+        n = r * c
+        keys = inputs.fp16_weights(n, inputs.weight_seed(4, i))
+        c0 = inputs.quantile_init(keys, 8)
+        g = inputs.upstream_grad(n, inputs.grad_seed(4, i))
+        host.append((keys, c0, g))
+        plans.append(edkm.Plan(n, 3, ITERS))
+        kd.append(dkeys(keys))
+        ci.append(torch.from_numpy(c0).to(DEV))
+        co.append(torch.empty(8, device=DEV))
+        wt.append(torch.empty(n, device=DEV))
+        it.append(torch.zeros(1, dtype=torch.int32, device=DEV))
+        gd.append(torch.from_numpy(g).to(DEV))
+        gw.append(torch.empty(n, device=DEV))
+        gc.append(torch.empty(8, device=DEV))
+    edkm.init_unique_batch(plans, kd)
+    edkm.forward_batch(plans, kd, TAU, 0.0, ci, co, wt, False, it)
+    edkm.backward_batch(plans, kd, gd, gw, gc)
+    torch.cuda.synchronize()
+    for i, (keys, c0, g) in enumerate(host):
+        res = dict(iters=it[i].cpu().numpy(), c_out=co[i].cpu().numpy(), w_tilde=wt[i].cpu().numpy(),
+                   grad_w=gw[i].cpu().numpy(), grad_c=gc[i].cpu().numpy())
+        check(res, oracle(keys, c0, g, form="table"), what=w["mats"][i][0])

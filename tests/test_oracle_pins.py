@@ -252,6 +252,20 @@ def test_backward_matches_central_differences(seed, k, T):
     assert rel(gc, fd_c) <= 1e-6
 
 
+@pytest.mark.parametrize("k,eps", [(8, 0.0), (4, 1e-6), (16, 0.0)])
+def test_unit_upstream_gradient_identity(k, eps):
+    """dL/dW~ = 1: sum_i W~_i = sum_j S^(T)_j C^(T)_j = sum_j P^(T)_j = sum_i w_i for any
+    C^(0), so dL/dw_i = 1 and dL/dC^(0) = 0 exactly."""
+    keys = inputs.fp16_weights(30_000, 40 + k, outliers=True)
+    c0 = inputs.quantile_init(keys, k)
+    f = dense.forward(keys, c0, 2e-3, 5, eps=eps)
+    v = keys.view(np.float16).astype(np.float64)
+    assert abs(f["w_tilde"].sum() - v.sum()) <= 1e-12 * np.abs(v).sum()
+    gw, gc = dense.backward(keys, f, np.ones(keys.size))
+    assert np.max(np.abs(gw - 1.0)) <= 1e-9
+    assert np.max(np.abs(gc)) <= 1e-9 * keys.size
+
+
 def test_backward_is_linear_in_upstream_per_key():
     """dL/dw_i = g_i H(key) + R(key): weights sharing a key differ only through g."""
     keys = np.array([0x2000, 0x2000, 0x2000, 0xA400, 0x1800, 0x2000], dtype=np.uint16)
