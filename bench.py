@@ -206,48 +206,57 @@ def copy_calibration():
     print(json.dumps({"copy_bytes": COPY_BYTES}), flush=True)
 
 
-def _pmc_rows(d):
+def _pmc_rows(d, prefix):
     import csv
-    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    files = glob.glob(os.path.join(d, "**", prefix + "*counter_collection.csv"), recursive=True)
     if not files:
-        sys.exit("no counter_collection.csv under %s" % d)
+        sys.exit("no %s*counter_collection.csv under %s" % (prefix, d))
     rows = []
     for f in files:
-        rows += list(csv.DictReader(open(f)))
+        rows += [dict(r, _file=f) for r in csv.DictReader(open(f))]
     return rows
 
 
 def pmc_summary(fetch_dir, write_dir):
-    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of the pass kernels, scaled by
-    what the same counters read for a plain copy of known size."""
-    def per_kernel(d, counter):
+    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of the pass kernels (run "bench"),
+    scaled by what the same counters read for the 1 GiB copies of the calibration
+    run ("copy")."""
+    def per_dispatch(d, prefix, counter):
         acc = {}
-        for r in _pmc_rows(d):
+        for r in _pmc_rows(d, prefix):
             if r.get("Counter_Name") != counter:
                 continue
-            name = r.get("Kernel_Name", "")
-            key = next((p for p in PASS_IDS if p in name), None)
-            if key is None and ("copy" in name.lower() or "elementwise" in name.lower()):
-                key = "copy"
-            if key is None:
-                continue
-            acc.setdefault(key, {}).setdefault(r.get("Dispatch_Id"), 0.0)
-            acc[key][r.get("Dispatch_Id")] += float(r["Counter_Value"])
-        return {k: sum(v.values()) / len(v) for k, v in acc.items()}
-    fetch = per_kernel(fetch_dir, "FETCH_SIZE")
-    write = per_kernel(write_dir, "WRITE_SIZE")
-    if "copy" not in fetch or "copy" not in write:
-        sys.exit("the copy-calibration kernel is missing from the counter runs")
-    f_scale = COPY_BYTES / (fetch["copy"] * 1024.0)
-    w_scale = COPY_BYTES / (write["copy"] * 1024.0)
+            key = (r["_file"], r.get("Dispatch_Id"), r.get("Kernel_Name", ""))
+            acc[key] = acc.get(key, 0.0) + float(r["Counter_Value"])
+        return acc
+
+    def passes(d, counter):
+        out = {}
+        for (_, _, name), v in per_dispatch(d, "bench", counter).items():
+            p = next((p for p in PASS_IDS if p in name), None)
+            if p:
+                out.setdefault(p, []).append(v)
+        return {p: sum(v) / len(v) for p, v in out.items()}
+
+    def copy(d, counter):
+        vals = [v for (_, _, name), v in per_dispatch(d, "copy", counter).items()
+                if "copyBuffer" in name]
+        big = [v for v in vals if v >= 0.5 * max(vals)]
+        return sum(big) / len(big)
+
+    fetch, write = passes(fetch_dir, "FETCH_SIZE"), passes(write_dir, "WRITE_SIZE")
+    cf, cw = copy(fetch_dir, "FETCH_SIZE"), copy(write_dir, "WRITE_SIZE")
+    f_scale = COPY_BYTES / (cf * 1024.0)
+    w_scale = COPY_BYTES / (cw * 1024.0)
     res = {"source_hash": source_hash(), "copy_bytes": COPY_BYTES,
-           "copy_fetch_kib": fetch["copy"], "copy_write_kib": write["copy"],
+           "copy_fetch_kib": cf, "copy_write_kib": cw,
            "fetch_scale": f_scale, "write_scale": w_scale, "kernels": {}}
     for p in PASS_IDS:
         if p in fetch and p in write:
             fb, wb = fetch[p] * 1024.0 * f_scale, write[p] * 1024.0 * w_scale
             res["kernels"][p] = {"fetch_kib": fetch[p], "write_kib": write[p],
-                                 "bytes_per_launch": fb + wb, "fetch_bytes": fb, "write_bytes": wb}
+                                 "bytes_per_launch": fb + wb, "fetch_bytes": fb, "write_bytes": wb,
+                                 "algorithmic_bytes": None}
     os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
     json.dump(res, open(TRAFFIC_FILE, "w"), indent=1)
     print(json.dumps(res))

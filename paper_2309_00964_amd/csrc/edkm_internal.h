@@ -8,7 +8,7 @@ namespace edkm {
 constexpr int NKEYS = 65536;          // every 16-bit pattern
 constexpr int FIN_MAGS = 0x7C00;      // magnitudes (low 15 bits) of finite fp16 values
 constexpr int W4 = 19456;             // magnitudes per sign in a 4-byte LDS window (152 KiB)
-constexpr int W8 = 10240;             // magnitudes per sign in the 8-byte LDS window (160 KiB)
+constexpr int W8 = 10232;             // magnitudes per sign in the 8-byte LDS window (<160 KiB)
 constexpr int NP_THREADS = 1024;      // N-pass workgroup size
 constexpr int NP_MAX_WG = 256;        // N-pass workgroups per matrix (one per CU)
 constexpr int NP_MIN_CHUNK = 16384;   // smallest slice of a matrix given to one workgroup

@@ -157,23 +157,37 @@ __device__ __forceinline__ int np_matrix(const BatchArgs& b) {
     return m;
 }
 
-// Apply f8(i) to 8-weight groups and f1(i) to single weights covering [beg, end).
-template <class F8, class F1>
-__device__ __forceinline__ void for_slice(uint64_t beg, uint64_t end, bool vec, F8 f8, F1 f1) {
+// Stream the slice [beg, end): ld(i) loads the 8-weight group at i into
+// registers, pr(i, r) consumes it, f1(i) handles single weights (tail, or all
+// of them when the buffers are not 16-byte aligned).  U groups are loaded
+// before any of them is processed, so each thread keeps U groups of loads in
+// flight: the stores and atomics of pr() may alias the inputs as far as the
+// compiler knows, and it would otherwise not issue a load ahead of them.
+template <int U, class Ld, class Pr, class F1>
+__device__ __forceinline__ void for_slice(uint64_t beg, uint64_t end, bool vec, Ld ld, Pr pr, F1 f1) {
     if (vec) {
         const uint64_t vend = beg + ((end - beg) & ~7ull);
         const uint64_t step = 8ull * NP_THREADS;
         uint64_t i = beg + 8ull * threadIdx.x;
-        for (; i + step < vend; i += 2 * step) {   // two groups in flight per thread
-            f8(i);
-            f8(i + step);
+        using R = decltype(ld(i));
+        for (; i + (U - 1) * step < vend; i += U * step) {
+            R r[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) r[u] = ld(i + u * step);
+            __builtin_amdgcn_sched_barrier(0);   // all U loads issue before any use
+#pragma unroll
+            for (int u = 0; u < U; ++u) pr(i + u * step, r[u]);
         }
-        if (i < vend) f8(i);
+        for (; i < vend; i += step) pr(i, ld(i));
         for (uint64_t j = vend + threadIdx.x; j < end; j += NP_THREADS) f1(j);
     } else {
         for (uint64_t j = beg + threadIdx.x; j < end; j += NP_THREADS) f1(j);
     }
 }
+
+// Register images of one 8-weight group.
+struct Keys8 { uint4 q; };
+struct KeysG8 { uint4 q; float4 ga, gb; };
 
 // ----------------------------------------------------------------------------
 // init_unique: zero, histogram, partial merge, window selection
@@ -214,13 +228,13 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
         if (mag < (uint32_t)W4) atomicAdd(&h[(key >> 15) * W4 + mag], 1u);
         else atomicAdd(&gcounts[key], 1u);
     };
-    for_slice(beg, end, M.vec != 0,
-        [&](uint64_t i) {
-            const uint4 q = *reinterpret_cast<const uint4*>(keys + i);
-            add(q.x & 0xFFFFu); add(q.x >> 16);
-            add(q.y & 0xFFFFu); add(q.y >> 16);
-            add(q.z & 0xFFFFu); add(q.z >> 16);
-            add(q.w & 0xFFFFu); add(q.w >> 16);
+    for_slice<4>(beg, end, M.vec != 0,
+        [&](uint64_t i) { return Keys8{*reinterpret_cast<const uint4*>(keys + i)}; },
+        [&](uint64_t, const Keys8& r) {
+            add(r.q.x & 0xFFFFu); add(r.q.x >> 16);
+            add(r.q.y & 0xFFFFu); add(r.q.y >> 16);
+            add(r.q.z & 0xFFFFu); add(r.q.z >> 16);
+            add(r.q.w & 0xFFFFu); add(r.q.w >> 16);
         },
         [&](uint64_t i) { add(keys[i]); });
     __syncthreads();
@@ -527,10 +541,10 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
     const uint16_t* keys = M.keys;
     if (b.out_fp16) {
         __half* out = reinterpret_cast<__half*>(M.wt);
-        for_slice(beg, end, M.vec != 0,
-            [&](uint64_t i) {
-                const uint4 q = *reinterpret_cast<const uint4*>(keys + i);
-                const uint32_t ks[4] = {q.x, q.y, q.z, q.w};
+        for_slice<4>(beg, end, M.vec != 0,
+            [&](uint64_t i) { return Keys8{*reinterpret_cast<const uint4*>(keys + i)}; },
+            [&](uint64_t i, const Keys8& r) {
+                const uint32_t ks[4] = {r.q.x, r.q.y, r.q.z, r.q.w};
                 uint32_t o[4];
 #pragma unroll
                 for (int p = 0; p < 4; ++p) {
@@ -543,9 +557,10 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
             [&](uint64_t i) { out[i] = __float2half_rn(look(keys[i])); });
     } else {
         float* out = reinterpret_cast<float*>(M.wt);
-        for_slice(beg, end, M.vec != 0,
-            [&](uint64_t i) {
-                const uint4 q = *reinterpret_cast<const uint4*>(keys + i);
+        for_slice<4>(beg, end, M.vec != 0,
+            [&](uint64_t i) { return Keys8{*reinterpret_cast<const uint4*>(keys + i)}; },
+            [&](uint64_t i, const Keys8& r) {
+                const uint4 q = r.q;
                 float4 a, c;
                 a.x = look(q.x & 0xFFFFu); a.y = look(q.x >> 16);
                 a.z = look(q.y & 0xFFFFu); a.w = look(q.y >> 16);
@@ -558,32 +573,66 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
     }
 }
 
-// G_u = sum over weights with pattern u of dL/dW~_i.  Window patterns add in
-// LDS (fp32 atomics), the rest into the global G; each workgroup then writes
-// its window as one partial row.
+// G_u = sum over weights with pattern u of dL/dW~_i.
+//
+// LDS fp32 atomics run at a fraction of the integer rate on this GPU, so the
+// window sums are kept in 64-bit fixed point: q = round(g 2^S), added with
+// integer LDS atomics.  Each workgroup chooses S from the largest exponent E of
+// a first sample of its own g: every value with exponent <= E + 6 then stays
+// below 2^(61 - b) in magnitude, where the slice holds at most 2^b weights, so
+// no sum can overflow; values above that (and Inf/NaN) are added in fp32 to the
+// global G, as are patterns outside the window.  The resolution is 2^(b - 55)
+// times the sample maximum.  G enters the backward only through the k-vector
+// sums gamma and E over all patterns, where this is far below fp32 rounding.
+// Each workgroup ends by writing its window as one fp32 partial row.
 __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
-    __shared__ float acc[2 * W4];
+    __shared__ unsigned long long acc[2 * W8];
+    __shared__ int emax_sh;
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
     const uint32_t wl = blockIdx.x - M.wg_begin;
     const uint64_t beg = (uint64_t)wl * M.chunk;
     const uint64_t end = min(M.n, beg + M.chunk);
-    const int lo = M.ws.st->lo4, w = M.ws.st->w4;
-    for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) acc[i] = 0.f;
-    __syncthreads();
-    float* G = M.ws.G;
-    auto add = [&](uint32_t key, float g) {
-        const uint32_t d = (key & 0x7FFFu) - (uint32_t)lo;
-        if (d < (uint32_t)w) atomicAdd(&acc[(key >> 15) * w + d], g);
-        else atomicAdd(&G[key], g);
-    };
+    const int lo = M.ws.st->lo8, w = M.ws.st->w8;
     const uint16_t* keys = M.keys;
     const float* g = M.g;
-    for_slice(beg, end, M.vec != 0,
+    for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) acc[i] = 0ull;
+    if (threadIdx.x == 0) emax_sh = 0;
+    __syncthreads();
+    {   // sample: one finite value per thread from the start of the slice
+        const uint64_t i = beg + threadIdx.x * ((end - beg + NP_THREADS - 1) / NP_THREADS);
+        int e = 0;
+        if (i < end) {
+            e = (int)((__float_as_uint(g[i]) >> 23) & 0xFFu);
+            if (e == 0xFF) e = 0;
+        }
+        atomicMax(&emax_sh, e);
+    }
+    __syncthreads();
+    const int bn = 64 - __clzll((unsigned long long)max<uint64_t>(end - beg, 2) - 1);   // 2^bn >= slice
+    const int emax = emax_sh;
+    const int S = 181 - bn - emax;               // 2^(emax-126) * 2^S = 2^(55-bn)
+    const uint32_t elim = (uint32_t)min(emax + 6, 0xFE);
+    float* G = M.ws.G;
+    auto add = [&](uint32_t key, float gv) {
+        const uint32_t d = (key & 0x7FFFu) - (uint32_t)lo;
+        const uint32_t e = (__float_as_uint(gv) >> 23) & 0xFFu;
+        if (d < (uint32_t)w && e <= elim) {
+            const long long q = __float2ll_rn(ldexpf(gv, S));
+            atomicAdd(&acc[(key >> 15) * w + d], (unsigned long long)q);
+        } else {
+            atomicAdd(&G[key], gv);
+        }
+    };
+    for_slice<4>(beg, end, M.vec != 0,
         [&](uint64_t i) {
-            const uint4 q = *reinterpret_cast<const uint4*>(keys + i);
-            const float4 ga = *reinterpret_cast<const float4*>(g + i);
-            const float4 gb = *reinterpret_cast<const float4*>(g + i + 4);
+            return KeysG8{*reinterpret_cast<const uint4*>(keys + i),
+                          *reinterpret_cast<const float4*>(g + i),
+                          *reinterpret_cast<const float4*>(g + i + 4)};
+        },
+        [&](uint64_t, const KeysG8& r) {
+            const uint4 q = r.q;
+            const float4 ga = r.ga, gb = r.gb;
             add(q.x & 0xFFFFu, ga.x); add(q.x >> 16, ga.y);
             add(q.y & 0xFFFFu, ga.z); add(q.y >> 16, ga.w);
             add(q.z & 0xFFFFu, gb.x); add(q.z >> 16, gb.y);
@@ -592,7 +641,8 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
         [&](uint64_t i) { add(keys[i], g[i]); });
     __syncthreads();
     float* row = reinterpret_cast<float*>(M.ws.part) + (size_t)wl * ROW4;
-    for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) row[i] = acc[i];
+    for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS)
+        row[i] = (float)ldexp((double)(long long)acc[i], -S);
 }
 
 // dL/dw_i = g_i H[bits_i] + R[bits_i]; the window [lo8, lo8 + w8) of (H, R) sits
@@ -641,11 +691,15 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
     const uint16_t* keys = M.keys;
     const float* g = M.g;
     float* out = M.gw;
-    for_slice(beg, end, M.vec != 0,
+    for_slice<4>(beg, end, M.vec != 0,
         [&](uint64_t i) {
-            const uint4 q = *reinterpret_cast<const uint4*>(keys + i);
-            const float4 ga = *reinterpret_cast<const float4*>(g + i);
-            const float4 gb = *reinterpret_cast<const float4*>(g + i + 4);
+            return KeysG8{*reinterpret_cast<const uint4*>(keys + i),
+                          *reinterpret_cast<const float4*>(g + i),
+                          *reinterpret_cast<const float4*>(g + i + 4)};
+        },
+        [&](uint64_t i, const KeysG8& r) {
+            const uint4 q = r.q;
+            const float4 ga = r.ga, gb = r.gb;
             float2 h;
             float4 oa, ob;
             h = look(q.x & 0xFFFFu); oa.x = fmaf(ga.x, h.x, h.y);
@@ -669,7 +723,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
 // backward table phase
 
 // Direct use of A^(T) and C^(T) by W~: G_u from the keyed-reduction partial
-// rows, then partials of gamma_j = sum_u G_u a^(T)_uj (= dL/dC^(T)_j) and
+// rows plus its fp32 remainder in G, then partials of gamma_j = sum_u G_u a^(T)_uj (= dL/dC^(T)_j) and
 // E_j = sum_u G_u a^(T)_uj (C^(T)_j - Tab_u) sgn(v_u - C^(T-1)_j).
 // Grid (T_WG, count).
 template <int K>
@@ -682,7 +736,7 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_top(BatchArgs b) {
     float c1[K], c0[K];
 #pragma unroll
     for (int j = 0; j < K; ++j) { c1[j] = M.ws.chist[T * KMAX + j]; c0[j] = M.ws.chist[(T - 1) * KMAX + j]; }
-    const int lo = st->lo4, w = st->w4;
+    const int lo = st->lo8, w = st->w8;       // the keyed reduction's window
     const int nrow = (int)M.wg_count;
     const float* part = reinterpret_cast<const float*>(M.ws.part);
     float acc[2 * K];
@@ -692,13 +746,10 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_top(BatchArgs b) {
     FOR_TABLE_KEYS(u) {
         if (counts[u] == 0u || !key_finite(u)) continue;
         const uint32_t d = (uint32_t)(u & 0x7FFF) - (uint32_t)lo;
-        float G;
+        float G = M.ws.G[u];                   // values added outside the fixed-point sums
         if (d < (uint32_t)w) {
             const float* p = part + (u >> 15) * w + d;
-            G = 0.f;
             for (int r = 0; r < nrow; ++r) G += p[(size_t)r * ROW4];
-        } else {
-            G = M.ws.G[u];
         }
         const float v = key_value(u);
         float a[K];
@@ -1143,6 +1194,7 @@ hipError_t launch_backward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, cons
 }
 
 static_assert(W4 % NP_THREADS == 0, "merge grid covers the window exactly");
+static_assert(2 * W8 <= ROW4, "keyed-reduction rows fit the partial-row stride");
 static_assert(NP_THREADS * 32 == 32768, "window scan: 32 magnitudes per thread");
 static_assert(T_WG == 64, "table partial reduction uses one lane per workgroup");
 static_assert(T_WG * T_THREADS * 4 == NKEYS, "table blocks cover every pattern");
