@@ -263,12 +263,14 @@ def pmc_summary(fetch_dir, write_dir):
 
 
 def main():
+    from paper_2309_00964_amd.inputs import LLAMA7B_LAYER
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample", nargs="+", default=["q_proj", "gate_proj"])
+    ap.add_argument("--cpu-sample", nargs="+", default=[m[0] for m in LLAMA7B_LAYER],
+                    help="matrices of the layer the CPU oracle is timed on (default: all seven)")
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     args = ap.parse_args()

@@ -6,8 +6,9 @@
 //   * N-sized passes, bound by HBM bandwidth: the pattern histogram, the W~
 //     gather, the keyed reduction of dL/dW~ and the dL/dw gather.  They run one
 //     1024-thread workgroup per CU, keep a window of the table in LDS (up to
-//     160 KiB), stream the weights with 16-byte loads and merge per-workgroup
-//     results through dense partial rows instead of global atomics;
+//     160 KiB), sweep each matrix in round-robin tiles with vector loads and
+//     merge per-workgroup results through dense partial rows instead of global
+//     atomics;
 //   * table-sized phases, bound by latency: the T softmax / centroid-update
 //     iterations and the unrolled analytic backward, one launch per iteration,
 //     64 workgroups per matrix, fixed-order tree reductions so the forward is
@@ -40,27 +41,26 @@ __device__ __forceinline__ bool key_finite(uint32_t h) { return (h & 0x7C00u) !=
 __device__ __forceinline__ float sgnf(float x) { return (float)((x > 0.f) - (x < 0.f)); }
 
 // One attention row: a_j = softmax_j(-|v - c_j| / tau), with s2 = log2(e) / tau.
-// Returns m, the nearest centroid.  The exponent -(|v - c_j| - |v - c_m|) / tau
+// m is the nearest centroid; attn_row_sel also returns e[m] for a companion
+// array e.  The exponent -(|v - c_j| - |v - c_m|) / tau
 // is formed without subtracting two distances of size |v|: when v lies on the
 // same side of c_j and c_m the difference is exactly |c_j - c_m|, otherwise v
 // lies between them and both distances are at most |c_j - c_m|.  (Subtracting
 // fp32 distances directly loses every digit once |v| is large against the
 // centroid spacing, e.g. an outlier far from the bulk.)
 template <int K>
-__device__ __forceinline__ int attn_row(float v, const float (&c)[K], float s2, float (&a)[K]) {
+__device__ __forceinline__ void attn_row_sel(float v, const float (&c)[K], float s2, float (&a)[K],
+                                             const float (&e)[K], float& em) {
     float t[K];
-    t[0] = v - c[0];
-    float xm = fabsf(t[0]);
-    int m = 0;
+#pragma unroll
+    for (int j = 0; j < K; ++j) t[j] = v - c[j];
+    // nearest centroid (first on ties), tracked by value: no run-time index
+    float xm = fabsf(t[0]), cm = c[0], tm = t[0];
+    em = e[0];
 #pragma unroll
     for (int j = 1; j < K; ++j) {
-        t[j] = v - c[j];
-        if (fabsf(t[j]) < xm) { xm = fabsf(t[j]); m = j; }
+        if (fabsf(t[j]) < xm) { xm = fabsf(t[j]); cm = c[j]; tm = t[j]; em = e[j]; }
     }
-    float cm = c[0], tm = t[0];
-#pragma unroll
-    for (int j = 1; j < K; ++j)
-        if (j == m) { cm = c[j]; tm = t[j]; }
     const uint32_t sm = __float_as_uint(tm) >> 31;
     float sum = 0.f;
 #pragma unroll
@@ -73,29 +73,23 @@ __device__ __forceinline__ int attn_row(float v, const float (&c)[K], float s2, 
     const float r = 1.0f / sum;
 #pragma unroll
     for (int j = 0; j < K; ++j) a[j] *= r;
-    return m;
 }
 
-// Select c[m] for a run-time index m without indexing a register array.
 template <int K>
-__device__ __forceinline__ float pick(const float (&c)[K], int m) {
-    float r = c[0];
-#pragma unroll
-    for (int j = 1; j < K; ++j)
-        if (j == m) r = c[j];
-    return r;
+__device__ __forceinline__ void attn_row(float v, const float (&c)[K], float s2, float (&a)[K]) {
+    float unused;
+    attn_row_sel<K>(v, c, s2, a, c, unused);
 }
 
 // Softmax-Jacobian deviations of one table row in the backward:
 //   dev_j = alpha_j - sum_i a_i alpha_i,  alpha_j = gS_j (v - c1_j),
-// written around the reference c1_m as
-//   dev_j = (gS_j - gbar)(v - c1_m) - (gS_j (c1_j - c1_m) - hb),
-//   gbar = sum_i a_i gS_i,  hb = sum_i a_i gS_i (c1_i - c1_m),
+// written around the reference cm = c1_m (m the nearest centroid) as
+//   dev_j = (gS_j - gbar)(v - cm) - (gS_j (c1_j - cm) - hb),
+//   gbar = sum_i a_i gS_i,  hb = sum_i a_i gS_i (c1_i - cm),
 // which never subtracts two terms of size |v|.  Returns gbar.
 template <int K>
 __device__ __forceinline__ float softmax_dev(float v, const float (&a)[K], const float (&gS)[K],
-                                             const float (&c1)[K], int m, float (&dev)[K]) {
-    const float cm = pick<K>(c1, m);
+                                             const float (&c1)[K], float cm, float (&dev)[K]) {
     float gbar = 0.f, hb = 0.f;
 #pragma unroll
     for (int j = 0; j < K; ++j) {
@@ -150,6 +144,18 @@ __device__ __forceinline__ void reduce_tparts(const float* part, int c0, int nco
     __syncthreads();
 }
 
+// As reduce_tparts for columns [0, ncol) of two partial blocks at once:
+// out[0..ncol) from pa, out[ncol..2 ncol) from pb.
+__device__ __forceinline__ void reduce_tparts2(const float* pa, const float* pb, int ncol, float* out) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (int j = wave; j < 2 * ncol; j += T_THREADS / 64) {
+        const float x = j < ncol ? pa[lane * PSTRIDE + j] : pb[lane * PSTRIDE + ncol + (j - ncol)];
+        const float s = wave_sum(x);
+        if (lane == 0) out[j] = s;
+    }
+    __syncthreads();
+}
+
 // Matrix of an N-pass workgroup, and its slice [beg, end).
 __device__ __forceinline__ int np_matrix(const BatchArgs& b) {
     int m = 0;
@@ -157,37 +163,85 @@ __device__ __forceinline__ int np_matrix(const BatchArgs& b) {
     return m;
 }
 
-// Stream the slice [beg, end): ld(i) loads the 8-weight group at i into
-// registers, pr(i, r) consumes it, f1(i) handles single weights (tail, or all
-// of them when the buffers are not 16-byte aligned).  U groups are loaded
-// before any of them is processed, so each thread keeps U groups of loads in
-// flight: the stores and atomics of pr() may alias the inputs as far as the
-// compiler knows, and it would otherwise not issue a load ahead of them.
-template <int U, class Ld, class Pr, class F1>
-__device__ __forceinline__ void for_slice(uint64_t beg, uint64_t end, bool vec, Ld ld, Pr pr, F1 f1) {
-    if (vec) {
-        const uint64_t vend = beg + ((end - beg) & ~7ull);
-        const uint64_t step = 8ull * NP_THREADS;
-        uint64_t i = beg + 8ull * threadIdx.x;
-        using R = decltype(ld(i));
-        for (; i + (U - 1) * step < vend; i += U * step) {
+// Stream a workgroup's share of a matrix.  The matrix is cut into tiles of
+// U x GW x NP_THREADS weights that its workgroups take round-robin, so they
+// sweep HBM together (measured: 10-20% faster than giving each workgroup one
+// contiguous slice).  In a tile a thread loads U groups of GW weights
+// (ld), then computes all U results (cp: table lookups, atomics), then stores
+// them (st); f1 handles single weights: the ragged tail, or everything when the
+// buffers are not 16-byte aligned.
+template <int U, int GW>
+__device__ __forceinline__ uint64_t tiles_bound(const MatArgs& M) {   // weights one workgroup handles, at most
+    constexpr uint64_t TILE = (uint64_t)U * GW * NP_THREADS;
+    const uint64_t ntiles = (M.n + TILE - 1) / TILE;
+    return ((ntiles + M.wg_count - 1) / M.wg_count) * TILE + NP_THREADS;
+}
+
+template <int U, int GW, class Ld, class Cp, class St, class F1>
+__device__ __forceinline__ void for_slice(const MatArgs& M, uint32_t wl, Ld ld, Cp cp, St st, F1 f1) {
+    const uint64_t n = M.n;
+    if (!M.vec) {
+        for (uint64_t j = (uint64_t)wl * NP_THREADS + threadIdx.x; j < n; j += (uint64_t)M.wg_count * NP_THREADS)
+            f1(j);
+        return;
+    }
+    constexpr uint64_t STEP = (uint64_t)GW * NP_THREADS;
+    constexpr uint64_t TILE = U * STEP;
+    const uint64_t nvec = n & ~(uint64_t)(GW - 1);
+    const uint64_t stride = (uint64_t)M.wg_count * TILE;
+    for (uint64_t base = (uint64_t)wl * TILE; base < nvec; base += stride) {
+        const uint64_t i0 = base + (uint64_t)GW * threadIdx.x;
+        if (base + TILE <= nvec) {
+            using R = decltype(ld(i0));
+            using O = decltype(cp(ld(i0)));
             R r[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) r[u] = ld(i + u * step);
+            for (int u = 0; u < U; ++u) r[u] = ld(i0 + u * STEP);
             __builtin_amdgcn_sched_barrier(0);   // all U loads issue before any use
+            O o[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) pr(i + u * step, r[u]);
+            for (int u = 0; u < U; ++u) o[u] = cp(r[u]);
+#pragma unroll
+            for (int u = 0; u < U; ++u) st(i0 + u * STEP, o[u]);
+        } else {
+            for (uint64_t i = i0; i < nvec && i < base + TILE; i += STEP) st(i, cp(ld(i)));
         }
-        for (; i < vend; i += step) pr(i, ld(i));
-        for (uint64_t j = vend + threadIdx.x; j < end; j += NP_THREADS) f1(j);
-    } else {
-        for (uint64_t j = beg + threadIdx.x; j < end; j += NP_THREADS) f1(j);
     }
+    if (wl == M.wg_count - 1)
+        for (uint64_t j = nvec + threadIdx.x; j < n; j += NP_THREADS) f1(j);
 }
+
+struct Nothing {};
 
 // Register images of one 8-weight group.
 struct Keys8 { uint4 q; };
-struct KeysG8 { uint4 q; float4 ga, gb; };
+// ... and of one 4-weight group.
+struct Keys4 { uint2 q; };
+struct KeysG4 { uint2 q; float4 g; };
+
+typedef unsigned int v4u_t __attribute__((ext_vector_type(4)));
+typedef unsigned int v2u_t __attribute__((ext_vector_type(2)));
+typedef float v4f_t __attribute__((ext_vector_type(4)));
+// Streaming loads.  Non-temporal loads (nt) help the passes that only read the
+// weights (histogram, keyed sum) and hurt the gathers, which use plain loads;
+// stores are always plain (nt stores halve the gathers' bandwidth here).
+__device__ __forceinline__ uint4 ld_u4(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+__device__ __forceinline__ uint2 ld_u2(const void* p) { return *reinterpret_cast<const uint2*>(p); }
+__device__ __forceinline__ float4 ld_f4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ uint4 ld_u4_nt(const void* p) {
+    const v4u_t v = __builtin_nontemporal_load(reinterpret_cast<const v4u_t*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ uint2 ld_u2_nt(const void* p) {
+    const v2u_t v = __builtin_nontemporal_load(reinterpret_cast<const v2u_t*>(p));
+    return make_uint2(v.x, v.y);
+}
+__device__ __forceinline__ float4 ld_f4_nt(const float* p) {
+    const v4f_t v = __builtin_nontemporal_load(reinterpret_cast<const v4f_t*>(p));
+    return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void st_f4(float* p, float4 x) { *reinterpret_cast<float4*>(p) = x; }
+__device__ __forceinline__ void st_u2(void* p, uint2 x) { *reinterpret_cast<uint2*>(p) = x; }
 
 // ----------------------------------------------------------------------------
 // init_unique: zero, histogram, partial merge, window selection
@@ -216,8 +270,6 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
     const uint32_t wl = blockIdx.x - M.wg_begin;
-    const uint64_t beg = (uint64_t)wl * M.chunk;
-    const uint64_t end = min(M.n, beg + M.chunk);
     for (int i = threadIdx.x; i < 2 * W4; i += NP_THREADS) h[i] = 0u;
     if (threadIdx.x == 0) { red[0] = W4; red[1] = 0; }
     __syncthreads();
@@ -228,14 +280,16 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
         if (mag < (uint32_t)W4) atomicAdd(&h[(key >> 15) * W4 + mag], 1u);
         else atomicAdd(&gcounts[key], 1u);
     };
-    for_slice<4>(beg, end, M.vec != 0,
-        [&](uint64_t i) { return Keys8{*reinterpret_cast<const uint4*>(keys + i)}; },
-        [&](uint64_t, const Keys8& r) {
+    for_slice<4, 8>(M, wl,
+        [&](uint64_t i) { return Keys8{ld_u4_nt(keys + i)}; },
+        [&](const Keys8& r) {
             add(r.q.x & 0xFFFFu); add(r.q.x >> 16);
             add(r.q.y & 0xFFFFu); add(r.q.y >> 16);
             add(r.q.z & 0xFFFFu); add(r.q.z >> 16);
             add(r.q.w & 0xFFFFu); add(r.q.w >> 16);
+            return Nothing{};
         },
+        [&](uint64_t, Nothing) {},
         [&](uint64_t i) { add(keys[i]); });
     __syncthreads();
     // occupied span [lo, hi) over both signs, rounded out to even magnitudes
@@ -262,21 +316,29 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
     if (threadIdx.x == 0) M.ws.span[wl] = make_int2(lo, hi);
 }
 
-// Sum the histogram partial rows of each matrix: one thread per pair of bins.
-// Grid (W4 / NP_THREADS, count).
-__global__ void __launch_bounds__(NP_THREADS) k_hist_merge(BatchArgs b) {
-    __shared__ int2 sp[NP_MAX_WG];
-    const MatArgs& M = b.m[blockIdx.y];
-    const int nrow = (int)M.wg_count;
-    for (int r = threadIdx.x; r < nrow; r += NP_THREADS) sp[r] = M.ws.span[r];
-    __syncthreads();
-    const int q = blockIdx.x * NP_THREADS + threadIdx.x;   // < W4
+// Partial-row merges.  Thread = one bin (or bin pair), blockIdx.y = a chunk of
+// MERGE_ROWS rows, blockIdx.z = matrix; each thread sums its chunk with
+// independent accumulators and adds the chunk total to the destination with
+// one atomic, so a matrix's merge is spread over many threads instead of
+// walking all of its rows in one.
+constexpr int MERGE_ROWS = 16;
+constexpr int MERGE_THREADS = 256;
+
+// Histogram rows (packed 16-bit pairs over per-row spans) into counts.
+// Grid (W4 / MERGE_THREADS, NP_MAX_WG / MERGE_ROWS, count).
+__global__ void __launch_bounds__(MERGE_THREADS) k_hist_merge(BatchArgs b) {
+    const MatArgs& M = b.m[blockIdx.z];
+    const int r0 = blockIdx.y * MERGE_ROWS;
+    const int r1 = min((int)M.wg_count, r0 + MERGE_ROWS);
+    if (r0 >= r1) return;
+    const int q = blockIdx.x * MERGE_THREADS + threadIdx.x;   // < W4 pairs
     const int s = q >= W4 / 2;
     const int mag = 2 * (q - s * (W4 / 2));
     uint32_t s0 = 0u, s1 = 0u;
     const uint32_t* part = M.ws.part;
-    for (int r = 0; r < nrow; ++r) {
-        const int2 lh = sp[r];
+#pragma unroll 4
+    for (int r = r0; r < r1; ++r) {
+        const int2 lh = M.ws.span[r];
         if (mag >= lh.x && mag < lh.y) {
             const int half = (lh.y - lh.x) >> 1;
             const uint32_t x = part[(size_t)r * ROW4 + s * half + ((mag - lh.x) >> 1)];
@@ -285,8 +347,32 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist_merge(BatchArgs b) {
         }
     }
     uint32_t* c = M.ws.counts + (s << 15) + mag;
-    c[0] += s0;   // the global counts may already hold this workgroup-overflow share
-    c[1] += s1;
+    if (s0) atomicAdd(c, s0);
+    if (s1) atomicAdd(c + 1, s1);
+}
+
+// Keyed-gradient rows (fp32 over the 8-byte window) into G.
+// Grid (2 * W8 / MERGE_THREADS rounded up, NP_MAX_WG / MERGE_ROWS, count).
+__global__ void __launch_bounds__(MERGE_THREADS) k_grad_merge(BatchArgs b) {
+    const MatArgs& M = b.m[blockIdx.z];
+    const int r0 = blockIdx.y * MERGE_ROWS;
+    const int r1 = min((int)M.wg_count, r0 + MERGE_ROWS);
+    const int w = M.ws.st->w8, lo = M.ws.st->lo8;
+    const int i = blockIdx.x * MERGE_THREADS + threadIdx.x;
+    if (r0 >= r1 || i >= 2 * w) return;
+    const float* part = reinterpret_cast<const float*>(M.ws.part) + i;
+    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+    int r = r0;
+    for (; r + 4 <= r1; r += 4) {
+        a0 += part[(size_t)r * ROW4];
+        a1 += part[(size_t)(r + 1) * ROW4];
+        a2 += part[(size_t)(r + 2) * ROW4];
+        a3 += part[(size_t)(r + 3) * ROW4];
+    }
+    for (; r < r1; ++r) a0 += part[(size_t)r * ROW4];
+    const float sum = (a0 + a1) + (a2 + a3);
+    const int sg = i >= w;
+    if (sum != 0.f) atomicAdd(&M.ws.G[(sg << 15) | (lo + i - sg * w)], sum);
 }
 
 // Block-wide exclusive scan of one uint32 per thread (1024 threads).
@@ -310,41 +396,43 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t x, uint32_t* tmp /*
 // occupied finite magnitude range, and the LDS windows of the later passes.
 // A window of width W covers the whole occupied range when it fits, else the
 // W consecutive magnitudes holding the most weights (lowest start on ties).
+// The counts are staged into LDS with coalesced loads, then scanned there.
 __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
-    __shared__ uint32_t P[FIN_MAGS + 1];
+    __shared__ uint32_t P[FIN_MAGS + 1];   // P[m] = weights with magnitude < m
     __shared__ uint32_t tmp[16];
     __shared__ int ired[4];
     __shared__ unsigned long long best[2];
     const MatArgs& M = b.m[blockIdx.y];
     const uint32_t* counts = M.ws.counts;
-    const int m0 = threadIdx.x * 32;   // 32 magnitudes per thread; threads >= 992 hold non-finite ones
-    uint32_t local = 0, nuniq = 0, nonfin = 0;
+    if (threadIdx.x == 0) { ired[0] = 1 << 30; ired[1] = -1; ired[2] = 0; ired[3] = 0; P[0] = 0u; }
+    uint32_t nuniq = 0, nonfin = 0;
     int lo = 1 << 30, hi = -1;
-    for (int j = 0; j < 32; ++j) {
-        const int mag = m0 + j;
+#pragma unroll 4
+    for (int mag = threadIdx.x; mag < 32768; mag += NP_THREADS) {
         const uint32_t cp = counts[mag], cn = counts[0x8000 | mag];
         nuniq += (cp != 0u) + (cn != 0u);
         if (mag < FIN_MAGS) {
             const uint32_t c = cp + cn;
-            if (c) { lo = min(lo, mag); hi = mag; }
-            local += c;
+            if (c) { lo = min(lo, mag); hi = max(hi, mag); }
+            P[mag + 1] = c;
         } else {
             nonfin |= (cp | cn) != 0u;
         }
     }
-    if (threadIdx.x == 0) { ired[0] = 1 << 30; ired[1] = -1; ired[2] = 0; ired[3] = 0; P[0] = 0u; }
     __syncthreads();
     atomicMin(&ired[0], lo);
     atomicMax(&ired[1], hi);
     atomicAdd(&ired[2], (int)nuniq);
     atomicOr(&ired[3], (int)nonfin);
+    // in-place prefix sums: thread t owns entries [31 t + 1, 31 t + 31]
+    constexpr int PER = FIN_MAGS / NP_THREADS;   // 31
+    static_assert(PER * NP_THREADS == FIN_MAGS, "scan split");
+    uint32_t local = 0;
+    for (int j = 1; j <= PER; ++j) local += P[threadIdx.x * PER + j];
     uint32_t run = block_excl_scan(local, tmp);
-    if (m0 < FIN_MAGS) {
-        for (int j = 0; j < 32; ++j) {
-            const int mag = m0 + j;
-            run += counts[mag] + counts[0x8000 | mag];
-            P[mag + 1] = run;                       // P[m] = weights with magnitude < m
-        }
+    for (int j = 1; j <= PER; ++j) {
+        run += P[threadIdx.x * PER + j];
+        P[threadIdx.x * PER + j] = run;
     }
     __syncthreads();
     const int mlo = ired[0], mhi = ired[1];
@@ -383,9 +471,12 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
 // ----------------------------------------------------------------------------
 // forward table phase
 
-// Table keys of block x (T_WG blocks x T_THREADS threads x 4 = 65,536).
-#define FOR_TABLE_KEYS(u) \
-    for (int r_ = 0, u = blockIdx.x * T_THREADS + threadIdx.x; r_ < 4; ++r_, u += T_WG * T_THREADS)
+// Table keys of a thread: 4 per thread over T_WG blocks x T_THREADS threads
+// (= 65,536).  Kernels load everything the 4 patterns need first and compute
+// afterwards, so the loads overlap instead of forming a chain.
+__device__ __forceinline__ int table_key(int r) {
+    return blockIdx.x * T_THREADS + threadIdx.x + r * (T_WG * T_THREADS);
+}
 
 // Iteration t (1..max_iter): C^(t-1) from the partials of iteration t-1 (or
 // c_in), early stop test, then this block's partial S_j = sum n_u a_uj and
@@ -436,8 +527,13 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
 #pragma unroll
     for (int j = 0; j < 2 * K; ++j) acc[j] = 0.f;
     const uint32_t* counts = M.ws.counts;
-    FOR_TABLE_KEYS(u) {
-        const uint32_t n = counts[u];
+    uint32_t n4[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) n4[r] = counts[table_key(r)];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int u = table_key(r);
+        const uint32_t n = n4[r];
         if (n == 0u || !key_finite(u)) continue;
         const float v = key_value(u);
         float a[K];
@@ -497,9 +593,14 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
 #pragma unroll
     for (int j = 0; j < K; ++j) { c1[j] = cT[j]; c0[j] = cP[j]; }
     const uint32_t* counts = M.ws.counts;
-    FOR_TABLE_KEYS(u) {
+    uint32_t n4[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) n4[r] = counts[table_key(r)];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int u = table_key(r);
         M.ws.G[u] = 0.f;
-        const uint32_t n = counts[u];
+        const uint32_t n = n4[r];
         if (n == 0u) continue;
         if (!key_finite(u)) { M.ws.tab[u] = __builtin_nanf(""); M.ws.H[u] = __builtin_nanf(""); continue; }
         const float v = key_value(u);
@@ -525,8 +626,6 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
     const uint32_t wl = blockIdx.x - M.wg_begin;
-    const uint64_t beg = (uint64_t)wl * M.chunk;
-    const uint64_t end = min(M.n, beg + M.chunk);
     const int lo = M.ws.st->lo4, w = M.ws.st->w4;
     const float* tab = M.ws.tab;
     for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) {
@@ -534,41 +633,39 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
         tw[i] = tab[(s << 15) | (lo + i - s * w)];
     }
     __syncthreads();
+    // The two-way lookup compiles to one flat load whose per-lane address is
+    // either the LDS window or the global table.  That measured faster than an
+    // LDS read plus a separately predicated global read, in both gathers.
     auto look = [&](uint32_t key) -> float {
         const uint32_t d = (key & 0x7FFFu) - (uint32_t)lo;
         return d < (uint32_t)w ? tw[(key >> 15) * w + d] : tab[key];
     };
+    auto look4 = [&](uint32_t k0, uint32_t k1, uint32_t k2, uint32_t k3) {
+        return make_float4(look(k0), look(k1), look(k2), look(k3));
+    };
     const uint16_t* keys = M.keys;
     if (b.out_fp16) {
         __half* out = reinterpret_cast<__half*>(M.wt);
-        for_slice<4>(beg, end, M.vec != 0,
-            [&](uint64_t i) { return Keys8{*reinterpret_cast<const uint4*>(keys + i)}; },
-            [&](uint64_t i, const Keys8& r) {
-                const uint32_t ks[4] = {r.q.x, r.q.y, r.q.z, r.q.w};
-                uint32_t o[4];
-#pragma unroll
-                for (int p = 0; p < 4; ++p) {
-                    const __half lo_h = __float2half_rn(look(ks[p] & 0xFFFFu));
-                    const __half hi_h = __float2half_rn(look(ks[p] >> 16));
-                    o[p] = (uint32_t)__half_as_ushort(lo_h) | ((uint32_t)__half_as_ushort(hi_h) << 16);
-                }
-                *reinterpret_cast<uint4*>(out + i) = make_uint4(o[0], o[1], o[2], o[3]);
+        auto h2 = [&](float a, float c) -> uint32_t {
+            return (uint32_t)__half_as_ushort(__float2half_rn(a)) |
+                   ((uint32_t)__half_as_ushort(__float2half_rn(c)) << 16);
+        };
+        for_slice<8, 4>(M, wl,
+            [&](uint64_t i) { return Keys4{ld_u2(keys + i)}; },
+            [&](const Keys4& r) {
+                const float4 v = look4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16);
+                return make_uint2(h2(v.x, v.y), h2(v.z, v.w));
             },
+            [&](uint64_t i, uint2 o) { st_u2(out + i, o); },
             [&](uint64_t i) { out[i] = __float2half_rn(look(keys[i])); });
     } else {
         float* out = reinterpret_cast<float*>(M.wt);
-        for_slice<4>(beg, end, M.vec != 0,
-            [&](uint64_t i) { return Keys8{*reinterpret_cast<const uint4*>(keys + i)}; },
-            [&](uint64_t i, const Keys8& r) {
-                const uint4 q = r.q;
-                float4 a, c;
-                a.x = look(q.x & 0xFFFFu); a.y = look(q.x >> 16);
-                a.z = look(q.y & 0xFFFFu); a.w = look(q.y >> 16);
-                c.x = look(q.z & 0xFFFFu); c.y = look(q.z >> 16);
-                c.z = look(q.w & 0xFFFFu); c.w = look(q.w >> 16);
-                *reinterpret_cast<float4*>(out + i) = a;
-                *reinterpret_cast<float4*>(out + i + 4) = c;
+        for_slice<8, 4>(M, wl,
+            [&](uint64_t i) { return Keys4{ld_u2(keys + i)}; },
+            [&](const Keys4& r) {
+                return look4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16);
             },
+            [&](uint64_t i, float4 o) { st_f4(out + i, o); },
             [&](uint64_t i) { out[i] = look(keys[i]); });
     }
 }
@@ -591,25 +688,23 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
     const uint32_t wl = blockIdx.x - M.wg_begin;
-    const uint64_t beg = (uint64_t)wl * M.chunk;
-    const uint64_t end = min(M.n, beg + M.chunk);
     const int lo = M.ws.st->lo8, w = M.ws.st->w8;
     const uint16_t* keys = M.keys;
     const float* g = M.g;
     for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) acc[i] = 0ull;
     if (threadIdx.x == 0) emax_sh = 0;
     __syncthreads();
-    {   // sample: one finite value per thread from the start of the slice
-        const uint64_t i = beg + threadIdx.x * ((end - beg + NP_THREADS - 1) / NP_THREADS);
+    {   // sample: one value per thread, spread over the matrix
+        const uint64_t i = (((uint64_t)wl * NP_THREADS + threadIdx.x) * 2654435761ull) % M.n;
         int e = 0;
-        if (i < end) {
+        {
             e = (int)((__float_as_uint(g[i]) >> 23) & 0xFFu);
             if (e == 0xFF) e = 0;
         }
         atomicMax(&emax_sh, e);
     }
     __syncthreads();
-    const int bn = 64 - __clzll((unsigned long long)max<uint64_t>(end - beg, 2) - 1);   // 2^bn >= slice
+    const int bn = 64 - __clzll((unsigned long long)tiles_bound<8, 4>(M) - 1);   // 2^bn >= weights added here
     const int emax = emax_sh;
     const int S = 181 - bn - emax;               // 2^(emax-126) * 2^S = 2^(55-bn)
     const uint32_t elim = (uint32_t)min(emax + 6, 0xFE);
@@ -624,20 +719,14 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
             atomicAdd(&G[key], gv);
         }
     };
-    for_slice<4>(beg, end, M.vec != 0,
-        [&](uint64_t i) {
-            return KeysG8{*reinterpret_cast<const uint4*>(keys + i),
-                          *reinterpret_cast<const float4*>(g + i),
-                          *reinterpret_cast<const float4*>(g + i + 4)};
+    for_slice<8, 4>(M, wl,
+        [&](uint64_t i) { return KeysG4{ld_u2_nt(keys + i), ld_f4_nt(g + i)}; },
+        [&](const KeysG4& r) {
+            add(r.q.x & 0xFFFFu, r.g.x); add(r.q.x >> 16, r.g.y);
+            add(r.q.y & 0xFFFFu, r.g.z); add(r.q.y >> 16, r.g.w);
+            return Nothing{};
         },
-        [&](uint64_t, const KeysG8& r) {
-            const uint4 q = r.q;
-            const float4 ga = r.ga, gb = r.gb;
-            add(q.x & 0xFFFFu, ga.x); add(q.x >> 16, ga.y);
-            add(q.y & 0xFFFFu, ga.z); add(q.y >> 16, ga.w);
-            add(q.z & 0xFFFFu, gb.x); add(q.z >> 16, gb.y);
-            add(q.w & 0xFFFFu, gb.z); add(q.w >> 16, gb.w);
-        },
+        [&](uint64_t, Nothing) {},
         [&](uint64_t i) { add(keys[i], g[i]); });
     __syncthreads();
     float* row = reinterpret_cast<float*>(M.ws.part) + (size_t)wl * ROW4;
@@ -653,8 +742,6 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
     const uint32_t wl = blockIdx.x - M.wg_begin;
-    const uint64_t beg = (uint64_t)wl * M.chunk;
-    const uint64_t end = min(M.n, beg + M.chunk);
     const DevState* st = M.ws.st;
     const int lo = st->lo8, w = st->w8;
     const float2* HR = M.ws.HR;
@@ -684,77 +771,73 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
         hw[i] = HR[(s << 15) | (lo + i - s * w)];
     }
     __syncthreads();
-    auto look = [&](uint32_t key) -> float2 {
+    auto look = [&](uint32_t key) -> float2 {   // one flat load, as in k_gather_wt
         const uint32_t d = (key & 0x7FFFu) - (uint32_t)lo;
         return d < (uint32_t)w ? hw[(key >> 15) * w + d] : HR[key];
+    };
+    auto dw4 = [&](uint32_t k0, uint32_t k1, uint32_t k2, uint32_t k3, float4 gv) {
+        const float2 h0 = look(k0), h1 = look(k1), h2 = look(k2), h3 = look(k3);
+        return make_float4(fmaf(gv.x, h0.x, h0.y), fmaf(gv.y, h1.x, h1.y),
+                           fmaf(gv.z, h2.x, h2.y), fmaf(gv.w, h3.x, h3.y));
     };
     const uint16_t* keys = M.keys;
     const float* g = M.g;
     float* out = M.gw;
-    for_slice<4>(beg, end, M.vec != 0,
-        [&](uint64_t i) {
-            return KeysG8{*reinterpret_cast<const uint4*>(keys + i),
-                          *reinterpret_cast<const float4*>(g + i),
-                          *reinterpret_cast<const float4*>(g + i + 4)};
-        },
-        [&](uint64_t i, const KeysG8& r) {
-            const uint4 q = r.q;
-            const float4 ga = r.ga, gb = r.gb;
-            float2 h;
-            float4 oa, ob;
-            h = look(q.x & 0xFFFFu); oa.x = fmaf(ga.x, h.x, h.y);
-            h = look(q.x >> 16);     oa.y = fmaf(ga.y, h.x, h.y);
-            h = look(q.y & 0xFFFFu); oa.z = fmaf(ga.z, h.x, h.y);
-            h = look(q.y >> 16);     oa.w = fmaf(ga.w, h.x, h.y);
-            h = look(q.z & 0xFFFFu); ob.x = fmaf(gb.x, h.x, h.y);
-            h = look(q.z >> 16);     ob.y = fmaf(gb.y, h.x, h.y);
-            h = look(q.w & 0xFFFFu); ob.z = fmaf(gb.z, h.x, h.y);
-            h = look(q.w >> 16);     ob.w = fmaf(gb.w, h.x, h.y);
-            *reinterpret_cast<float4*>(out + i) = oa;
-            *reinterpret_cast<float4*>(out + i + 4) = ob;
-        },
-        [&](uint64_t i) {
-            const float2 h = look(keys[i]);
-            out[i] = fmaf(g[i], h.x, h.y);
-        });
+    auto dw = [&](uint32_t key, float gv) {
+        const float2 h = look(key);
+        return fmaf(gv, h.x, h.y);
+    };
+    for_slice<8, 4>(M, wl,
+        [&](uint64_t i) { return KeysG4{ld_u2(keys + i), ld_f4(g + i)}; },
+        [&](const KeysG4& r) { return dw4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16, r.g); },
+        [&](uint64_t i, float4 o) { st_f4(out + i, o); },
+        [&](uint64_t i) { out[i] = dw(keys[i], g[i]); });
 }
 
 // ----------------------------------------------------------------------------
 // backward table phase
 
-// Direct use of A^(T) and C^(T) by W~: G_u from the keyed-reduction partial
-// rows plus its fp32 remainder in G, then partials of gamma_j = sum_u G_u a^(T)_uj (= dL/dC^(T)_j) and
+// Direct use of A^(T) and C^(T) by W~: with G_u (merged keyed sums), partials of gamma_j = sum_u G_u a^(T)_uj (= dL/dC^(T)_j) and
 // E_j = sum_u G_u a^(T)_uj (C^(T)_j - Tab_u) sgn(v_u - C^(T-1)_j).
 // Grid (T_WG, count).
 template <int K>
 __global__ void __launch_bounds__(T_THREADS) k_bwd_top(BatchArgs b) {
     __shared__ float tot[2 * K];
     __shared__ float scratch[T_THREADS / 64 * 2 * K];
+    __shared__ float c1sh[K], c0sh[K];
     const MatArgs& M = b.m[blockIdx.y];
     const DevState* st = M.ws.st;
     const int T = st->teff;
+    if (threadIdx.x < K) {
+        c1sh[threadIdx.x] = M.ws.chist[T * KMAX + threadIdx.x];
+        c0sh[threadIdx.x] = M.ws.chist[(T - 1) * KMAX + threadIdx.x];
+    }
+    __syncthreads();
     float c1[K], c0[K];
 #pragma unroll
-    for (int j = 0; j < K; ++j) { c1[j] = M.ws.chist[T * KMAX + j]; c0[j] = M.ws.chist[(T - 1) * KMAX + j]; }
-    const int lo = st->lo8, w = st->w8;       // the keyed reduction's window
-    const int nrow = (int)M.wg_count;
-    const float* part = reinterpret_cast<const float*>(M.ws.part);
+    for (int j = 0; j < K; ++j) { c1[j] = c1sh[j]; c0[j] = c0sh[j]; }
     float acc[2 * K];
 #pragma unroll
     for (int j = 0; j < 2 * K; ++j) acc[j] = 0.f;
     const uint32_t* counts = M.ws.counts;
-    FOR_TABLE_KEYS(u) {
-        if (counts[u] == 0u || !key_finite(u)) continue;
-        const uint32_t d = (uint32_t)(u & 0x7FFF) - (uint32_t)lo;
-        float G = M.ws.G[u];                   // values added outside the fixed-point sums
-        if (d < (uint32_t)w) {
-            const float* p = part + (u >> 15) * w + d;
-            for (int r = 0; r < nrow; ++r) G += p[(size_t)r * ROW4];
-        }
+    uint32_t n4[4];
+    float G4[4], t4[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int u = table_key(r);
+        n4[r] = counts[u];
+        G4[r] = M.ws.G[u];
+        t4[r] = M.ws.tab[u];
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int u = table_key(r);
+        if (n4[r] == 0u || !key_finite(u)) continue;
+        const float G = G4[r];
         const float v = key_value(u);
         float a[K];
         attn_row<K>(v, c0, b.s2, a);
-        const float tv = M.ws.tab[u];
+        const float tv = t4[r];
 #pragma unroll
         for (int j = 0; j < K; ++j) {
             const float ga = G * a[j];
@@ -778,7 +861,7 @@ template <int K>
 __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
     __shared__ float tot[2 * K];
     __shared__ float scratch[T_THREADS / 64 * K];
-    __shared__ float gsh[K];
+    __shared__ float gsh[K], gSsh[K], c1sh[K], c0sh[K];
     const MatArgs& M = b.m[blockIdx.y];
     const DevState* st = M.ws.st;
     const int T = st->teff;
@@ -789,8 +872,7 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
         reduce_tparts(M.ws.bpart, 0, K, tot);
         if (threadIdx.x < K) gsh[threadIdx.x] = tot[threadIdx.x];
     } else {
-        reduce_tparts(M.ws.bpart + (size_t)(t + 1) * T_WG * PSTRIDE, 0, K, tot);
-        reduce_tparts(M.ws.bpart, K, K, tot + K);
+        reduce_tparts2(M.ws.bpart + (size_t)(t + 1) * T_WG * PSTRIDE, M.ws.bpart, K, tot);
         if (threadIdx.x < K) {
             const int j = threadIdx.x;
             float gm = tot[j] * b.inv_tau;
@@ -799,42 +881,58 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
             gsh[j] = gm;
         }
     }
+    if (threadIdx.x < K) {
+        const int j = threadIdx.x;
+        c1sh[j] = M.ws.chist[t * KMAX + j];
+        c0sh[j] = M.ws.chist[(t - 1) * KMAX + j];
+    }
     __syncthreads();
-    if (lead && threadIdx.x < K) M.ws.ghist[t * KMAX + threadIdx.x] = gsh[threadIdx.x];
+    if (threadIdx.x < K) {
+        const int j = threadIdx.x;
+        const float S = M.ws.shist[t * KMAX + j];
+        gSsh[j] = S > 0.f ? gsh[j] / S : 0.f;
+        if (lead) M.ws.ghist[t * KMAX + j] = gsh[j];
+    }
+    __syncthreads();
     float c1[K], c0[K], gS[K];
 #pragma unroll
-    for (int j = 0; j < K; ++j) {
-        c1[j] = M.ws.chist[t * KMAX + j];
-        c0[j] = M.ws.chist[(t - 1) * KMAX + j];
-        const float S = M.ws.shist[t * KMAX + j];
-        gS[j] = S > 0.f ? gsh[j] / S : 0.f;
-    }
+    for (int j = 0; j < K; ++j) { c1[j] = c1sh[j]; c0[j] = c0sh[j]; gS[j] = gSsh[j]; }
     float acc[K];
 #pragma unroll
     for (int j = 0; j < K; ++j) acc[j] = 0.f;
     const uint32_t* counts = M.ws.counts;
-    FOR_TABLE_KEYS(u) {
-        const uint32_t n = counts[u];
+    uint32_t n4[4];
+    float R4[4], H4[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int u = table_key(r);
+        n4[r] = counts[u];
+        R4[r] = t != T ? M.ws.R[u] : 0.f;
+        H4[r] = t == 1 ? M.ws.H[u] : 0.f;
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int u = table_key(r);
+        const uint32_t n = n4[r];
         if (n == 0u) continue;
         if (!key_finite(u)) {
             if (t == 1) M.ws.HR[u] = make_float2(__builtin_nanf(""), __builtin_nanf(""));
             continue;
         }
         const float v = key_value(u);
-        float a[K], dev[K];
-        const int m = attn_row<K>(v, c0, b.s2, a);
-        const float direct = softmax_dev<K>(v, a, gS, c1, m, dev);
+        float a[K], dev[K], cm;
+        attn_row_sel<K>(v, c0, b.s2, a, c1, cm);
+        const float direct = softmax_dev<K>(v, a, gS, c1, cm, dev);
         const float nf = (float)n;
-        float r = 0.f;
+        float r_ = 0.f;
 #pragma unroll
         for (int j = 0; j < K; ++j) {
             const float dl = a[j] * dev[j] * sgnf(v - c0[j]);
-            r += dl;
+            r_ += dl;
             acc[j] = fmaf(nf, dl, acc[j]);
         }
-        float Ru = fmaf(-r, b.inv_tau, direct);
-        if (t != T) Ru += M.ws.R[u];
-        if (t == 1) M.ws.HR[u] = make_float2(M.ws.H[u], Ru);
+        const float Ru = fmaf(-r_, b.inv_tau, direct) + R4[r];
+        if (t == 1) M.ws.HR[u] = make_float2(H4[r], Ru);
         else M.ws.R[u] = Ru;
     }
     block_sum<K, T_THREADS>(acc, scratch, tot);
@@ -874,12 +972,15 @@ template <int K>
 __global__ void __launch_bounds__(D_THREADS) k_dense_iter(BatchArgs b) {
     __shared__ float tot[2 * K];
     __shared__ float scratch[D_THREADS / 64 * 2 * K];
+    __shared__ float csh[K];
     const MatArgs& M = b.m[0];
     const int t = b.t;
     if (t > 1 && M.ws.st->conv) return;
+    if (threadIdx.x < K) csh[threadIdx.x] = t == 1 ? M.c_in[threadIdx.x] : M.ws.chist[(t - 1) * KMAX + threadIdx.x];
+    __syncthreads();
     float c[K];
 #pragma unroll
-    for (int j = 0; j < K; ++j) c[j] = t == 1 ? M.c_in[j] : M.ws.chist[(t - 1) * KMAX + j];
+    for (int j = 0; j < K; ++j) c[j] = csh[j];
     float acc[2 * K];
 #pragma unroll
     for (int j = 0; j < 2 * K; ++j) acc[j] = 0.f;
@@ -935,9 +1036,15 @@ template <int K>
 __global__ void __launch_bounds__(D_THREADS) k_dense_out(BatchArgs b) {
     const MatArgs& M = b.m[0];
     const int T = M.ws.st->teff;
+    __shared__ float c1sh[K], c0sh[K];
+    if (threadIdx.x < K) {
+        c1sh[threadIdx.x] = M.ws.chist[T * KMAX + threadIdx.x];
+        c0sh[threadIdx.x] = M.ws.chist[(T - 1) * KMAX + threadIdx.x];
+    }
+    __syncthreads();
     float c1[K], c0[K];
 #pragma unroll
-    for (int j = 0; j < K; ++j) { c1[j] = M.ws.chist[T * KMAX + j]; c0[j] = M.ws.chist[(T - 1) * KMAX + j]; }
+    for (int j = 0; j < K; ++j) { c1[j] = c1sh[j]; c0[j] = c0sh[j]; }
     if (blockIdx.x == 0) {
         if (threadIdx.x < K) M.c_out[threadIdx.x] = M.ws.chist[T * KMAX + threadIdx.x];
         if (threadIdx.x == 0 && M.iters_out) *M.iters_out = T;
@@ -975,9 +1082,15 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_btop(BatchArgs b) {
     __shared__ float scratch[D_THREADS / 64 * 2 * K];
     const MatArgs& M = b.m[0];
     const int T = M.ws.st->teff;
+    __shared__ float c1sh[K], c0sh[K];
+    if (threadIdx.x < K) {
+        c1sh[threadIdx.x] = M.ws.chist[T * KMAX + threadIdx.x];
+        c0sh[threadIdx.x] = M.ws.chist[(T - 1) * KMAX + threadIdx.x];
+    }
+    __syncthreads();
     float c1[K], c0[K];
 #pragma unroll
-    for (int j = 0; j < K; ++j) { c1[j] = M.ws.chist[T * KMAX + j]; c0[j] = M.ws.chist[(T - 1) * KMAX + j]; }
+    for (int j = 0; j < K; ++j) { c1[j] = c1sh[j]; c0[j] = c0sh[j]; }
     float acc[2 * K];
 #pragma unroll
     for (int j = 0; j < 2 * K; ++j) acc[j] = 0.f;
@@ -1012,18 +1125,22 @@ template <int K>
 __global__ void __launch_bounds__(D_THREADS) k_dense_biter(BatchArgs b) {
     __shared__ float tot[K];
     __shared__ float scratch[D_THREADS / 64 * K];
+    __shared__ float c1sh[K], c0sh[K], gSsh[K];
     const MatArgs& M = b.m[0];
     const int T = M.ws.st->teff;
     const int t = b.t;
     if (t > T) return;
+    if (threadIdx.x < K) {
+        const int j = threadIdx.x;
+        c1sh[j] = M.ws.chist[t * KMAX + j];
+        c0sh[j] = M.ws.chist[(t - 1) * KMAX + j];
+        const float S = M.ws.shist[t * KMAX + j];
+        gSsh[j] = S > 0.f ? M.ws.ghist[t * KMAX + j] / S : 0.f;
+    }
+    __syncthreads();
     float c1[K], c0[K], gS[K];
 #pragma unroll
-    for (int j = 0; j < K; ++j) {
-        c1[j] = M.ws.chist[t * KMAX + j];
-        c0[j] = M.ws.chist[(t - 1) * KMAX + j];
-        const float S = M.ws.shist[t * KMAX + j];
-        gS[j] = S > 0.f ? M.ws.ghist[t * KMAX + j] / S : 0.f;
-    }
+    for (int j = 0; j < K; ++j) { c1[j] = c1sh[j]; c0[j] = c0sh[j]; gS[j] = gSsh[j]; }
     float acc[K];
 #pragma unroll
     for (int j = 0; j < K; ++j) acc[j] = 0.f;
@@ -1033,9 +1150,9 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_biter(BatchArgs b) {
         const uint32_t key = M.keys[i];
         if (!key_finite(key)) continue;
         const float v = key_value(key);
-        float a[K], dev[K];
-        const int m = attn_row<K>(v, c0, b.s2, a);
-        const float direct = softmax_dev<K>(v, a, gS, c1, m, dev);
+        float a[K], dev[K], cm;
+        attn_row_sel<K>(v, c0, b.s2, a, c1, cm);
+        const float direct = softmax_dev<K>(v, a, gS, c1, cm, dev);
         float r = 0.f;
 #pragma unroll
         for (int j = 0; j < K; ++j) {
@@ -1117,6 +1234,9 @@ static hipError_t backward_k(BatchArgs& b, uint32_t grid_np, int max_t, hipStrea
                              const PassEvents* ev) {
     const dim3 tg(T_WG, b.count);
     EDKM_NPASS(PASS_KEYED_GRAD, "k_keyed_grad", k_keyed_grad, dim3(grid_np), dim3(NP_THREADS), b);
+    EDKM_LAUNCH("k_grad_merge", k_grad_merge,
+                dim3((2 * W8 + MERGE_THREADS - 1) / MERGE_THREADS, NP_MAX_WG / MERGE_ROWS, b.count),
+                dim3(MERGE_THREADS), b);
     EDKM_LAUNCH("k_bwd_top", k_bwd_top<K>, tg, dim3(T_THREADS), b);
     for (int t = max_t; t >= 1; --t) {
         b.t = t;
@@ -1166,7 +1286,8 @@ hipError_t launch_init_unique(BatchArgs& b, uint32_t grid_np, hipStream_t s, con
     (void)hipGetLastError();   // an earlier, unrelated failure is not ours to report
     EDKM_LAUNCH("k_init_zero", k_init_zero, dim3(T_WG, b.count), dim3(T_THREADS), b);
     EDKM_NPASS(PASS_HIST, "k_hist", k_hist, dim3(grid_np), dim3(NP_THREADS), b);
-    EDKM_LAUNCH("k_hist_merge", k_hist_merge, dim3(W4 / NP_THREADS, b.count), dim3(NP_THREADS), b);
+    EDKM_LAUNCH("k_hist_merge", k_hist_merge, dim3(W4 / MERGE_THREADS, NP_MAX_WG / MERGE_ROWS, b.count),
+                dim3(MERGE_THREADS), b);
     EDKM_LAUNCH("k_window", k_window, dim3(1, b.count), dim3(NP_THREADS), b);
     return hipSuccess;
 }
