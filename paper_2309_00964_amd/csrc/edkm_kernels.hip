@@ -336,15 +336,21 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_hist_merge(BatchArgs b) {
     const int mag = 2 * (q - s * (W4 / 2));
     uint32_t s0 = 0u, s1 = 0u;
     const uint32_t* part = M.ws.part;
-#pragma unroll 4
-    for (int r = r0; r < r1; ++r) {
-        const int2 lh = M.ws.span[r];
-        if (mag >= lh.x && mag < lh.y) {
-            const int half = (lh.y - lh.x) >> 1;
-            const uint32_t x = part[(size_t)r * ROW4 + s * half + ((mag - lh.x) >> 1)];
-            s0 += x & 0xFFFFu;
-            s1 += x >> 16;
+    uint32_t x[MERGE_ROWS];                    // every row's word in flight at once
+#pragma unroll
+    for (int q2 = 0; q2 < MERGE_ROWS; ++q2) {
+        const int r = r0 + q2;
+        x[q2] = 0u;
+        if (r < r1) {
+            const int2 lh = M.ws.span[r];
+            if (mag >= lh.x && mag < lh.y)
+                x[q2] = part[(size_t)r * ROW4 + s * ((lh.y - lh.x) >> 1) + ((mag - lh.x) >> 1)];
         }
+    }
+#pragma unroll
+    for (int q2 = 0; q2 < MERGE_ROWS; ++q2) {
+        s0 += x[q2] & 0xFFFFu;
+        s1 += x[q2] >> 16;
     }
     uint32_t* c = M.ws.counts + (s << 15) + mag;
     if (s0) atomicAdd(c, s0);
@@ -361,16 +367,14 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_grad_merge(BatchArgs b) {
     const int i = blockIdx.x * MERGE_THREADS + threadIdx.x;
     if (r0 >= r1 || i >= 2 * w) return;
     const float* part = reinterpret_cast<const float*>(M.ws.part) + i;
-    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
-    int r = r0;
-    for (; r + 4 <= r1; r += 4) {
-        a0 += part[(size_t)r * ROW4];
-        a1 += part[(size_t)(r + 1) * ROW4];
-        a2 += part[(size_t)(r + 2) * ROW4];
-        a3 += part[(size_t)(r + 3) * ROW4];
-    }
-    for (; r < r1; ++r) a0 += part[(size_t)r * ROW4];
-    const float sum = (a0 + a1) + (a2 + a3);
+    float x[MERGE_ROWS];                       // every row's value in flight at once
+#pragma unroll
+    for (int q = 0; q < MERGE_ROWS; ++q) x[q] = r0 + q < r1 ? part[(size_t)(r0 + q) * ROW4] : 0.f;
+#pragma unroll
+    for (int h = MERGE_ROWS / 2; h > 0; h /= 2)   // pairwise sum
+#pragma unroll
+        for (int q = 0; q < h; ++q) x[q] += x[q + h];
+    const float sum = x[0];
     const int sg = i >= w;
     if (sum != 0.f) atomicAdd(&M.ws.G[(sg << 15) | (lo + i - sg * w)], sum);
 }
@@ -392,50 +396,62 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t x, uint32_t* tmp /*
     return base + inc - x;
 }
 
-// Per matrix, one block: occupied-pattern count, non-finite flag, the
-// occupied finite magnitude range, and the LDS windows of the later passes.
-// A window of width W covers the whole occupied range when it fits, else the
-// W consecutive magnitudes holding the most weights (lowest start on ties).
-// The counts are staged into LDS with coalesced loads, then scanned there.
-__global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
-    __shared__ uint32_t P[FIN_MAGS + 1];   // P[m] = weights with magnitude < m
+// Window selection, first half.  Grid (32, count): block x covers magnitudes
+// [1024 x, 1024 x + 1024) of both signs.  Writes, per magnitude below 0x7C00,
+// the running count of weights within the block (inclusive), and per block its
+// total, occupied-pattern count, occupied magnitude range and non-finite flag.
+__global__ void __launch_bounds__(NP_THREADS) k_window_scan(BatchArgs b) {
     __shared__ uint32_t tmp[16];
-    __shared__ int ired[4];
-    __shared__ unsigned long long best[2];
+    __shared__ int ired[5];
     const MatArgs& M = b.m[blockIdx.y];
     const uint32_t* counts = M.ws.counts;
-    if (threadIdx.x == 0) { ired[0] = 1 << 30; ired[1] = -1; ired[2] = 0; ired[3] = 0; P[0] = 0u; }
-    uint32_t nuniq = 0, nonfin = 0;
-    int lo = 1 << 30, hi = -1;
-#pragma unroll 4
-    for (int mag = threadIdx.x; mag < 32768; mag += NP_THREADS) {
-        const uint32_t cp = counts[mag], cn = counts[0x8000 | mag];
-        nuniq += (cp != 0u) + (cn != 0u);
-        if (mag < FIN_MAGS) {
-            const uint32_t c = cp + cn;
-            if (c) { lo = min(lo, mag); hi = max(hi, mag); }
-            P[mag + 1] = c;
-        } else {
-            nonfin |= (cp | cn) != 0u;
+    const int mag = blockIdx.x * NP_THREADS + threadIdx.x;   // < 32768
+    const uint32_t cp = counts[mag], cn = counts[0x8000 | mag];
+    if (threadIdx.x == 0) { ired[0] = 1 << 30; ired[1] = -1; ired[2] = 0; ired[3] = 0; ired[4] = 0; }
+    const bool fin = mag < FIN_MAGS;
+    const uint32_t c = fin ? cp + cn : 0u;
+    const uint32_t incl = block_excl_scan(c, tmp) + c;        // (has block barriers)
+    if (fin) M.ws.wscan[mag] = incl;
+    if (c) { atomicMin(&ired[0], mag); atomicMax(&ired[1], mag); }
+    const int nu = (cp != 0u) + (cn != 0u);
+    if (nu) atomicAdd(&ired[2], nu);
+    if (!fin && (cp | cn)) atomicOr(&ired[3], 1);
+    if (threadIdx.x == NP_THREADS - 1) ired[4] = (int)incl;
+    __syncthreads();
+    if (threadIdx.x < 5) M.ws.wstat[blockIdx.x * 8 + threadIdx.x] = ired[threadIdx.x];
+}
+
+// Window selection, second half; one block per matrix.  Combines the block
+// results into the occupied-pattern count, the non-finite flag, the occupied
+// finite magnitude range and the LDS windows of the later passes.  A window of
+// width W covers the whole occupied range when it fits, else the W consecutive
+// magnitudes holding the most weights (lowest start on ties).
+__global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
+    __shared__ uint32_t off[33];   // weights with magnitude < 1024 x
+    __shared__ int st5[5];
+    __shared__ unsigned long long best[2];
+    const MatArgs& M = b.m[blockIdx.y];
+    if (threadIdx.x == 0) {
+        int lo = 1 << 30, hi = -1, nu = 0, nf = 0;
+        uint32_t run = 0;
+        for (int x = 0; x < 32; ++x) {
+            const int* w = M.ws.wstat + x * 8;
+            lo = min(lo, w[0]);
+            hi = max(hi, w[1]);
+            nu += w[2];
+            nf |= w[3];
+            off[x] = run;
+            run += (uint32_t)w[4];
         }
+        off[32] = run;
+        st5[0] = lo; st5[1] = hi; st5[2] = nu; st5[3] = nf;
     }
     __syncthreads();
-    atomicMin(&ired[0], lo);
-    atomicMax(&ired[1], hi);
-    atomicAdd(&ired[2], (int)nuniq);
-    atomicOr(&ired[3], (int)nonfin);
-    // in-place prefix sums: thread t owns entries [31 t + 1, 31 t + 31]
-    constexpr int PER = FIN_MAGS / NP_THREADS;   // 31
-    static_assert(PER * NP_THREADS == FIN_MAGS, "scan split");
-    uint32_t local = 0;
-    for (int j = 1; j <= PER; ++j) local += P[threadIdx.x * PER + j];
-    uint32_t run = block_excl_scan(local, tmp);
-    for (int j = 1; j <= PER; ++j) {
-        run += P[threadIdx.x * PER + j];
-        P[threadIdx.x * PER + j] = run;
-    }
-    __syncthreads();
-    const int mlo = ired[0], mhi = ired[1];
+    const int mlo = st5[0], mhi = st5[1];
+    const uint32_t* scan = M.ws.wscan;
+    auto P = [&](int x) -> uint32_t {   // weights with magnitude < x
+        return x == 0 ? 0u : scan[x - 1] + off[(x - 1) / NP_THREADS];
+    };
     int wl[2], ww[2];
     const int widths[2] = {W4, W8};
     for (int w = 0; w < 2; ++w) {
@@ -446,7 +462,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
         __syncthreads();
         unsigned long long mine = 0ull;
         for (int s = mlo + threadIdx.x; s <= mhi - W + 1; s += NP_THREADS) {
-            const uint32_t cov = P[s + W] - P[s];
+            const uint32_t cov = P(s + W) - P(s);
             // larger coverage wins, then the smaller start
             const unsigned long long key = ((unsigned long long)cov << 32) | (uint32_t)(0x7FFFFFFF - s);
             mine = key > mine ? key : mine;
@@ -458,13 +474,13 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
     }
     if (threadIdx.x == 0) {
         DevState* st = M.ws.st;
-        st->num_unique = (uint32_t)ired[2];
-        st->nonfinite = (uint32_t)ired[3];
+        st->num_unique = (uint32_t)st5[2];
+        st->nonfinite = (uint32_t)st5[3];
         st->mlo = mlo;
         st->mhi = mhi;
         st->lo4 = wl[0]; st->w4 = ww[0];
         st->lo8 = wl[1]; st->w8 = ww[1];
-        if (M.nuniq_out) *M.nuniq_out = (uint32_t)ired[2];
+        if (M.nuniq_out) *M.nuniq_out = (uint32_t)st5[2];
     }
 }
 
@@ -490,6 +506,10 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
     const MatArgs& M = b.m[blockIdx.y];
     const int t = b.t;
     if (t > M.max_iter) return;
+    // pattern counts do not depend on the centroids: issue their loads first
+    uint32_t n4[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) n4[r] = M.ws.counts[table_key(r)];
     DevState* st = M.ws.st;
     const bool lead = blockIdx.x == 0;
     if (t == 1) {
@@ -526,10 +546,6 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
     float acc[2 * K];
 #pragma unroll
     for (int j = 0; j < 2 * K; ++j) acc[j] = 0.f;
-    const uint32_t* counts = M.ws.counts;
-    uint32_t n4[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) n4[r] = counts[table_key(r)];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int u = table_key(r);
@@ -560,6 +576,9 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
     __shared__ float tot[2 * K];
     __shared__ float cT[K], cP[K];
     const MatArgs& M = b.m[blockIdx.y];
+    uint32_t n4[4];   // independent of the centroids: loaded first
+#pragma unroll
+    for (int r = 0; r < 4; ++r) n4[r] = M.ws.counts[table_key(r)];
     DevState* st = M.ws.st;
     const bool lead = blockIdx.x == 0;
     int T;
@@ -592,10 +611,6 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
     float c1[K], c0[K];
 #pragma unroll
     for (int j = 0; j < K; ++j) { c1[j] = cT[j]; c0[j] = cP[j]; }
-    const uint32_t* counts = M.ws.counts;
-    uint32_t n4[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) n4[r] = counts[table_key(r)];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int u = table_key(r);
@@ -806,6 +821,15 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_top(BatchArgs b) {
     __shared__ float scratch[T_THREADS / 64 * 2 * K];
     __shared__ float c1sh[K], c0sh[K];
     const MatArgs& M = b.m[blockIdx.y];
+    uint32_t n4[4];   // per-pattern inputs first: they do not depend on the centroids
+    float G4[4], t4[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int u = table_key(r);
+        n4[r] = M.ws.counts[u];
+        G4[r] = M.ws.G[u];
+        t4[r] = M.ws.tab[u];
+    }
     const DevState* st = M.ws.st;
     const int T = st->teff;
     if (threadIdx.x < K) {
@@ -819,16 +843,6 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_top(BatchArgs b) {
     float acc[2 * K];
 #pragma unroll
     for (int j = 0; j < 2 * K; ++j) acc[j] = 0.f;
-    const uint32_t* counts = M.ws.counts;
-    uint32_t n4[4];
-    float G4[4], t4[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int u = table_key(r);
-        n4[r] = counts[u];
-        G4[r] = M.ws.G[u];
-        t4[r] = M.ws.tab[u];
-    }
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int u = table_key(r);
@@ -867,6 +881,15 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
     const int T = st->teff;
     const int t = b.t;
     if (t > T) return;
+    uint32_t n4[4];   // per-pattern inputs first: they do not depend on gamma
+    float R4[4], H4[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int u = table_key(r);
+        n4[r] = M.ws.counts[u];
+        R4[r] = t != T ? M.ws.R[u] : 0.f;
+        H4[r] = t == 1 ? M.ws.H[u] : 0.f;
+    }
     const bool lead = blockIdx.x == 0;
     if (t == T) {
         reduce_tparts(M.ws.bpart, 0, K, tot);
@@ -900,16 +923,6 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
     float acc[K];
 #pragma unroll
     for (int j = 0; j < K; ++j) acc[j] = 0.f;
-    const uint32_t* counts = M.ws.counts;
-    uint32_t n4[4];
-    float R4[4], H4[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int u = table_key(r);
-        n4[r] = counts[u];
-        R4[r] = t != T ? M.ws.R[u] : 0.f;
-        H4[r] = t == 1 ? M.ws.H[u] : 0.f;
-    }
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int u = table_key(r);
@@ -1288,6 +1301,7 @@ hipError_t launch_init_unique(BatchArgs& b, uint32_t grid_np, hipStream_t s, con
     EDKM_NPASS(PASS_HIST, "k_hist", k_hist, dim3(grid_np), dim3(NP_THREADS), b);
     EDKM_LAUNCH("k_hist_merge", k_hist_merge, dim3(W4 / MERGE_THREADS, NP_MAX_WG / MERGE_ROWS, b.count),
                 dim3(MERGE_THREADS), b);
+    EDKM_LAUNCH("k_window_scan", k_window_scan, dim3(32, b.count), dim3(NP_THREADS), b);
     EDKM_LAUNCH("k_window", k_window, dim3(1, b.count), dim3(NP_THREADS), b);
     return hipSuccess;
 }
@@ -1316,7 +1330,7 @@ hipError_t launch_backward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, cons
 
 static_assert(W4 % NP_THREADS == 0, "merge grid covers the window exactly");
 static_assert(2 * W8 <= ROW4, "keyed-reduction rows fit the partial-row stride");
-static_assert(NP_THREADS * 32 == 32768, "window scan: 32 magnitudes per thread");
+static_assert(NP_THREADS * 32 == 32768, "window scan: 32 blocks of 1024 magnitudes");
 static_assert(T_WG == 64, "table partial reduction uses one lane per workgroup");
 static_assert(T_WG * T_THREADS * 4 == NKEYS, "table blocks cover every pattern");
 
