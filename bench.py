@@ -12,6 +12,12 @@ Output: one JSON line with weights/s, the HBM roofline of the dominant
 N-sized kernel (timed live with HIP events around its launches), and the CPU
 oracle timed on a bounded sample on this host.
 
+Other workloads (--workload; one JSON line each, same fields):
+  mlp_outliers [--bits 3|4]   the 11008x4096 MLP matrix with 0.1% outliers; the
+                              dense per-weight-map path is timed beside it ("dense")
+  stack [--bits 2|3|4]        32 decoder layers (224 matrices, 6.48e9 weights,
+                              drawn on the GPU), one step over every matrix
+
 Other modes (measurement helpers):
   --copy-calibration          run a plain 1 GiB device copy (HBM counter calibration)
   --pmc-summary FETCH WRITE   turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE)
@@ -34,6 +40,15 @@ PEAK_HBM_GBS = 8000.0
 # algorithmic bytes per weight of each N-sized pass (fp32 W~ output)
 PASS_BYTES = {"k_hist": 2, "k_gather_wt": 6, "k_keyed_grad": 6, "k_gather_grad": 10}
 PASS_IDS = {"k_hist": 0, "k_gather_wt": 1, "k_keyed_grad": 2, "k_gather_grad": 3}
+# dense comparison path: timed kernels and algorithmic fp32 operations per map
+# entry (weight, centroid).  Map row: difference, absolute value, scale,
+# exponential, row sum, normalisation (6).  Forward iteration adds S_j += a and
+# P_j += a v (3).  Backward iteration adds alpha_j = gamma_j / S_j (v - C_j) (2),
+# sum a alpha (2), a (alpha - mean) (2), sign product (1), row and column sums (2).
+DENSE_PASS_IDS = {"k_dense_iter": 4, "k_dense_biter": 5}
+DENSE_OPS_PER_ENTRY = {"k_dense_iter": 9, "k_dense_biter": 15}
+PEAK_FP32_TFLOPS = 157.3
+GROUP = 8        # matrices per launch group of the batched calls
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 COPY_BYTES = 1 << 30
 
@@ -54,12 +69,17 @@ class HipEvents:
         self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
                                                  ctypes.c_void_p]
         self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
 
     def create(self):
         e = ctypes.c_void_p()
         if self.lib.hipEventCreate(ctypes.byref(e)) != 0:
             raise RuntimeError("hipEventCreate failed")
         return e.value
+
+    def record(self, e, stream):
+        if self.lib.hipEventRecord(e, stream) != 0:
+            raise RuntimeError("hipEventRecord failed")
 
     def elapsed_ms(self, a, b):
         ms = ctypes.c_float()
@@ -71,90 +91,61 @@ class HipEvents:
         self.lib.hipEventDestroy(e)
 
 
-def cpu_baseline(host, names):
-    """The fp64 dense oracle, as it stands, on the named matrices of the layer."""
+def cpu_baseline(samples, k):
+    """The fp64 dense oracle, as it stands, on a bounded sample of the workload:
+    ``samples`` is a list of (name, keys, c0, g) host arrays."""
     from oracle import dense
     from paper_2309_00964_amd import inputs
     n = 0
     t0 = time.perf_counter()
-    for name in names:
-        keys, c0, g = host[name]
+    for _, keys, c0, g in samples:
         f = dense.forward(keys, c0.astype("float64"), inputs.TAU, inputs.ITERS)
         dense.backward(keys, f, g.astype("float64"))
         n += keys.size
     dt = time.perf_counter() - t0
     return {"value": n / dt, "unit": "weights/s", "cores": dense.threads(), "kind": "oracle",
-            "sample": "fp64 dense DKM forward+backward (5 iterations, k=8) of %s (%d weights) "
-                      "in %.1f s" % ("+".join(names), n, dt)}
+            "sample": "fp64 dense DKM forward+backward (%d iterations, k=%d) of %s (%d weights) "
+                      "in %.1f s" % (inputs.ITERS, k, "+".join(s[0] for s in samples), n, dt)}
 
 
-def bench(args):
-    import numpy as np
+def timed(step, plan, pass_ids, steps, warmup):
+    """Warm up, then time `steps` calls of step() between two HIP events on the
+    current stream, with per-pass events recorded by the library on `plan`.
+    Returns (seconds, {pass: average launch ms})."""
     import torch
-    from paper_2309_00964_amd import edkm, inputs
-
-    if not torch.cuda.is_available():
-        sys.exit("bench.py needs a GPU")
-    dev = torch.device("cuda:0")
-    w = inputs.WORKLOADS[4]
-    bits, k = 3, 8
-    plans, keys, c_in, c_out, wt, iters, grads, gw, gc, host = [], [], [], [], [], [], [], [], [], {}
-    total = 0
-    for i, (name, r, c) in enumerate(w["mats"]):
-        n = r * c
-        total += n
-        kh = inputs.fp16_weights(n, inputs.weight_seed(4, i))
-        c0 = inputs.quantile_init(kh, k)
-        g = inputs.upstream_grad(n, inputs.grad_seed(4, i))
-        if name in args.cpu_sample:
-            host[name] = (kh, c0, g)
-        plans.append(edkm.Plan(n, bits, inputs.ITERS, device=dev))
-        keys.append(torch.from_numpy(kh.view(np.int16)).to(dev))
-        c_in.append(torch.from_numpy(c0).to(dev))
-        c_out.append(torch.empty(k, device=dev))
-        wt.append(torch.empty(n, device=dev))
-        iters.append(torch.zeros(1, dtype=torch.int32, device=dev))
-        grads.append(torch.from_numpy(g).to(dev))
-        gw.append(torch.empty(n, device=dev))
-        gc.append(torch.empty(k, device=dev))
-    torch.cuda.synchronize()
-
-    def step():
-        edkm.init_unique_batch(plans, keys)
-        edkm.forward_batch(plans, keys, inputs.TAU, 0.0, c_in, c_out, wt, False, iters)
-        edkm.backward_batch(plans, keys, grads, gw, gc)
-
-    for _ in range(args.warmup):
+    from paper_2309_00964_amd import edkm
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-
     hip = HipEvents()
-    ev = {p: [(hip.create(), hip.create()) for _ in range(args.steps)] for p in PASS_IDS}
+    ev = {p: [(hip.create(), hip.create()) for _ in range(steps)] for p in pass_ids}
     t_start, t_stop = hip.create(), hip.create()
     stream = torch.cuda.current_stream().cuda_stream
-    hip.lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
-
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    hip.lib.hipEventRecord(t_start, stream)
-    for s in range(args.steps):
-        for p, pid in PASS_IDS.items():
-            edkm.plan_set_pass_events(plans[0], pid, ev[p][s][0], ev[p][s][1])
+    hip.record(t_start, stream)
+    for s in range(steps):
+        for p, pid in pass_ids.items():
+            edkm.plan_set_pass_events(plan, pid, ev[p][s][0], ev[p][s][1])
         step()
-    hip.lib.hipEventRecord(t_stop, stream)
+    hip.record(t_stop, stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    for pid in PASS_IDS.values():
-        edkm.plan_set_pass_events(plans[0], pid, None, None)
-    gpu_ms = hip.elapsed_ms(t_start, t_stop)
-    elapsed = max(wall, gpu_ms / 1000.0)
+    for pid in pass_ids.values():
+        edkm.plan_set_pass_events(plan, pid, None, None)
+    gpu_s = hip.elapsed_ms(t_start, t_stop) / 1000.0
+    avg = {p: sum(hip.elapsed_ms(a, b) for a, b in ev[p]) / steps for p in pass_ids}
+    for e in [t_start, t_stop] + [x for p in ev for pair in ev[p] for x in pair]:
+        hip.destroy(e)
+    return max(wall, gpu_s), avg
 
+
+def hbm_roofline(avg_ms, total):
+    """Roofline of the dominant N-sized pass (HBM-bound) plus all passes."""
     passes = {}
-    for p in PASS_IDS:
-        d = [hip.elapsed_ms(a, b) for a, b in ev[p]]
-        avg = sum(d) / len(d)
+    for p, ms in avg_ms.items():
         nbytes = PASS_BYTES[p] * total
-        passes[p] = {"avg_us": avg * 1000.0, "bytes": nbytes, "GBps": nbytes / (avg * 1e-3) / 1e9}
+        passes[p] = {"avg_us": ms * 1000.0, "bytes": nbytes, "GBps": nbytes / (ms * 1e-3) / 1e9}
     dom = max(passes, key=lambda p: passes[p]["avg_us"])
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
@@ -163,18 +154,96 @@ def bench(args):
             traffic = tf["kernels"][dom]["bytes_per_launch"]
     n_bytes_all = sum(v["bytes"] for v in passes.values())
     t_all = sum(v["avg_us"] for v in passes.values()) * 1e-6
-    roof = {"bound": "hbm", "kernel": dom, "achieved": passes[dom]["GBps"], "peak": PEAK_HBM_GBS,
+    return {"bound": "hbm", "kernel": dom, "achieved": passes[dom]["GBps"], "peak": PEAK_HBM_GBS,
             "unit": "GB/s", "frac": passes[dom]["GBps"] / PEAK_HBM_GBS, "traffic": traffic,
             "n_pass_total_GBps": n_bytes_all / t_all / 1e9,
             "n_pass_total_frac": n_bytes_all / t_all / 1e9 / PEAK_HBM_GBS,
             "passes": {p: {"avg_us": round(v["avg_us"], 2), "GBps": round(v["GBps"], 1)}
                        for p, v in passes.items()}}
-    for e in [t_start, t_stop] + [x for p in ev for pair in ev[p] for x in pair]:
-        hip.destroy(e)
 
-    out = {
+
+def alu_roofline(avg_ms, n, k):
+    """Roofline of the dominant dense kernel (fp32 VALU-bound): algorithmic
+    fp32 operations per map entry x n*k entries per launch."""
+    kern = {p: {"avg_us": ms * 1000.0,
+                "TFLOPs": DENSE_OPS_PER_ENTRY[p] * n * k / (ms * 1e-3) / 1e12}
+            for p, ms in avg_ms.items()}
+    dom = max(kern, key=lambda p: kern[p]["avg_us"])
+    return {"bound": "alu", "kernel": dom, "achieved": kern[dom]["TFLOPs"], "peak": PEAK_FP32_TFLOPS,
+            "unit": "TFLOP/s", "frac": kern[dom]["TFLOPs"] / PEAK_FP32_TFLOPS, "traffic": None,
+            "ops_per_entry": DENSE_OPS_PER_ENTRY[dom],
+            "kernels": {p: {"avg_us": round(v["avg_us"], 2), "TFLOPs": round(v["TFLOPs"], 2)}
+                        for p, v in kern.items()}}
+
+
+class Matrices:
+    """Device inputs and outputs of a list of (name, rows, cols) matrices, each
+    with its own plan and centroids."""
+
+    def __init__(self, config, mats, bits, outliers=False, on_device=False, keep_host=()):
+        import numpy as np
+        import torch
+        from paper_2309_00964_amd import edkm, inputs
+        dev = torch.device("cuda:0")
+        k = 1 << bits
+        self.names, self.plans, self.keys, self.c_in, self.c_out = [], [], [], [], []
+        self.wt, self.iters, self.grads, self.gw, self.gc, self.host = [], [], [], [], [], []
+        self.total = 0
+        for i, (name, r, c) in enumerate(mats):
+            n = r * c
+            self.total += n
+            if on_device:
+                kt = inputs.fp16_weights_device(n, inputs.weight_seed(config, i), dev, outliers)
+                c0 = inputs.quantile_init_device(kt, k)
+                gt = inputs.upstream_grad_device(n, inputs.grad_seed(config, i), dev)
+                if name in keep_host:
+                    self.host.append((name, kt.cpu().numpy().view(np.uint16), c0.cpu().numpy(),
+                                      gt.cpu().numpy()))
+            else:
+                kh = inputs.fp16_weights(n, inputs.weight_seed(config, i), outliers)
+                c0h = inputs.quantile_init(kh, k)
+                g = inputs.upstream_grad(n, inputs.grad_seed(config, i))
+                if name in keep_host:
+                    self.host.append((name, kh, c0h, g))
+                kt = torch.from_numpy(kh.view(np.int16)).to(dev)
+                c0 = torch.from_numpy(c0h).to(dev)
+                gt = torch.from_numpy(g).to(dev)
+            self.names.append(name)
+            self.plans.append(edkm.Plan(n, bits, inputs.ITERS, device=dev))
+            self.keys.append(kt)
+            self.c_in.append(c0)
+            self.c_out.append(torch.empty(k, device=dev))
+            self.wt.append(torch.empty(n, device=dev))
+            self.iters.append(torch.zeros(1, dtype=torch.int32, device=dev))
+            self.grads.append(gt)
+            self.gw.append(torch.empty(n, device=dev))
+            self.gc.append(torch.empty(k, device=dev))
+        torch.cuda.synchronize()
+
+    def step(self):
+        from paper_2309_00964_amd import edkm, inputs
+        edkm.init_unique_batch(self.plans, self.keys)
+        edkm.forward_batch(self.plans, self.keys, inputs.TAU, 0.0, self.c_in, self.c_out, self.wt,
+                           False, self.iters)
+        edkm.backward_batch(self.plans, self.keys, self.grads, self.gw, self.gc)
+
+    def dense_step(self):
+        from paper_2309_00964_amd import edkm, inputs
+        for i, p in enumerate(self.plans):
+            edkm.forward_dense(p, self.keys[i], inputs.TAU, 0.0, self.c_in[i], self.c_out[i],
+                               self.wt[i], False, self.iters[i])
+            edkm.backward_dense(p, self.keys[i], self.grads[i], self.gw[i], self.gc[i])
+
+
+def result_line(args, workload, m, bits, elapsed, roof, extra_cfg=None):
+    from paper_2309_00964_amd import inputs
+    cfg = {"workload": workload, "matrices": len(m.plans), "weights": m.total, "bits": bits,
+           "k": 1 << bits, "tau": inputs.TAU, "iters": inputs.ITERS, "w_tilde": "fp32",
+           "weights_dtype": "fp16", "parallelism": "single_gpu"}
+    cfg.update(extra_cfg or {})
+    return {
         "metric": METRIC,
-        "value": total * args.steps / elapsed,
+        "value": m.total * args.steps / elapsed,
         "unit": "weights/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -185,15 +254,62 @@ def bench(args):
         "vs_baseline": None,
         "dtype": "fp32",
         "data": "synthetic",
-        "config": {"workload": "llama7b_decoder_layer_3bit", "matrices": len(plans),
-                   "weights": total, "bits": bits, "k": k, "tau": inputs.TAU,
-                   "iters": inputs.ITERS, "w_tilde": "fp32", "weights_dtype": "fp16",
-                   "parallelism": "single_gpu"},
+        "config": cfg,
         "roofline": roof,
     }
+
+
+def bench_decoder_layer(args):
+    """One LLaMA-7B decoder layer at 3 bits: the seven matrices as batched calls."""
+    from paper_2309_00964_amd import inputs
+    bits = 3
+    keep = () if args.no_cpu_baseline else tuple(args.cpu_sample)
+    m = Matrices(4, inputs.WORKLOADS[4]["mats"], bits, keep_host=keep)
+    elapsed, avg = timed(m.step, m.plans[0], PASS_IDS, args.steps, args.warmup)
+    out = result_line(args, "llama7b_decoder_layer_3bit", m, bits, elapsed, hbm_roofline(avg, m.total))
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(host, args.cpu_sample)
-    print(json.dumps(out), flush=True)
+        out["cpu_baseline"] = cpu_baseline(m.host, 1 << bits)
+    return out
+
+
+def bench_mlp_outliers(args):
+    """The 11008x4096 MLP matrix with 0.1% outliers: the uniquified path, and the
+    dense (per-weight map) path timed beside it on the same inputs."""
+    from paper_2309_00964_amd import inputs
+    bits = args.bits or 4
+    w = inputs.WORKLOADS[3]
+    keep = () if args.no_cpu_baseline else ("w",)
+    m = Matrices(3, w["mats"], bits, outliers=True, keep_host=keep)
+    elapsed, avg = timed(m.step, m.plans[0], PASS_IDS, args.steps, args.warmup)
+    out = result_line(args, "llama7b_mlp_11008x4096_outliers_%dbit" % bits, m, bits, elapsed,
+                      hbm_roofline(avg, m.total), {"outliers": inputs.OUTLIER_P})
+    d_el, d_avg = timed(m.dense_step, m.plans[0], DENSE_PASS_IDS, args.steps, args.warmup)
+    out["dense"] = {"value": m.total * args.steps / d_el, "unit": "weights/s",
+                    "ms_per_step": d_el * 1000.0 / args.steps,
+                    "unique_speedup": d_el / elapsed,
+                    "roofline": alu_roofline(d_avg, m.total, 1 << bits)}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(m.host, 1 << bits)
+    return out
+
+
+def bench_stack(args):
+    """A 32-layer stack of decoder-layer shapes (224 matrices, 6.48e9 weights),
+    drawn on the device; one step clusters every matrix forward and backward."""
+    from paper_2309_00964_amd import inputs
+    bits = args.bits or 3
+    w = inputs.WORKLOADS[5]
+    keep = () if args.no_cpu_baseline else ("L0.q_proj",)
+    m = Matrices(5, w["mats"], bits, on_device=True, keep_host=keep)
+    elapsed, avg = timed(m.step, m.plans[0], PASS_IDS, args.steps, args.warmup)
+    # the pass events bracket the first launch group of each step: the first
+    # GROUP matrices (layer 0 and the first projection of layer 1)
+    roof = hbm_roofline(avg, sum(r * c for _, r, c in w["mats"][:GROUP]))
+    roof["note"] = "pass events cover the first launch group (%d matrices) of each step" % GROUP
+    out = result_line(args, "llama7b_32_layer_stack_%dbit" % bits, m, bits, elapsed, roof)
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(m.host, 1 << bits)
+    return out
 
 
 def copy_calibration():
@@ -268,6 +384,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", choices=("decoder_layer", "mlp_outliers", "stack"),
+                    default="decoder_layer")
+    ap.add_argument("--bits", type=int, choices=(2, 3, 4), default=None,
+                    help="mlp_outliers: 3 or 4 (default 4); stack: 2, 3 or 4 (default 3)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", nargs="+", default=[m[0] for m in LLAMA7B_LAYER],
                     help="matrices of the layer the CPU oracle is timed on (default: all seven)")
@@ -281,7 +401,14 @@ def main():
                  % args.gpus)
     if args.copy_calibration:
         return copy_calibration()
-    bench(args)
+    import torch
+    if not torch.cuda.is_available():
+        sys.exit("bench.py needs a GPU")
+    fn = {"decoder_layer": bench_decoder_layer, "mlp_outliers": bench_mlp_outliers,
+          "stack": bench_stack}[args.workload]
+    if args.workload == "decoder_layer" and args.bits not in (None, 3):
+        sys.exit("the decoder-layer workload is 3-bit")
+    print(json.dumps(fn(args)), flush=True)
 
 
 if __name__ == "__main__":

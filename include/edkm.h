@@ -127,8 +127,10 @@ edkm_status edkm_backward(edkm_plan* plan, const uint16_t* w_bits, const float* 
                           float* grad_w, float* grad_c, hipStream_t stream);
 
 /* Batched forms: `count` independent matrices (own plan, keys and outputs;
- * same tau and eps) processed together, with one launch per step for the
- * whole batch.  Arrays are host arrays of `count` entries; entries of the
+ * same tau and eps) processed together.  The batch is cut into launch groups
+ * of up to 8 consecutive matrices with the same bit width, and each step of
+ * the path is one launch per group.  Arrays are host arrays of `count`
+ * entries (count >= 1, any size: groups are formed by the library); entries of the
  * nullable output arrays may be NULL, and the arrays themselves may be NULL.
  * Equivalent to calling the single-matrix form on each. */
 edkm_status edkm_init_unique_batch(int count, edkm_plan* const* plans,
@@ -168,7 +170,12 @@ enum {
     EDKM_PASS_HIST = 0,         /* init_unique: pattern histogram, reads 2 B/weight */
     EDKM_PASS_GATHER_WT = 1,    /* forward: W~ gather, 2 B + 4 B (fp16 out: 2 B) */
     EDKM_PASS_KEYED_GRAD = 2,   /* backward: keyed sum of dL/dW~, 2 B + 4 B */
-    EDKM_PASS_GATHER_GRAD = 3   /* backward: dL/dw gather, 2 B + 4 B + 4 B */
+    EDKM_PASS_GATHER_GRAD = 3,  /* backward: dL/dw gather, 2 B + 4 B + 4 B */
+    /* Dense comparison path: one map evaluation over all N weights, k
+     * exponentials per weight.  A call launches several; the events bracket
+     * the last one of the call. */
+    EDKM_PASS_DENSE_ITER = 4,   /* forward_dense: one centroid iteration, reads 2 B */
+    EDKM_PASS_DENSE_BITER = 5   /* backward_dense: one unrolled iteration, 2 B + 4 B + 4 B */
 };
 /* When set (non-NULL), later calls on this plan record `start` on the stream
  * right before that pass's launch and `stop` right after it; in a batched call

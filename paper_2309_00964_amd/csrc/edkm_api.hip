@@ -4,7 +4,10 @@
 
 #include "../../include/edkm.h"
 #include "edkm_internal.h"
+#include "edkm_partition.h"
 
+#include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstring>
 
@@ -76,28 +79,38 @@ bool plan_ok(const edkm_plan* p) {
     return p && reinterpret_cast<const PlanImpl*>(p)->magic == PLAN_MAGIC;
 }
 
-// Split the N-sized passes of a group over workgroups: about NP_MAX_WG in
-// total, shared in proportion to matrix size, at least one and at most
-// NP_MAX_WG per matrix, each slice a multiple of 8 weights.
-uint32_t partition(BatchArgs& b) {
-    uint64_t total = 0;
-    for (int i = 0; i < b.count; ++i) total += b.m[i].n;
-    uint32_t wg = 0;
-    for (int i = 0; i < b.count; ++i) {
-        MatArgs& M = b.m[i];
-        uint64_t want = (uint64_t)std::llround((double)NP_MAX_WG * (double)M.n / (double)total);
-        const uint64_t cap = (M.n + NP_MIN_CHUNK - 1) / NP_MIN_CHUNK;
-        if (want > cap) want = cap;
-        if (want > (uint64_t)NP_MAX_WG) want = NP_MAX_WG;
-        if (want < 1) want = 1;
-        uint64_t chunk = (M.n + want - 1) / want;
-        chunk = (chunk + 7) & ~7ull;
-        M.chunk = chunk;
-        M.wg_count = (uint32_t)((M.n + chunk - 1) / chunk);
-        M.wg_begin = wg;
-        wg += M.wg_count;
+// Workgroups one N-sized pass may use: one per compute unit of the current
+// device (each workgroup holds a whole CU's LDS, so a larger grid would run a
+// second, nearly empty wave), at most NP_MAX_WG.  Cached per device.
+int np_budget() {
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return NP_MAX_WG;
+    int v = cache[dev].load(std::memory_order_relaxed);
+    if (v == 0) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus < 1)
+            cus = NP_MAX_WG;
+        v = std::min(cus, NP_MAX_WG);
+        cache[dev].store(v, std::memory_order_relaxed);
     }
-    return wg;
+    return v;
+}
+
+// Split the N-sized passes of a group over at most `budget` workgroups
+// (split_passes); the slices go into the matrices' launch arguments.
+uint32_t partition(BatchArgs& b, int budget) {
+    uint64_t n[MAXB], chunk[MAXB];
+    uint32_t cnt[MAXB], beg[MAXB];
+    for (int i = 0; i < b.count; ++i) n[i] = b.m[i].n;
+    const uint32_t grid = split_passes(n, b.count, budget, NP_MIN_CHUNK, chunk, cnt, beg);
+    for (int i = 0; i < b.count; ++i) {
+        b.m[i].chunk = chunk[i];
+        b.m[i].wg_count = cnt[i];
+        b.m[i].wg_begin = beg[i];
+    }
+    return grid;
 }
 
 float tau_s2(float tau) { return (float)(1.4426950408889634 / (double)tau); }
@@ -231,7 +244,7 @@ edkm_status edkm_init_unique_batch(int count, edkm_plan* const* plans,
             vec = vec && aligned16(w_bits[first + i]);
         }
         for (int i = 0; i < cnt; ++i) b.m[i].vec = vec;
-        const uint32_t grid = partition(b);
+        const uint32_t grid = partition(b, np_budget());
         const char* where = "";
         const hipError_t e = launch_init_unique(b, grid, stream, &where, &impl(plans[first])->ev);
         if (e != hipSuccess) return hip_fail(plans, first, cnt, e, where);
@@ -311,7 +324,7 @@ edkm_status edkm_forward_batch(int count, edkm_plan* const* plans, const uint16_
             if (P->max_iter > max_t) max_t = P->max_iter;
         }
         for (int i = 0; i < cnt; ++i) b.m[i].vec = vec;
-        const uint32_t grid = partition(b);
+        const uint32_t grid = partition(b, np_budget());
         const char* where = "";
         const hipError_t e = launch_forward(b, grid, max_t, stream, &where, &impl(plans[first])->ev);
         if (e != hipSuccess) return hip_fail(plans, first, cnt, e, where);
@@ -373,7 +386,7 @@ edkm_status edkm_backward_batch(int count, edkm_plan* const* plans, const uint16
                 if (P->max_iter > max_t) max_t = P->max_iter;
             }
             for (int i = 0; i < b.count; ++i) b.m[i].vec = vec;
-            const uint32_t grid = partition(b);
+            const uint32_t grid = partition(b, np_budget());
             const char* where = "";
             const hipError_t e =
                 launch_backward(b, grid, max_t, stream, &where, &impl(plans[first + i0])->ev);
@@ -415,7 +428,7 @@ edkm_status edkm_forward_dense(edkm_plan* plan, const uint16_t* w_bits, float ta
     if (nwg > (uint64_t)D_WG) nwg = D_WG;
     M.chunk = (P->n + nwg - 1) / nwg;
     const char* where = "";
-    const hipError_t e = launch_forward_dense(b, (uint32_t)nwg, stream, &where);
+    const hipError_t e = launch_forward_dense(b, (uint32_t)nwg, stream, &where, &P->ev);
     if (e != hipSuccess) return hip_fail(&plan, 0, 1, e, where);
     P->stage = DENSE_FORWARD;
     P->keys = w_bits;
@@ -443,7 +456,7 @@ edkm_status edkm_backward_dense(edkm_plan* plan, const uint16_t* w_bits, const f
     if (nwg > (uint64_t)D_WG) nwg = D_WG;
     M.chunk = (P->n + nwg - 1) / nwg;
     const char* where = "";
-    const hipError_t e = launch_backward_dense(b, (uint32_t)nwg, stream, &where);
+    const hipError_t e = launch_backward_dense(b, (uint32_t)nwg, stream, &where, &P->ev);
     if (e != hipSuccess) return hip_fail(&plan, 0, 1, e, where);
     return EDKM_OK;
 }

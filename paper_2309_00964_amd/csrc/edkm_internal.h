@@ -10,7 +10,7 @@ constexpr int FIN_MAGS = 0x7C00;      // magnitudes (low 15 bits) of finite fp16
 constexpr int W4 = 19456;             // magnitudes per sign in a 4-byte LDS window (152 KiB)
 constexpr int W8 = 10232;             // magnitudes per sign in the 8-byte LDS window (<160 KiB)
 constexpr int NP_THREADS = 1024;      // N-pass workgroup size
-constexpr int NP_MAX_WG = 256;        // N-pass workgroups per matrix (one per CU)
+constexpr int NP_MAX_WG = 256;        // N-pass workgroups per launch group, at most (one per CU)
 constexpr int NP_MIN_CHUNK = 16384;   // smallest slice of a matrix given to one workgroup
 constexpr int ROW4 = 2 * W4;          // 32-bit words per N-pass partial row
 constexpr int T_WG = 64;              // table-phase workgroups per matrix (= wave size)
@@ -88,7 +88,8 @@ struct BatchArgs {
 };
 
 // Optional timing events recorded around the N-sized passes (diagnostics).
-enum Pass { PASS_HIST = 0, PASS_GATHER_WT = 1, PASS_KEYED_GRAD = 2, PASS_GATHER_GRAD = 3, NPASS = 4 };
+enum Pass { PASS_HIST = 0, PASS_GATHER_WT = 1, PASS_KEYED_GRAD = 2, PASS_GATHER_GRAD = 3,
+            PASS_DENSE_ITER = 4, PASS_DENSE_BITER = 5, NPASS = 6 };
 struct PassEvents {
     hipEvent_t start[NPASS];
     hipEvent_t stop[NPASS];
@@ -105,7 +106,9 @@ hipError_t launch_forward(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_t
                               const PassEvents* ev = nullptr);
 hipError_t launch_backward(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_t s, const char** where,
                               const PassEvents* ev = nullptr);
-hipError_t launch_forward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where);
-hipError_t launch_backward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where);
+hipError_t launch_forward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where,
+                                const PassEvents* ev = nullptr);
+hipError_t launch_backward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where,
+                                 const PassEvents* ev = nullptr);
 
 }  // namespace edkm

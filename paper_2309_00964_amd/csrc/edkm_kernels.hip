@@ -1260,11 +1260,12 @@ static hipError_t backward_k(BatchArgs& b, uint32_t grid_np, int max_t, hipStrea
 }
 
 template <int K>
-static hipError_t forward_dense_k(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where) {
+static hipError_t forward_dense_k(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where,
+                                  const PassEvents* ev) {
     const int max_t = b.m[0].max_iter;
     for (int t = 1; t <= max_t; ++t) {
         b.t = t;
-        EDKM_LAUNCH("k_dense_iter", k_dense_iter<K>, dim3(nwg), dim3(D_THREADS), b);
+        EDKM_NPASS(PASS_DENSE_ITER, "k_dense_iter", k_dense_iter<K>, dim3(nwg), dim3(D_THREADS), b);
         EDKM_LAUNCH("k_dense_fin", k_dense_fin<K>, dim3(1), dim3(1024), b, (int)nwg);
     }
     EDKM_LAUNCH("k_dense_out", k_dense_out<K>, dim3(nwg), dim3(D_THREADS), b);
@@ -1272,14 +1273,15 @@ static hipError_t forward_dense_k(BatchArgs& b, uint32_t nwg, hipStream_t s, con
 }
 
 template <int K>
-static hipError_t backward_dense_k(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where) {
+static hipError_t backward_dense_k(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where,
+                                   const PassEvents* ev) {
     const int max_t = b.m[0].max_iter;
     EDKM_LAUNCH("k_dense_btop", k_dense_btop<K>, dim3(nwg), dim3(D_THREADS), b);
     b.t = 0;
     EDKM_LAUNCH("k_dense_bfin", k_dense_bfin<K>, dim3(1), dim3(1024), b, (int)nwg);
     for (int t = max_t; t >= 1; --t) {
         b.t = t;
-        EDKM_LAUNCH("k_dense_biter", k_dense_biter<K>, dim3(nwg), dim3(D_THREADS), b);
+        EDKM_NPASS(PASS_DENSE_BITER, "k_dense_biter", k_dense_biter<K>, dim3(nwg), dim3(D_THREADS), b);
         EDKM_LAUNCH("k_dense_bfin", k_dense_bfin<K>, dim3(1), dim3(1024), b, (int)nwg);
     }
     return hipSuccess;
@@ -1318,14 +1320,16 @@ hipError_t launch_backward(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_
     EDKM_DISPATCH_K(b.m[0].k, backward_k, b, grid_np, max_t, s, where, ev);
 }
 
-hipError_t launch_forward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where) {
+hipError_t launch_forward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where,
+                                const PassEvents* ev) {
     (void)hipGetLastError();
-    EDKM_DISPATCH_K(b.m[0].k, forward_dense_k, b, nwg, s, where);
+    EDKM_DISPATCH_K(b.m[0].k, forward_dense_k, b, nwg, s, where, ev);
 }
 
-hipError_t launch_backward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where) {
+hipError_t launch_backward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where,
+                                 const PassEvents* ev) {
     (void)hipGetLastError();
-    EDKM_DISPATCH_K(b.m[0].k, backward_dense_k, b, nwg, s, where);
+    EDKM_DISPATCH_K(b.m[0].k, backward_dense_k, b, nwg, s, where, ev);
 }
 
 static_assert(W4 % NP_THREADS == 0, "merge grid covers the window exactly");

@@ -49,6 +49,7 @@ ERR_STATE = -4
 ERR_HIP = -5
 NKEYS = 65536
 PASS_HIST, PASS_GATHER_WT, PASS_KEYED_GRAD, PASS_GATHER_GRAD = 0, 1, 2, 3
+PASS_DENSE_ITER, PASS_DENSE_BITER = 4, 5
 
 
 class EdkmError(RuntimeError):

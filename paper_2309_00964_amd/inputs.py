@@ -15,7 +15,9 @@ weights are available, so these draws stand in for them):
 * upstream gradient dL/dW~: fp32 draws from N(0, 1).
 
 Generators are numpy PCG64 streams; seeds follow 1000*config + matrix index for
-weights and that plus 500 for gradients.
+weights and that plus 500 for gradients.  The 32-layer stack (6.5e9 weights) is
+drawn on the GPU instead, from torch's device generator with the same seeds and
+the same recipe (``*_device``); a test copies a sampled matrix back to the host.
 """
 from __future__ import annotations
 
@@ -83,3 +85,34 @@ def upstream_grad(n: int, seed: int) -> np.ndarray:
     """dL/dW~ ~ N(0, 1), fp32."""
     rng = np.random.Generator(np.random.PCG64(seed))
     return rng.standard_normal(n, dtype=np.float32)
+
+
+def fp16_weights_device(n: int, seed: int, device, outliers: bool = False):
+    """n fp16 weights as raw bit patterns (torch.int16 on ``device``), drawn by
+    torch's generator on that device (same recipe as fp16_weights)."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    w = torch.randn(n, generator=gen, device=device, dtype=torch.float32)
+    w *= SIGMA
+    if outliers:
+        mask = torch.rand(n, generator=gen, device=device) < OUTLIER_P
+        w[mask] = torch.randn(int(mask.sum()), generator=gen, device=device) * OUTLIER_SIGMA
+    return w.to(torch.float16).view(torch.int16)
+
+
+def quantile_init_device(keys, k: int):
+    """quantile_init for device keys (torch.int16 bit patterns): fp32 on the same device."""
+    import torch
+    n = keys.numel()
+    vals = torch.sort(keys.view(torch.float16).float()).values
+    ranks = torch.tensor([((2 * j + 1) * n) // (2 * k) for j in range(k)], device=keys.device)
+    return vals[ranks].contiguous()
+
+
+def upstream_grad_device(n: int, seed: int, device):
+    """dL/dW~ ~ N(0, 1), fp32, drawn on ``device``."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    return torch.randn(n, generator=gen, device=device, dtype=torch.float32)

@@ -120,3 +120,15 @@ def test_status_strings():
     for s in (0, -1, -2, -3, -4, -5):
         assert edkm.status_str(s) and edkm.status_str(s) != "unknown status"
     assert edkm.status_str(-99) == "unknown status"
+
+
+def test_pass_event_ids_match_header():
+    text = open(HEADER).read()
+    ids = dict((k, int(v)) for k, v in re.findall(r"\bEDKM_(PASS_[A-Z_]+)\s*=\s*(\d+)", text))
+    assert ids == {name: getattr(edkm, name) for name in ids}
+    assert sorted(ids.values()) == list(range(len(ids)))
+    p = _plan()
+    for pid in ids.values():     # NULL events switch the hook off: host only
+        assert lib.edkm_plan_set_pass_events(ctypes.byref(p), pid, None, None) == edkm.OK
+    assert lib.edkm_plan_set_pass_events(ctypes.byref(p), len(ids), None, None) == edkm.ERR_ARG
+    assert lib.edkm_plan_set_pass_events(ctypes.byref(p), -1, None, None) == edkm.ERR_ARG

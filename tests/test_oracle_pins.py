@@ -266,6 +266,27 @@ def test_unit_upstream_gradient_identity(k, eps):
     assert np.max(np.abs(gc)) <= 1e-9 * keys.size
 
 
+@pytest.mark.parametrize("form", ["dense", "table"])
+@pytest.mark.parametrize("k,eps", [(4, 0.0), (8, 0.0), (16, 1e-5)])
+def test_translation_gradient_identity(form, k, eps):
+    """Shifting every weight and every initial centroid by d leaves |w - c| and so
+    every map unchanged, and shifts each C^(t) and every W~_i by exactly d (map
+    rows sum to one).  Hence L(w + d, C^(0) + d) = L + d sum_i g_i and, for any
+    upstream g, sum_i dL/dw_i + sum_j dL/dC^(0)_j = sum_i g_i.  A wrong sign or a
+    dropped term in the centroid path breaks it; the quantile initial centroids
+    sit exactly on weights, so the sgn(0) = 0 convention is exercised too."""
+    mod = dense if form == "dense" else table
+    keys = inputs.fp16_weights(40_000, 90 + k, outliers=True)
+    c0 = inputs.quantile_init(keys, k).astype(np.float64)
+    g = inputs.upstream_grad(keys.size, 91 + k).astype(np.float64)
+    f = mod.forward(keys, c0, 2e-3, 5, eps=eps)
+    gw, gc = mod.backward(keys, f, g)[:2]
+    lhs = gw.sum() + gc.sum()
+    assert abs(lhs - g.sum()) <= 1e-11 * (np.abs(gw).sum() + np.abs(g).sum())
+    # the centroid gradient is not trivially zero here
+    assert np.max(np.abs(gc)) > 1e-3 * np.abs(g).sum() / np.sqrt(keys.size)
+
+
 def test_backward_is_linear_in_upstream_per_key():
     """dL/dw_i = g_i H(key) + R(key): weights sharing a key differ only through g."""
     keys = np.array([0x2000, 0x2000, 0x2000, 0xA400, 0x1800, 0x2000], dtype=np.uint16)
