@@ -163,52 +163,89 @@ __device__ __forceinline__ int np_matrix(const BatchArgs& b) {
     return m;
 }
 
-// Stream a workgroup's share of a matrix.  The matrix is cut into tiles of
-// U x GW x NP_THREADS weights that its workgroups take round-robin, so they
-// sweep HBM together (measured: 10-20% faster than giving each workgroup one
-// contiguous slice).  In a tile a thread loads U groups of GW weights
-// (ld), then computes all U results (cp: table lookups, atomics), then stores
-// them (st); f1 handles single weights: the ragged tail, or everything when the
-// buffers are not 16-byte aligned.
+// Stream a workgroup's share of a matrix.  Full rounds: the matrix is cut into
+// tiles of U x GW x NP_THREADS weights that its workgroups take round-robin, so
+// they sweep HBM together (measured: 10-20% faster than giving each workgroup
+// one contiguous slice).  What is left after the last full round (under one
+// tile per workgroup, plus the short last tile) is split evenly over the
+// workgroups in steps of GW x NP_THREADS, so that no workgroup runs a whole
+// extra tile after the others have finished.  In a tile a thread loads U groups
+// of GW weights (ld), then computes all U results (cp: table lookups,
+// atomics), then stores them (st); f1 handles single weights: the ragged tail,
+// or everything when the buffers are not 16-byte aligned.
 template <int U, int GW>
-__device__ __forceinline__ uint64_t tiles_bound(const MatArgs& M) {   // weights one workgroup handles, at most
-    constexpr uint64_t TILE = (uint64_t)U * GW * NP_THREADS;
-    const uint64_t ntiles = (M.n + TILE - 1) / TILE;
-    return ((ntiles + M.wg_count - 1) / M.wg_count) * TILE + NP_THREADS;
-}
+struct Slice {
+    static constexpr uint64_t STEP = (uint64_t)GW * NP_THREADS;
+    static constexpr uint64_t TILE = U * STEP;
+    uint64_t nvec;     // weights in whole groups of GW
+    uint64_t rounds;   // full rounds of tiles
+    uint64_t rest0;    // first weight after the full rounds
+    uint64_t per;      // steps of the rest per workgroup
+    __device__ __forceinline__ explicit Slice(const MatArgs& M) {
+        const uint64_t a = M.wg_count;
+        nvec = M.n & ~(uint64_t)(GW - 1);
+        rounds = nvec / TILE / a;
+        rest0 = rounds * a * TILE;
+        per = ((nvec - rest0 + STEP - 1) / STEP + a - 1) / a;
+    }
+    // weights one workgroup handles, at most (either path)
+    __device__ __forceinline__ uint64_t bound(const MatArgs& M) const {
+        const uint64_t scalar = (M.n + (uint64_t)M.wg_count * NP_THREADS - 1) /
+                                ((uint64_t)M.wg_count * NP_THREADS) * NP_THREADS;
+        return max(rounds * TILE + per * STEP, scalar) + NP_THREADS;
+    }
+};
 
-template <int U, int GW, class Ld, class Cp, class St, class F1>
+// REV walks the same work in descending order (the rest first, then the rounds
+// from the last), so that the grid sweeps the matrix from its end.
+template <int U, int GW, bool REV = false, class Ld, class Cp, class St, class F1>
 __device__ __forceinline__ void for_slice(const MatArgs& M, uint32_t wl, Ld ld, Cp cp, St st, F1 f1) {
     const uint64_t n = M.n;
+    const uint64_t a = M.wg_count;
     if (!M.vec) {
-        for (uint64_t j = (uint64_t)wl * NP_THREADS + threadIdx.x; j < n; j += (uint64_t)M.wg_count * NP_THREADS)
-            f1(j);
+        for (uint64_t j = (uint64_t)wl * NP_THREADS + threadIdx.x; j < n; j += a * NP_THREADS) f1(j);
         return;
     }
-    constexpr uint64_t STEP = (uint64_t)GW * NP_THREADS;
-    constexpr uint64_t TILE = U * STEP;
-    const uint64_t nvec = n & ~(uint64_t)(GW - 1);
-    const uint64_t stride = (uint64_t)M.wg_count * TILE;
-    for (uint64_t base = (uint64_t)wl * TILE; base < nvec; base += stride) {
-        const uint64_t i0 = base + (uint64_t)GW * threadIdx.x;
-        if (base + TILE <= nvec) {
-            using R = decltype(ld(i0));
-            using O = decltype(cp(ld(i0)));
+    using S = Slice<U, GW>;
+    const S sh(M);
+    using R = decltype(ld(0));
+    using O = decltype(cp(ld(0)));
+    auto round = [&](uint64_t q) {         // this workgroup's full tile of round q
+        const uint64_t i0 = ((uint64_t)wl + q * a) * S::TILE + (uint64_t)GW * threadIdx.x;
+        R r[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) r[u] = ld(i0 + u * S::STEP);
+        __builtin_amdgcn_sched_barrier(0);   // all U loads issue before any use
+        O o[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) o[u] = cp(r[u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u) st(i0 + u * S::STEP, o[u]);
+    };
+    auto rest = [&]() {                    // this workgroup's steps of the rest
+        const uint64_t s0 = sh.rest0 + (uint64_t)wl * sh.per * S::STEP;
+        const uint64_t s1 = min(sh.nvec, s0 + sh.per * S::STEP);
+        for (uint64_t b0 = s0; b0 < s1; b0 += S::TILE) {
+            const uint64_t i0 = b0 + (uint64_t)GW * threadIdx.x;
             R r[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) r[u] = ld(i0 + u * STEP);
-            __builtin_amdgcn_sched_barrier(0);   // all U loads issue before any use
-            O o[U];
+            for (int u = 0; u < U; ++u)
+                if (i0 + u * S::STEP < s1) r[u] = ld(i0 + u * S::STEP);
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int u = 0; u < U; ++u) o[u] = cp(r[u]);
-#pragma unroll
-            for (int u = 0; u < U; ++u) st(i0 + u * STEP, o[u]);
-        } else {
-            for (uint64_t i = i0; i < nvec && i < base + TILE; i += STEP) st(i, cp(ld(i)));
+            for (int u = 0; u < U; ++u)
+                if (i0 + u * S::STEP < s1) st(i0 + u * S::STEP, cp(r[u]));
         }
+    };
+    if (REV) {
+        rest();
+        for (uint64_t q = sh.rounds; q-- > 0;) round(q);
+    } else {
+        for (uint64_t q = 0; q < sh.rounds; ++q) round(q);
+        rest();
     }
-    if (wl == M.wg_count - 1)
-        for (uint64_t j = nvec + threadIdx.x; j < n; j += NP_THREADS) f1(j);
+    if (wl == a - 1)
+        for (uint64_t j = sh.nvec + threadIdx.x; j < n; j += NP_THREADS) f1(j);
 }
 
 struct Nothing {};
@@ -648,12 +685,17 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
         tw[i] = tab[(s << 15) | (lo + i - s * w)];
     }
     __syncthreads();
-    // The two-way lookup compiles to one flat load whose per-lane address is
-    // either the LDS window or the global table.  That measured faster than an
-    // LDS read plus a separately predicated global read, in both gathers.
+    // Lookup: an LDS read at a clamped index, then a global read only for the
+    // lanes outside the window.  With the interleaved tile sweep this measured
+    // as fast as a single flat load that picks either address per lane here,
+    // and faster in the gradient gather, where flat loads compete with the
+    // streaming loads for the vector-memory pipeline.
     auto look = [&](uint32_t key) -> float {
         const uint32_t d = (key & 0x7FFFu) - (uint32_t)lo;
-        return d < (uint32_t)w ? tw[(key >> 15) * w + d] : tab[key];
+        const bool in = d < (uint32_t)w;
+        float v = tw[(key >> 15) * w + (in ? d : 0u)];
+        if (!in) v = tab[key];
+        return v;
     };
     auto look4 = [&](uint32_t k0, uint32_t k1, uint32_t k2, uint32_t k3) {
         return make_float4(look(k0), look(k1), look(k2), look(k3));
@@ -665,7 +707,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
             return (uint32_t)__half_as_ushort(__float2half_rn(a)) |
                    ((uint32_t)__half_as_ushort(__float2half_rn(c)) << 16);
         };
-        for_slice<8, 4>(M, wl,
+        for_slice<8, 4, true>(M, wl,
             [&](uint64_t i) { return Keys4{ld_u2(keys + i)}; },
             [&](const Keys4& r) {
                 const float4 v = look4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16);
@@ -675,7 +717,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
             [&](uint64_t i) { out[i] = __float2half_rn(look(keys[i])); });
     } else {
         float* out = reinterpret_cast<float*>(M.wt);
-        for_slice<8, 4>(M, wl,
+        for_slice<8, 4, true>(M, wl,
             [&](uint64_t i) { return Keys4{ld_u2(keys + i)}; },
             [&](const Keys4& r) {
                 return look4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16);
@@ -719,7 +761,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
         atomicMax(&emax_sh, e);
     }
     __syncthreads();
-    const int bn = 64 - __clzll((unsigned long long)tiles_bound<8, 4>(M) - 1);   // 2^bn >= weights added here
+    const int bn = 64 - __clzll((unsigned long long)Slice<8, 4>(M).bound(M) - 1);   // 2^bn >= weights added here
     const int emax = emax_sh;
     const int S = 181 - bn - emax;               // 2^(emax-126) * 2^S = 2^(55-bn)
     const uint32_t elim = (uint32_t)min(emax + 6, 0xFE);
@@ -786,9 +828,12 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
         hw[i] = HR[(s << 15) | (lo + i - s * w)];
     }
     __syncthreads();
-    auto look = [&](uint32_t key) -> float2 {   // one flat load, as in k_gather_wt
+    auto look = [&](uint32_t key) -> float2 {
         const uint32_t d = (key & 0x7FFFu) - (uint32_t)lo;
-        return d < (uint32_t)w ? hw[(key >> 15) * w + d] : HR[key];
+        const bool in = d < (uint32_t)w;
+        float2 v = hw[(key >> 15) * w + (in ? d : 0u)];
+        if (!in) v = HR[key];
+        return v;
     };
     auto dw4 = [&](uint32_t k0, uint32_t k1, uint32_t k2, uint32_t k3, float4 gv) {
         const float2 h0 = look(k0), h1 = look(k1), h2 = look(k2), h3 = look(k3);
@@ -802,7 +847,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
         const float2 h = look(key);
         return fmaf(gv, h.x, h.y);
     };
-    for_slice<8, 4>(M, wl,
+    for_slice<8, 4, true>(M, wl,
         [&](uint64_t i) { return KeysG4{ld_u2(keys + i), ld_f4(g + i)}; },
         [&](const KeysG4& r) { return dw4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16, r.g); },
         [&](uint64_t i, float4 o) { st_f4(out + i, o); },
