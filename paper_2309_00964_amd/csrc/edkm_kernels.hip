@@ -81,6 +81,24 @@ __device__ __forceinline__ void attn_row(float v, const float (&c)[K], float s2,
     attn_row_sel<K>(v, c, s2, a, c, unused);
 }
 
+// Deviations d_j = C^(T)_j - W~ of one map row a, W~ = sum_j a_j C^(T)_j,
+// written around c1m = C^(T)_m of the nearest centroid m:
+//   d_j = (C_j - c1m) - sum_i a_i (C_i - c1m),   W~ = c1m + sum_i a_i (C_i - c1m).
+// For a nearly one-hot row the d_j are tiny; forming W~ first and subtracting
+// it would leave them with the rounding error of W~ (one ulp of |C|), which
+// the direct derivative -(1/tau) sum_j a_j d_j sgn(v - C^(T-1)_j) multiplies
+// into every dL/dw_i of the pattern.  Returns W~.
+template <int K>
+__device__ __forceinline__ float centroid_dev(const float (&a)[K], const float (&c1)[K], float c1m,
+                                              float (&d)[K]) {
+    float dt = 0.f;
+#pragma unroll
+    for (int j = 0; j < K; ++j) dt = fmaf(a[j], c1[j] - c1m, dt);
+#pragma unroll
+    for (int j = 0; j < K; ++j) d[j] = (c1[j] - c1m) - dt;
+    return c1m + dt;
+}
+
 // Softmax-Jacobian deviations of one table row in the backward:
 //   dev_j = alpha_j - sum_i a_i alpha_i,  alpha_j = gS_j (v - c1_j),
 // written around the reference cm = c1_m (m the nearest centroid) as
@@ -187,12 +205,6 @@ struct Slice {
         rounds = nvec / TILE / a;
         rest0 = rounds * a * TILE;
         per = ((nvec - rest0 + STEP - 1) / STEP + a - 1) / a;
-    }
-    // weights one workgroup handles, at most (either path)
-    __device__ __forceinline__ uint64_t bound(const MatArgs& M) const {
-        const uint64_t scalar = (M.n + (uint64_t)M.wg_count * NP_THREADS - 1) /
-                                ((uint64_t)M.wg_count * NP_THREADS) * NP_THREADS;
-        return max(rounds * TILE + per * STEP, scalar) + NP_THREADS;
     }
 };
 
@@ -394,13 +406,13 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_hist_merge(BatchArgs b) {
     if (s1) atomicAdd(c + 1, s1);
 }
 
-// Keyed-gradient rows (fp32 over the 8-byte window) into G.
-// Grid (2 * W8 / MERGE_THREADS rounded up, NP_MAX_WG / MERGE_ROWS, count).
+// Keyed-gradient rows (fp32 over the 4-byte window) into G.
+// Grid (2 * W4 / MERGE_THREADS, NP_MAX_WG / MERGE_ROWS, count).
 __global__ void __launch_bounds__(MERGE_THREADS) k_grad_merge(BatchArgs b) {
     const MatArgs& M = b.m[blockIdx.z];
     const int r0 = blockIdx.y * MERGE_ROWS;
     const int r1 = min((int)M.wg_count, r0 + MERGE_ROWS);
-    const int w = M.ws.st->w8, lo = M.ws.st->lo8;
+    const int w = M.ws.st->w4, lo = M.ws.st->lo4;
     const int i = blockIdx.x * MERGE_THREADS + threadIdx.x;
     if (r0 >= r1 || i >= 2 * w) return;
     const float* part = reinterpret_cast<const float*>(M.ws.part) + i;
@@ -656,14 +668,12 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
         if (n == 0u) continue;
         if (!key_finite(u)) { M.ws.tab[u] = __builtin_nanf(""); M.ws.H[u] = __builtin_nanf(""); continue; }
         const float v = key_value(u);
-        float a[K];
-        attn_row<K>(v, c0, b.s2, a);
-        float tv = 0.f;
-#pragma unroll
-        for (int j = 0; j < K; ++j) tv = fmaf(a[j], c1[j], tv);
+        float a[K], d[K], c1m;
+        attn_row_sel<K>(v, c0, b.s2, a, c1, c1m);
+        const float tv = centroid_dev<K>(a, c1, c1m, d);
         float h = 0.f;
 #pragma unroll
-        for (int j = 0; j < K; ++j) h = fmaf(a[j] * (c1[j] - tv), sgnf(v - c0[j]), h);
+        for (int j = 0; j < K; ++j) h = fmaf(a[j] * d[j], sgnf(v - c0[j]), h);
         M.ws.tab[u] = tv;
         M.ws.H[u] = -h * b.inv_tau;
     }
@@ -730,48 +740,67 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
 // G_u = sum over weights with pattern u of dL/dW~_i.
 //
 // LDS fp32 atomics run at a fraction of the integer rate on this GPU, so the
-// window sums are kept in 64-bit fixed point: q = round(g 2^S), added with
-// integer LDS atomics.  Each workgroup chooses S from the largest exponent E of
-// a first sample of its own g: every value with exponent <= E + 6 then stays
-// below 2^(61 - b) in magnitude, where the slice holds at most 2^b weights, so
-// no sum can overflow; values above that (and Inf/NaN) are added in fp32 to the
-// global G, as are patterns outside the window.  The resolution is 2^(b - 55)
-// times the sample maximum.  G enters the backward only through the k-vector
-// sums gamma and E over all patterns, where this is far below fp32 rounding.
-// Each workgroup ends by writing its window as one fp32 partial row.
+// window sums are kept in 32-bit fixed point: q = round(g 2^S), added with
+// integer LDS atomics that return the previous value.  Each workgroup chooses S
+// from a first sample of its own g (one value per thread): every value with
+// exponent <= L quantises below 2^30 in magnitude, where L is the sample's
+// largest exponent, or its mean exponent + 8 if that is smaller, plus 2; the
+// resolution is then at least 2^-19 of a value of mean exponent.  Values above
+// that (and Inf/NaN) are added in fp32 to the global G, as are patterns outside
+// the window.  A sum that wraps past the
+// 32-bit range is detected from the returned value and the wrap (exactly
+// +-2^32 quanta) is added to G in fp32, so no sum is ever lost.  G enters the
+// backward only through the k-vector sums gamma and E over all patterns, where
+// this resolution is far below fp32 rounding.  Each workgroup ends by writing
+// its window as one fp32 partial row.
 __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
-    __shared__ unsigned long long acc[2 * W8];
-    __shared__ int emax_sh;
+    __shared__ int acc[2 * W4];
+    __shared__ int emax_sh, esum_sh, ecnt_sh;
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
     const uint32_t wl = blockIdx.x - M.wg_begin;
-    const int lo = M.ws.st->lo8, w = M.ws.st->w8;
+    const int lo = M.ws.st->lo4, w = M.ws.st->w4;
     const uint16_t* keys = M.keys;
     const float* g = M.g;
-    for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) acc[i] = 0ull;
-    if (threadIdx.x == 0) emax_sh = 0;
+    for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) acc[i] = 0;
+    if (threadIdx.x == 0) { emax_sh = 0; esum_sh = 0; ecnt_sh = 0; }
     __syncthreads();
-    {   // sample: one value per thread, spread over the matrix
+    {   // sample: one value per thread, spread over the matrix; exponents of the
+        // normal finite values: largest, sum and count
         const uint64_t i = (((uint64_t)wl * NP_THREADS + threadIdx.x) * 2654435761ull) % M.n;
-        int e = 0;
-        {
-            e = (int)((__float_as_uint(g[i]) >> 23) & 0xFFu);
-            if (e == 0xFF) e = 0;
+        const int e = (int)((__float_as_uint(g[i]) >> 23) & 0xFFu);
+        const bool use = e != 0 && e != 0xFF;
+        int smax = use ? e : 0, ssum = smax, scnt = use ? 1 : 0;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+            smax = max(smax, __shfl_xor(smax, o, 64));
+            ssum += __shfl_xor(ssum, o, 64);
+            scnt += __shfl_xor(scnt, o, 64);
         }
-        atomicMax(&emax_sh, e);
+        if ((threadIdx.x & 63) == 0) {
+            atomicMax(&emax_sh, smax);
+            atomicAdd(&esum_sh, ssum);
+            atomicAdd(&ecnt_sh, scnt);
+        }
     }
     __syncthreads();
-    const int bn = 64 - __clzll((unsigned long long)Slice<8, 4>(M).bound(M) - 1);   // 2^bn >= weights added here
-    const int emax = emax_sh;
-    const int S = 181 - bn - emax;               // 2^(emax-126) * 2^S = 2^(55-bn)
-    const uint32_t elim = (uint32_t)min(emax + 6, 0xFE);
+    // Values with exponent <= elim go to LDS: the sample maximum, but at most
+    // 2^10 above the mean exponent, so that a few huge values in the sample
+    // (they take the fp32 path) cannot coarsen the resolution of the bulk.
+    // Capped so the wrap value 2^(32 - S) stays finite.
+    const int emean = ecnt_sh > 0 ? (esum_sh + ecnt_sh / 2) / ecnt_sh : 0;
+    const int elim = min(min(emax_sh, emean + 8) + 2, 190);
+    const int S = 156 - elim;                    // |g 2^S| < 2^30
+    const float wrap = ldexpf(1.0f, 32 - S);     // one turn of the 32-bit accumulator, as a value
     float* G = M.ws.G;
     auto add = [&](uint32_t key, float gv) {
         const uint32_t d = (key & 0x7FFFu) - (uint32_t)lo;
-        const uint32_t e = (__float_as_uint(gv) >> 23) & 0xFFu;
+        const int e = (int)((__float_as_uint(gv) >> 23) & 0xFFu);
         if (d < (uint32_t)w && e <= elim) {
-            const long long q = __float2ll_rn(ldexpf(gv, S));
-            atomicAdd(&acc[(key >> 15) * w + d], (unsigned long long)q);
+            const int q = __float2int_rn(ldexpf(gv, S));
+            const int old = atomicAdd(&acc[(key >> 15) * w + d], q);
+            const int sum = (int)((uint32_t)old + (uint32_t)q);
+            if (((old ^ sum) & (q ^ sum)) < 0) atomicAdd(&G[key], q > 0 ? wrap : -wrap);
         } else {
             atomicAdd(&G[key], gv);
         }
@@ -787,8 +816,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
         [&](uint64_t i) { add(keys[i], g[i]); });
     __syncthreads();
     float* row = reinterpret_cast<float*>(M.ws.part) + (size_t)wl * ROW4;
-    for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS)
-        row[i] = (float)ldexp((double)(long long)acc[i], -S);
+    for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) row[i] = ldexpf((float)acc[i], -S);
 }
 
 // dL/dw_i = g_i H[bits_i] + R[bits_i]; the window [lo8, lo8 + w8) of (H, R) sits
@@ -867,13 +895,12 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_top(BatchArgs b) {
     __shared__ float c1sh[K], c0sh[K];
     const MatArgs& M = b.m[blockIdx.y];
     uint32_t n4[4];   // per-pattern inputs first: they do not depend on the centroids
-    float G4[4], t4[4];
+    float G4[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int u = table_key(r);
         n4[r] = M.ws.counts[u];
         G4[r] = M.ws.G[u];
-        t4[r] = M.ws.tab[u];
     }
     const DevState* st = M.ws.st;
     const int T = st->teff;
@@ -894,14 +921,14 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_top(BatchArgs b) {
         if (n4[r] == 0u || !key_finite(u)) continue;
         const float G = G4[r];
         const float v = key_value(u);
-        float a[K];
-        attn_row<K>(v, c0, b.s2, a);
-        const float tv = t4[r];
+        float a[K], d[K], c1m;
+        attn_row_sel<K>(v, c0, b.s2, a, c1, c1m);
+        centroid_dev<K>(a, c1, c1m, d);
 #pragma unroll
         for (int j = 0; j < K; ++j) {
             const float ga = G * a[j];
             acc[j] += ga;
-            acc[K + j] = fmaf(ga * (c1[j] - tv), sgnf(v - c0[j]), acc[K + j]);
+            acc[K + j] = fmaf(ga * d[j], sgnf(v - c0[j]), acc[K + j]);
         }
     }
     block_sum<2 * K, T_THREADS>(acc, scratch, tot);
@@ -1159,15 +1186,13 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_btop(BatchArgs b) {
         if (!key_finite(key)) { M.gw[i] = __builtin_nanf(""); continue; }
         const float v = key_value(key);
         const float g = M.g[i];
-        float a[K];
-        attn_row<K>(v, c0, b.s2, a);
-        float tv = 0.f;
-#pragma unroll
-        for (int j = 0; j < K; ++j) tv = fmaf(a[j], c1[j], tv);
+        float a[K], d[K], c1m;
+        attn_row_sel<K>(v, c0, b.s2, a, c1, c1m);
+        centroid_dev<K>(a, c1, c1m, d);
         float h = 0.f;
 #pragma unroll
         for (int j = 0; j < K; ++j) {
-            const float q = a[j] * (c1[j] - tv) * sgnf(v - c0[j]);
+            const float q = a[j] * d[j] * sgnf(v - c0[j]);
             h += q;
             acc[j] = fmaf(g, a[j], acc[j]);
             acc[K + j] = fmaf(g, q, acc[K + j]);
@@ -1293,7 +1318,7 @@ static hipError_t backward_k(BatchArgs& b, uint32_t grid_np, int max_t, hipStrea
     const dim3 tg(T_WG, b.count);
     EDKM_NPASS(PASS_KEYED_GRAD, "k_keyed_grad", k_keyed_grad, dim3(grid_np), dim3(NP_THREADS), b);
     EDKM_LAUNCH("k_grad_merge", k_grad_merge,
-                dim3((2 * W8 + MERGE_THREADS - 1) / MERGE_THREADS, NP_MAX_WG / MERGE_ROWS, b.count),
+                dim3(2 * W4 / MERGE_THREADS, NP_MAX_WG / MERGE_ROWS, b.count),
                 dim3(MERGE_THREADS), b);
     EDKM_LAUNCH("k_bwd_top", k_bwd_top<K>, tg, dim3(T_THREADS), b);
     for (int t = max_t; t >= 1; --t) {

@@ -225,6 +225,44 @@ def test_nonfinite_weights():
     assert_close(res["grad_c"], ref["gc"], TOL_BWD, "grad_c")
 
 
+def test_keyed_sum_wraps_fixed_point_range():
+    """Five patterns repeated over a million weights; dL/dW~ is a small bulk
+    (N(0, 1e-3^2)) with 5% of entries +-0.75.  The fixed-point scale follows
+    the bulk, so each +-0.75 is about 2^29.6 quanta and the per-workgroup sum
+    of every pattern wanders past the 32-bit range in both directions: the wrap
+    (carry) path of the keyed reduction is taken thousands of times.  (Random
+    signs keep dL/dC^(0) well conditioned; with dL/dW~ all positive it is a
+    1e-6 residual of the sums, below what fp32 resolves.)"""
+    vals = np.array([-0.011, -0.004, 0.0005, 0.006, 0.013], dtype=np.float16)
+    n = 1_000_003
+    rng = np.random.default_rng(81)
+    keys = vals.view(np.uint16)[rng.integers(0, vals.size, n)]
+    g = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    big = rng.random(n) < 0.05
+    g[big] = np.where(rng.random(int(big.sum())) < 0.5, -0.75, 0.75).astype(np.float32)
+    c0 = np.array([-0.01, -0.002, 0.004, 0.012], np.float32)
+    say("keyed sum: fixed-point wraps")
+    res = gpu(keys, c0, 2, g=g)
+    check(res, oracle(keys, c0, g, form="table"), what="fixed-point wraps")
+
+
+def test_keyed_sum_heavy_tailed_gradient():
+    """dL/dW~ with rare huge values (1e6 times the bulk), exact zeros and
+    subnormals: the fixed-point scale must follow the bulk, the huge values
+    take the exact fp32 path."""
+    n = 300_007
+    keys = inputs.fp16_weights(n, 82, outliers=True)
+    c0 = inputs.quantile_init(keys, 8)
+    rng = np.random.default_rng(83)
+    g = inputs.upstream_grad(n, 84)
+    g[rng.random(n) < 5e-4] *= np.float32(1e6)
+    g[rng.random(n) < 1e-2] = 0.0
+    g[rng.random(n) < 1e-3] = np.float32(1e-40)
+    say("keyed sum: heavy-tailed gradient")
+    res = gpu(keys, c0, 3, g=g)
+    check(res, oracle(keys, c0, g), what="heavy-tailed g")
+
+
 def test_unit_upstream_gradient_identity():
     """With dL/dW~ = 1 the loss is sum_i w_i whatever the centroids (sum_i W~_i =
     sum_j S_j C_j = sum_j P_j), so dL/dw_i = 1 and dL/dC^(0) = 0."""
