@@ -91,10 +91,14 @@ class HipEvents:
         self.lib.hipEventDestroy(e)
 
 
-def cpu_baseline(samples, k):
-    """The fp64 dense oracle, as it stands, on a bounded sample of the workload:
-    ``samples`` is a list of (name, keys, c0, g) host arrays."""
-    from oracle import dense
+def cpu_baseline(samples, k, table_names=("q_proj", "gate_proj", "w", "L0.q_proj")):
+    """The fp64 oracles, as they stand, on bounded samples of the workload:
+    ``samples`` is a list of (name, keys, c0, g) host arrays.  The headline
+    value is the dense oracle on all host threads over every sample; beside it
+    the same on one thread (first 2^20 weights of the first sample) and the
+    table-form oracle (numpy) on the samples named in ``table_names``."""
+    import numpy as np
+    from oracle import dense, table
     from paper_2309_00964_amd import inputs
     n = 0
     t0 = time.perf_counter()
@@ -103,9 +107,33 @@ def cpu_baseline(samples, k):
         dense.backward(keys, f, g.astype("float64"))
         n += keys.size
     dt = time.perf_counter() - t0
-    return {"value": n / dt, "unit": "weights/s", "cores": dense.threads(), "kind": "oracle",
-            "sample": "fp64 dense DKM forward+backward (%d iterations, k=%d) of %s (%d weights) "
-                      "in %.1f s" % (inputs.ITERS, k, "+".join(s[0] for s in samples), n, dt)}
+    out = {"value": n / dt, "unit": "weights/s", "cores": dense.threads(), "kind": "oracle",
+           "sample": "fp64 dense DKM forward+backward (%d iterations, k=%d) of %s (%d weights) "
+                     "in %.1f s" % (inputs.ITERS, k, "+".join(s[0] for s in samples), n, dt)}
+    name, keys, c0, g = samples[0]
+    m = min(keys.size, 1 << 20)
+    nth = dense.threads()
+    dense.set_threads(1)
+    t0 = time.perf_counter()
+    f = dense.forward(keys[:m], c0.astype("float64"), inputs.TAU, inputs.ITERS)
+    dense.backward(keys[:m], f, g[:m].astype("float64"))
+    dt1 = time.perf_counter() - t0
+    dense.set_threads(nth)
+    out["single_thread"] = {"value": m / dt1, "unit": "weights/s", "cores": 1,
+                            "sample": "the same oracle on the first %d weights of %s in %.1f s"
+                                      % (m, name, dt1)}
+    tab = [x for x in samples if x[0] in table_names] or samples[:1]
+    nt = 0
+    t0 = time.perf_counter()
+    for _, keys, c0, g in tab:
+        f = table.forward(keys, c0.astype(np.float64), inputs.TAU, inputs.ITERS)
+        table.backward(keys, f, g.astype(np.float64))
+        nt += keys.size
+    dt2 = time.perf_counter() - t0
+    out["table_form"] = {"value": nt / dt2, "unit": "weights/s", "kind": "oracle (table form, numpy)",
+                         "sample": "fp64 uniquified DKM forward+backward of %s (%d weights) in %.1f s"
+                                   % ("+".join(x[0] for x in tab), nt, dt2)}
+    return out
 
 
 def timed(step, plan, pass_ids, steps, warmup):

@@ -39,6 +39,8 @@ def _load():
         lib.dkm_decode_fp16.restype = None
         lib.dkm_threads.argtypes = []
         lib.dkm_threads.restype = i32
+        lib.dkm_set_threads.argtypes = [i32]
+        lib.dkm_set_threads.restype = None
         for name in ("dkm_dense_forward", "dkm_dense_forward_f64"):
             fn = getattr(lib, name)
             fn.argtypes = [P, i64, i32, f64, i32, f64, P, P, P, P, P]
@@ -58,6 +60,11 @@ def _ptr(a: np.ndarray):
 def threads() -> int:
     """OpenMP threads the oracle runs on."""
     return int(_load().dkm_threads())
+
+
+def set_threads(n: int) -> None:
+    """OpenMP threads for later calls (results do not depend on it)."""
+    _load().dkm_set_threads(int(n))
 
 
 def fp16_value(h: int) -> float:

@@ -69,6 +69,17 @@ int dkm_threads(void)
 #endif
 }
 
+/* Threads for later calls (timing only: the fixed-block sums make every
+ * result independent of the thread count). */
+void dkm_set_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 static double sgn(double x) { return (x > 0.0) - (x < 0.0); }
 
 /* One row of the attention map: softmax_j(-|v - c_j| / tau). */

@@ -339,3 +339,25 @@ def test_inputs_are_seeded_and_shaped():
     assert np.all(np.isin(c.astype(np.float16).view(np.uint16), a))
     gr = inputs.upstream_grad(1000, 1)
     assert gr.dtype == np.float32
+
+
+def test_dense_oracle_independent_of_thread_count():
+    """Fixed-block sums: the dense oracle gives bitwise the same results on one
+    thread as on all of them (so its timing on any thread count times the same
+    computation)."""
+    keys = inputs.fp16_weights(200_003, 95, outliers=True)
+    c0 = inputs.quantile_init(keys, 8).astype(np.float64)
+    g = inputs.upstream_grad(keys.size, 96).astype(np.float64)
+    nth = dense.threads()
+    f1 = dense.forward(keys, c0, 2e-3, 5)
+    r1 = dense.backward(keys, f1, g)
+    dense.set_threads(1)
+    try:
+        f2 = dense.forward(keys, c0, 2e-3, 5)
+        r2 = dense.backward(keys, f2, g)
+    finally:
+        dense.set_threads(nth)
+    for name in ("c_out", "w_tilde", "c_hist", "s_hist"):
+        np.testing.assert_array_equal(f1[name], f2[name])
+    np.testing.assert_array_equal(r1[0], r2[0])
+    np.testing.assert_array_equal(r1[1], r2[1])
