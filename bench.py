@@ -12,6 +12,8 @@ Output: one JSON line with weights/s, the HBM roofline of the dominant
 N-sized kernel (timed live with HIP events around its launches), and the CPU
 oracle timed on a bounded sample on this host.
 
+Weight format: --key-format fp16 (default) or bf16 (any workload).
+
 Other workloads (--workload; one JSON line each, same fields):
   mlp_outliers [--bits 3|4]   the 11008x4096 MLP matrix with 0.1% outliers; the
                               dense per-weight-map path is timed beside it ("dense")
@@ -91,7 +93,7 @@ class HipEvents:
         self.lib.hipEventDestroy(e)
 
 
-def cpu_baseline(samples, k, table_names=("q_proj", "gate_proj", "w", "L0.q_proj")):
+def cpu_baseline(samples, k, table_names=("q_proj", "gate_proj", "w", "L0.q_proj"), fmt="fp16"):
     """The fp64 oracles, as they stand, on bounded samples of the workload:
     ``samples`` is a list of (name, keys, c0, g) host arrays.  The headline
     value is the dense oracle on all host threads over every sample; beside it
@@ -103,7 +105,7 @@ def cpu_baseline(samples, k, table_names=("q_proj", "gate_proj", "w", "L0.q_proj
     n = 0
     t0 = time.perf_counter()
     for _, keys, c0, g in samples:
-        f = dense.forward(keys, c0.astype("float64"), inputs.TAU, inputs.ITERS)
+        f = dense.forward(keys, c0.astype("float64"), inputs.TAU, inputs.ITERS, fmt=fmt)
         dense.backward(keys, f, g.astype("float64"))
         n += keys.size
     dt = time.perf_counter() - t0
@@ -115,7 +117,7 @@ def cpu_baseline(samples, k, table_names=("q_proj", "gate_proj", "w", "L0.q_proj
     nth = dense.threads()
     dense.set_threads(1)
     t0 = time.perf_counter()
-    f = dense.forward(keys[:m], c0.astype("float64"), inputs.TAU, inputs.ITERS)
+    f = dense.forward(keys[:m], c0.astype("float64"), inputs.TAU, inputs.ITERS, fmt=fmt)
     dense.backward(keys[:m], f, g[:m].astype("float64"))
     dt1 = time.perf_counter() - t0
     dense.set_threads(nth)
@@ -126,7 +128,7 @@ def cpu_baseline(samples, k, table_names=("q_proj", "gate_proj", "w", "L0.q_proj
     nt = 0
     t0 = time.perf_counter()
     for _, keys, c0, g in tab:
-        f = table.forward(keys, c0.astype(np.float64), inputs.TAU, inputs.ITERS)
+        f = table.forward(keys, c0.astype(np.float64), inputs.TAU, inputs.ITERS, fmt=fmt)
         table.backward(keys, f, g.astype(np.float64))
         nt += keys.size
     dt2 = time.perf_counter() - t0
@@ -208,7 +210,7 @@ class Matrices:
     """Device inputs and outputs of a list of (name, rows, cols) matrices, each
     with its own plan and centroids."""
 
-    def __init__(self, config, mats, bits, outliers=False, on_device=False, keep_host=()):
+    def __init__(self, config, mats, bits, outliers=False, on_device=False, keep_host=(), fmt="fp16"):
         import numpy as np
         import torch
         from paper_2309_00964_amd import edkm, inputs
@@ -221,15 +223,15 @@ class Matrices:
             n = r * c
             self.total += n
             if on_device:
-                kt = inputs.fp16_weights_device(n, inputs.weight_seed(config, i), dev, outliers)
-                c0 = inputs.quantile_init_device(kt, k)
+                kt = inputs.fp16_weights_device(n, inputs.weight_seed(config, i), dev, outliers, fmt)
+                c0 = inputs.quantile_init_device(kt, k, fmt)
                 gt = inputs.upstream_grad_device(n, inputs.grad_seed(config, i), dev)
                 if name in keep_host:
                     self.host.append((name, kt.cpu().numpy().view(np.uint16), c0.cpu().numpy(),
                                       gt.cpu().numpy()))
             else:
-                kh = inputs.fp16_weights(n, inputs.weight_seed(config, i), outliers)
-                c0h = inputs.quantile_init(kh, k)
+                kh = inputs.weights(n, inputs.weight_seed(config, i), outliers, fmt)
+                c0h = inputs.quantile_init(kh, k, fmt)
                 g = inputs.upstream_grad(n, inputs.grad_seed(config, i))
                 if name in keep_host:
                     self.host.append((name, kh, c0h, g))
@@ -237,7 +239,7 @@ class Matrices:
                 c0 = torch.from_numpy(c0h).to(dev)
                 gt = torch.from_numpy(g).to(dev)
             self.names.append(name)
-            self.plans.append(edkm.Plan(n, bits, inputs.ITERS, device=dev))
+            self.plans.append(edkm.Plan(n, bits, inputs.ITERS, device=dev, key_format=fmt))
             self.keys.append(kt)
             self.c_in.append(c0)
             self.c_out.append(torch.empty(k, device=dev))
@@ -246,6 +248,7 @@ class Matrices:
             self.grads.append(gt)
             self.gw.append(torch.empty(n, device=dev))
             self.gc.append(torch.empty(k, device=dev))
+        self.fmt = fmt
         torch.cuda.synchronize()
 
     def step(self):
@@ -263,11 +266,15 @@ class Matrices:
             edkm.backward_dense(p, self.keys[i], self.grads[i], self.gw[i], self.gc[i])
 
 
+def _fmt_tag(args):
+    return "" if args.key_format == "fp16" else "_" + args.key_format
+
+
 def result_line(args, workload, m, bits, elapsed, roof, extra_cfg=None):
     from paper_2309_00964_amd import inputs
     cfg = {"workload": workload, "matrices": len(m.plans), "weights": m.total, "bits": bits,
            "k": 1 << bits, "tau": inputs.TAU, "iters": inputs.ITERS, "w_tilde": "fp32",
-           "weights_dtype": "fp16", "parallelism": "single_gpu"}
+           "weights_dtype": m.fmt, "parallelism": "single_gpu"}
     cfg.update(extra_cfg or {})
     return {
         "metric": METRIC,
@@ -292,11 +299,12 @@ def bench_decoder_layer(args):
     from paper_2309_00964_amd import inputs
     bits = 3
     keep = () if args.no_cpu_baseline else tuple(args.cpu_sample)
-    m = Matrices(4, inputs.WORKLOADS[4]["mats"], bits, keep_host=keep)
+    m = Matrices(4, inputs.WORKLOADS[4]["mats"], bits, keep_host=keep, fmt=args.key_format)
     elapsed, avg = timed(m.step, m.plans[0], PASS_IDS, args.steps, args.warmup)
-    out = result_line(args, "llama7b_decoder_layer_3bit", m, bits, elapsed, hbm_roofline(avg, m.total))
+    out = result_line(args, "llama7b_decoder_layer_3bit" + _fmt_tag(args), m, bits, elapsed,
+                      hbm_roofline(avg, m.total))
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(m.host, 1 << bits)
+        out["cpu_baseline"] = cpu_baseline(m.host, 1 << bits, fmt=m.fmt)
     return out
 
 
@@ -307,9 +315,9 @@ def bench_mlp_outliers(args):
     bits = args.bits or 4
     w = inputs.WORKLOADS[3]
     keep = () if args.no_cpu_baseline else ("w",)
-    m = Matrices(3, w["mats"], bits, outliers=True, keep_host=keep)
+    m = Matrices(3, w["mats"], bits, outliers=True, keep_host=keep, fmt=args.key_format)
     elapsed, avg = timed(m.step, m.plans[0], PASS_IDS, args.steps, args.warmup)
-    out = result_line(args, "llama7b_mlp_11008x4096_outliers_%dbit" % bits, m, bits, elapsed,
+    out = result_line(args, "llama7b_mlp_11008x4096_outliers_%dbit%s" % (bits, _fmt_tag(args)), m, bits, elapsed,
                       hbm_roofline(avg, m.total), {"outliers": inputs.OUTLIER_P})
     d_el, d_avg = timed(m.dense_step, m.plans[0], DENSE_PASS_IDS, args.steps, args.warmup)
     out["dense"] = {"value": m.total * args.steps / d_el, "unit": "weights/s",
@@ -317,7 +325,7 @@ def bench_mlp_outliers(args):
                     "unique_speedup": d_el / elapsed,
                     "roofline": alu_roofline(d_avg, m.total, 1 << bits)}
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(m.host, 1 << bits)
+        out["cpu_baseline"] = cpu_baseline(m.host, 1 << bits, fmt=m.fmt)
     return out
 
 
@@ -328,15 +336,15 @@ def bench_stack(args):
     bits = args.bits or 3
     w = inputs.WORKLOADS[5]
     keep = () if args.no_cpu_baseline else ("L0.q_proj",)
-    m = Matrices(5, w["mats"], bits, on_device=True, keep_host=keep)
+    m = Matrices(5, w["mats"], bits, on_device=True, keep_host=keep, fmt=args.key_format)
     elapsed, avg = timed(m.step, m.plans[0], PASS_IDS, args.steps, args.warmup)
     # the pass events bracket the first launch group of each step: the first
     # GROUP matrices (layer 0 and the first projection of layer 1)
     roof = hbm_roofline(avg, sum(r * c for _, r, c in w["mats"][:GROUP]))
     roof["note"] = "pass events cover the first launch group (%d matrices) of each step" % GROUP
-    out = result_line(args, "llama7b_32_layer_stack_%dbit" % bits, m, bits, elapsed, roof)
+    out = result_line(args, "llama7b_32_layer_stack_%dbit%s" % (bits, _fmt_tag(args)), m, bits, elapsed, roof)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(m.host, 1 << bits)
+        out["cpu_baseline"] = cpu_baseline(m.host, 1 << bits, fmt=m.fmt)
     return out
 
 
@@ -416,6 +424,8 @@ def main():
                     default="decoder_layer")
     ap.add_argument("--bits", type=int, choices=(2, 3, 4), default=None,
                     help="mlp_outliers: 3 or 4 (default 4); stack: 2, 3 or 4 (default 3)")
+    ap.add_argument("--key-format", choices=("fp16", "bf16"), default="fp16",
+                    help="weight format (default fp16, the metric's; bf16 is the paper's training format)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", nargs="+", default=[m[0] for m in LLAMA7B_LAYER],
                     help="matrices of the layer the CPU oracle is timed on (default: all seven)")

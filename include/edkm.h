@@ -19,9 +19,11 @@
  *   gathers.
  *
  * Conventions for every entry point:
- *   - Weights are fp16 passed as their raw bit patterns (uint16_t), flat, any
- *     shape (all operations are elementwise in the weight index).  A pattern
- *     is a table key; +0 and -0 are distinct keys of equal value.
+ *   - Weights are 16-bit floats, fp16 (IEEE binary16, the default) or bf16
+ *     (bfloat16, the paper's training format, Sec. 3), chosen per plan and
+ *     passed as their raw bit patterns (uint16_t), flat, any shape (all
+ *     operations are elementwise in the weight index).  A pattern is a table
+ *     key; +0 and -0 are distinct keys of equal value.
  *   - Device pointers are HIP device memory owned by the caller.  The library
  *     allocates nothing and keeps no global state; all calls are asynchronous
  *     on the given stream except where noted.  Pointers need only natural
@@ -74,11 +76,24 @@ typedef struct edkm_plan {
  * It is about 40 MiB and does not grow with n. */
 size_t edkm_workspace_bytes(uint64_t n, int bits, int max_iter);
 
-/* Set up a plan for n (1..EDKM_MAX_N) weights, bits in 1..4, max_iter in
+/* Weight formats. */
+enum {
+    EDKM_KEYS_FP16 = 0,   /* IEEE 754 binary16 */
+    EDKM_KEYS_BF16 = 1    /* bfloat16: the upper half of a binary32 */
+};
+
+/* Set up a plan for n (1..EDKM_MAX_N) fp16 weights, bits in 1..4, max_iter in
  * 1..EDKM_MAX_ITER, with ws a device buffer of ws_bytes >= the size above,
  * 256-byte aligned, used only by this plan.  Host only; no HIP call. */
 edkm_status edkm_plan_init(edkm_plan* plan, uint64_t n, int bits, int max_iter,
                            void* ws, size_t ws_bytes);
+
+/* edkm_plan_init for weights of the given format (EDKM_KEYS_FP16 or
+ * EDKM_KEYS_BF16; anything else is EDKM_ERR_ARG).  The format decides how a
+ * pattern decodes to its value, which patterns are Inf/NaN, and the type of
+ * 16-bit W~ outputs.  Host only; no HIP call. */
+edkm_status edkm_plan_init_ex(edkm_plan* plan, uint64_t n, int bits, int max_iter,
+                              int key_format, void* ws, size_t ws_bytes);
 
 /* Uniquification (Sec. 2.2): counts[u] = #{i : w_bits[i] = u} for all 65,536
  * patterns, kept in the workspace for forward/backward.
@@ -95,7 +110,7 @@ edkm_status edkm_init_unique(edkm_plan* plan, const uint16_t* w_bits,
 
 /* DKM forward on the table (Sec. 2, Sec. 2.2).  For t = 1..T:
  *   a_uj = softmax_j(-|v_u - C^(t-1)_j| / tau) for each occupied pattern u
- *   (v_u its fp16 value), S_j = sum_u n_u a_uj, P_j = sum_u n_u a_uj v_u,
+ *   (v_u its value), S_j = sum_u n_u a_uj, P_j = sum_u n_u a_uj v_u,
  *   C^(t)_j = P_j / S_j (a centroid with S_j = 0 keeps its value).
  * T = max_iter, or the first t with max_j |C^(t)_j - C^(t-1)_j| <= eps when
  * eps > 0.  Output W~_i = sum_j a^(T)_{w_i, j} C^(T)_j, i.e. a gather of the
@@ -104,13 +119,14 @@ edkm_status edkm_init_unique(edkm_plan* plan, const uint16_t* w_bits,
  *   tau        > 0, finite;  eps >= 0 (0: exactly max_iter iterations)
  *   c_in       device float[k]: C^(0)
  *   c_out      device float[k]: C^(T)
- *   w_tilde    device, n outputs: float, or fp16 bits (uint16) if out_fp16 = 1
- *              (round to nearest even)
+ *   w_tilde    device, n outputs: float, or, if out_half = 1, 16-bit floats
+ *              of the plan's weight format (fp16 or bf16 bits, uint16; round to
+ *              nearest even)
  *   iters_out  nullable, device int32[1]: T
  * Arithmetic is fp32 with fixed-order reductions: results are bitwise
  * repeatable.  Saves C^(0..T), S^(1..T) and the table in the workspace. */
 edkm_status edkm_forward(edkm_plan* plan, const uint16_t* w_bits, float tau, float eps,
-                         const float* c_in, float* c_out, void* w_tilde, int out_fp16,
+                         const float* c_in, float* c_out, void* w_tilde, int out_half,
                          int32_t* iters_out, hipStream_t stream);
 
 /* DKM backward (the gradient that autograd of the dense map gives, Sec. 2.2),
@@ -128,11 +144,12 @@ edkm_status edkm_backward(edkm_plan* plan, const uint16_t* w_bits, const float* 
 
 /* Batched forms: `count` independent matrices (own plan, keys and outputs;
  * same tau and eps) processed together.  The batch is cut into launch groups
- * of up to 8 consecutive matrices with the same bit width, and each step of
- * the path is one launch per group.  Arrays are host arrays of `count`
- * entries (count >= 1, any size: groups are formed by the library); entries of the
- * nullable output arrays may be NULL, and the arrays themselves may be NULL.
- * Equivalent to calling the single-matrix form on each. */
+ * of up to 8 consecutive matrices with the same bit width and weight format,
+ * and each step of the path is one launch per group.  Arrays are host arrays
+ * of `count` entries (count >= 1, any size: groups are formed by the
+ * library); entries of the nullable output arrays may be NULL, and the arrays
+ * themselves may be NULL.  Equivalent to calling the single-matrix form on
+ * each. */
 edkm_status edkm_init_unique_batch(int count, edkm_plan* const* plans,
                                    const uint16_t* const* w_bits,
                                    uint32_t* const* counts_out,
@@ -141,7 +158,7 @@ edkm_status edkm_init_unique_batch(int count, edkm_plan* const* plans,
 edkm_status edkm_forward_batch(int count, edkm_plan* const* plans,
                                const uint16_t* const* w_bits, float tau, float eps,
                                const float* const* c_in, float* const* c_out,
-                               void* const* w_tilde, int out_fp16,
+                               void* const* w_tilde, int out_half,
                                int32_t* const* iters_out, hipStream_t stream);
 edkm_status edkm_backward_batch(int count, edkm_plan* const* plans,
                                 const uint16_t* const* w_bits,
@@ -155,7 +172,7 @@ edkm_status edkm_backward_batch(int count, edkm_plan* const* plans,
  * edkm_forward; needs no init_unique.  attn_out (nullable, device
  * float[n * k], row-major) receives the final map A^(T). */
 edkm_status edkm_forward_dense(edkm_plan* plan, const uint16_t* w_bits, float tau, float eps,
-                               const float* c_in, float* c_out, void* w_tilde, int out_fp16,
+                               const float* c_in, float* c_out, void* w_tilde, int out_half,
                                int32_t* iters_out, float* attn_out, hipStream_t stream);
 
 /* Backward of edkm_forward_dense, same contract as edkm_backward
@@ -168,7 +185,7 @@ edkm_status edkm_backward_dense(edkm_plan* plan, const uint16_t* w_bits,
  * call (per launch group in the batched forms): */
 enum {
     EDKM_PASS_HIST = 0,         /* init_unique: pattern histogram, reads 2 B/weight */
-    EDKM_PASS_GATHER_WT = 1,    /* forward: W~ gather, 2 B + 4 B (fp16 out: 2 B) */
+    EDKM_PASS_GATHER_WT = 1,    /* forward: W~ gather, 2 B + 4 B (16-bit out: 2 B) */
     EDKM_PASS_KEYED_GRAD = 2,   /* backward: keyed sum of dL/dW~, 2 B + 4 B */
     EDKM_PASS_GATHER_GRAD = 3,  /* backward: dL/dw gather, 2 B + 4 B + 4 B */
     /* Dense comparison path: one map evaluation over all N weights, k
@@ -183,6 +200,20 @@ enum {
  * the events (created with timing enabled) and reads them with
  * hipEventElapsedTime.  NULL events switch the hook off.  Host only. */
 edkm_status edkm_plan_set_pass_events(edkm_plan* plan, int pass, hipEvent_t start, hipEvent_t stop);
+
+/* Keyed-gradient accumulators (the backward's keyed reduction).  AUTO, the
+ * default, chooses per matrix at init_unique from how concentrated the
+ * weight patterns are: 32-bit fixed point with returning LDS atomics when few
+ * lanes of an atomic share a pattern (fp16 weights), 64-bit fixed point with
+ * plain atomics when many do (bf16 weights, low-entropy data).  Both are exact
+ * in the sense that no sum is lost; they differ in speed and in the last bits.
+ * The setting takes effect at the next init_unique on this plan.  Host only. */
+enum {
+    EDKM_KEYED_AUTO = -1,
+    EDKM_KEYED_I32 = 0,
+    EDKM_KEYED_U64 = 1
+};
+edkm_status edkm_plan_set_keyed_mode(edkm_plan* plan, int mode);
 
 /* Diagnostics for the last EDKM_ERR_HIP returned on this plan: the HIP error
  * code (0 if none), the launch or runtime call that failed, and the HIP

@@ -37,6 +37,10 @@ def _load():
         lib.dkm_fp16_value.restype = f64
         lib.dkm_decode_fp16.argtypes = [P, i64, P]
         lib.dkm_decode_fp16.restype = None
+        lib.dkm_bf16_value.argtypes = [ctypes.c_uint16]
+        lib.dkm_bf16_value.restype = f64
+        lib.dkm_decode_bf16.argtypes = [P, i64, P]
+        lib.dkm_decode_bf16.restype = None
         lib.dkm_threads.argtypes = []
         lib.dkm_threads.restype = i32
         lib.dkm_set_threads.argtypes = [i32]
@@ -79,24 +83,45 @@ def decode_fp16(keys: np.ndarray) -> np.ndarray:
     return out
 
 
+def bf16_value(h: int) -> float:
+    """Real value of one bfloat16 bit pattern (by the format's definition)."""
+    return float(_load().dkm_bf16_value(int(h) & 0xFFFF))
+
+
+def decode_bf16(keys: np.ndarray) -> np.ndarray:
+    keys = np.ascontiguousarray(keys, dtype=np.uint16)
+    out = np.empty(keys.shape, dtype=np.float64)
+    _load().dkm_decode_bf16(_ptr(keys), keys.size, _ptr(out))
+    return out
+
+
+def _values(x: np.ndarray, fmt: str):
+    """(array, keyed?) for the C entry points: fp16 patterns go to the keyed
+    entry points, bf16 patterns are decoded here, values pass through."""
+    if x.dtype == np.uint16:
+        if fmt == "fp16":
+            return np.ascontiguousarray(x).ravel(), True
+        if fmt == "bf16":
+            return decode_bf16(x).ravel(), False
+        raise ValueError("fmt must be 'fp16' or 'bf16'")
+    return np.ascontiguousarray(x, dtype=np.float64).ravel(), False
+
+
 def forward(x: np.ndarray, c0, tau: float, max_iter: int, eps: float = 0.0,
-            want_attn: bool = False) -> dict:
+            want_attn: bool = False, fmt: str = "fp16") -> dict:
     """Dense DKM forward.
 
-    ``x`` is either raw fp16 bit patterns (uint16) or real values (float64;
-    used by the finite-difference tests).  Returns a dict with ``T`` (iterations
-    executed), ``c_hist`` ((max_iter+1) x k; rows 0..T valid), ``s_hist``,
-    ``c_out`` (= C^(T)), ``w_tilde`` (N) and optionally ``attn`` (A^(T), N x k).
+    ``x`` is either raw 16-bit patterns (uint16; fp16 or, with ``fmt="bf16"``,
+    bfloat16) or real values (float64; used by the finite-difference tests).
+    Returns a dict with ``T`` (iterations executed), ``c_hist`` ((max_iter+1) x
+    k; rows 0..T valid), ``s_hist``, ``c_out`` (= C^(T)), ``w_tilde`` (N) and
+    optionally ``attn`` (A^(T), N x k).
     """
     lib = _load()
     c0 = np.ascontiguousarray(c0, dtype=np.float64).ravel()
     k = c0.size
-    if x.dtype == np.uint16:
-        xs = np.ascontiguousarray(x).ravel()
-        fn = lib.dkm_dense_forward
-    else:
-        xs = np.ascontiguousarray(x, dtype=np.float64).ravel()
-        fn = lib.dkm_dense_forward_f64
+    xs, keyed = _values(x, fmt)
+    fn = lib.dkm_dense_forward if keyed else lib.dkm_dense_forward_f64
     n = xs.size
     c_hist = np.zeros((max_iter + 1, k))
     s_hist = np.zeros((max_iter + 1, k))
@@ -107,7 +132,7 @@ def forward(x: np.ndarray, c0, tau: float, max_iter: int, eps: float = 0.0,
     if T < 1:
         raise ValueError("dense oracle rejected its arguments (status %d)" % T)
     out = dict(T=T, c_hist=c_hist, s_hist=s_hist, c_out=c_hist[T].copy(), w_tilde=w,
-               tau=float(tau), k=k)
+               tau=float(tau), k=k, fmt=fmt)
     if want_attn:
         out["attn"] = attn
     return out
@@ -116,12 +141,8 @@ def forward(x: np.ndarray, c0, tau: float, max_iter: int, eps: float = 0.0,
 def backward(x: np.ndarray, fwd: dict, g: np.ndarray):
     """Dense DKM backward of L = sum_i g_i W~_i.  Returns (dL/dw, dL/dC^(0))."""
     lib = _load()
-    if x.dtype == np.uint16:
-        xs = np.ascontiguousarray(x).ravel()
-        fn = lib.dkm_dense_backward
-    else:
-        xs = np.ascontiguousarray(x, dtype=np.float64).ravel()
-        fn = lib.dkm_dense_backward_f64
+    xs, keyed = _values(x, fwd.get("fmt", "fp16"))
+    fn = lib.dkm_dense_backward if keyed else lib.dkm_dense_backward_f64
     n = xs.size
     gg = np.ascontiguousarray(g, dtype=np.float64).ravel()
     assert gg.size == n

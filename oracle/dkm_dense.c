@@ -10,7 +10,9 @@
  * uniquification reproduces exactly because equal 16-bit patterns give equal
  * attention rows):
  *
- *   v_i          = the real value of the i-th fp16 weight (IEEE 754 binary16)
+ *   v_i          = the real value of the i-th weight: an fp16 (IEEE 754
+ *                  binary16) pattern for the keyed entry points; bf16 patterns
+ *                  are decoded by dkm_decode_bf16 and passed as values
  *   for t = 1..T:
  *     D_ij       = -|v_i - C^(t-1)_j| / tau
  *     A^(t)_ij   = exp(D_ij) / sum_m exp(D_im)          (softmax over centroids)
@@ -58,6 +60,29 @@ double dkm_fp16_value(uint16_t h)
 void dkm_decode_fp16(const uint16_t* keys, int64_t n, double* out)
 {
     for (int64_t i = 0; i < n; ++i) out[i] = dkm_fp16_value(keys[i]);
+}
+
+/* bfloat16 -> double, by its definition: 1 sign, 8 exponent (bias 127) and 7
+ * mantissa bits (the upper half of an IEEE 754 binary32); exact for every
+ * pattern. */
+double dkm_bf16_value(uint16_t h)
+{
+    int sign = (h >> 15) & 1;
+    int e = (h >> 7) & 0xFF;
+    int m = h & 0x7F;
+    double mag;
+    if (e == 0)
+        mag = ldexp((double)m, -133);              /* subnormal: m * 2^-126 * 2^-7 */
+    else if (e == 0xFF)
+        mag = m ? NAN : INFINITY;
+    else
+        mag = ldexp((double)(m + 128), e - 134);   /* (1 + m/128) * 2^(e-127) */
+    return sign ? -mag : mag;
+}
+
+void dkm_decode_bf16(const uint16_t* keys, int64_t n, double* out)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = dkm_bf16_value(keys[i]);
 }
 
 int dkm_threads(void)

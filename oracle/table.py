@@ -13,8 +13,9 @@ This module computes exactly what ``dense`` computes, grouped by key.  In exact
 arithmetic the two agree; the tests pin this module to ``dense`` (<= 1e-12
 relative) before it is trusted at sizes the dense oracle cannot finish.
 
-The fp16 decode here goes through numpy's float16 type, independently of the C
-oracle's bit-level decode.
+The decode here goes through numpy's own types (float16 for fp16 patterns, the
+upper half of a float32 for bf16 ones), independently of the C oracle's
+bit-level decode.
 """
 from __future__ import annotations
 
@@ -36,8 +37,13 @@ def unique_keys(keys: np.ndarray):
     return u, inv.astype(np.uint32)
 
 
-def key_values(u: np.ndarray) -> np.ndarray:
-    return np.asarray(u, dtype=np.uint16).view(np.float16).astype(np.float64)
+def key_values(u: np.ndarray, fmt: str = "fp16") -> np.ndarray:
+    u = np.asarray(u, dtype=np.uint16)
+    if fmt == "fp16":
+        return u.view(np.float16).astype(np.float64)
+    if fmt == "bf16":
+        return (u.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    raise ValueError("fmt must be 'fp16' or 'bf16'")
 
 
 def _softmax_rows(v: np.ndarray, c: np.ndarray, tau: float) -> np.ndarray:
@@ -48,15 +54,16 @@ def _softmax_rows(v: np.ndarray, c: np.ndarray, tau: float) -> np.ndarray:
 
 
 def forward(keys: np.ndarray, c0, tau: float, max_iter: int, eps: float = 0.0,
-            counts: np.ndarray | None = None) -> dict:
+            counts: np.ndarray | None = None, fmt: str = "fp16") -> dict:
     """Table-form DKM forward.  Same outputs as ``dense.forward`` plus the
-    per-key tables (``u``, ``n_u``, ``tab``)."""
+    per-key tables (``u``, ``n_u``, ``tab``).  ``fmt`` says how the 16-bit
+    patterns decode ("fp16" or "bf16")."""
     keys = np.asarray(keys, dtype=np.uint16).ravel()
     if counts is None:
         counts = histogram(keys)
     u = np.flatnonzero(counts)
     n_u = counts[u].astype(np.float64)
-    v = key_values(u)
+    v = key_values(u, fmt)
     c0 = np.asarray(c0, dtype=np.float64).ravel()
     k = c0.size
     c_hist = np.zeros((max_iter + 1, k))

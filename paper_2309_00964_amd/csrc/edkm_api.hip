@@ -22,6 +22,8 @@ struct PlanImpl {
     uint64_t magic;
     uint64_t n;
     int32_t bits, k, max_iter, stage;
+    int32_t fmt;             // FMT_FP16 or FMT_BF16
+    int32_t kforce;          // EDKM_KEYED_AUTO, _I32 or _U64
     void* ws;
     size_t ws_bytes;
     const uint16_t* keys;   // key buffer of the current sequence
@@ -32,6 +34,8 @@ struct PlanImpl {
     PassEvents ev;           // caller's timing events (diagnostics), null when unset
 };
 static_assert(sizeof(PlanImpl) <= sizeof(edkm_plan), "edkm_plan too small");
+static_assert(EDKM_KEYS_FP16 != EDKM_KEYS_BF16, "key formats");
+static_assert(EDKM_KEYED_I32 == KEYED_I32 && EDKM_KEYED_U64 == KEYED_U64, "keyed-sum modes");
 static_assert(EDKM_PASS_HIST == PASS_HIST && EDKM_PASS_GATHER_WT == PASS_GATHER_WT &&
                   EDKM_PASS_KEYED_GRAD == PASS_KEYED_GRAD && EDKM_PASS_GATHER_GRAD == PASS_GATHER_GRAD,
               "pass ids");
@@ -66,7 +70,7 @@ Layout layout(int max_iter) {
     L.bpart = take(tp);
     L.dpart = take((size_t)D_WG * PSTRIDE * sizeof(float));
     L.span = take(NP_MAX_WG * sizeof(int2));
-    L.wscan = take(FIN_MAGS * sizeof(uint32_t));
+    L.wscan = take(MAGS * sizeof(uint32_t));
     L.wstat = take(32 * 8 * sizeof(int));
     L.part = take((size_t)NP_MAX_WG * ROW4 * sizeof(uint32_t));
     L.total = o;
@@ -161,6 +165,8 @@ void fill_mat(MatArgs& M, const PlanImpl* P, const uint16_t* keys) {
     M.n = P->n;
     M.k = P->k;
     M.max_iter = P->max_iter;
+    M.fmt = P->fmt;
+    M.kforce = P->kforce;
     M.ws = carve_workspace(P->ws, P->max_iter);
 }
 
@@ -178,13 +184,16 @@ edkm_status check_batch(int count, edkm_plan* const* plans, const uint16_t* cons
 bool tau_ok(float tau) { return std::isfinite(tau) && tau > 0.f && std::isfinite(1.0f / tau); }
 bool eps_ok(float eps) { return std::isfinite(eps) && eps >= 0.f; }
 
-// Launch groups: consecutive matrices with the same k, at most MAXB each.
+// Launch groups: consecutive matrices with the same k and weight format, at
+// most MAXB each.
 template <class Fn>
 edkm_status for_groups(int count, edkm_plan* const* plans, Fn fn) {
     int i = 0;
     while (i < count) {
         int j = i + 1;
-        while (j < count && j - i < MAXB && impl(plans[j])->k == impl(plans[i])->k) ++j;
+        while (j < count && j - i < MAXB && impl(plans[j])->k == impl(plans[i])->k &&
+               impl(plans[j])->fmt == impl(plans[i])->fmt)
+            ++j;
         edkm_status st = fn(i, j - i);
         if (st != EDKM_OK) return st;
         i = j;
@@ -208,7 +217,12 @@ size_t edkm_workspace_bytes(uint64_t n, int bits, int max_iter) {
 
 edkm_status edkm_plan_init(edkm_plan* plan, uint64_t n, int bits, int max_iter, void* ws,
                            size_t ws_bytes) {
-    if (!plan) return EDKM_ERR_ARG;
+    return edkm_plan_init_ex(plan, n, bits, max_iter, EDKM_KEYS_FP16, ws, ws_bytes);
+}
+
+edkm_status edkm_plan_init_ex(edkm_plan* plan, uint64_t n, int bits, int max_iter, int key_format,
+                              void* ws, size_t ws_bytes) {
+    if (!plan || (key_format != EDKM_KEYS_FP16 && key_format != EDKM_KEYS_BF16)) return EDKM_ERR_ARG;
     const size_t need = edkm_workspace_bytes(n, bits, max_iter);
     if (need == 0) return EDKM_ERR_ARG;
     if (!ws || ws_bytes < need || ((uintptr_t)ws & 255u)) return EDKM_ERR_WORKSPACE;
@@ -218,6 +232,8 @@ edkm_status edkm_plan_init(edkm_plan* plan, uint64_t n, int bits, int max_iter, 
     P->bits = bits;
     P->k = 1 << bits;
     P->max_iter = max_iter;
+    P->fmt = key_format == EDKM_KEYS_BF16 ? FMT_BF16 : FMT_FP16;
+    P->kforce = EDKM_KEYED_AUTO;
     P->ws = ws;
     P->ws_bytes = ws_bytes;
     P->stage = PLANNED;
@@ -287,12 +303,12 @@ edkm_status edkm_init_unique(edkm_plan* plan, const uint16_t* w_bits, uint32_t* 
 
 edkm_status edkm_forward_batch(int count, edkm_plan* const* plans, const uint16_t* const* w_bits,
                                float tau, float eps, const float* const* c_in,
-                               float* const* c_out, void* const* w_tilde, int out_fp16,
+                               float* const* c_out, void* const* w_tilde, int out_half,
                                int32_t* const* iters_out, hipStream_t stream) {
     edkm_status st = check_batch(count, plans, w_bits);
     if (st != EDKM_OK) return st;
     if (!tau_ok(tau) || !eps_ok(eps) || !c_in || !c_out || !w_tilde ||
-        (out_fp16 != 0 && out_fp16 != 1))
+        (out_half != 0 && out_half != 1))
         return EDKM_ERR_ARG;
     for (int i = 0; i < count; ++i)
         if (!c_in[i] || !c_out[i] || !w_tilde[i]) return EDKM_ERR_ARG;
@@ -305,7 +321,7 @@ edkm_status edkm_forward_batch(int count, edkm_plan* const* plans, const uint16_
         BatchArgs b;
         std::memset(&b, 0, sizeof(b));
         b.count = cnt;
-        b.out_fp16 = out_fp16;
+        b.out_half = out_half;
         b.s2 = tau_s2(tau);
         b.inv_tau = 1.0f / tau;
         b.eps = eps;
@@ -341,9 +357,9 @@ edkm_status edkm_forward_batch(int count, edkm_plan* const* plans, const uint16_
 }
 
 edkm_status edkm_forward(edkm_plan* plan, const uint16_t* w_bits, float tau, float eps,
-                         const float* c_in, float* c_out, void* w_tilde, int out_fp16,
+                         const float* c_in, float* c_out, void* w_tilde, int out_half,
                          int32_t* iters_out, hipStream_t stream) {
-    return edkm_forward_batch(1, &plan, &w_bits, tau, eps, &c_in, &c_out, &w_tilde, out_fp16,
+    return edkm_forward_batch(1, &plan, &w_bits, tau, eps, &c_in, &c_out, &w_tilde, out_half,
                               &iters_out, stream);
 }
 
@@ -404,16 +420,16 @@ edkm_status edkm_backward(edkm_plan* plan, const uint16_t* w_bits, const float* 
 }
 
 edkm_status edkm_forward_dense(edkm_plan* plan, const uint16_t* w_bits, float tau, float eps,
-                               const float* c_in, float* c_out, void* w_tilde, int out_fp16,
+                               const float* c_in, float* c_out, void* w_tilde, int out_half,
                                int32_t* iters_out, float* attn_out, hipStream_t stream) {
     if (!plan_ok(plan) || !w_bits || !tau_ok(tau) || !eps_ok(eps) || !c_in || !c_out ||
-        !w_tilde || (out_fp16 != 0 && out_fp16 != 1))
+        !w_tilde || (out_half != 0 && out_half != 1))
         return EDKM_ERR_ARG;
     PlanImpl* P = impl(plan);
     BatchArgs b;
     std::memset(&b, 0, sizeof(b));
     b.count = 1;
-    b.out_fp16 = out_fp16;
+    b.out_half = out_half;
     b.s2 = tau_s2(tau);
     b.inv_tau = 1.0f / tau;
     b.eps = eps;
@@ -466,6 +482,12 @@ edkm_status edkm_plan_set_pass_events(edkm_plan* plan, int pass, hipEvent_t star
     PlanImpl* P = impl(plan);
     P->ev.start[pass] = start;
     P->ev.stop[pass] = stop;
+    return EDKM_OK;
+}
+
+edkm_status edkm_plan_set_keyed_mode(edkm_plan* plan, int mode) {
+    if (!plan_ok(plan) || mode < EDKM_KEYED_AUTO || mode > EDKM_KEYED_U64) return EDKM_ERR_ARG;
+    impl(plan)->kforce = mode;
     return EDKM_OK;
 }
 

@@ -6,7 +6,12 @@
 namespace edkm {
 
 constexpr int NKEYS = 65536;          // every 16-bit pattern
-constexpr int FIN_MAGS = 0x7C00;      // magnitudes (low 15 bits) of finite fp16 values
+constexpr int MAGS = 0x8000;          // magnitudes (low 15 bits) of a 16-bit pattern
+// Weight formats (the key is the raw 16-bit pattern either way).
+constexpr int FMT_FP16 = 0;           // IEEE binary16: 5 exponent, 10 mantissa bits
+constexpr int FMT_BF16 = 1;           // bfloat16: 8 exponent, 7 mantissa bits
+// Magnitudes below this are finite in the format (above: Inf/NaN).
+__host__ __device__ constexpr int fin_mags(int fmt) { return fmt == FMT_BF16 ? 0x7F80 : 0x7C00; }
 constexpr int W4 = 19456;             // magnitudes per sign in a 4-byte LDS window (152 KiB)
 constexpr int W8 = 10232;             // magnitudes per sign in the 8-byte LDS window (<160 KiB)
 constexpr int NP_THREADS = 1024;      // N-pass workgroup size
@@ -30,7 +35,8 @@ struct DevState {
     int lo4, w4;         // 4-byte table window: magnitudes [lo4, lo4 + w4), both signs
     int lo8, w8;         // 8-byte table window
     int mlo, mhi;        // occupied finite magnitude range
-    int pad[6];
+    int kmode;           // keyed-sum accumulators: KEYED_I32 or KEYED_U64 (chosen by k_window)
+    int pad[5];
 };
 
 // Device pointers into one plan's workspace.
@@ -49,11 +55,18 @@ struct Ws {
     float* bpart;       // [(max_iter+1) * T_WG * PSTRIDE]  backward table partials
     float* dpart;       // [D_WG * PSTRIDE]  dense-path partials
     int2* span;         // [NP_MAX_WG]  histogram partial spans
-    uint32_t* wscan;    // [FIN_MAGS]  block-local running counts (window selection)
+    uint32_t* wscan;    // [MAGS]  block-local running counts (window selection)
     int* wstat;         // [32 * 8]  per-block totals and ranges (window selection)
     uint32_t* part;     // [NP_MAX_WG * ROW4]  N-pass partial rows
     DevState* st;
 };
+
+// Keyed-sum accumulator modes (see k_keyed_grad).
+constexpr int KEYED_I32 = 0;          // 32-bit, returning atomics, 4-byte window
+constexpr int KEYED_U64 = 1;          // 64-bit, plain atomics, 8-byte window
+// Switch to KEYED_U64 above this expected number of other lanes sharing an
+// address per 64-lane atomic, 2016 sum_u (n_u / N)^2.
+constexpr double KEYED_U64_ABOVE = 0.6;
 
 // Everything a kernel needs about one matrix.
 struct MatArgs {
@@ -75,12 +88,14 @@ struct MatArgs {
     uint32_t wg_count;        // N-pass workgroups (= partial rows)
     uint64_t chunk;           // weights per N-pass workgroup (multiple of 8)
     int vec;                  // all N-sized buffers 16-byte aligned
+    int fmt;                  // FMT_FP16 or FMT_BF16 (the same within a launch group)
+    int kforce;               // keyed-sum mode forced by the caller, or -1 (chosen from the data)
 };
 
 struct BatchArgs {
     int count;
     int t;                    // iteration index of a per-iteration launch
-    int out_fp16;
+    int out_half;             // W~ as 16-bit floats of the weight format
     float s2;                 // log2(e) / tau
     float inv_tau;
     float eps;

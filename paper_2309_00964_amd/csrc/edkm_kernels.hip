@@ -27,16 +27,30 @@ namespace edkm {
 // ----------------------------------------------------------------------------
 // small device helpers
 
-// fp16 bit pattern -> fp32, exact for finite values including subnormals
-// (integer decode, independent of the denormal mode).
-__device__ __forceinline__ float key_value(uint32_t h) {
+// 16-bit pattern -> fp32, exact for finite values including subnormals.
+// fp16: integer decode, independent of the denormal mode.  bf16: the upper
+// half of the binary32 pattern; its subnormals are fp32 subnormals, which the
+// kernels keep (fp32 denormal mode "preserve", the HIP default).
+__device__ __forceinline__ float key_value(uint32_t h, int fmt) {
+    if (fmt == FMT_BF16) return __uint_as_float(h << 16);
     const uint32_t e = (h >> 10) & 0x1Fu;
     const uint32_t m = h & 0x3FFu;
     float mag = e ? __uint_as_float(((e + 112u) << 23) | (m << 13)) : (float)m * 0x1p-24f;
     return __uint_as_float(__float_as_uint(mag) | ((h & 0x8000u) << 16));
 }
 
-__device__ __forceinline__ bool key_finite(uint32_t h) { return (h & 0x7C00u) != 0x7C00u; }
+__device__ __forceinline__ bool key_finite(uint32_t h, int fmt) {
+    return (int)(h & 0x7FFFu) < fin_mags(fmt);
+}
+
+// fp32 -> 16-bit pattern of the weight format, round to nearest even (NaN
+// stays NaN).
+__device__ __forceinline__ uint32_t to_half_bits(float x, int fmt) {
+    if (fmt == FMT_FP16) return (uint32_t)__half_as_ushort(__float2half_rn(x));
+    const uint32_t u = __float_as_uint(x);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x40u;
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
 
 __device__ __forceinline__ float sgnf(float x) { return (float)((x > 0.f) - (x < 0.f)); }
 
@@ -205,6 +219,12 @@ struct Slice {
         rounds = nvec / TILE / a;
         rest0 = rounds * a * TILE;
         per = ((nvec - rest0 + STEP - 1) / STEP + a - 1) / a;
+    }
+    // weights one workgroup handles, at most (either path)
+    __device__ __forceinline__ uint64_t bound(const MatArgs& M) const {
+        const uint64_t scalar = (M.n + (uint64_t)M.wg_count * NP_THREADS - 1) /
+                                ((uint64_t)M.wg_count * NP_THREADS) * NP_THREADS;
+        return max(rounds * TILE + per * STEP, scalar) + NP_THREADS;
     }
 };
 
@@ -406,13 +426,15 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_hist_merge(BatchArgs b) {
     if (s1) atomicAdd(c + 1, s1);
 }
 
-// Keyed-gradient rows (fp32 over the 4-byte window) into G.
-// Grid (2 * W4 / MERGE_THREADS, NP_MAX_WG / MERGE_ROWS, count).
+// Keyed-gradient rows (fp32 over the window of the matrix's keyed-sum mode)
+// into G.  Grid (2 * W4 / MERGE_THREADS, NP_MAX_WG / MERGE_ROWS, count).
 __global__ void __launch_bounds__(MERGE_THREADS) k_grad_merge(BatchArgs b) {
     const MatArgs& M = b.m[blockIdx.z];
     const int r0 = blockIdx.y * MERGE_ROWS;
     const int r1 = min((int)M.wg_count, r0 + MERGE_ROWS);
-    const int w = M.ws.st->w4, lo = M.ws.st->lo4;
+    const DevState* st = M.ws.st;
+    const bool wide = st->kmode == KEYED_U64;
+    const int w = wide ? st->w8 : st->w4, lo = wide ? st->lo8 : st->lo4;
     const int i = blockIdx.x * MERGE_THREADS + threadIdx.x;
     if (r0 >= r1 || i >= 2 * w) return;
     const float* part = reinterpret_cast<const float*>(M.ws.part) + i;
@@ -446,18 +468,19 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t x, uint32_t* tmp /*
 }
 
 // Window selection, first half.  Grid (32, count): block x covers magnitudes
-// [1024 x, 1024 x + 1024) of both signs.  Writes, per magnitude below 0x7C00,
+// [1024 x, 1024 x + 1024) of both signs.  Writes, per finite magnitude,
 // the running count of weights within the block (inclusive), and per block its
 // total, occupied-pattern count, occupied magnitude range and non-finite flag.
 __global__ void __launch_bounds__(NP_THREADS) k_window_scan(BatchArgs b) {
     __shared__ uint32_t tmp[16];
     __shared__ int ired[5];
+    __shared__ unsigned long long sqsum;
     const MatArgs& M = b.m[blockIdx.y];
     const uint32_t* counts = M.ws.counts;
     const int mag = blockIdx.x * NP_THREADS + threadIdx.x;   // < 32768
     const uint32_t cp = counts[mag], cn = counts[0x8000 | mag];
-    if (threadIdx.x == 0) { ired[0] = 1 << 30; ired[1] = -1; ired[2] = 0; ired[3] = 0; ired[4] = 0; }
-    const bool fin = mag < FIN_MAGS;
+    if (threadIdx.x == 0) { ired[0] = 1 << 30; ired[1] = -1; ired[2] = 0; ired[3] = 0; ired[4] = 0; sqsum = 0ull; }
+    const bool fin = mag < fin_mags(M.fmt);
     const uint32_t c = fin ? cp + cn : 0u;
     const uint32_t incl = block_excl_scan(c, tmp) + c;        // (has block barriers)
     if (fin) M.ws.wscan[mag] = incl;
@@ -466,8 +489,15 @@ __global__ void __launch_bounds__(NP_THREADS) k_window_scan(BatchArgs b) {
     if (nu) atomicAdd(&ired[2], nu);
     if (!fin && (cp | cn)) atomicOr(&ired[3], 1);
     if (threadIdx.x == NP_THREADS - 1) ired[4] = (int)incl;
+    // sum of squared counts (< N^2 < 2^64), for the keyed-sum mode
+    unsigned long long sq = fin ? (unsigned long long)cp * cp + (unsigned long long)cn * cn : 0ull;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) sq += __shfl_xor(sq, o, 64);
+    if ((threadIdx.x & 63) == 0) atomicAdd(&sqsum, sq);
     __syncthreads();
     if (threadIdx.x < 5) M.ws.wstat[blockIdx.x * 8 + threadIdx.x] = ired[threadIdx.x];
+    if (threadIdx.x == 5) M.ws.wstat[blockIdx.x * 8 + 5] = (int)(uint32_t)sqsum;
+    if (threadIdx.x == 6) M.ws.wstat[blockIdx.x * 8 + 6] = (int)(uint32_t)(sqsum >> 32);
 }
 
 // Window selection, second half; one block per matrix.  Combines the block
@@ -483,6 +513,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
     if (threadIdx.x == 0) {
         int lo = 1 << 30, hi = -1, nu = 0, nf = 0;
         uint32_t run = 0;
+        unsigned long long sq = 0ull;
         for (int x = 0; x < 32; ++x) {
             const int* w = M.ws.wstat + x * 8;
             lo = min(lo, w[0]);
@@ -491,9 +522,13 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
             nf |= w[3];
             off[x] = run;
             run += (uint32_t)w[4];
+            sq += (unsigned long long)(uint32_t)w[5] | ((unsigned long long)(uint32_t)w[6] << 32);
         }
         off[32] = run;
+        // expected number of other lanes sharing an address in a 64-lane keyed atomic
+        const double e = run ? 2016.0 * (double)sq / ((double)run * (double)run) : 0.0;
         st5[0] = lo; st5[1] = hi; st5[2] = nu; st5[3] = nf;
+        st5[4] = e > KEYED_U64_ABOVE ? KEYED_U64 : KEYED_I32;
     }
     __syncthreads();
     const int mlo = st5[0], mhi = st5[1];
@@ -529,6 +564,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
         st->mhi = mhi;
         st->lo4 = wl[0]; st->w4 = ww[0];
         st->lo8 = wl[1]; st->w8 = ww[1];
+        st->kmode = M.kforce >= 0 ? M.kforce : st5[4];
         if (M.nuniq_out) *M.nuniq_out = (uint32_t)st5[2];
     }
 }
@@ -599,8 +635,8 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
     for (int r = 0; r < 4; ++r) {
         const int u = table_key(r);
         const uint32_t n = n4[r];
-        if (n == 0u || !key_finite(u)) continue;
-        const float v = key_value(u);
+        if (n == 0u || !key_finite(u, M.fmt)) continue;
+        const float v = key_value(u, M.fmt);
         float a[K];
         attn_row<K>(v, c, b.s2, a);
         const float nf = (float)n;
@@ -666,8 +702,8 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
         M.ws.G[u] = 0.f;
         const uint32_t n = n4[r];
         if (n == 0u) continue;
-        if (!key_finite(u)) { M.ws.tab[u] = __builtin_nanf(""); M.ws.H[u] = __builtin_nanf(""); continue; }
-        const float v = key_value(u);
+        if (!key_finite(u, M.fmt)) { M.ws.tab[u] = __builtin_nanf(""); M.ws.H[u] = __builtin_nanf(""); continue; }
+        const float v = key_value(u, M.fmt);
         float a[K], d[K], c1m;
         attn_row_sel<K>(v, c0, b.s2, a, c1, c1m);
         const float tv = centroid_dev<K>(a, c1, c1m, d);
@@ -712,11 +748,10 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
         return make_float4(look(k0), look(k1), look(k2), look(k3));
     };
     const uint16_t* keys = M.keys;
-    if (b.out_fp16) {
-        __half* out = reinterpret_cast<__half*>(M.wt);
+    if (b.out_half) {
+        uint16_t* out = reinterpret_cast<uint16_t*>(M.wt);
         auto h2 = [&](float a, float c) -> uint32_t {
-            return (uint32_t)__half_as_ushort(__float2half_rn(a)) |
-                   ((uint32_t)__half_as_ushort(__float2half_rn(c)) << 16);
+            return to_half_bits(a, M.fmt) | (to_half_bits(c, M.fmt) << 16);
         };
         for_slice<8, 4, true>(M, wl,
             [&](uint64_t i) { return Keys4{ld_u2(keys + i)}; },
@@ -725,7 +760,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
                 return make_uint2(h2(v.x, v.y), h2(v.z, v.w));
             },
             [&](uint64_t i, uint2 o) { st_u2(out + i, o); },
-            [&](uint64_t i) { out[i] = __float2half_rn(look(keys[i])); });
+            [&](uint64_t i) { out[i] = (uint16_t)to_half_bits(look(keys[i]), M.fmt); });
     } else {
         float* out = reinterpret_cast<float*>(M.wt);
         for_slice<8, 4, true>(M, wl,
@@ -741,29 +776,50 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
 // G_u = sum over weights with pattern u of dL/dW~_i.
 //
 // LDS fp32 atomics run at a fraction of the integer rate on this GPU, so the
-// window sums are kept in 32-bit fixed point: q = round(g 2^S), added with
-// integer LDS atomics that return the previous value.  Each workgroup chooses S
-// from a first sample of its own g (one value per thread): every value with
-// exponent <= L quantises below 2^30 in magnitude, where L is the sample's
-// largest exponent, or its mean exponent + 8 if that is smaller, plus 2; the
-// resolution is then at least 2^-19 of a value of mean exponent.  Values above
-// that (and Inf/NaN) are added in fp32 to the global G, as are patterns outside
-// the window.  A sum that wraps past the
-// 32-bit range is detected from the returned value and the wrap (exactly
-// +-2^32 quanta) is added to G in fp32, so no sum is ever lost.  G enters the
-// backward only through the k-vector sums gamma and E over all patterns, where
-// this resolution is far below fp32 rounding.  Each workgroup ends by writing
-// its window as one fp32 partial row.
+// window sums are kept in fixed point, q = round(g 2^S), added with integer LDS
+// atomics.  Each workgroup chooses S from a first sample of its own g (one
+// value per thread).  Values above the sample-based limit (and Inf/NaN) are
+// added in fp32 to the global G, as are patterns outside the window.  G enters
+// the backward only through the k-vector sums gamma and E over all patterns,
+// where the fixed-point resolution is far below fp32 rounding.  Each workgroup
+// ends by writing its window as one fp32 partial row.  Two accumulator modes,
+// chosen per matrix by k_window from how concentrated the patterns are:
+//
+// KEYED_I32: 32-bit sums over the 4-byte window, added with atomics that
+// return the previous value.  Every value with exponent <= L quantises below
+// 2^30, where L is the sample's largest exponent, or its mean exponent + 8 if
+// that is smaller, plus 2 (resolution at least 2^-19 of a value of mean
+// exponent; a few huge values in the sample cannot coarsen the bulk).  A sum
+// that wraps past the 32-bit range is detected from the returned value and the
+// wrap (exactly +-2^32 quanta) goes to G in fp32, so no sum is ever lost.
+//
+// KEYED_U64: 64-bit sums over the 8-byte window with plain atomics.  Every
+// value with exponent <= E + 6 (E the sample maximum) stays below 2^(61 - b)
+// for a slice of at most 2^b weights, so no sum can overflow; the resolution
+// is 2^(b - 55) of the sample maximum.
+//
+// Returning atomics serialise lanes that hit the same address, plain ones do
+// not: with fp16 weights (about 0.23 other lanes per 64-lane atomic share an
+// address) the 32-bit mode is 10% faster, with bf16 weights (about 1.8) the
+// 64-bit mode is 30% faster.
 __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
-    __shared__ int acc[2 * W4];
+    __shared__ unsigned long long lds[2 * W8];   // 64-bit sums, or the 32-bit ones
     __shared__ int emax_sh, esum_sh, ecnt_sh;
+    static_assert(2 * W4 * sizeof(int) <= sizeof(lds), "32-bit window fits the LDS buffer");
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
     const uint32_t wl = blockIdx.x - M.wg_begin;
-    const int lo = M.ws.st->lo4, w = M.ws.st->w4;
+    const DevState* st = M.ws.st;
+    const bool wide = st->kmode == KEYED_U64;
+    const int lo = wide ? st->lo8 : st->lo4, w = wide ? st->w8 : st->w4;
     const uint16_t* keys = M.keys;
     const float* g = M.g;
-    for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) acc[i] = 0;
+    int* acc32 = reinterpret_cast<int*>(lds);
+    if (wide) {
+        for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) lds[i] = 0ull;
+    } else {
+        for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) acc32[i] = 0;
+    }
     if (threadIdx.x == 0) { emax_sh = 0; esum_sh = 0; ecnt_sh = 0; }
     __syncthreads();
     {   // sample: one value per thread, spread over the matrix; exponents of the
@@ -785,39 +841,60 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
         }
     }
     __syncthreads();
-    // Values with exponent <= elim go to LDS: the sample maximum, but at most
-    // 2^10 above the mean exponent, so that a few huge values in the sample
-    // (they take the fp32 path) cannot coarsen the resolution of the bulk.
-    // Capped so the wrap value 2^(32 - S) stays finite.
-    const int emean = ecnt_sh > 0 ? (esum_sh + ecnt_sh / 2) / ecnt_sh : 0;
-    const int elim = min(min(emax_sh, emean + 8) + 2, 190);
-    const int S = 156 - elim;                    // |g 2^S| < 2^30
-    const float wrap = ldexpf(1.0f, 32 - S);     // one turn of the 32-bit accumulator, as a value
     float* G = M.ws.G;
-    auto add = [&](uint32_t key, float gv) {
-        const uint32_t d = (key & 0x7FFFu) - (uint32_t)lo;
-        const int e = (int)((__float_as_uint(gv) >> 23) & 0xFFu);
-        if (d < (uint32_t)w && e <= elim) {
-            const int q = __float2int_rn(ldexpf(gv, S));
-            const int old = atomicAdd(&acc[(key >> 15) * w + d], q);
-            const int sum = (int)((uint32_t)old + (uint32_t)q);
-            if (((old ^ sum) & (q ^ sum)) < 0) atomicAdd(&G[key], q > 0 ? wrap : -wrap);
-        } else {
-            atomicAdd(&G[key], gv);
-        }
+    auto stream = [&](auto add) {
+        for_slice<8, 4>(M, wl,
+            [&](uint64_t i) { return KeysG4{ld_u2_nt(keys + i), ld_f4_nt(g + i)}; },
+            [&](const KeysG4& r) {
+                add(r.q.x & 0xFFFFu, r.g.x); add(r.q.x >> 16, r.g.y);
+                add(r.q.y & 0xFFFFu, r.g.z); add(r.q.y >> 16, r.g.w);
+                return Nothing{};
+            },
+            [&](uint64_t, Nothing) {},
+            [&](uint64_t i) { add(keys[i], g[i]); });
     };
-    for_slice<8, 4>(M, wl,
-        [&](uint64_t i) { return KeysG4{ld_u2_nt(keys + i), ld_f4_nt(g + i)}; },
-        [&](const KeysG4& r) {
-            add(r.q.x & 0xFFFFu, r.g.x); add(r.q.x >> 16, r.g.y);
-            add(r.q.y & 0xFFFFu, r.g.z); add(r.q.y >> 16, r.g.w);
-            return Nothing{};
-        },
-        [&](uint64_t, Nothing) {},
-        [&](uint64_t i) { add(keys[i], g[i]); });
-    __syncthreads();
     float* row = reinterpret_cast<float*>(M.ws.part) + (size_t)wl * ROW4;
-    for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) row[i] = ldexpf((float)acc[i], -S);
+    if (wide) {
+        const int bn = 64 - __clzll((unsigned long long)Slice<8, 4>(M).bound(M) - 1);   // 2^bn >= weights added here
+        const int emax = emax_sh;
+        const int S = 181 - bn - emax;               // 2^(emax-126) * 2^S = 2^(55-bn)
+        const uint32_t elim = (uint32_t)min(emax + 6, 0xFE);
+        stream([&](uint32_t key, float gv) {
+            const uint32_t d = (key & 0x7FFFu) - (uint32_t)lo;
+            const uint32_t e = (__float_as_uint(gv) >> 23) & 0xFFu;
+            if (d < (uint32_t)w && e <= elim) {
+                const long long q = __float2ll_rn(ldexpf(gv, S));
+                atomicAdd(&lds[(key >> 15) * w + d], (unsigned long long)q);
+            } else {
+                atomicAdd(&G[key], gv);
+            }
+        });
+        __syncthreads();
+        for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS)
+            row[i] = (float)ldexp((double)(long long)lds[i], -S);
+    } else {
+        // Values with exponent <= elim go to LDS: the sample maximum, but at most
+        // 2^10 above the mean exponent.  Capped so the wrap value 2^(32 - S)
+        // stays finite.
+        const int emean = ecnt_sh > 0 ? (esum_sh + ecnt_sh / 2) / ecnt_sh : 0;
+        const int elim = min(min(emax_sh, emean + 8) + 2, 190);
+        const int S = 156 - elim;                    // |g 2^S| < 2^30
+        const float wrap = ldexpf(1.0f, 32 - S);     // one turn of the 32-bit accumulator, as a value
+        stream([&](uint32_t key, float gv) {
+            const uint32_t d = (key & 0x7FFFu) - (uint32_t)lo;
+            const int e = (int)((__float_as_uint(gv) >> 23) & 0xFFu);
+            if (d < (uint32_t)w && e <= elim) {
+                const int q = __float2int_rn(ldexpf(gv, S));
+                const int old = atomicAdd(&acc32[(key >> 15) * w + d], q);
+                const int sum = (int)((uint32_t)old + (uint32_t)q);
+                if (((old ^ sum) & (q ^ sum)) < 0) atomicAdd(&G[key], q > 0 ? wrap : -wrap);
+            } else {
+                atomicAdd(&G[key], gv);
+            }
+        });
+        __syncthreads();
+        for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) row[i] = ldexpf((float)acc32[i], -S);
+    }
 }
 
 // dL/dw_i = g_i H[bits_i] + R[bits_i]; the window [lo8, lo8 + w8) of (H, R) sits
@@ -919,9 +996,9 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_top(BatchArgs b) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int u = table_key(r);
-        if (n4[r] == 0u || !key_finite(u)) continue;
+        if (n4[r] == 0u || !key_finite(u, M.fmt)) continue;
         const float G = G4[r];
-        const float v = key_value(u);
+        const float v = key_value(u, M.fmt);
         float a[K], d[K], c1m;
         attn_row_sel<K>(v, c0, b.s2, a, c1, c1m);
         centroid_dev<K>(a, c1, c1m, d);
@@ -1001,11 +1078,11 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
         const int u = table_key(r);
         const uint32_t n = n4[r];
         if (n == 0u) continue;
-        if (!key_finite(u)) {
+        if (!key_finite(u, M.fmt)) {
             if (t == 1) M.ws.HR[u] = make_float2(__builtin_nanf(""), __builtin_nanf(""));
             continue;
         }
-        const float v = key_value(u);
+        const float v = key_value(u, M.fmt);
         float a[K], dev[K], cm;
         attn_row_sel<K>(v, c0, b.s2, a, c1, cm);
         const float direct = softmax_dev<K>(v, a, gS, c1, cm, dev);
@@ -1074,8 +1151,8 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_iter(BatchArgs b) {
     dense_range(M, beg, end);
     for (uint64_t i = beg + threadIdx.x; i < end; i += D_THREADS) {
         const uint32_t key = M.keys[i];
-        if (!key_finite(key)) continue;
-        const float v = key_value(key);
+        if (!key_finite(key, M.fmt)) continue;
+        const float v = key_value(key, M.fmt);
         float a[K];
         attn_row<K>(v, c, b.s2, a);
 #pragma unroll
@@ -1141,8 +1218,8 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_out(BatchArgs b) {
         const uint32_t key = M.keys[i];
         float wv;
         float a[K];
-        if (key_finite(key)) {
-            const float v = key_value(key);
+        if (key_finite(key, M.fmt)) {
+            const float v = key_value(key, M.fmt);
             attn_row<K>(v, c0, b.s2, a);
             wv = 0.f;
 #pragma unroll
@@ -1152,7 +1229,7 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_out(BatchArgs b) {
 #pragma unroll
             for (int j = 0; j < K; ++j) a[j] = __builtin_nanf("");
         }
-        if (b.out_fp16) reinterpret_cast<__half*>(M.wt)[i] = __float2half_rn(wv);
+        if (b.out_half) reinterpret_cast<uint16_t*>(M.wt)[i] = (uint16_t)to_half_bits(wv, M.fmt);
         else reinterpret_cast<float*>(M.wt)[i] = wv;
         if (M.attn) {
 #pragma unroll
@@ -1184,8 +1261,8 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_btop(BatchArgs b) {
     dense_range(M, beg, end);
     for (uint64_t i = beg + threadIdx.x; i < end; i += D_THREADS) {
         const uint32_t key = M.keys[i];
-        if (!key_finite(key)) { M.gw[i] = __builtin_nanf(""); continue; }
-        const float v = key_value(key);
+        if (!key_finite(key, M.fmt)) { M.gw[i] = __builtin_nanf(""); continue; }
+        const float v = key_value(key, M.fmt);
         const float g = M.g[i];
         float a[K], d[K], c1m;
         attn_row_sel<K>(v, c0, b.s2, a, c1, c1m);
@@ -1232,8 +1309,8 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_biter(BatchArgs b) {
     dense_range(M, beg, end);
     for (uint64_t i = beg + threadIdx.x; i < end; i += D_THREADS) {
         const uint32_t key = M.keys[i];
-        if (!key_finite(key)) continue;
-        const float v = key_value(key);
+        if (!key_finite(key, M.fmt)) continue;
+        const float v = key_value(key, M.fmt);
         float a[K], dev[K], cm;
         attn_row_sel<K>(v, c0, b.s2, a, c1, cm);
         const float direct = softmax_dev<K>(v, a, gS, c1, cm, dev);

@@ -50,6 +50,9 @@ ERR_HIP = -5
 NKEYS = 65536
 PASS_HIST, PASS_GATHER_WT, PASS_KEYED_GRAD, PASS_GATHER_GRAD = 0, 1, 2, 3
 PASS_DENSE_ITER, PASS_DENSE_BITER = 4, 5
+KEYS_FP16, KEYS_BF16 = 0, 1
+KEYED_AUTO, KEYED_I32, KEYED_U64 = -1, 0, 1
+KEY_FORMATS = {"fp16": KEYS_FP16, "bf16": KEYS_BF16}
 
 
 class EdkmError(RuntimeError):
@@ -71,6 +74,8 @@ _PLAN = ctypes.POINTER(edkm_plan)
 _SIGS = {
     "edkm_workspace_bytes": (_sz, [_u64, _i32, _i32]),
     "edkm_plan_init": (_i32, [_PLAN, _u64, _i32, _i32, _P, _sz]),
+    "edkm_plan_init_ex": (_i32, [_PLAN, _u64, _i32, _i32, _i32, _P, _sz]),
+    "edkm_plan_set_keyed_mode": (_i32, [_PLAN, _i32]),
     "edkm_init_unique": (_i32, [_PLAN, _P, _P, _P, _i32, _P]),
     "edkm_forward": (_i32, [_PLAN, _P, _f32, _f32, _P, _P, _P, _i32, _P, _P]),
     "edkm_backward": (_i32, [_PLAN, _P, _P, _P, _P, _P]),
@@ -147,9 +152,13 @@ def workspace_bytes(n: int, bits: int, max_iter: int) -> int:
 class Plan:
     """An ``edkm_plan`` plus its device workspace (allocated through torch)."""
 
-    def __init__(self, n: int, bits: int, max_iter: int, device="cuda", workspace=None):
+    def __init__(self, n: int, bits: int, max_iter: int, device="cuda", workspace=None,
+                 key_format: str = "fp16"):
         import torch
         self.n, self.bits, self.k, self.max_iter = int(n), int(bits), 1 << int(bits), int(max_iter)
+        if key_format not in KEY_FORMATS:
+            raise EdkmError(ERR_ARG, "plan_init", "key_format must be one of %s" % sorted(KEY_FORMATS))
+        self.key_format = key_format
         nbytes = workspace_bytes(n, bits, max_iter)
         if nbytes == 0:
             raise EdkmError(ERR_ARG, "workspace_bytes")
@@ -157,13 +166,19 @@ class Plan:
             workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
         self.workspace = workspace
         self.plan = edkm_plan()
-        _check(_lib.edkm_plan_init(ctypes.byref(self.plan), self.n, self.bits, self.max_iter,
-                                   _ptr(workspace), workspace.numel() * workspace.element_size()),
+        _check(_lib.edkm_plan_init_ex(ctypes.byref(self.plan), self.n, self.bits, self.max_iter,
+                                      KEY_FORMATS[key_format], _ptr(workspace),
+                                      workspace.numel() * workspace.element_size()),
                "plan_init")
 
     @property
     def ref(self):
         return ctypes.byref(self.plan)
+
+
+def plan_set_keyed_mode(plan: Plan, mode: int) -> None:
+    """KEYED_AUTO (default), KEYED_I32 or KEYED_U64; effective at the next init_unique."""
+    _check(_lib.edkm_plan_set_keyed_mode(plan.ref, int(mode)), "plan_set_keyed_mode", (plan,))
 
 
 def plan_set_pass_events(plan: Plan, pass_id: int, start, stop) -> None:
@@ -182,11 +197,11 @@ def init_unique(plan: Plan, w_bits, counts_out=None, num_unique_out=None, check_
            "init_unique", (plan,))
 
 
-def forward(plan: Plan, w_bits, tau: float, eps: float, c_in, c_out, w_tilde, out_fp16=False,
+def forward(plan: Plan, w_bits, tau: float, eps: float, c_in, c_out, w_tilde, out_half=False,
             iters_out=None, stream=None) -> None:
     _check(_lib.edkm_forward(plan.ref, _ptr(w_bits, 2, "w_bits"), float(tau), float(eps),
-                             _ptr(c_in, 4), _ptr(c_out, 4), _ptr(w_tilde, 2 if out_fp16 else 4),
-                             int(bool(out_fp16)), _ptr(iters_out, 4), _stream(stream)),
+                             _ptr(c_in, 4), _ptr(c_out, 4), _ptr(w_tilde, 2 if out_half else 4),
+                             int(bool(out_half)), _ptr(iters_out, 4), _stream(stream)),
            "forward", (plan,))
 
 
@@ -197,10 +212,10 @@ def backward(plan: Plan, w_bits, grad_w_tilde, grad_w, grad_c, stream=None) -> N
 
 
 def forward_dense(plan: Plan, w_bits, tau: float, eps: float, c_in, c_out, w_tilde,
-                  out_fp16=False, iters_out=None, attn_out=None, stream=None) -> None:
+                  out_half=False, iters_out=None, attn_out=None, stream=None) -> None:
     _check(_lib.edkm_forward_dense(plan.ref, _ptr(w_bits, 2, "w_bits"), float(tau), float(eps),
                                    _ptr(c_in, 4), _ptr(c_out, 4),
-                                   _ptr(w_tilde, 2 if out_fp16 else 4), int(bool(out_fp16)),
+                                   _ptr(w_tilde, 2 if out_half else 4), int(bool(out_half)),
                                    _ptr(iters_out, 4), _ptr(attn_out, 4), _stream(stream)),
            "forward_dense", (plan,))
 
@@ -232,17 +247,17 @@ def init_unique_batch(plans, w_bits, counts_out=None, num_unique_out=None, check
            "init_unique_batch", plans)
 
 
-def forward_batch(plans, w_bits, tau, eps, c_in, c_out, w_tilde, out_fp16=False, iters_out=None,
+def forward_batch(plans, w_bits, tau, eps, c_in, c_out, w_tilde, out_half=False, iters_out=None,
                   stream=None) -> None:
     n = len(plans)
     pp, _a = _plans(plans)
     kk, _b = _parr(w_bits, 2)
     ci, _c = _parr(c_in, 4)
     co, _d = _parr(c_out, 4)
-    wt, _e = _parr(w_tilde, 2 if out_fp16 else 4)
+    wt, _e = _parr(w_tilde, 2 if out_half else 4)
     it, _f = _parr(iters_out, 4) if iters_out is not None else (None, None)
     _check(_lib.edkm_forward_batch(n, pp, kk, float(tau), float(eps), ci, co, wt,
-                                   int(bool(out_fp16)), it, _stream(stream)),
+                                   int(bool(out_half)), it, _stream(stream)),
            "forward_batch", plans)
 
 

@@ -7,7 +7,8 @@ path and the CPU oracle see identical data.
 Recipe (the paper's workload is LLaMA-7B weights fine-tuned in 16 bits; no
 weights are available, so these draws stand in for them):
 
-* weights: fp32 draws from N(0, 0.02^2) rounded to fp16 (round-to-nearest-even);
+* weights: fp32 draws from N(0, 0.02^2) rounded to fp16, or for bf16 weights
+  to bfloat16 (round-to-nearest-even either way);
   with ``outliers`` each element independently, with probability 1e-3, is
   replaced before rounding by a draw from N(0, 0.2^2);
 * initial centroids: the k evenly spaced quantiles of the fp16 values, i.e. the
@@ -72,9 +73,36 @@ def fp16_weights(n: int, seed: int, outliers: bool = False) -> np.ndarray:
     return w.astype(np.float16).view(np.uint16)
 
 
-def quantile_init(keys: np.ndarray, k: int) -> np.ndarray:
-    """The k evenly spaced quantiles of the fp16 values (fp32, exact)."""
-    vals = np.asarray(keys, dtype=np.uint16).ravel().view(np.float16).astype(np.float32)
+def bf16_weights(n: int, seed: int, outliers: bool = False) -> np.ndarray:
+    """The same fp32 draws as fp16_weights, rounded to bfloat16 (to nearest,
+    ties to even) instead: n bf16 weights as raw bit patterns (uint16)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    w = rng.standard_normal(n, dtype=np.float32)
+    w *= np.float32(SIGMA)
+    if outliers:
+        mask = rng.random(n, dtype=np.float32) < np.float32(OUTLIER_P)
+        m = int(mask.sum())
+        w[mask] = rng.standard_normal(m, dtype=np.float32) * np.float32(OUTLIER_SIGMA)
+    u = w.view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def weights(n: int, seed: int, outliers: bool = False, fmt: str = "fp16") -> np.ndarray:
+    """fp16_weights or bf16_weights by format name."""
+    return (bf16_weights if fmt == "bf16" else fp16_weights)(n, seed, outliers)
+
+
+def values(keys: np.ndarray, fmt: str = "fp16") -> np.ndarray:
+    """16-bit patterns -> their fp32 values (exact)."""
+    u = np.asarray(keys, dtype=np.uint16).ravel()
+    if fmt == "bf16":
+        return (u.astype(np.uint32) << 16).view(np.float32)
+    return u.view(np.float16).astype(np.float32)
+
+
+def quantile_init(keys: np.ndarray, k: int, fmt: str = "fp16") -> np.ndarray:
+    """The k evenly spaced quantiles of the weight values (fp32, exact)."""
+    vals = values(keys, fmt)
     n = vals.size
     ranks = np.array([((2 * j + 1) * n) // (2 * k) for j in range(k)], dtype=np.int64)
     part = np.partition(vals, np.unique(ranks))
@@ -87,9 +115,10 @@ def upstream_grad(n: int, seed: int) -> np.ndarray:
     return rng.standard_normal(n, dtype=np.float32)
 
 
-def fp16_weights_device(n: int, seed: int, device, outliers: bool = False):
-    """n fp16 weights as raw bit patterns (torch.int16 on ``device``), drawn by
-    torch's generator on that device (same recipe as fp16_weights)."""
+def fp16_weights_device(n: int, seed: int, device, outliers: bool = False, fmt: str = "fp16"):
+    """n fp16 (or, with fmt="bf16", bf16) weights as raw bit patterns
+    (torch.int16 on ``device``), drawn by torch's generator on that device
+    (same recipe as fp16_weights; torch rounds to nearest even)."""
     import torch
     gen = torch.Generator(device=device)
     gen.manual_seed(seed)
@@ -98,14 +127,14 @@ def fp16_weights_device(n: int, seed: int, device, outliers: bool = False):
     if outliers:
         mask = torch.rand(n, generator=gen, device=device) < OUTLIER_P
         w[mask] = torch.randn(int(mask.sum()), generator=gen, device=device) * OUTLIER_SIGMA
-    return w.to(torch.float16).view(torch.int16)
+    return w.to(torch.bfloat16 if fmt == "bf16" else torch.float16).view(torch.int16)
 
 
-def quantile_init_device(keys, k: int):
+def quantile_init_device(keys, k: int, fmt: str = "fp16"):
     """quantile_init for device keys (torch.int16 bit patterns): fp32 on the same device."""
     import torch
     n = keys.numel()
-    vals = torch.sort(keys.view(torch.float16).float()).values
+    vals = torch.sort(keys.view(torch.bfloat16 if fmt == "bf16" else torch.float16).float()).values
     ranks = torch.tensor([((2 * j + 1) * n) // (2 * k) for j in range(k)], device=keys.device)
     return vals[ranks].contiguous()
 

@@ -37,3 +37,25 @@ def assert_fp16_within_ulp(x_bits, ref, what="fp16 W~"):
     ulp = np.abs(np.spacing(r16).astype(np.float64))
     bad = np.abs(x - r16.astype(np.float64)) > ulp
     assert not np.any(bad), "%s: %d entries beyond one ulp" % (what, int(bad.sum()))
+
+
+def _bf16_bits(x32):
+    """float32 -> bfloat16 patterns, round to nearest even."""
+    u = np.asarray(x32, np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def _bf16_values(b):
+    return (np.asarray(b, np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def assert_bf16_within_ulp(x_bits, ref, what="bf16 W~"):
+    """x_bits: bf16 patterns; ref: fp64 oracle values.  Within one bf16 ulp of
+    the oracle value rounded to bf16 (through fp32: the double rounding moves
+    it by at most half an ulp)."""
+    r = _bf16_bits(np.asarray(ref, np.float64).astype(np.float32))
+    rv = _bf16_values(r)
+    ulp = np.abs(_bf16_values(r + np.uint16(1)) - rv)
+    x = _bf16_values(x_bits)
+    bad = ~(np.abs(x - rv) <= ulp)
+    assert not np.any(bad), "%s: %d entries beyond one ulp" % (what, int(bad.sum()))

@@ -132,3 +132,21 @@ def test_pass_event_ids_match_header():
         assert lib.edkm_plan_set_pass_events(ctypes.byref(p), pid, None, None) == edkm.OK
     assert lib.edkm_plan_set_pass_events(ctypes.byref(p), len(ids), None, None) == edkm.ERR_ARG
     assert lib.edkm_plan_set_pass_events(ctypes.byref(p), -1, None, None) == edkm.ERR_ARG
+
+
+def test_keyed_mode_setting():
+    p = _plan()
+    for mode in (edkm.KEYED_AUTO, edkm.KEYED_I32, edkm.KEYED_U64):
+        assert lib.edkm_plan_set_keyed_mode(ctypes.byref(p), mode) == edkm.OK
+    assert lib.edkm_plan_set_keyed_mode(ctypes.byref(p), -2) == edkm.ERR_ARG
+    assert lib.edkm_plan_set_keyed_mode(ctypes.byref(p), 2) == edkm.ERR_ARG
+    assert lib.edkm_plan_set_keyed_mode(None, 0) == edkm.ERR_ARG
+
+
+def test_plan_init_ex_key_formats():
+    p = edkm.edkm_plan()
+    ws = edkm.workspace_bytes(1000, 3, 5)
+    for fmt in (edkm.KEYS_FP16, edkm.KEYS_BF16):
+        assert lib.edkm_plan_init_ex(ctypes.byref(p), 1000, 3, 5, fmt, FAKE_WS, ws) == edkm.OK
+    for fmt in (-1, 2):
+        assert lib.edkm_plan_init_ex(ctypes.byref(p), 1000, 3, 5, fmt, FAKE_WS, ws) == edkm.ERR_ARG

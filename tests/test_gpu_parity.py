@@ -19,8 +19,8 @@ torch = pytest.importorskip("torch")
 from oracle import dense, table                                  # noqa: E402
 from paper_2309_00964_amd import edkm, inputs                     # noqa: E402
 from paper_2309_00964_amd.runner import run                       # noqa: E402
-from parity_util import (TOL_BWD, TOL_FWD, assert_close,          # noqa: E402
-                         assert_fp16_within_ulp)
+from parity_util import (TOL_BWD, TOL_FWD, assert_bf16_within_ulp,  # noqa: E402
+                         assert_close, assert_fp16_within_ulp)
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -43,13 +43,15 @@ def gpu(keys, c0, bits, g=None, tau=TAU, iters=ITERS, eps=0.0, **kw):
     res = {}
     for k, v in out.items():
         if isinstance(v, torch.Tensor):
+            if v.dtype == torch.bfloat16:      # numpy has no bfloat16: hand back the patterns
+                v = v.view(torch.int16)
             res[k] = v.cpu().numpy()
     return res
 
 
-def oracle(keys, c0, g=None, tau=TAU, iters=ITERS, eps=0.0, form="dense"):
+def oracle(keys, c0, g=None, tau=TAU, iters=ITERS, eps=0.0, form="dense", fmt="fp16"):
     mod = dense if form == "dense" else table
-    f = mod.forward(keys, np.asarray(c0, np.float64), tau, iters, eps=eps)
+    f = mod.forward(keys, np.asarray(c0, np.float64), tau, iters, eps=eps, fmt=fmt)
     if g is not None:
         r = mod.backward(keys, f, np.asarray(g, np.float64))
         f["gw"], f["gc"] = r[0], r[1]
@@ -169,7 +171,7 @@ def test_fp16_output_within_one_ulp(dense_path):
     keys = inputs.fp16_weights(65536 + 5, 41)
     c0 = inputs.quantile_init(keys, 8)
     say("fp16 out", dense_path)
-    res = gpu(keys, c0, 3, out_fp16=True, dense=dense_path)
+    res = gpu(keys, c0, 3, out_half=True, dense=dense_path)
     ref = oracle(keys, c0)
     assert_fp16_within_ulp(res["w_tilde"].view(np.uint16), ref["w_tilde"])
 
@@ -242,8 +244,27 @@ def test_keyed_sum_wraps_fixed_point_range():
     g[big] = np.where(rng.random(int(big.sum())) < 0.5, -0.75, 0.75).astype(np.float32)
     c0 = np.array([-0.01, -0.002, 0.004, 0.012], np.float32)
     say("keyed sum: fixed-point wraps")
-    res = gpu(keys, c0, 2, g=g)
+    plan = edkm.Plan(n, 2, ITERS)     # five patterns would choose the 64-bit mode: force 32-bit
+    edkm.plan_set_keyed_mode(plan, edkm.KEYED_I32)
+    res = gpu(keys, c0, 2, g=g, plan=plan)
     check(res, oracle(keys, c0, g, form="table"), what="fixed-point wraps")
+
+
+@pytest.mark.parametrize("fmt", ["fp16", "bf16"])
+@pytest.mark.parametrize("mode", ["auto", "i32", "u64"])
+def test_keyed_sum_modes_match_oracle(fmt, mode):
+    """Both keyed-sum accumulator modes, forced or chosen from the data (fp16
+    patterns choose 32-bit, bf16 ones 64-bit), give the oracle's gradients."""
+    n = 300_007
+    keys = inputs.weights(n, 86, True, fmt)
+    c0 = inputs.quantile_init(keys, 8, fmt)
+    g = inputs.upstream_grad(n, 87)
+    plan = edkm.Plan(n, 3, ITERS, key_format=fmt)
+    edkm.plan_set_keyed_mode(plan, {"auto": edkm.KEYED_AUTO, "i32": edkm.KEYED_I32,
+                                    "u64": edkm.KEYED_U64}[mode])
+    say("keyed modes", fmt, mode)
+    res = gpu(keys, c0, 3, g=g, plan=plan, key_format=fmt)
+    check(res, oracle(keys, c0, g, fmt=fmt), what="keyed %s %s" % (fmt, mode))
 
 
 def test_keyed_sum_heavy_tailed_gradient():
@@ -408,18 +429,19 @@ def test_call_order_and_key_buffer_checks():
 
 # ------------------------------------------------------------------ full workload shapes
 
-@pytest.mark.parametrize("cfg,bits", [(2, 3), (3, 3), (3, 4)])
-def test_full_size_matrix(cfg, bits):
+@pytest.mark.parametrize("cfg,bits,fmt", [(2, 3, "fp16"), (3, 3, "fp16"), (3, 4, "fp16"),
+                                          (2, 3, "bf16"), (3, 4, "bf16")])
+def test_full_size_matrix(cfg, bits, fmt):
     w = inputs.WORKLOADS[cfg]
     _, r, c = w["mats"][0]
     n = r * c
-    keys = inputs.fp16_weights(n, inputs.weight_seed(cfg, 0), outliers=w["outliers"])
-    c0 = inputs.quantile_init(keys, 1 << bits)
+    keys = inputs.weights(n, inputs.weight_seed(cfg, 0), w["outliers"], fmt)
+    c0 = inputs.quantile_init(keys, 1 << bits, fmt)
     g = inputs.upstream_grad(n, inputs.grad_seed(cfg, 0))
-    say("full", cfg, bits, n)
-    res = gpu(keys, c0, bits, g=g, want_counts=True)
+    say("full", cfg, bits, fmt, n)
+    res = gpu(keys, c0, bits, g=g, want_counts=True, key_format=fmt)
     assert np.array_equal(res["counts"].view(np.uint32), table.histogram(keys))
-    check(res, oracle(keys, c0, g, form="table"), what="cfg%d bits=%d" % (cfg, bits))
+    check(res, oracle(keys, c0, g, form="table", fmt=fmt), what="cfg%d bits=%d %s" % (cfg, bits, fmt))
 
 
 def test_decoder_layer_batch_full_size():
@@ -451,3 +473,136 @@ def test_decoder_layer_batch_full_size():
         res = dict(iters=it[i].cpu().numpy(), c_out=co[i].cpu().numpy(), w_tilde=wt[i].cpu().numpy(),
                    grad_w=gw[i].cpu().numpy(), grad_c=gc[i].cpu().numpy())
         check(res, oracle(keys, c0, g, form="table"), what=w["mats"][i][0])
+
+
+# ------------------------------------------------------------------ bf16 weights
+
+BF16_CASES = [(1, 3, False, 31), (4097, 2, True, 32), (65573, 3, True, 33), (300_007, 4, True, 34),
+              (1_000_003, 3, False, 35)]
+
+
+@pytest.mark.parametrize("n,bits,outl,seed", BF16_CASES)
+def test_bf16_unique_path_matches_oracle(n, bits, outl, seed):
+    """bfloat16 weights: the same table machinery with the bf16 decode."""
+    keys = inputs.bf16_weights(n, seed, outl)
+    c0 = inputs.quantile_init(keys, 1 << bits, "bf16")
+    g = inputs.upstream_grad(n, seed + 1)
+    say("bf16 unique", n, bits)
+    res = gpu(keys, c0, bits, g=g, want_counts=True, key_format="bf16")
+    np.testing.assert_array_equal(res["counts"].view(np.uint32), table.histogram(keys))
+    assert int(res["num_unique"][0]) == np.unique(keys).size
+    form = "dense" if n <= 300_007 else "table"
+    check(res, oracle(keys, c0, g, form=form, fmt="bf16"), what="bf16 n=%d" % n)
+
+
+def test_bf16_dense_path_matches_oracle():
+    keys = inputs.bf16_weights(65573, 36, outliers=True)
+    c0 = inputs.quantile_init(keys, 8, "bf16")
+    g = inputs.upstream_grad(keys.size, 37)
+    say("bf16 dense")
+    res = gpu(keys, c0, 3, g=g, dense=True, key_format="bf16")
+    check(res, oracle(keys, c0, g, fmt="bf16"), what="bf16 dense")
+
+
+@pytest.mark.parametrize("dense_path", [False, True])
+def test_bf16_output_within_one_ulp(dense_path):
+    """16-bit W~ outputs take the weight format: bf16, round to nearest even."""
+    keys = inputs.bf16_weights(65536 + 5, 38)
+    c0 = inputs.quantile_init(keys, 8, "bf16")
+    say("bf16 out", dense_path)
+    res = gpu(keys, c0, 3, out_half=True, dense=dense_path, key_format="bf16")
+    assert_bf16_within_ulp(res["w_tilde"].view(np.uint16), oracle(keys, c0, fmt="bf16")["w_tilde"])
+
+
+def test_bf16_special_values():
+    """Signed zeros, bf16 subnormals (fp32 subnormals), the smallest normals and
+    +-1: exact decode, and the zero/subnormal magnitudes fall outside the 8-byte
+    window (global fallback)."""
+    keys = inputs.bf16_weights(100_003, 39)
+    rng = np.random.default_rng(39)
+    extra = np.array([0x0000, 0x8000, 0x0001, 0x8001, 0x007F, 0x807F, 0x0080, 0x8080, 0x3F80,
+                      0xBF80], dtype=np.uint16)
+    pos = rng.choice(keys.size, size=4 * extra.size, replace=False)
+    keys[pos] = np.resize(extra, pos.size)
+    c0 = inputs.quantile_init(keys, 16, "bf16")
+    g = inputs.upstream_grad(keys.size, 40)
+    say("bf16 special")
+    res = gpu(keys, c0, 4, g=g, key_format="bf16")
+    check(res, oracle(keys, c0, g, fmt="bf16"), what="bf16 special")
+
+
+def test_bf16_far_values_take_the_global_tables():
+    """2,000 weights at +-1e30 (magnitudes far outside both LDS windows) with a
+    centroid on each: every lookup of theirs goes to the global tables.  (Values
+    that drag a centroid into the empty space between clusters are avoided: once
+    every attention to a centroid is below fp32's range but not fp64's, the
+    two precisions legitimately take different empty-cluster decisions.)"""
+    keys = inputs.bf16_weights(100_003, 44)
+    rng = np.random.default_rng(44)
+    pos = rng.choice(keys.size, size=2000, replace=False)
+    keys[pos[:1000]] = 0x7149
+    keys[pos[1000:]] = 0xF149
+    normal = np.ones(keys.size, bool)
+    normal[pos] = False
+    far = float(inputs.values(np.array([0x7149], np.uint16), "bf16")[0])
+    c0 = np.sort(np.concatenate([inputs.quantile_init(keys[normal], 14, "bf16"),
+                                 np.float32([far, -far])])).astype(np.float32)
+    g = inputs.upstream_grad(keys.size, 45)
+    say("bf16 far values")
+    res = gpu(keys, c0, 4, g=g, key_format="bf16")
+    check(res, oracle(keys, c0, g, fmt="bf16"), what="bf16 far values")
+
+
+def test_bf16_nonfinite_weights():
+    keys = inputs.bf16_weights(50_000, 42)
+    bad = keys.copy()
+    idx = [5, 777, 40_000, 49_999]
+    bad[idx] = [0x7F80, 0xFF80, 0x7FC0, 0x7F81]
+    c0 = inputs.quantile_init(keys, 8, "bf16")
+    say("bf16 non-finite checked")
+    with pytest.raises(edkm.EdkmError) as e:
+        gpu(bad, c0, 3, check_finite=True, key_format="bf16")
+    assert e.value.status == edkm.ERR_NONFINITE
+    say("bf16 non-finite unchecked")
+    g = inputs.upstream_grad(bad.size, 43)
+    res = gpu(bad, c0, 3, g=g, key_format="bf16")
+    finite = np.ones(bad.size, bool)
+    finite[idx] = False
+    ref = oracle(bad[finite], c0, g[finite], fmt="bf16")
+    assert np.all(np.isnan(res["w_tilde"][~finite]))
+    assert np.all(np.isnan(res["grad_w"][~finite]))
+    assert_close(res["c_out"], ref["c_out"], TOL_FWD, "c_out")
+    assert_close(res["w_tilde"][finite], ref["w_tilde"], TOL_FWD, "w_tilde")
+    assert_close(res["grad_w"][finite], ref["gw"], TOL_BWD, "grad_w")
+    assert_close(res["grad_c"], ref["gc"], TOL_BWD, "grad_c")
+
+
+def test_mixed_format_batch_equals_single_calls():
+    """A batch mixing fp16 and bf16 matrices is cut into launch groups of one
+    format each; every matrix equals its single-matrix call bitwise in the
+    forward."""
+    spec = [(65536, "fp16"), (100_003, "bf16"), (70_001, "bf16"), (30_000, "fp16")]
+    ks = [inputs.weights(n, 150 + i, i == 1, fmt) for i, (n, fmt) in enumerate(spec)]
+    c0s = [inputs.quantile_init(k, 8, fmt) for k, (_, fmt) in zip(ks, spec)]
+    gs = [inputs.upstream_grad(n, 160 + i) for i, (n, _) in enumerate(spec)]
+    say("mixed-format batch")
+    plans = [edkm.Plan(n, 3, ITERS, key_format=fmt) for n, fmt in spec]
+    kd = [dkeys(k) for k in ks]
+    ci = [torch.from_numpy(c).to(DEV) for c in c0s]
+    co = [torch.empty(8, device=DEV) for _ in spec]
+    wt = [torch.empty(n, device=DEV) for n, _ in spec]
+    it = [torch.zeros(1, dtype=torch.int32, device=DEV) for _ in spec]
+    gd = [torch.from_numpy(g).to(DEV) for g in gs]
+    gw = [torch.empty(n, device=DEV) for n, _ in spec]
+    gc = [torch.empty(8, device=DEV) for _ in spec]
+    edkm.init_unique_batch(plans, kd)
+    edkm.forward_batch(plans, kd, TAU, 0.0, ci, co, wt, False, it)
+    edkm.backward_batch(plans, kd, gd, gw, gc)
+    torch.cuda.synchronize()
+    for i, (n, fmt) in enumerate(spec):
+        single = gpu(ks[i], c0s[i], 3, g=gs[i], key_format=fmt)
+        assert np.array_equal(co[i].cpu().numpy(), single["c_out"])
+        assert np.array_equal(wt[i].cpu().numpy(), single["w_tilde"])
+        res = dict(iters=it[i].cpu().numpy(), c_out=co[i].cpu().numpy(), w_tilde=wt[i].cpu().numpy(),
+                   grad_w=gw[i].cpu().numpy(), grad_c=gc[i].cpu().numpy())
+        check(res, oracle(ks[i], c0s[i], gs[i], fmt=fmt), what="mixed %d %s" % (i, fmt))

@@ -127,6 +127,21 @@ def test_two_point_fp16_keys():
     assert abs(f["w_tilde"][0] - wt) <= 1e-15
 
 
+def test_two_point_bf16_keys():
+    """The two-point closed form through the bf16 key path: x = 0.01 rounds to
+    the bf16 value 0x3C24 = 0.010009765625, and C^(0) = (-0.004, 0.004) keeps
+    min(x, c) = c in the first step as in the fp16 case."""
+    x = float(np.float32(0.010009765625))
+    keys = np.array([0x3C24, 0xBC24] * 64, dtype=np.uint16)
+    assert dense.bf16_value(0x3C24) == x and table.key_values(np.array([0xBC24]), "bf16")[0] == -x
+    f = dense.forward(keys, [-0.004, 0.004], 2e-3, 5, fmt="bf16")
+    cs, wt = _two_point(x, 0.004, 2e-3, 5)
+    assert abs(f["c_out"][1] - cs[5]) <= 1e-15
+    assert abs(f["w_tilde"][0] - wt) <= 1e-15
+    ft = table.forward(keys, [-0.004, 0.004], 2e-3, 5, fmt="bf16")
+    assert abs(ft["w_tilde"][1] + wt) <= 1e-15
+
+
 def _lloyd(v, c0, T):
     """Textbook hard k-means: argmin assignment (lowest index on ties), cluster means,
     an empty cluster keeps its centroid."""
@@ -267,8 +282,9 @@ def test_unit_upstream_gradient_identity(k, eps):
 
 
 @pytest.mark.parametrize("form", ["dense", "table"])
-@pytest.mark.parametrize("k,eps", [(4, 0.0), (8, 0.0), (16, 1e-5)])
-def test_translation_gradient_identity(form, k, eps):
+@pytest.mark.parametrize("k,eps,fmt", [(4, 0.0, "fp16"), (8, 0.0, "fp16"), (16, 1e-5, "fp16"),
+                                       (8, 0.0, "bf16")])
+def test_translation_gradient_identity(form, k, eps, fmt):
     """Shifting every weight and every initial centroid by d leaves |w - c| and so
     every map unchanged, and shifts each C^(t) and every W~_i by exactly d (map
     rows sum to one).  Hence L(w + d, C^(0) + d) = L + d sum_i g_i and, for any
@@ -276,10 +292,10 @@ def test_translation_gradient_identity(form, k, eps):
     dropped term in the centroid path breaks it; the quantile initial centroids
     sit exactly on weights, so the sgn(0) = 0 convention is exercised too."""
     mod = dense if form == "dense" else table
-    keys = inputs.fp16_weights(40_000, 90 + k, outliers=True)
-    c0 = inputs.quantile_init(keys, k).astype(np.float64)
+    keys = inputs.weights(40_000, 90 + k, True, fmt)
+    c0 = inputs.quantile_init(keys, k, fmt).astype(np.float64)
     g = inputs.upstream_grad(keys.size, 91 + k).astype(np.float64)
-    f = mod.forward(keys, c0, 2e-3, 5, eps=eps)
+    f = mod.forward(keys, c0, 2e-3, 5, eps=eps, fmt=fmt)
     gw, gc = mod.backward(keys, f, g)[:2]
     lhs = gw.sum() + gc.sum()
     assert abs(lhs - g.sum()) <= 1e-11 * (np.abs(gw).sum() + np.abs(g).sum())
@@ -302,16 +318,17 @@ def test_backward_is_linear_in_upstream_per_key():
 
 # --------------------------------------------------------------------------- second oracle
 
-@pytest.mark.parametrize("bits,outliers,eps", [(3, False, 0.0), (2, False, 0.0), (4, True, 0.0),
-                                                (3, True, 1e-6)])
-def test_table_oracle_equals_dense(bits, outliers, eps):
+@pytest.mark.parametrize("bits,outliers,eps,fmt", [(3, False, 0.0, "fp16"), (2, False, 0.0, "fp16"),
+                                                    (4, True, 0.0, "fp16"), (3, True, 1e-6, "fp16"),
+                                                    (3, True, 0.0, "bf16"), (4, False, 1e-6, "bf16")])
+def test_table_oracle_equals_dense(bits, outliers, eps, fmt):
     """Uniquification is exact (Sec. 2.2): the table form equals the dense map."""
-    keys = inputs.fp16_weights(65536, seed=inputs.weight_seed(1, bits), outliers=outliers)
+    keys = inputs.weights(65536, inputs.weight_seed(1, bits), outliers, fmt)
     k = 1 << bits
-    c0 = inputs.quantile_init(keys, k)
+    c0 = inputs.quantile_init(keys, k, fmt)
     g = inputs.upstream_grad(keys.size, inputs.grad_seed(1, bits)).astype(np.float64)
-    fd = dense.forward(keys, c0, 2e-3, 5, eps=eps)
-    ft = table.forward(keys, c0, 2e-3, 5, eps=eps)
+    fd = dense.forward(keys, c0, 2e-3, 5, eps=eps, fmt=fmt)
+    ft = table.forward(keys, c0, 2e-3, 5, eps=eps, fmt=fmt)
     assert fd["T"] == ft["T"]
     assert rel(ft["c_hist"][: fd["T"] + 1], fd["c_hist"][: fd["T"] + 1]) <= 1e-12
     assert rel(ft["w_tilde"], fd["w_tilde"]) <= 1e-12
@@ -361,3 +378,35 @@ def test_dense_oracle_independent_of_thread_count():
         np.testing.assert_array_equal(f1[name], f2[name])
     np.testing.assert_array_equal(r1[0], r2[0])
     np.testing.assert_array_equal(r1[1], r2[1])
+
+
+def test_bf16_decode_matches_binary32_upper_half():
+    """bfloat16 is the upper half of an IEEE binary32: the C oracle's decode by
+    the format's fields and the table oracle's numpy decode both equal numpy's
+    float32 for all 65,536 patterns (Inf/NaN patterns included)."""
+    k = np.arange(65536, dtype=np.uint16)
+    ref = (k.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    for got in (dense.decode_bf16(k), table.key_values(k, "bf16")):
+        fin = np.isfinite(ref)
+        np.testing.assert_array_equal(got[fin], ref[fin])
+        np.testing.assert_array_equal(np.isnan(got), np.isnan(ref))
+        np.testing.assert_array_equal(np.isinf(got), np.isinf(ref))
+        np.testing.assert_array_equal(np.signbit(got[fin]), np.signbit(ref[fin]))
+    assert dense.bf16_value(0x0001) == 2.0 ** -133 and dense.bf16_value(0x7F7F) == 3.3895313892515355e38
+
+
+def test_bf16_inputs_round_like_torch():
+    """The bf16 input recipe rounds the same fp32 draws as the fp16 one to
+    nearest-even, as torch's own float32 -> bfloat16 conversion does."""
+    torch = pytest.importorskip("torch")
+    n, seed = 300_007, 12
+    keys = inputs.bf16_weights(n, seed, outliers=True)
+    rng = np.random.Generator(np.random.PCG64(seed))
+    w = rng.standard_normal(n, dtype=np.float32) * np.float32(inputs.SIGMA)
+    mask = rng.random(n, dtype=np.float32) < np.float32(inputs.OUTLIER_P)
+    w[mask] = rng.standard_normal(int(mask.sum()), dtype=np.float32) * np.float32(inputs.OUTLIER_SIGMA)
+    ref = torch.from_numpy(w).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(keys, ref)
+    c0 = inputs.quantile_init(keys, 8, "bf16")
+    v = np.sort(inputs.values(keys, "bf16"))
+    np.testing.assert_array_equal(c0, v[[((2 * j + 1) * n) // 16 for j in range(8)]])
