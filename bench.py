@@ -19,6 +19,8 @@ Other workloads (--workload; one JSON line each, same fields):
                               dense per-weight-map path is timed beside it ("dense")
   stack [--bits 2|3|4]        32 decoder layers (224 matrices, 6.48e9 weights,
                               drawn on the GPU), one step over every matrix
+  palettize [--bits 1..4]     export of the decoder layer after a clustering step:
+                              packed b-bit nearest-centroid indices per weight
 
 Other modes (measurement helpers):
   --copy-calibration          run a plain 1 GiB device copy (HBM counter calibration)
@@ -329,6 +331,57 @@ def bench_mlp_outliers(args):
     return out
 
 
+def bench_palettize(args):
+    """Export of the decoder layer: after one clustering step, the packed b-bit
+    nearest-entry indices of every weight against its matrix's final centroids
+    (edkm_palettize, seven calls on one stream).  Pass events time the packing
+    kernel of each call; the roofline is its 2 + b/8 bytes per weight."""
+    import torch
+    from paper_2309_00964_amd import edkm, inputs
+    bits = args.bits or 3
+    m = Matrices(4, inputs.WORKLOADS[4]["mats"], bits, fmt=args.key_format)
+    m.step()
+    outs = [torch.empty((p.n * bits + 7) // 8, dtype=torch.uint8, device="cuda") for p in m.plans]
+    hip = HipEvents()
+    evs = [(hip.create(), hip.create()) for _ in m.plans]
+    for p, (a, e) in zip(m.plans, evs):
+        edkm.plan_set_pass_events(p, edkm.PASS_PALETTIZE, a, e)
+
+    def step():
+        for i, p in enumerate(m.plans):
+            edkm.palettize(p, m.keys[i], m.c_out[i], outs[i])
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0, t1 = hip.create(), hip.create()
+    stream = torch.cuda.current_stream().cuda_stream
+    kern_ms = [0.0] * len(m.plans)
+    wall0 = time.perf_counter()
+    hip.record(t0, stream)
+    for _ in range(args.steps):
+        step()
+        torch.cuda.synchronize()
+        for i, (a, e) in enumerate(evs):
+            kern_ms[i] += hip.elapsed_ms(a, e)
+    hip.record(t1, stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    for p in m.plans:
+        edkm.plan_set_pass_events(p, edkm.PASS_PALETTIZE, None, None)
+    elapsed = max(wall, hip.elapsed_ms(t0, t1) / 1000.0)
+    for x in [t0, t1] + [x for pair in evs for x in pair]:
+        hip.destroy(x)
+    per_w = 2.0 + bits / 8.0
+    kern_s = sum(kern_ms) / args.steps / 1000.0
+    achieved = per_w * m.total / kern_s / 1e9
+    roof = {"bound": "hbm", "kernel": "k_palettize", "achieved": achieved, "peak": PEAK_HBM_GBS,
+            "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+            "bytes_per_weight": per_w, "kernel_us_per_step": kern_s * 1e6,
+            "note": "synchronised after every step to read the per-call events"}
+    return result_line(args, "llama7b_decoder_layer_palettize_%dbit%s" % (bits, _fmt_tag(args)), m,
+                       bits, elapsed, roof, {"w_tilde": None, "output": "packed %d-bit indices" % bits})
+
+
 def bench_stack(args):
     """A 32-layer stack of decoder-layer shapes (224 matrices, 6.48e9 weights),
     drawn on the device; one step clusters every matrix forward and backward."""
@@ -420,10 +473,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", choices=("decoder_layer", "mlp_outliers", "stack"),
+    ap.add_argument("--workload", choices=("decoder_layer", "mlp_outliers", "stack", "palettize"),
                     default="decoder_layer")
-    ap.add_argument("--bits", type=int, choices=(2, 3, 4), default=None,
-                    help="mlp_outliers: 3 or 4 (default 4); stack: 2, 3 or 4 (default 3)")
+    ap.add_argument("--bits", type=int, choices=(1, 2, 3, 4), default=None,
+                    help="mlp_outliers: 3 or 4 (default 4); stack: 2, 3 or 4 (default 3); "
+                         "palettize: 1-4 (default 3)")
     ap.add_argument("--key-format", choices=("fp16", "bf16"), default="fp16",
                     help="weight format (default fp16, the metric's; bf16 is the paper's training format)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -443,7 +497,7 @@ def main():
     if not torch.cuda.is_available():
         sys.exit("bench.py needs a GPU")
     fn = {"decoder_layer": bench_decoder_layer, "mlp_outliers": bench_mlp_outliers,
-          "stack": bench_stack}[args.workload]
+          "stack": bench_stack, "palettize": bench_palettize}[args.workload]
     if args.workload == "decoder_layer" and args.bits not in (None, 3):
         sys.exit("the decoder-layer workload is 3-bit")
     print(json.dumps(fn(args)), flush=True)

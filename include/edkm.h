@@ -68,7 +68,7 @@ enum {
 /* Host-side per-matrix record.  Opaque; the caller owns the memory (stack or
  * heap) and must not copy it between calls. */
 typedef struct edkm_plan {
-    uint64_t opaque[24];
+    uint64_t opaque[32];
 } edkm_plan;
 
 /* Device workspace size for one matrix of n weights with k = 2^bits
@@ -192,7 +192,8 @@ enum {
      * exponentials per weight.  A call launches several; the events bracket
      * the last one of the call. */
     EDKM_PASS_DENSE_ITER = 4,   /* forward_dense: one centroid iteration, reads 2 B */
-    EDKM_PASS_DENSE_BITER = 5   /* backward_dense: one unrolled iteration, 2 B + 4 B + 4 B */
+    EDKM_PASS_DENSE_BITER = 5,  /* backward_dense: one unrolled iteration, 2 B + 4 B + 4 B */
+    EDKM_PASS_PALETTIZE = 6     /* palettize: packed indices, 2 B + b/8 B */
 };
 /* When set (non-NULL), later calls on this plan record `start` on the stream
  * right before that pass's launch and `stop` right after it; in a batched call
@@ -200,6 +201,24 @@ enum {
  * the events (created with timing enabled) and reads them with
  * hipEventElapsedTime.  NULL events switch the hook off.  Host only. */
 edkm_status edkm_plan_set_pass_events(edkm_plan* plan, int pass, hipEvent_t start, hipEvent_t stop);
+
+/* Palettization: the compressed artefact of weight clustering, a lookup
+ * table of k entries plus a b-bit index per weight (Sec. 2).  Each weight
+ * takes the index of its nearest table entry,
+ *   index_i = the j minimising |w_i - lut[j]|   (lowest j on ties),
+ * decided in fp32 (w_i is exact in fp32; one fp32 subtraction per entry);
+ * non-finite weights get index 0.  The indices are packed little-endian, b =
+ * bits of the plan: index i occupies bits [b i, b i + b) of the output bit
+ * stream, byte m holding stream bits 8m..8m+7 (least significant first);
+ * bits past n b are zero.
+ *   w_bits       device, n patterns (the plan's weight format)
+ *   lut          device float[k]: the table, e.g. c_out of edkm_forward
+ *   indices_out  device uint8[ceil(n b / 8)]
+ * Needs no init_unique and leaves the plan's forward/backward state alone
+ * (it uses its own part of the workspace).  Cost: one read of the keys and
+ * one write of n b / 8 bytes. */
+edkm_status edkm_palettize(edkm_plan* plan, const uint16_t* w_bits, const float* lut,
+                           uint8_t* indices_out, hipStream_t stream);
 
 /* Keyed-gradient accumulators (the backward's keyed reduction).  AUTO, the
  * default, chooses per matrix at init_unique from how concentrated the

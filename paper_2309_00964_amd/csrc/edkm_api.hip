@@ -46,7 +46,7 @@ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
     size_t counts, tab, H, R, HR, G, chist, shist, ghist, ehist, tpart, bpart, dpart, span, wscan, wstat,
-        part, st, total;
+        part, pidx, st, total;
 };
 
 Layout layout(int max_iter) {
@@ -73,6 +73,7 @@ Layout layout(int max_iter) {
     L.wscan = take(MAGS * sizeof(uint32_t));
     L.wstat = take(32 * 8 * sizeof(int));
     L.part = take((size_t)NP_MAX_WG * ROW4 * sizeof(uint32_t));
+    L.pidx = take(NKEYS);
     L.total = o;
     return L;
 }
@@ -136,6 +137,7 @@ Ws carve_workspace(void* base, int max_iter) {
     const Layout L = layout(max_iter);
     char* c = static_cast<char*>(base);
     Ws w;
+    w.pidx = reinterpret_cast<uint8_t*>(c + L.pidx);
     w.st = reinterpret_cast<DevState*>(c + L.st);
     w.counts = reinterpret_cast<uint32_t*>(c + L.counts);
     w.tab = reinterpret_cast<float*>(c + L.tab);
@@ -482,6 +484,24 @@ edkm_status edkm_plan_set_pass_events(edkm_plan* plan, int pass, hipEvent_t star
     PlanImpl* P = impl(plan);
     P->ev.start[pass] = start;
     P->ev.stop[pass] = stop;
+    return EDKM_OK;
+}
+
+edkm_status edkm_palettize(edkm_plan* plan, const uint16_t* w_bits, const float* lut,
+                           uint8_t* indices_out, hipStream_t stream) {
+    if (!plan_ok(plan) || !w_bits || !lut || !indices_out) return EDKM_ERR_ARG;
+    PlanImpl* P = impl(plan);
+    BatchArgs b;
+    std::memset(&b, 0, sizeof(b));
+    b.count = 1;
+    MatArgs& M = b.m[0];
+    fill_mat(M, P, w_bits);
+    M.c_in = lut;
+    M.wt = indices_out;
+    M.vec = aligned16(w_bits) && ((uintptr_t)indices_out & 3u) == 0;
+    const char* where = "";
+    const hipError_t e = launch_palettize(b, stream, &where, &P->ev);
+    if (e != hipSuccess) return hip_fail(&plan, 0, 1, e, where);
     return EDKM_OK;
 }
 

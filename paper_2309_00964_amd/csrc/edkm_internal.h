@@ -58,6 +58,7 @@ struct Ws {
     uint32_t* wscan;    // [MAGS]  block-local running counts (window selection)
     int* wstat;         // [32 * 8]  per-block totals and ranges (window selection)
     uint32_t* part;     // [NP_MAX_WG * ROW4]  N-pass partial rows
+    uint8_t* pidx;      // [NKEYS]  palettization: nearest lookup-table entry per pattern
     DevState* st;
 };
 
@@ -104,7 +105,7 @@ struct BatchArgs {
 
 // Optional timing events recorded around the N-sized passes (diagnostics).
 enum Pass { PASS_HIST = 0, PASS_GATHER_WT = 1, PASS_KEYED_GRAD = 2, PASS_GATHER_GRAD = 3,
-            PASS_DENSE_ITER = 4, PASS_DENSE_BITER = 5, NPASS = 6 };
+            PASS_DENSE_ITER = 4, PASS_DENSE_BITER = 5, PASS_PALETTIZE = 6, NPASS = 7 };
 struct PassEvents {
     hipEvent_t start[NPASS];
     hipEvent_t stop[NPASS];
@@ -121,6 +122,8 @@ hipError_t launch_forward(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_t
                               const PassEvents* ev = nullptr);
 hipError_t launch_backward(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_t s, const char** where,
                               const PassEvents* ev = nullptr);
+hipError_t launch_palettize(BatchArgs& b, hipStream_t s, const char** where,
+                            const PassEvents* ev = nullptr);
 hipError_t launch_forward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where,
                                 const PassEvents* ev = nullptr);
 hipError_t launch_backward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where,

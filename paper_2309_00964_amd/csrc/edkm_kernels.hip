@@ -21,6 +21,7 @@
 #include "edkm_internal.h"
 
 #include <hip/hip_fp16.h>
+#include <algorithm>
 
 namespace edkm {
 
@@ -961,6 +962,86 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
 }
 
 // ----------------------------------------------------------------------------
+// palettization: the lookup table of k entries and a b-bit index per weight
+
+// Nearest lookup-table entry for every pattern: fp32 distance |v - lut_j|,
+// lowest entry on ties; non-finite patterns get 0.  Grid NKEYS / 256.
+__global__ void __launch_bounds__(256) k_pal_table(BatchArgs b) {
+    __shared__ float lut[KMAX];
+    const MatArgs& M = b.m[0];
+    if (threadIdx.x < M.k) lut[threadIdx.x] = M.c_in[threadIdx.x];
+    __syncthreads();
+    const uint32_t u = blockIdx.x * 256 + threadIdx.x;
+    uint32_t best = 0;
+    if (key_finite(u, M.fmt)) {
+        const float v = key_value(u, M.fmt);
+        float bd = fabsf(v - lut[0]);
+        for (int j = 1; j < M.k; ++j) {
+            const float d = fabsf(v - lut[j]);
+            if (d < bd) { bd = d; best = (uint32_t)j; }
+        }
+    }
+    M.ws.pidx[u] = (uint8_t)best;
+}
+
+// Packed indices: index i occupies bits [B i, B i + B) of a little-endian bit
+// stream.  A thread packs a group of 32 weights into B 32-bit words (4 B bytes
+// at byte 4 B g for group g); the per-pattern index table (64 KiB) sits in LDS.
+// The matrix's last, partial group and unaligned buffers are written byte by
+// byte, never past the ceil(n B / 8) output bytes.  Grid-stride over groups.
+template <int B>
+__global__ void __launch_bounds__(1024) k_palettize(BatchArgs b) {
+    __shared__ uint4 tbl4[NKEYS / 16];
+    const MatArgs& M = b.m[0];
+    const uint4* src = reinterpret_cast<const uint4*>(M.ws.pidx);
+    for (int i = threadIdx.x; i < NKEYS / 16; i += blockDim.x) tbl4[i] = src[i];
+    __syncthreads();
+    const uint8_t* tbl = reinterpret_cast<const uint8_t*>(tbl4);
+    const uint16_t* keys = M.keys;
+    uint32_t* out32 = reinterpret_cast<uint32_t*>(M.wt);
+    uint8_t* out8 = reinterpret_cast<uint8_t*>(M.wt);
+    const uint64_t n = M.n;
+    const uint64_t groups = (n + 31) / 32;
+    const uint64_t nbytes = (n * B + 7) / 8;
+    for (uint64_t gi = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; gi < groups;
+         gi += (uint64_t)gridDim.x * blockDim.x) {
+        const uint64_t base = gi * 32;
+        uint32_t w[B];
+#pragma unroll
+        for (int q = 0; q < B; ++q) w[q] = 0u;
+        auto put = [&](int t, uint32_t idx) {   // t is a compile-time constant after unrolling
+            const int pos = t * B;
+            w[pos >> 5] |= idx << (pos & 31);
+            if ((pos & 31) + B > 32) w[(pos >> 5) + 1] |= idx >> (32 - (pos & 31));
+        };
+        if (base + 32 <= n && M.vec) {
+            uint4 q[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) q[r] = ld_u4(keys + base + 8 * r);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const uint32_t x[4] = {q[r].x, q[r].y, q[r].z, q[r].w};
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    put(8 * r + 2 * h, tbl[x[h] & 0xFFFFu]);
+                    put(8 * r + 2 * h + 1, tbl[x[h] >> 16]);
+                }
+            }
+#pragma unroll
+            for (int q2 = 0; q2 < B; ++q2) out32[gi * B + q2] = w[q2];
+        } else {
+#pragma unroll
+            for (int t = 0; t < 32; ++t)
+                if (base + t < n) put(t, tbl[keys[base + t]]);
+            const uint64_t b0 = gi * 4 * B;
+#pragma unroll
+            for (int q2 = 0; q2 < 4 * B; ++q2)
+                if (b0 + q2 < nbytes) out8[b0 + q2] = (uint8_t)(w[q2 >> 2] >> (8 * (q2 & 3)));
+        }
+    }
+}
+
+// ----------------------------------------------------------------------------
 // backward table phase
 
 // Direct use of A^(T) and C^(T) by W~: with G_u (merged keyed sums), partials of gamma_j = sum_u G_u a^(T)_uj (= dL/dC^(T)_j) and
@@ -1466,6 +1547,21 @@ hipError_t launch_backward(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_
                            const PassEvents* ev) {
     (void)hipGetLastError();
     EDKM_DISPATCH_K(b.m[0].k, backward_k, b, grid_np, max_t, s, where, ev);
+}
+
+hipError_t launch_palettize(BatchArgs& b, hipStream_t s, const char** where, const PassEvents* ev) {
+    (void)hipGetLastError();
+    EDKM_LAUNCH("k_pal_table", k_pal_table, dim3(NKEYS / 256), dim3(256), b);
+    const uint64_t groups = (b.m[0].n + 31) / 32;
+    const dim3 grid((uint32_t)std::min<uint64_t>(512, (groups + 1023) / 1024));
+    switch (b.m[0].k) {
+    case 2: EDKM_NPASS(PASS_PALETTIZE, "k_palettize", k_palettize<1>, grid, dim3(1024), b); break;
+    case 4: EDKM_NPASS(PASS_PALETTIZE, "k_palettize", k_palettize<2>, grid, dim3(1024), b); break;
+    case 8: EDKM_NPASS(PASS_PALETTIZE, "k_palettize", k_palettize<3>, grid, dim3(1024), b); break;
+    case 16: EDKM_NPASS(PASS_PALETTIZE, "k_palettize", k_palettize<4>, grid, dim3(1024), b); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipSuccess;
 }
 
 hipError_t launch_forward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where,

@@ -49,7 +49,7 @@ ERR_STATE = -4
 ERR_HIP = -5
 NKEYS = 65536
 PASS_HIST, PASS_GATHER_WT, PASS_KEYED_GRAD, PASS_GATHER_GRAD = 0, 1, 2, 3
-PASS_DENSE_ITER, PASS_DENSE_BITER = 4, 5
+PASS_DENSE_ITER, PASS_DENSE_BITER, PASS_PALETTIZE = 4, 5, 6
 KEYS_FP16, KEYS_BF16 = 0, 1
 KEYED_AUTO, KEYED_I32, KEYED_U64 = -1, 0, 1
 KEY_FORMATS = {"fp16": KEYS_FP16, "bf16": KEYS_BF16}
@@ -63,7 +63,7 @@ class EdkmError(RuntimeError):
 
 
 class edkm_plan(ctypes.Structure):
-    _fields_ = [("opaque", ctypes.c_uint64 * 24)]
+    _fields_ = [("opaque", ctypes.c_uint64 * 32)]
 
 
 _P = ctypes.c_void_p
@@ -76,6 +76,7 @@ _SIGS = {
     "edkm_plan_init": (_i32, [_PLAN, _u64, _i32, _i32, _P, _sz]),
     "edkm_plan_init_ex": (_i32, [_PLAN, _u64, _i32, _i32, _i32, _P, _sz]),
     "edkm_plan_set_keyed_mode": (_i32, [_PLAN, _i32]),
+    "edkm_palettize": (_i32, [_PLAN, _P, _P, _P, _P]),
     "edkm_init_unique": (_i32, [_PLAN, _P, _P, _P, _i32, _P]),
     "edkm_forward": (_i32, [_PLAN, _P, _f32, _f32, _P, _P, _P, _i32, _P, _P]),
     "edkm_backward": (_i32, [_PLAN, _P, _P, _P, _P, _P]),
@@ -174,6 +175,16 @@ class Plan:
     @property
     def ref(self):
         return ctypes.byref(self.plan)
+
+
+def palettize(plan: Plan, w_bits, lut, indices_out, stream=None) -> None:
+    """Packed b-bit nearest-entry indices of every weight against ``lut``
+    (device float[k]); ``indices_out`` holds ceil(n b / 8) bytes."""
+    need = (plan.n * plan.bits + 7) // 8
+    if indices_out.numel() * indices_out.element_size() < need:
+        raise EdkmError(ERR_ARG, "palettize", "indices_out needs %d bytes" % need)
+    _check(_lib.edkm_palettize(plan.ref, _ptr(w_bits, 2, "w_bits"), _ptr(lut, 4), _ptr(indices_out, 1),
+                               _stream(stream)), "palettize", (plan,))
 
 
 def plan_set_keyed_mode(plan: Plan, mode: int) -> None:

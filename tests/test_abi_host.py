@@ -150,3 +150,8 @@ def test_plan_init_ex_key_formats():
         assert lib.edkm_plan_init_ex(ctypes.byref(p), 1000, 3, 5, fmt, FAKE_WS, ws) == edkm.OK
     for fmt in (-1, 2):
         assert lib.edkm_plan_init_ex(ctypes.byref(p), 1000, 3, 5, fmt, FAKE_WS, ws) == edkm.ERR_ARG
+
+
+def test_plan_record_size_matches_header():
+    m = re.search(r"uint64_t\s+opaque\[(\d+)\]", open(HEADER).read())
+    assert m and ctypes.sizeof(edkm.edkm_plan) == 8 * int(m.group(1))
