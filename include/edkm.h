@@ -226,6 +226,12 @@ edkm_status edkm_palettize(edkm_plan* plan, const uint16_t* w_bits, const float*
  * lanes of an atomic share a pattern (fp16 weights), 64-bit fixed point with
  * plain atomics when many do (bf16 weights, low-entropy data).  Both are exact
  * in the sense that no sum is lost; they differ in speed and in the last bits.
+ * Limit of the 32-bit mode: its overflow carries are added to fp32 sums, which
+ * stay exact while a pattern's same-sign gradient sum is below about 2^28
+ * times a typical |gradient|.  AUTO picks the 32-bit mode only when every
+ * pattern holds under 1.7% of the weights (at most 7.4e7 of 2^32), so it
+ * never reaches that; forcing EDKM_KEYED_I32 on data where one pattern holds
+ * more than 2^28 weights can lose precision.
  * The setting takes effect at the next init_unique on this plan.  Host only. */
 enum {
     EDKM_KEYED_AUTO = -1,
