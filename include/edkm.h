@@ -38,6 +38,10 @@
  *     GPU.  Distinct plans with distinct workspaces may be used concurrently.
  *   - Errors are returned, never thrown; argument errors are detected on the
  *     host before any HIP call and leave the plan unchanged.
+ *   - Every entry point can be captured in a HIP graph (no allocation, no
+ *     memset, no synchronisation), except init_unique with check_finite = 1,
+ *     which synchronises.  A replay repeats the device work of the captured
+ *     calls on the buffers they were given.
  */
 #ifndef EDKM_H
 #define EDKM_H
