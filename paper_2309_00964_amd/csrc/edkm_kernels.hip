@@ -1,8 +1,8 @@
 // eDKM hot-path kernels for gfx950 (MI355X).
 //
-// Uniquified DKM (paper Sec. 2.2): the attention map of N fp16 weights against
-// k <= 16 centroids is kept as a 65,536-row table indexed by the weights' own
-// bit patterns.  Work splits into
+// Uniquified DKM (paper Sec. 2.2): the attention map of N 16-bit weights (fp16
+// or bf16) against k <= 16 centroids is kept as a 65,536-row table indexed by
+// the weights' own bit patterns.  Work splits into
 //   * N-sized passes, bound by HBM bandwidth: the pattern histogram, the W~
 //     gather, the keyed reduction of dL/dW~ and the dL/dw gather.  They run one
 //     1024-thread workgroup per CU, keep a window of the table in LDS (up to
@@ -12,7 +12,9 @@
 //   * table-sized phases, bound by latency: the T softmax / centroid-update
 //     iterations and the unrolled analytic backward, one launch per iteration,
 //     64 workgroups per matrix, fixed-order tree reductions so the forward is
-//     bitwise repeatable.
+//     bitwise repeatable;
+//   * the dense comparison path (the same mathematics per weight over the
+//     N x k map) and the palettization export (packed nearest-entry indices).
 // Every launch carries up to MAXB matrices (blockIdx.y or a workgroup range per
 // matrix), so a whole decoder layer pays each launch latency once.
 //
@@ -898,7 +900,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
     }
 }
 
-// dL/dw_i = g_i H[bits_i] + R[bits_i]; the window [lo8, lo8 + w8) of (H, R) sits
+// dL/dw_i = g_i H[bits_i] + R[bits_i]; the 8-byte window [lo8, lo8 + w8) of (H, R) sits
 // in LDS.  The first workgroup of each matrix also finishes dL/dC^(0); every
 // workgroup clears a slice of G for the next backward.
 __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {

@@ -85,3 +85,18 @@ def test_cpu_baseline_record():
     assert r["kind"] == "oracle" and r["unit"] == "weights/s" and r["value"] > 0 and r["cores"] >= 1
     assert r["single_thread"]["cores"] == 1 and r["single_thread"]["value"] > 0
     assert r["table_form"]["value"] > 0 and "q_proj" in r["table_form"]["sample"]
+
+
+def test_source_hash_ignores_comments_only(tmp_path, monkeypatch):
+    src = os.path.join(ROOT, "paper_2309_00964_amd", "csrc")
+    dst = tmp_path / "paper_2309_00964_amd" / "csrc"
+    dst.mkdir(parents=True)
+    for f in os.listdir(src):
+        (dst / f).write_text(open(os.path.join(src, f)).read())
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    base = bench.source_hash()
+    k = dst / "edkm_kernels.hip"
+    k.write_text("// a new comment line\n" + k.read_text().replace("namespace edkm {", "namespace edkm {  /* x */", 1))
+    assert bench.source_hash() == base
+    k.write_text(k.read_text() + "\nstatic int unused_probe_value = 1;\n")
+    assert bench.source_hash() != base
