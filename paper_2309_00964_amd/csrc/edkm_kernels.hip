@@ -294,9 +294,13 @@ struct KeysG4 { uint2 q; float4 g; };
 typedef unsigned int v4u_t __attribute__((ext_vector_type(4)));
 typedef unsigned int v2u_t __attribute__((ext_vector_type(2)));
 typedef float v4f_t __attribute__((ext_vector_type(4)));
-// Streaming loads.  Non-temporal loads (nt) help the passes that only read the
-// weights (histogram, keyed sum) and hurt the gathers, which use plain loads;
-// stores are always plain (nt stores halve the gathers' bandwidth here).
+// Streaming loads and stores.  Measured with the round-robin tile sweep:
+// non-temporal (nt) loads help the read-only passes (histogram, keyed sum) and
+// the gradient gather; the W~ gather keeps plain loads, which leave the keys
+// in the caches for the keyed sum when a backward follows.  The gathers'
+// float4 outputs use nt stores (gradient gather 404 -> 381 us on the decoder
+// layer, and the kernel after the W~ gather no longer inherits its dirty
+// lines).
 __device__ __forceinline__ uint4 ld_u4(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 __device__ __forceinline__ uint2 ld_u2(const void* p) { return *reinterpret_cast<const uint2*>(p); }
 __device__ __forceinline__ float4 ld_f4(const float* p) { return *reinterpret_cast<const float4*>(p); }
@@ -312,7 +316,9 @@ __device__ __forceinline__ float4 ld_f4_nt(const float* p) {
     const v4f_t v = __builtin_nontemporal_load(reinterpret_cast<const v4f_t*>(p));
     return make_float4(v.x, v.y, v.z, v.w);
 }
-__device__ __forceinline__ void st_f4(float* p, float4 x) { *reinterpret_cast<float4*>(p) = x; }
+__device__ __forceinline__ void st_f4_nt(float* p, float4 x) {
+    __builtin_nontemporal_store(v4f_t{x.x, x.y, x.z, x.w}, reinterpret_cast<v4f_t*>(p));
+}
 __device__ __forceinline__ void st_u2(void* p, uint2 x) { *reinterpret_cast<uint2*>(p) = x; }
 
 // ----------------------------------------------------------------------------
@@ -771,7 +777,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
             [&](const Keys4& r) {
                 return look4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16);
             },
-            [&](uint64_t i, float4 o) { st_f4(out + i, o); },
+            [&](uint64_t i, float4 o) { st_f4_nt(out + i, o); },
             [&](uint64_t i) { out[i] = look(keys[i]); });
     }
 }
@@ -957,9 +963,9 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
         return fmaf(gv, h.x, h.y);
     };
     for_slice<8, 4, true>(M, wl,
-        [&](uint64_t i) { return KeysG4{ld_u2(keys + i), ld_f4(g + i)}; },
+        [&](uint64_t i) { return KeysG4{ld_u2_nt(keys + i), ld_f4_nt(g + i)}; },
         [&](const KeysG4& r) { return dw4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16, r.g); },
-        [&](uint64_t i, float4 o) { st_f4(out + i, o); },
+        [&](uint64_t i, float4 o) { st_f4_nt(out + i, o); },
         [&](uint64_t i) { out[i] = dw(keys[i], g[i]); });
 }
 
