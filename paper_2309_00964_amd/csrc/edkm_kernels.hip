@@ -762,7 +762,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
         auto h2 = [&](float a, float c) -> uint32_t {
             return to_half_bits(a, M.fmt) | (to_half_bits(c, M.fmt) << 16);
         };
-        for_slice<8, 4, true>(M, wl,
+        for_slice<16, 4, true>(M, wl,
             [&](uint64_t i) { return Keys4{ld_u2(keys + i)}; },
             [&](const Keys4& r) {
                 const float4 v = look4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16);
@@ -772,7 +772,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
             [&](uint64_t i) { out[i] = (uint16_t)to_half_bits(look(keys[i]), M.fmt); });
     } else {
         float* out = reinterpret_cast<float*>(M.wt);
-        for_slice<8, 4, true>(M, wl,
+        for_slice<16, 4, true>(M, wl,
             [&](uint64_t i) { return Keys4{ld_u2(keys + i)}; },
             [&](const Keys4& r) {
                 return look4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16);
@@ -852,7 +852,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
     __syncthreads();
     float* G = M.ws.G;
     auto stream = [&](auto add) {
-        for_slice<8, 4>(M, wl,
+        for_slice<4, 4>(M, wl,
             [&](uint64_t i) { return KeysG4{ld_u2_nt(keys + i), ld_f4_nt(g + i)}; },
             [&](const KeysG4& r) {
                 add(r.q.x & 0xFFFFu, r.g.x); add(r.q.x >> 16, r.g.y);
@@ -864,7 +864,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
     };
     float* row = reinterpret_cast<float*>(M.ws.part) + (size_t)wl * ROW4;
     if (wide) {
-        const int bn = 64 - __clzll((unsigned long long)Slice<8, 4>(M).bound(M) - 1);   // 2^bn >= weights added here
+        const int bn = 64 - __clzll((unsigned long long)Slice<4, 4>(M).bound(M) - 1);   // 2^bn >= weights added here
         const int emax = emax_sh;
         const int S = 181 - bn - emax;               // 2^(emax-126) * 2^S = 2^(55-bn)
         const uint32_t elim = (uint32_t)min(emax + 6, 0xFE);
