@@ -45,8 +45,8 @@ inline PlanImpl* impl(edkm_plan* p) { return reinterpret_cast<PlanImpl*>(p); }
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
-    size_t counts, tab, H, R, HR, G, chist, shist, ghist, ehist, tpart, bpart, dpart, span, wscan, wstat,
-        part, pidx, st, total;
+    size_t counts, tab, H, R, HR, G, chist, shist, ghist, ehist, tpart, bpart, dpart, span, part, pidx,
+        st, total;
 };
 
 Layout layout(int max_iter) {
@@ -70,8 +70,6 @@ Layout layout(int max_iter) {
     L.bpart = take(tp);
     L.dpart = take((size_t)D_WG * PSTRIDE * sizeof(float));
     L.span = take(NP_MAX_WG * sizeof(int2));
-    L.wscan = take(MAGS * sizeof(uint32_t));
-    L.wstat = take(32 * 8 * sizeof(int));
     L.part = take((size_t)NP_MAX_WG * ROW4 * sizeof(uint32_t));
     L.pidx = take(NKEYS);
     L.total = o;
@@ -153,8 +151,6 @@ Ws carve_workspace(void* base, int max_iter) {
     w.bpart = reinterpret_cast<float*>(c + L.bpart);
     w.dpart = reinterpret_cast<float*>(c + L.dpart);
     w.span = reinterpret_cast<int2*>(c + L.span);
-    w.wscan = reinterpret_cast<uint32_t*>(c + L.wscan);
-    w.wstat = reinterpret_cast<int*>(c + L.wstat);
     w.part = reinterpret_cast<uint32_t*>(c + L.part);
     return w;
 }

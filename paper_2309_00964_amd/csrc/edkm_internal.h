@@ -55,8 +55,6 @@ struct Ws {
     float* bpart;       // [(max_iter+1) * T_WG * PSTRIDE]  backward table partials
     float* dpart;       // [D_WG * PSTRIDE]  dense-path partials
     int2* span;         // [NP_MAX_WG]  histogram partial spans
-    uint32_t* wscan;    // [MAGS]  block-local running counts (window selection)
-    int* wstat;         // [32 * 8]  per-block totals and ranges (window selection)
     uint32_t* part;     // [NP_MAX_WG * ROW4]  N-pass partial rows
     uint8_t* pidx;      // [NKEYS]  palettization: nearest lookup-table entry per pattern
     DevState* st;

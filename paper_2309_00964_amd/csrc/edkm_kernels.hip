@@ -476,83 +476,109 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t x, uint32_t* tmp /*
     return base + inc - x;
 }
 
-// Window selection, first half.  Grid (32, count): block x covers magnitudes
-// [1024 x, 1024 x + 1024) of both signs.  Writes, per finite magnitude,
-// the running count of weights within the block (inclusive), and per block its
-// total, occupied-pattern count, occupied magnitude range and non-finite flag.
-__global__ void __launch_bounds__(NP_THREADS) k_window_scan(BatchArgs b) {
-    __shared__ uint32_t tmp[16];
-    __shared__ int ired[5];
-    __shared__ unsigned long long sqsum;
-    const MatArgs& M = b.m[blockIdx.y];
-    const uint32_t* counts = M.ws.counts;
-    const int mag = blockIdx.x * NP_THREADS + threadIdx.x;   // < 32768
-    const uint32_t cp = counts[mag], cn = counts[0x8000 | mag];
-    if (threadIdx.x == 0) { ired[0] = 1 << 30; ired[1] = -1; ired[2] = 0; ired[3] = 0; ired[4] = 0; sqsum = 0ull; }
-    const bool fin = mag < fin_mags(M.fmt);
-    const uint32_t c = fin ? cp + cn : 0u;
-    const uint32_t incl = block_excl_scan(c, tmp) + c;        // (has block barriers)
-    if (fin) M.ws.wscan[mag] = incl;
-    if (c) { atomicMin(&ired[0], mag); atomicMax(&ired[1], mag); }
-    const int nu = (cp != 0u) + (cn != 0u);
-    if (nu) atomicAdd(&ired[2], nu);
-    if (!fin && (cp | cn)) atomicOr(&ired[3], 1);
-    if (threadIdx.x == NP_THREADS - 1) ired[4] = (int)incl;
-    // sum of squared counts (< N^2 < 2^64), for the keyed-sum mode
-    unsigned long long sq = fin ? (unsigned long long)cp * cp + (unsigned long long)cn * cn : 0ull;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) sq += __shfl_xor(sq, o, 64);
-    if ((threadIdx.x & 63) == 0) atomicAdd(&sqsum, sq);
-    __syncthreads();
-    if (threadIdx.x < 5) M.ws.wstat[blockIdx.x * 8 + threadIdx.x] = ired[threadIdx.x];
-    if (threadIdx.x == 5) M.ws.wstat[blockIdx.x * 8 + 5] = (int)(uint32_t)sqsum;
-    if (threadIdx.x == 6) M.ws.wstat[blockIdx.x * 8 + 6] = (int)(uint32_t)(sqsum >> 32);
-}
-
-// Window selection, second half; one block per matrix.  Combines the block
-// results into the occupied-pattern count, the non-finite flag, the occupied
-// finite magnitude range and the LDS windows of the later passes.  A window of
+// Window selection: one block per matrix, grid (1, count).  Wave w owns the
+// SPAN = 2048 magnitudes [2048 w, 2048 w + 2048) of both signs, in NCH = 8
+// chunks of 256; lane l holds the 4 consecutive magnitudes 4 l .. 4 l + 3 of
+// each chunk, so that loads and LDS stores are contiguous across the wave.  The
+// block builds in LDS the running count of weights over finite magnitudes
+// (within each wave's span, plus a per-wave offset) and reduces the
+// occupied-pattern count, the non-finite flag, the occupied finite magnitude
+// range and the sum of squared counts (for the keyed-sum mode).  A window of
 // width W covers the whole occupied range when it fits, else the W consecutive
 // magnitudes holding the most weights (lowest start on ties).
 __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
-    __shared__ uint32_t off[33];   // weights with magnitude < 1024 x
-    __shared__ int st5[5];
-    __shared__ unsigned long long best[2];
+    constexpr int NW = NP_THREADS / 64;
+    constexpr int SPAN = MAGS / NW;
+    constexpr int NCH = SPAN / 256;
+    __shared__ __align__(16) uint32_t pre[MAGS];   // weights with finite magnitude in [2048 w, x], w = x / 2048
+    __shared__ uint32_t woff[NW + 1];     // weights with finite magnitude < 2048 w
+    __shared__ int red[4];                // lo, hi, occupied patterns, non-finite
+    __shared__ unsigned long long sqsum, best[2];
     const MatArgs& M = b.m[blockIdx.y];
+    const int fin = fin_mags(M.fmt);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int mw = wave * SPAN + 4 * lane;   // this lane's first magnitude; chunk j adds 256 j
     if (threadIdx.x == 0) {
-        int lo = 1 << 30, hi = -1, nu = 0, nf = 0;
-        uint32_t run = 0;
-        unsigned long long sq = 0ull;
-        for (int x = 0; x < 32; ++x) {
-            const int* w = M.ws.wstat + x * 8;
-            lo = min(lo, w[0]);
-            hi = max(hi, w[1]);
-            nu += w[2];
-            nf |= w[3];
-            off[x] = run;
-            run += (uint32_t)w[4];
-            sq += (unsigned long long)(uint32_t)w[5] | ((unsigned long long)(uint32_t)w[6] << 32);
+        red[0] = 1 << 30; red[1] = -1; red[2] = 0; red[3] = 0;
+        sqsum = 0ull; best[0] = 0ull; best[1] = 0ull;
+    }
+    uint4 p[NCH], q[NCH];
+    {
+        const uint4* p4 = reinterpret_cast<const uint4*>(M.ws.counts + mw);
+        const uint4* q4 = reinterpret_cast<const uint4*>(M.ws.counts + MAGS + mw);
+#pragma unroll
+        for (int j = 0; j < NCH; ++j) { p[j] = p4[64 * j]; q[j] = q4[64 * j]; }
+    }
+    // bit 4 j + e of the masks: magnitude mw + 256 j + e (ascending with the bit)
+    uint32_t occp = 0u, occn = 0u, finm = 0u, carry = 0u;
+    unsigned long long sq = 0ull;
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) {
+        const bool f = mw + 256 * j < fin;     // the finite ranges end on a multiple of 4
+        const uint32_t a[4] = {p[j].x, p[j].y, p[j].z, p[j].w};
+        const uint32_t c[4] = {q[j].x, q[j].y, q[j].z, q[j].w};
+        uint32_t s4[4], run = 0u;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            occp |= (uint32_t)(a[e] != 0u) << (4 * j + e);
+            occn |= (uint32_t)(c[e] != 0u) << (4 * j + e);
+            const uint32_t ae = f ? a[e] : 0u, ce = f ? c[e] : 0u;
+            sq += (unsigned long long)ae * ae;
+            sq += (unsigned long long)ce * ce;
+            run += ae + ce;
+            s4[e] = run;
         }
-        off[32] = run;
-        // expected number of other lanes sharing an address in a 64-lane keyed atomic
-        const double e = run ? 2016.0 * (double)sq / ((double)run * (double)run) : 0.0;
-        st5[0] = lo; st5[1] = hi; st5[2] = nu; st5[3] = nf;
-        st5[4] = e > KEYED_U64_ABOVE ? KEYED_U64 : KEYED_I32;
+        finm |= (f ? 0xFu : 0u) << (4 * j);
+        uint32_t x = run;                      // inclusive scan over the wave's lanes
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t y = __shfl_up(x, o, 64);
+            if (lane >= o) x += y;
+        }
+        const uint32_t base = carry + x - run;
+        *reinterpret_cast<uint4*>(pre + mw + 256 * j) =
+            make_uint4(base + s4[0], base + s4[1], base + s4[2], base + s4[3]);
+        carry += (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+    }
+    const uint32_t occ = (occp | occn) & finm;
+    auto bit_mag = [&](int bit) { return mw + 256 * (bit >> 2) + (bit & 3); };
+    int lo = occ ? bit_mag(__builtin_ctz(occ)) : 1 << 30;
+    int hi = occ ? bit_mag(31 - __builtin_clz(occ)) : -1;
+    int nu = __builtin_popcount(occp) + __builtin_popcount(occn);
+    int nf = ((occp | occn) & ~finm) != 0u;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        lo = min(lo, __shfl_xor(lo, o, 64));
+        hi = max(hi, __shfl_xor(hi, o, 64));
+        nu += __shfl_xor(nu, o, 64);
+        nf |= __shfl_xor(nf, o, 64);
+        sq += __shfl_xor(sq, o, 64);
+    }
+    if (lane == 0) {
+        woff[wave + 1] = carry;
+        atomicMin(&red[0], lo);
+        atomicMax(&red[1], hi);
+        atomicAdd(&red[2], nu);
+        atomicOr(&red[3], nf);
+        atomicAdd(&sqsum, sq);
     }
     __syncthreads();
-    const int mlo = st5[0], mhi = st5[1];
-    const uint32_t* scan = M.ws.wscan;
-    auto P = [&](int x) -> uint32_t {   // weights with magnitude < x
-        return x == 0 ? 0u : scan[x - 1] + off[(x - 1) / NP_THREADS];
+    if (threadIdx.x == 0) {
+        woff[0] = 0u;
+        for (int w = 1; w <= NW; ++w) woff[w] += woff[w - 1];
+    }
+    __syncthreads();
+    const int mlo = red[0], mhi = red[1];
+    auto P = [&](int x) -> uint32_t {   // weights with finite magnitude < x
+        return x == 0 ? 0u : pre[x - 1] + woff[(x - 1) / SPAN];
     };
     int wl[2], ww[2];
     const int widths[2] = {W4, W8};
+#pragma unroll
     for (int w = 0; w < 2; ++w) {
         const int W = widths[w];
         if (mhi < 0) { wl[w] = 0; ww[w] = 0; continue; }
         if (mhi - mlo + 1 <= W) { wl[w] = mlo; ww[w] = mhi - mlo + 1; continue; }
-        if (threadIdx.x == 0) best[w] = 0ull;
-        __syncthreads();
         unsigned long long mine = 0ull;
         for (int s = mlo + threadIdx.x; s <= mhi - W + 1; s += NP_THREADS) {
             const uint32_t cov = P(s + W) - P(s);
@@ -566,15 +592,18 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
         ww[w] = W;
     }
     if (threadIdx.x == 0) {
+        const uint32_t total = woff[NW];
+        // expected number of other lanes sharing an address in a 64-lane keyed atomic
+        const double e = total ? 2016.0 * (double)sqsum / ((double)total * (double)total) : 0.0;
         DevState* st = M.ws.st;
-        st->num_unique = (uint32_t)st5[2];
-        st->nonfinite = (uint32_t)st5[3];
+        st->num_unique = (uint32_t)red[2];
+        st->nonfinite = (uint32_t)red[3];
         st->mlo = mlo;
         st->mhi = mhi;
         st->lo4 = wl[0]; st->w4 = ww[0];
         st->lo8 = wl[1]; st->w8 = ww[1];
-        st->kmode = M.kforce >= 0 ? M.kforce : st5[4];
-        if (M.nuniq_out) *M.nuniq_out = (uint32_t)st5[2];
+        st->kmode = M.kforce >= 0 ? M.kforce : (e > KEYED_U64_ABOVE ? KEYED_U64 : KEYED_I32);
+        if (M.nuniq_out) *M.nuniq_out = (uint32_t)red[2];
     }
 }
 
@@ -1540,7 +1569,6 @@ hipError_t launch_init_unique(BatchArgs& b, uint32_t grid_np, hipStream_t s, con
     EDKM_NPASS(PASS_HIST, "k_hist", k_hist, dim3(grid_np), dim3(NP_THREADS), b);
     EDKM_LAUNCH("k_hist_merge", k_hist_merge, dim3(W4 / MERGE_THREADS, NP_MAX_WG / MERGE_ROWS, b.count),
                 dim3(MERGE_THREADS), b);
-    EDKM_LAUNCH("k_window_scan", k_window_scan, dim3(32, b.count), dim3(NP_THREADS), b);
     EDKM_LAUNCH("k_window", k_window, dim3(1, b.count), dim3(NP_THREADS), b);
     return hipSuccess;
 }
@@ -1586,7 +1614,9 @@ hipError_t launch_backward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, cons
 
 static_assert(W4 % NP_THREADS == 0, "merge grid covers the window exactly");
 static_assert(2 * W8 <= ROW4, "keyed-reduction rows fit the partial-row stride");
-static_assert(NP_THREADS * 32 == 32768, "window scan: 32 blocks of 1024 magnitudes");
+static_assert(MAGS == (NP_THREADS / 64) * 8 * 256, "window selection: 8 chunks of 256 magnitudes per wave");
+static_assert(fin_mags(FMT_FP16) % 4 == 0 && fin_mags(FMT_BF16) % 4 == 0,
+              "window selection: a lane's 4 magnitudes are all finite or all not");
 static_assert(T_WG == 64, "table partial reduction uses one lane per workgroup");
 static_assert(T_WG * T_THREADS * 4 == NKEYS, "table blocks cover every pattern");
 
