@@ -340,50 +340,25 @@ def bench_mlp_outliers(args):
 def bench_palettize(args):
     """Export of the decoder layer: after one clustering step, the packed b-bit
     nearest-entry indices of every weight against its matrix's final centroids
-    (edkm_palettize, seven calls on one stream).  Pass events time the packing
-    kernel of each call; the roofline is its 2 + b/8 bytes per weight."""
+    (edkm_palettize_batch: one table launch and one packing launch for the
+    seven matrices).  Pass events time the packing kernel; the roofline is its
+    2 + b/8 bytes per weight."""
     import torch
     from paper_2309_00964_amd import edkm, inputs
     bits = args.bits or 3
     m = Matrices(4, inputs.WORKLOADS[4]["mats"], bits, fmt=args.key_format)
     m.step()
     outs = [torch.empty((p.n * bits + 7) // 8, dtype=torch.uint8, device="cuda") for p in m.plans]
-    hip = HipEvents()
-    evs = [(hip.create(), hip.create()) for _ in m.plans]
-    for p, (a, e) in zip(m.plans, evs):
-        edkm.plan_set_pass_events(p, edkm.PASS_PALETTIZE, a, e)
 
     def step():
-        for i, p in enumerate(m.plans):
-            edkm.palettize(p, m.keys[i], m.c_out[i], outs[i])
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    t0, t1 = hip.create(), hip.create()
-    stream = torch.cuda.current_stream().cuda_stream
-    kern_ms = [0.0] * len(m.plans)
-    wall0 = time.perf_counter()
-    hip.record(t0, stream)
-    for _ in range(args.steps):
-        step()
-        torch.cuda.synchronize()
-        for i, (a, e) in enumerate(evs):
-            kern_ms[i] += hip.elapsed_ms(a, e)
-    hip.record(t1, stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    for p in m.plans:
-        edkm.plan_set_pass_events(p, edkm.PASS_PALETTIZE, None, None)
-    elapsed = max(wall, hip.elapsed_ms(t0, t1) / 1000.0)
-    for x in [t0, t1] + [x for pair in evs for x in pair]:
-        hip.destroy(x)
+        edkm.palettize_batch(m.plans, m.keys, m.c_out, outs)
+    elapsed, avg = timed(step, m.plans[0], {"k_palettize": edkm.PASS_PALETTIZE}, args.steps, args.warmup)
     per_w = 2.0 + bits / 8.0
-    kern_s = sum(kern_ms) / args.steps / 1000.0
+    kern_s = avg["k_palettize"] / 1000.0
     achieved = per_w * m.total / kern_s / 1e9
     roof = {"bound": "hbm", "kernel": "k_palettize", "achieved": achieved, "peak": PEAK_HBM_GBS,
             "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": None,
-            "bytes_per_weight": per_w, "kernel_us_per_step": kern_s * 1e6,
-            "note": "synchronised after every step to read the per-call events"}
+            "bytes_per_weight": per_w, "kernel_us_per_step": kern_s * 1e6}
     return result_line(args, "llama7b_decoder_layer_palettize_%dbit%s" % (bits, _fmt_tag(args)), m,
                        bits, elapsed, roof, {"w_tilde": None, "output": "packed %d-bit indices" % bits})
 

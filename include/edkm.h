@@ -223,6 +223,14 @@ edkm_status edkm_plan_set_pass_events(edkm_plan* plan, int pass, hipEvent_t star
  * one write of n b / 8 bytes. */
 edkm_status edkm_palettize(edkm_plan* plan, const uint16_t* w_bits, const float* lut,
                            uint8_t* indices_out, hipStream_t stream);
+/* Batched form: `count` matrices, each with its own plan, keys, table and
+ * output, cut into launch groups of up to 8 consecutive matrices with the same
+ * bit width and weight format; each group is one table launch and one packing
+ * launch.  Host arrays of `count` entries, none NULL.  Equivalent to calling
+ * edkm_palettize on each. */
+edkm_status edkm_palettize_batch(int count, edkm_plan* const* plans, const uint16_t* const* w_bits,
+                                 const float* const* lut, uint8_t* const* indices_out,
+                                 hipStream_t stream);
 
 /* Keyed-gradient accumulators (the backward's keyed reduction).  AUTO, the
  * default, chooses per matrix at init_unique from how concentrated the

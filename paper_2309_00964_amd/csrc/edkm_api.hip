@@ -485,20 +485,36 @@ edkm_status edkm_plan_set_pass_events(edkm_plan* plan, int pass, hipEvent_t star
 
 edkm_status edkm_palettize(edkm_plan* plan, const uint16_t* w_bits, const float* lut,
                            uint8_t* indices_out, hipStream_t stream) {
-    if (!plan_ok(plan) || !w_bits || !lut || !indices_out) return EDKM_ERR_ARG;
-    PlanImpl* P = impl(plan);
-    BatchArgs b;
-    std::memset(&b, 0, sizeof(b));
-    b.count = 1;
-    MatArgs& M = b.m[0];
-    fill_mat(M, P, w_bits);
-    M.c_in = lut;
-    M.wt = indices_out;
-    M.vec = aligned16(w_bits) && ((uintptr_t)indices_out & 3u) == 0;
-    const char* where = "";
-    const hipError_t e = launch_palettize(b, stream, &where, &P->ev);
-    if (e != hipSuccess) return hip_fail(&plan, 0, 1, e, where);
-    return EDKM_OK;
+    return edkm_palettize_batch(1, &plan, &w_bits, &lut, &indices_out, stream);
+}
+
+edkm_status edkm_palettize_batch(int count, edkm_plan* const* plans, const uint16_t* const* w_bits,
+                                 const float* const* lut, uint8_t* const* indices_out,
+                                 hipStream_t stream) {
+    edkm_status st = check_batch(count, plans, w_bits);
+    if (st != EDKM_OK) return st;
+    if (!lut || !indices_out) return EDKM_ERR_ARG;
+    for (int i = 0; i < count; ++i)
+        if (!lut[i] || !indices_out[i]) return EDKM_ERR_ARG;
+    return for_groups(count, plans, [&](int first, int cnt) -> edkm_status {
+        BatchArgs b;
+        std::memset(&b, 0, sizeof(b));
+        b.count = cnt;
+        for (int i = 0; i < cnt; ++i) {
+            const int q = first + i;
+            MatArgs& M = b.m[i];
+            fill_mat(M, impl(plans[q]), w_bits[q]);
+            M.c_in = lut[q];
+            M.wt = indices_out[q];
+            M.vec = aligned16(w_bits[q]) && ((uintptr_t)indices_out[q] & 3u) == 0;
+        }
+        // the packing kernel's 64 KiB index table leaves room for two workgroups per CU
+        const uint32_t grid = partition(b, 2 * np_budget());
+        const char* where = "";
+        const hipError_t e = launch_palettize(b, grid, stream, &where, &impl(plans[first])->ev);
+        if (e != hipSuccess) return hip_fail(plans, first, cnt, e, where);
+        return EDKM_OK;
+    });
 }
 
 edkm_status edkm_plan_set_keyed_mode(edkm_plan* plan, int mode) {

@@ -120,8 +120,8 @@ hipError_t launch_forward(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_t
                               const PassEvents* ev = nullptr);
 hipError_t launch_backward(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_t s, const char** where,
                               const PassEvents* ev = nullptr);
-hipError_t launch_palettize(BatchArgs& b, hipStream_t s, const char** where,
-                            const PassEvents* ev = nullptr);
+hipError_t launch_palettize(BatchArgs& b, uint32_t grid_np, hipStream_t s, const char** where,
+                            const PassEvents* ev);
 hipError_t launch_forward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where,
                                 const PassEvents* ev = nullptr);
 hipError_t launch_backward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where,

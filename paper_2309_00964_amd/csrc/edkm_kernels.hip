@@ -1002,10 +1002,10 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
 // palettization: the lookup table of k entries and a b-bit index per weight
 
 // Nearest lookup-table entry for every pattern: fp32 distance |v - lut_j|,
-// lowest entry on ties; non-finite patterns get 0.  Grid NKEYS / 256.
+// lowest entry on ties; non-finite patterns get 0.  Grid (NKEYS / 256, count).
 __global__ void __launch_bounds__(256) k_pal_table(BatchArgs b) {
     __shared__ float lut[KMAX];
-    const MatArgs& M = b.m[0];
+    const MatArgs& M = b.m[blockIdx.y];
     if (threadIdx.x < M.k) lut[threadIdx.x] = M.c_in[threadIdx.x];
     __syncthreads();
     const uint32_t u = blockIdx.x * 256 + threadIdx.x;
@@ -1025,11 +1025,13 @@ __global__ void __launch_bounds__(256) k_pal_table(BatchArgs b) {
 // stream.  A thread packs a group of 32 weights into B 32-bit words (4 B bytes
 // at byte 4 B g for group g); the per-pattern index table (64 KiB) sits in LDS.
 // The matrix's last, partial group and unaligned buffers are written byte by
-// byte, never past the ceil(n B / 8) output bytes.  Grid-stride over groups.
+// byte, never past the ceil(n B / 8) output bytes.  A matrix's workgroups
+// [wg_begin, wg_begin + wg_count) take its groups round-robin, 1024 at a time.
 template <int B>
 __global__ void __launch_bounds__(1024) k_palettize(BatchArgs b) {
     __shared__ uint4 tbl4[NKEYS / 16];
-    const MatArgs& M = b.m[0];
+    const MatArgs& M = b.m[np_matrix(b)];
+    const uint32_t wl = blockIdx.x - M.wg_begin;
     const uint4* src = reinterpret_cast<const uint4*>(M.ws.pidx);
     for (int i = threadIdx.x; i < NKEYS / 16; i += blockDim.x) tbl4[i] = src[i];
     __syncthreads();
@@ -1040,8 +1042,8 @@ __global__ void __launch_bounds__(1024) k_palettize(BatchArgs b) {
     const uint64_t n = M.n;
     const uint64_t groups = (n + 31) / 32;
     const uint64_t nbytes = (n * B + 7) / 8;
-    for (uint64_t gi = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; gi < groups;
-         gi += (uint64_t)gridDim.x * blockDim.x) {
+    for (uint64_t gi = (uint64_t)wl * blockDim.x + threadIdx.x; gi < groups;
+         gi += (uint64_t)M.wg_count * blockDim.x) {
         const uint64_t base = gi * 32;
         uint32_t w[B];
 #pragma unroll
@@ -1585,11 +1587,11 @@ hipError_t launch_backward(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_
     EDKM_DISPATCH_K(b.m[0].k, backward_k, b, grid_np, max_t, s, where, ev);
 }
 
-hipError_t launch_palettize(BatchArgs& b, hipStream_t s, const char** where, const PassEvents* ev) {
+hipError_t launch_palettize(BatchArgs& b, uint32_t grid_np, hipStream_t s, const char** where,
+                            const PassEvents* ev) {
     (void)hipGetLastError();
-    EDKM_LAUNCH("k_pal_table", k_pal_table, dim3(NKEYS / 256), dim3(256), b);
-    const uint64_t groups = (b.m[0].n + 31) / 32;
-    const dim3 grid((uint32_t)std::min<uint64_t>(512, (groups + 1023) / 1024));
+    EDKM_LAUNCH("k_pal_table", k_pal_table, dim3(NKEYS / 256, b.count), dim3(256), b);
+    const dim3 grid(grid_np);
     switch (b.m[0].k) {
     case 2: EDKM_NPASS(PASS_PALETTIZE, "k_palettize", k_palettize<1>, grid, dim3(1024), b); break;
     case 4: EDKM_NPASS(PASS_PALETTIZE, "k_palettize", k_palettize<2>, grid, dim3(1024), b); break;

@@ -77,6 +77,7 @@ _SIGS = {
     "edkm_plan_init_ex": (_i32, [_PLAN, _u64, _i32, _i32, _i32, _P, _sz]),
     "edkm_plan_set_keyed_mode": (_i32, [_PLAN, _i32]),
     "edkm_palettize": (_i32, [_PLAN, _P, _P, _P, _P]),
+    "edkm_palettize_batch": (_i32, [_i32, _PP, _PP, _PP, _PP, _P]),
     "edkm_init_unique": (_i32, [_PLAN, _P, _P, _P, _i32, _P]),
     "edkm_forward": (_i32, [_PLAN, _P, _f32, _f32, _P, _P, _P, _i32, _P, _P]),
     "edkm_backward": (_i32, [_PLAN, _P, _P, _P, _P, _P]),
@@ -247,8 +248,17 @@ def _plans(plans):
     return ctypes.cast(arr, _PP), arr
 
 
+def _same_len(where, plans, **lists):
+    """Every per-matrix list of a batched call has one entry per plan (the C
+    side reads `count` entries of each host array)."""
+    for name, items in lists.items():
+        if items is not None and len(items) != len(plans):
+            raise EdkmError(ERR_ARG, where, "%s has %d entries for %d plans" % (name, len(items), len(plans)))
+
+
 def init_unique_batch(plans, w_bits, counts_out=None, num_unique_out=None, check_finite=False,
                       stream=None) -> None:
+    _same_len("init_unique_batch", plans, w_bits=w_bits, counts_out=counts_out, num_unique_out=num_unique_out)
     n = len(plans)
     pp, _a = _plans(plans)
     kk, _b = _parr(w_bits, 2)
@@ -260,6 +270,7 @@ def init_unique_batch(plans, w_bits, counts_out=None, num_unique_out=None, check
 
 def forward_batch(plans, w_bits, tau, eps, c_in, c_out, w_tilde, out_half=False, iters_out=None,
                   stream=None) -> None:
+    _same_len("forward_batch", plans, w_bits=w_bits, c_in=c_in, c_out=c_out, w_tilde=w_tilde, iters_out=iters_out)
     n = len(plans)
     pp, _a = _plans(plans)
     kk, _b = _parr(w_bits, 2)
@@ -273,6 +284,7 @@ def forward_batch(plans, w_bits, tau, eps, c_in, c_out, w_tilde, out_half=False,
 
 
 def backward_batch(plans, w_bits, grad_w_tilde, grad_w, grad_c, stream=None) -> None:
+    _same_len("backward_batch", plans, w_bits=w_bits, grad_w_tilde=grad_w_tilde, grad_w=grad_w, grad_c=grad_c)
     n = len(plans)
     pp, _a = _plans(plans)
     kk, _b = _parr(w_bits, 2)
@@ -280,3 +292,19 @@ def backward_batch(plans, w_bits, grad_w_tilde, grad_w, grad_c, stream=None) -> 
     gw, _d = _parr(grad_w, 4)
     gc, _e = _parr(grad_c, 4)
     _check(_lib.edkm_backward_batch(n, pp, kk, g, gw, gc, _stream(stream)), "backward_batch", plans)
+
+
+def palettize_batch(plans, w_bits, lut, indices_out, stream=None) -> None:
+    """palettize over a batch: one table launch and one packing launch per
+    launch group (up to 8 matrices with the same bit width and format)."""
+    _same_len("palettize_batch", plans, w_bits=w_bits, lut=lut, indices_out=indices_out)
+    for p, o in zip(plans, indices_out):
+        need = (p.n * p.bits + 7) // 8
+        if o.numel() * o.element_size() < need:
+            raise EdkmError(ERR_ARG, "palettize_batch", "indices_out needs %d bytes" % need)
+    n = len(plans)
+    pp, _a = _plans(plans)
+    kk, _b = _parr(w_bits, 2)
+    lt, _c = _parr(lut, 4)
+    oo, _d = _parr(indices_out, 1)
+    _check(_lib.edkm_palettize_batch(n, pp, kk, lt, oo, _stream(stream)), "palettize_batch", plans)

@@ -116,6 +116,45 @@ def test_batch_argument_errors():
     assert lib.edkm_init_unique_batch(2, None, kk, None, None, 0, None) == edkm.ERR_ARG
 
 
+def test_palettize_batch_argument_errors():
+    p, q = _plan(), _plan()          # q shares p's (fake) workspace
+    one = lambda v: ctypes.cast((ctypes.c_void_p * 1)(v), edkm._PP)
+    pp, kk, good, nul = one(ctypes.addressof(p)), one(1 << 41), one(1 << 42), one(None)
+    assert lib.edkm_palettize_batch(1, pp, kk, None, good, None) == edkm.ERR_ARG
+    assert lib.edkm_palettize_batch(1, pp, kk, good, None, None) == edkm.ERR_ARG
+    assert lib.edkm_palettize_batch(1, pp, kk, nul, good, None) == edkm.ERR_ARG
+    assert lib.edkm_palettize_batch(1, pp, kk, good, nul, None) == edkm.ERR_ARG
+    assert lib.edkm_palettize_batch(1, pp, nul, good, good, None) == edkm.ERR_ARG
+    assert lib.edkm_palettize_batch(0, pp, kk, good, good, None) == edkm.ERR_ARG
+    assert lib.edkm_palettize_batch(1, None, kk, good, good, None) == edkm.ERR_ARG
+    two = ctypes.cast((ctypes.c_void_p * 2)(ctypes.addressof(p), ctypes.addressof(q)), edkm._PP)
+    k2 = ctypes.cast((ctypes.c_void_p * 2)(1 << 41, 1 << 41), edkm._PP)
+    g2 = ctypes.cast((ctypes.c_void_p * 2)(1 << 42, 1 << 42), edkm._PP)
+    assert lib.edkm_palettize_batch(2, two, k2, g2, g2, None) == edkm.ERR_ARG
+
+
+def test_batch_bindings_reject_lists_of_other_lengths():
+    """The C side reads `count` entries of every host array: a short list must
+    be refused by the binding before the library is called."""
+    from types import SimpleNamespace
+    plans = [SimpleNamespace(n=100, bits=3), SimpleNamespace(n=100, bits=3)]
+    one, two = [object()], [object(), object()]
+    with pytest.raises(edkm.EdkmError, match="w_bits has 1 entries"):
+        edkm.init_unique_batch(plans, one)
+    with pytest.raises(edkm.EdkmError, match="num_unique_out"):
+        edkm.init_unique_batch(plans, two, num_unique_out=one)
+    with pytest.raises(edkm.EdkmError, match="c_out"):
+        edkm.forward_batch(plans, two, 2e-3, 0.0, two, one, two)
+    with pytest.raises(edkm.EdkmError, match="iters_out"):
+        edkm.forward_batch(plans, two, 2e-3, 0.0, two, two, two, iters_out=one)
+    with pytest.raises(edkm.EdkmError, match="grad_c"):
+        edkm.backward_batch(plans, two, two, two, one)
+    with pytest.raises(edkm.EdkmError, match="lut"):
+        edkm.palettize_batch(plans, two, one, two)
+    with pytest.raises(edkm.EdkmError, match="indices_out"):
+        edkm.palettize_batch(plans, two, two, [object(), object(), object()])
+
+
 def test_status_strings():
     for s in (0, -1, -2, -3, -4, -5):
         assert edkm.status_str(s) and edkm.status_str(s) != "unknown status"

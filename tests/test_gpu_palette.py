@@ -123,3 +123,64 @@ def test_palettize_full_size(fmt):
     got, guard = gpu_palettize(keys, lut, 3, fmt)
     np.testing.assert_array_equal(got, palette.palettize(keys, lut, 3, fmt))
     assert np.all(guard == 0xAB)
+
+
+def gpu_palettize_batch(keys_list, luts, bits_list, fmt, offsets=None):
+    """edkm_palettize_batch over several matrices; offsets[i] = (key_offset,
+    out_offset) places matrix i off alignment.  Returns [(packed, guard)]."""
+    offsets = offsets or [(0, 0)] * len(keys_list)
+    plans, kv, lv, ov, obufs, nb = [], [], [], [], [], []
+    for keys, lut, bits, (ko, oo) in zip(keys_list, luts, bits_list, offsets):
+        n = keys.size
+        nbytes = (n * bits + 7) // 8
+        kbuf = torch.zeros(n + ko, dtype=torch.int16, device=DEV)
+        kbuf[ko:] = torch.from_numpy(keys.view(np.int16)).to(DEV)
+        obuf = torch.full((oo + nbytes + GUARD,), 0xAB, dtype=torch.uint8, device=DEV)
+        plans.append(edkm.Plan(n, bits, inputs.ITERS, key_format=fmt))
+        kv.append(kbuf[ko:])
+        lv.append(torch.from_numpy(np.asarray(lut, np.float32)).to(DEV))
+        ov.append(obuf[oo:])
+        obufs.append((obuf, oo))
+        nb.append(nbytes)
+    edkm.palettize_batch(plans, kv, lv, ov)
+    torch.cuda.synchronize()
+    out = []
+    for (obuf, oo), nbytes in zip(obufs, nb):
+        o = obuf.cpu().numpy()
+        out.append((o[oo:oo + nbytes], o[oo + nbytes:]))
+    return out
+
+
+@pytest.mark.parametrize("fmt", ["fp16", "bf16"])
+def test_palettize_batch_bit_exact(fmt):
+    """Eleven matrices: two launch groups cut by size (8 + 3) and by bit width,
+    ragged sizes, one matrix off alignment (its scalar path beside vectorised
+    neighbours)."""
+    sizes = [1, 31, 65537, 1_000_003, 33, 300_007, 16, 2_000_001, 999, 70_000, 8]
+    bits = [3, 3, 3, 3, 3, 3, 3, 3, 2, 2, 4]
+    offsets = [(0, 0)] * len(sizes)
+    offsets[5] = (1, 1)
+    keys = [inputs.weights(n, 220 + i, i % 2 == 1, fmt) for i, n in enumerate(sizes)]
+    luts = [inputs.quantile_init(k, 1 << b, fmt) for k, b in zip(keys, bits)]
+    say("palettize batch", fmt)
+    got = gpu_palettize_batch(keys, luts, bits, fmt, offsets)
+    for i, ((packed, guard), k, lut, b) in enumerate(zip(got, keys, luts, bits)):
+        np.testing.assert_array_equal(packed, palette.palettize(k, lut, b, fmt), err_msg="matrix %d" % i)
+        assert np.all(guard == 0xAB), i
+
+
+def test_palettize_batch_layer_shapes():
+    """The seven decoder-layer matrices at 3 bits in one batched call: every
+    matrix's bytes equal its single-matrix call, and q_proj and gate_proj equal
+    the oracle."""
+    mats = inputs.WORKLOADS[4]["mats"]
+    keys = [inputs.weights(r * c, inputs.weight_seed(4, i), False, "fp16") for i, (_, r, c) in enumerate(mats)]
+    luts = [inputs.quantile_init(k, 8) for k in keys]
+    say("palettize batch, decoder layer")
+    got = gpu_palettize_batch(keys, luts, [3] * len(keys), "fp16")
+    for i, (k, lut) in enumerate(zip(keys, luts)):
+        single, _ = gpu_palettize(k, lut, 3, "fp16")
+        np.testing.assert_array_equal(got[i][0], single, err_msg=mats[i][0])
+        assert np.all(got[i][1] == 0xAB), mats[i][0]
+    for i in (0, 4):
+        np.testing.assert_array_equal(got[i][0], palette.palettize(keys[i], luts[i], 3), err_msg=mats[i][0])
