@@ -918,18 +918,49 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
         const int elim = min(min(emax_sh, emean + 8) + 2, 190);
         const int S = 156 - elim;                    // |g 2^S| < 2^30
         const float wrap = ldexpf(1.0f, 32 - S);     // one turn of the 32-bit accumulator, as a value
-        stream([&](uint32_t key, float gv) {
+        // One weight: its LDS atomic (returning the previous value), plus the
+        // global add when it is not taken in LDS.  Every lane issues the LDS
+        // atomic, the others adding 0 to a spare word of their own past the
+        // window (one per lane: a shared one would be a uniform address, which
+        // the compiler turns back into a branch): no branch then writes the
+        // registers a pending return targets, and the wrap test (separate)
+        // lets a whole tile's atomics issue before the first return is awaited.
+        auto issue = [&](uint32_t key, float gv, int& q, int& old) {
             const uint32_t d = (key & 0x7FFFu) - (uint32_t)lo;
             const int e = (int)((__float_as_uint(gv) >> 23) & 0xFFu);
-            if (d < (uint32_t)w && e <= elim) {
-                const int q = __float2int_rn(ldexpf(gv, S));
-                const int old = atomicAdd(&acc32[(key >> 15) * w + d], q);
-                const int sum = (int)((uint32_t)old + (uint32_t)q);
-                if (((old ^ sum) & (q ^ sum)) < 0) atomicAdd(&G[key], q > 0 ? wrap : -wrap);
-            } else {
-                atomicAdd(&G[key], gv);
-            }
-        });
+            const bool in = d < (uint32_t)w && e <= elim;
+            q = in ? __float2int_rn(ldexpf(gv, S)) : 0;
+            old = atomicAdd(&acc32[in ? (key >> 15) * w + d : 2 * W4 + (threadIdx.x & 63)], q);
+            if (!in) atomicAdd(&G[key], gv);
+        };
+        auto settle = [&](uint32_t key, int q, int old) {   // (q, old) = (0, 0) never wraps
+            const int sum = (int)((uint32_t)old + (uint32_t)q);
+            if (((old ^ sum) & (q ^ sum)) < 0) atomicAdd(&G[key], q > 0 ? wrap : -wrap);
+        };
+        struct Pend4 { uint2 keys; int q[4], old[4]; };
+        for_slice<3, 4>(M, wl,
+            [&](uint64_t i) { return KeysG4{ld_u2_nt(keys + i), ld_f4_nt(g + i)}; },
+            [&](const KeysG4& r) {
+                Pend4 p;
+                p.keys = r.q;
+                issue(r.q.x & 0xFFFFu, r.g.x, p.q[0], p.old[0]);
+                issue(r.q.x >> 16, r.g.y, p.q[1], p.old[1]);
+                issue(r.q.y & 0xFFFFu, r.g.z, p.q[2], p.old[2]);
+                issue(r.q.y >> 16, r.g.w, p.q[3], p.old[3]);
+                return p;
+            },
+            [&](uint64_t, const Pend4& p) {
+                settle(p.keys.x & 0xFFFFu, p.q[0], p.old[0]);
+                settle(p.keys.x >> 16, p.q[1], p.old[1]);
+                settle(p.keys.y & 0xFFFFu, p.q[2], p.old[2]);
+                settle(p.keys.y >> 16, p.q[3], p.old[3]);
+            },
+            [&](uint64_t i) {
+                int q, old;
+                const uint32_t key = keys[i];
+                issue(key, g[i], q, old);
+                settle(key, q, old);
+            });
         __syncthreads();
         for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) row[i] = ldexpf((float)acc32[i], -S);
     }
@@ -1616,6 +1647,7 @@ hipError_t launch_backward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, cons
 
 static_assert(W4 % NP_THREADS == 0, "merge grid covers the window exactly");
 static_assert(2 * W8 <= ROW4, "keyed-reduction rows fit the partial-row stride");
+static_assert(2 * W4 + 64 <= 2 * W8 * 2, "keyed sum: the 32-bit window and its spare words fit the LDS array");
 static_assert(MAGS == (NP_THREADS / 64) * 8 * 256, "window selection: 8 chunks of 256 magnitudes per wave");
 static_assert(fin_mags(FMT_FP16) % 4 == 0 && fin_mags(FMT_BF16) % 4 == 0,
               "window selection: a lane's 4 magnitudes are all finite or all not");
