@@ -147,31 +147,37 @@ def cpu_baseline(samples, k, table_names=("q_proj", "gate_proj", "w", "L0.q_proj
 
 
 def timed(step, plan, pass_ids, steps, warmup):
-    """Warm up, then time `steps` calls of step() between two HIP events on the
-    current stream, with per-pass events recorded by the library on `plan`.
-    Returns (seconds, {pass: average launch ms})."""
+    """Warm up, then run `steps` calls of step() twice on the current stream:
+    first as the library runs them, timed between two HIP events (the step
+    time), then with the library recording per-pass events on `plan` around
+    each timed pass (the per-launch kernel times of the roofline).  The event
+    records add a few microseconds per pass, so they stay out of the step time.
+    Returns (seconds for `steps` steps, {pass: average launch ms})."""
     import torch
     from paper_2309_00964_amd import edkm
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
     hip = HipEvents()
-    ev = {p: [(hip.create(), hip.create()) for _ in range(steps)] for p in pass_ids}
-    t_start, t_stop = hip.create(), hip.create()
     stream = torch.cuda.current_stream().cuda_stream
+    t_start, t_stop = hip.create(), hip.create()
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     hip.record(t_start, stream)
-    for s in range(steps):
-        for p, pid in pass_ids.items():
-            edkm.plan_set_pass_events(plan, pid, ev[p][s][0], ev[p][s][1])
+    for _ in range(steps):
         step()
     hip.record(t_stop, stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
+    gpu_s = hip.elapsed_ms(t_start, t_stop) / 1000.0
+    ev = {p: [(hip.create(), hip.create()) for _ in range(steps)] for p in pass_ids}
+    for s in range(steps):
+        for p, pid in pass_ids.items():
+            edkm.plan_set_pass_events(plan, pid, ev[p][s][0], ev[p][s][1])
+        step()
+    torch.cuda.synchronize()
     for pid in pass_ids.values():
         edkm.plan_set_pass_events(plan, pid, None, None)
-    gpu_s = hip.elapsed_ms(t_start, t_stop) / 1000.0
     avg = {p: sum(hip.elapsed_ms(a, b) for a, b in ev[p]) / steps for p in pass_ids}
     for e in [t_start, t_stop] + [x for p in ev for pair in ev[p] for x in pair]:
         hip.destroy(e)
