@@ -53,7 +53,6 @@ PASS_IDS = {"k_hist": 0, "k_gather_wt": 1, "k_keyed_grad": 2, "k_gather_grad": 3
 DENSE_PASS_IDS = {"k_dense_iter": 4, "k_dense_biter": 5}
 DENSE_OPS_PER_ENTRY = {"k_dense_iter": 9, "k_dense_biter": 15}
 PEAK_FP32_TFLOPS = 157.3
-GROUP = 8        # matrices per launch group of the batched calls
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 COPY_BYTES = 1 << 30
 
@@ -378,10 +377,12 @@ def bench_stack(args):
     keep = () if args.no_cpu_baseline else ("L0.q_proj",)
     m = Matrices(5, w["mats"], bits, on_device=True, keep_host=keep, fmt=args.key_format)
     elapsed, avg = timed(m.step, m.plans[0], PASS_IDS, args.steps, args.warmup)
-    # the pass events bracket the first launch group of each step: the first
-    # GROUP matrices (layer 0 and the first projection of layer 1)
-    roof = hbm_roofline(avg, sum(r * c for _, r, c in w["mats"][:GROUP]))
-    roof["note"] = "pass events cover the first launch group (%d matrices) of each step" % GROUP
+    # the pass events bracket the first launch group of each step: its first
+    # LAUNCH_GROUP matrices (layers 0-3)
+    from paper_2309_00964_amd import edkm
+    group = edkm.LAUNCH_GROUP
+    roof = hbm_roofline(avg, sum(r * c for _, r, c in w["mats"][:group]))
+    roof["note"] = "pass events cover the first launch group (%d matrices) of each step" % group
     out = result_line(args, "llama7b_32_layer_stack_%dbit%s" % (bits, _fmt_tag(args)), m, bits, elapsed, roof)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(m.host, 1 << bits, fmt=m.fmt)

@@ -58,6 +58,7 @@ extern "C" {
 #define EDKM_MAX_BITS 4         /* k = 2^bits <= 16 centroids */
 #define EDKM_MAX_ITER 1024
 #define EDKM_MAX_N 4294967295ull /* per matrix; counts are uint32 */
+#define EDKM_LAUNCH_GROUP 28    /* matrices per launch in the batched forms (four decoder layers) */
 
 typedef int edkm_status;
 enum {
@@ -148,12 +149,12 @@ edkm_status edkm_backward(edkm_plan* plan, const uint16_t* w_bits, const float* 
 
 /* Batched forms: `count` independent matrices (own plan, keys and outputs;
  * same tau and eps) processed together.  The batch is cut into launch groups
- * of up to 8 consecutive matrices with the same bit width and weight format,
- * and each step of the path is one launch per group.  Arrays are host arrays
- * of `count` entries (count >= 1, any size: groups are formed by the
- * library); entries of the nullable output arrays may be NULL, and the arrays
- * themselves may be NULL.  Equivalent to calling the single-matrix form on
- * each. */
+ * of up to EDKM_LAUNCH_GROUP consecutive matrices with the same bit width and
+ * weight format, and each step of the path is one launch per group.  Arrays
+ * are host arrays of `count` entries (count >= 1, any size: groups are formed
+ * by the library); entries of the nullable output arrays may be NULL, and the
+ * arrays themselves may be NULL.  Equivalent to calling the single-matrix
+ * form on each. */
 edkm_status edkm_init_unique_batch(int count, edkm_plan* const* plans,
                                    const uint16_t* const* w_bits,
                                    uint32_t* const* counts_out,
@@ -224,7 +225,7 @@ edkm_status edkm_plan_set_pass_events(edkm_plan* plan, int pass, hipEvent_t star
 edkm_status edkm_palettize(edkm_plan* plan, const uint16_t* w_bits, const float* lut,
                            uint8_t* indices_out, hipStream_t stream);
 /* Batched form: `count` matrices, each with its own plan, keys, table and
- * output, cut into launch groups of up to 8 consecutive matrices with the same
+ * output, cut into launch groups of up to EDKM_LAUNCH_GROUP consecutive matrices with the same
  * bit width and weight format; each group is one table launch and one packing
  * launch.  Host arrays of `count` entries, none NULL.  Equivalent to calling
  * edkm_palettize on each. */

@@ -42,40 +42,6 @@ static_assert(EDKM_PASS_HIST == PASS_HIST && EDKM_PASS_GATHER_WT == PASS_GATHER_
 
 inline PlanImpl* impl(edkm_plan* p) { return reinterpret_cast<PlanImpl*>(p); }
 
-inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
-
-struct Layout {
-    size_t counts, tab, H, R, HR, G, chist, shist, ghist, ehist, tpart, bpart, dpart, span, part, pidx,
-        st, total;
-};
-
-Layout layout(int max_iter) {
-    Layout L{};
-    size_t o = 0;
-    auto take = [&](size_t bytes) { size_t at = o; o = align256(o + bytes); return at; };
-    const size_t hist = (size_t)(max_iter + 1) * KMAX * sizeof(float);
-    const size_t tp = (size_t)(max_iter + 1) * T_WG * PSTRIDE * sizeof(float);
-    L.st = take(sizeof(DevState));
-    L.counts = take(NKEYS * sizeof(uint32_t));
-    L.tab = take(NKEYS * sizeof(float));
-    L.H = take(NKEYS * sizeof(float));
-    L.R = take(NKEYS * sizeof(float));
-    L.HR = take(NKEYS * sizeof(float2));
-    L.G = take(NKEYS * sizeof(float));
-    L.chist = take(hist);
-    L.shist = take(hist);
-    L.ghist = take(hist);
-    L.ehist = take(KMAX * sizeof(float));
-    L.tpart = take(tp);
-    L.bpart = take(tp);
-    L.dpart = take((size_t)D_WG * PSTRIDE * sizeof(float));
-    L.span = take(NP_MAX_WG * sizeof(int2));
-    L.part = take((size_t)NP_MAX_WG * ROW4 * sizeof(uint32_t));
-    L.pidx = take(NKEYS);
-    L.total = o;
-    return L;
-}
-
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 bool plan_ok(const edkm_plan* p) {
@@ -129,32 +95,6 @@ edkm_status hip_fail(edkm_plan* const* plans, int first, int cnt, hipError_t e, 
 
 }  // namespace
 
-size_t workspace_bytes(int max_iter) { return layout(max_iter).total; }
-
-Ws carve_workspace(void* base, int max_iter) {
-    const Layout L = layout(max_iter);
-    char* c = static_cast<char*>(base);
-    Ws w;
-    w.pidx = reinterpret_cast<uint8_t*>(c + L.pidx);
-    w.st = reinterpret_cast<DevState*>(c + L.st);
-    w.counts = reinterpret_cast<uint32_t*>(c + L.counts);
-    w.tab = reinterpret_cast<float*>(c + L.tab);
-    w.H = reinterpret_cast<float*>(c + L.H);
-    w.R = reinterpret_cast<float*>(c + L.R);
-    w.HR = reinterpret_cast<float2*>(c + L.HR);
-    w.G = reinterpret_cast<float*>(c + L.G);
-    w.chist = reinterpret_cast<float*>(c + L.chist);
-    w.shist = reinterpret_cast<float*>(c + L.shist);
-    w.ghist = reinterpret_cast<float*>(c + L.ghist);
-    w.ehist = reinterpret_cast<float*>(c + L.ehist);
-    w.tpart = reinterpret_cast<float*>(c + L.tpart);
-    w.bpart = reinterpret_cast<float*>(c + L.bpart);
-    w.dpart = reinterpret_cast<float*>(c + L.dpart);
-    w.span = reinterpret_cast<int2*>(c + L.span);
-    w.part = reinterpret_cast<uint32_t*>(c + L.part);
-    return w;
-}
-
 namespace {
 
 void fill_mat(MatArgs& M, const PlanImpl* P, const uint16_t* keys) {
@@ -165,7 +105,7 @@ void fill_mat(MatArgs& M, const PlanImpl* P, const uint16_t* keys) {
     M.max_iter = P->max_iter;
     M.fmt = P->fmt;
     M.kforce = P->kforce;
-    M.ws = carve_workspace(P->ws, P->max_iter);
+    M.wsb = P->ws;
 }
 
 // Common checks of a batch: plans valid and distinct, key buffers non-null.

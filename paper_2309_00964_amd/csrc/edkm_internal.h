@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "edkm.h"
+
 namespace edkm {
 
 constexpr int NKEYS = 65536;          // every 16-bit pattern
@@ -22,7 +24,7 @@ constexpr int T_WG = 64;              // table-phase workgroups per matrix (= wa
 constexpr int T_THREADS = 256;
 constexpr int KMAX = 16;
 constexpr int PSTRIDE = 32;           // floats per table-phase partial row (2 * KMAX)
-constexpr int MAXB = 8;               // matrices per launch
+constexpr int MAXB = EDKM_LAUNCH_GROUP;   // matrices per launch
 constexpr int D_WG = 1024;            // dense path: max workgroups
 constexpr int D_THREADS = 256;
 
@@ -80,7 +82,7 @@ struct MatArgs {
     float* gw;                // dL/dw
     float* gc;                // dL/dC^(0)
     float* attn;              // dense map output (nullable)
-    Ws ws;
+    void* wsb;                // workspace base (regions: carve_workspace)
     int k;
     int max_iter;
     uint32_t wg_begin;        // first N-pass workgroup of this matrix
@@ -101,6 +103,70 @@ struct BatchArgs {
     MatArgs m[MAXB];
 };
 
+// Kernel arguments are passed by value; the launch limit is 4 KiB.
+static_assert(sizeof(BatchArgs) <= 4096, "launch arguments fit the kernel-argument limit");
+
+// Workspace layout: byte offsets of every region, each 256-byte aligned.  A
+// function of max_iter only, evaluated on the host (sizing, plan checks) and
+// in every kernel (from the workspace base in the launch arguments).
+struct Layout {
+    size_t counts, tab, H, R, HR, G, chist, shist, ghist, ehist, tpart, bpart, dpart, span, part, pidx,
+        st, total;
+};
+
+__host__ __device__ inline Layout layout(int max_iter) {
+    Layout L{};
+    size_t o = 0;
+    auto take = [&](size_t bytes) { size_t at = o; o = (o + bytes + 255) & ~size_t(255); return at; };
+    const size_t hist = (size_t)(max_iter + 1) * KMAX * sizeof(float);
+    const size_t tp = (size_t)(max_iter + 1) * T_WG * PSTRIDE * sizeof(float);
+    L.st = take(sizeof(DevState));
+    L.counts = take(NKEYS * sizeof(uint32_t));
+    L.tab = take(NKEYS * sizeof(float));
+    L.H = take(NKEYS * sizeof(float));
+    L.R = take(NKEYS * sizeof(float));
+    L.HR = take(NKEYS * sizeof(float2));
+    L.G = take(NKEYS * sizeof(float));
+    L.chist = take(hist);
+    L.shist = take(hist);
+    L.ghist = take(hist);
+    L.ehist = take(KMAX * sizeof(float));
+    L.tpart = take(tp);
+    L.bpart = take(tp);
+    L.dpart = take((size_t)D_WG * PSTRIDE * sizeof(float));
+    L.span = take(NP_MAX_WG * sizeof(int2));
+    L.part = take((size_t)NP_MAX_WG * ROW4 * sizeof(uint32_t));
+    L.pidx = take(NKEYS);
+    L.total = o;
+    return L;
+}
+
+inline size_t workspace_bytes(int max_iter) { return layout(max_iter).total; }
+
+__host__ __device__ inline Ws carve_workspace(void* base, int max_iter) {
+    const Layout L = layout(max_iter);
+    char* c = static_cast<char*>(base);
+    Ws w;
+    w.pidx = reinterpret_cast<uint8_t*>(c + L.pidx);
+    w.st = reinterpret_cast<DevState*>(c + L.st);
+    w.counts = reinterpret_cast<uint32_t*>(c + L.counts);
+    w.tab = reinterpret_cast<float*>(c + L.tab);
+    w.H = reinterpret_cast<float*>(c + L.H);
+    w.R = reinterpret_cast<float*>(c + L.R);
+    w.HR = reinterpret_cast<float2*>(c + L.HR);
+    w.G = reinterpret_cast<float*>(c + L.G);
+    w.chist = reinterpret_cast<float*>(c + L.chist);
+    w.shist = reinterpret_cast<float*>(c + L.shist);
+    w.ghist = reinterpret_cast<float*>(c + L.ghist);
+    w.ehist = reinterpret_cast<float*>(c + L.ehist);
+    w.tpart = reinterpret_cast<float*>(c + L.tpart);
+    w.bpart = reinterpret_cast<float*>(c + L.bpart);
+    w.dpart = reinterpret_cast<float*>(c + L.dpart);
+    w.span = reinterpret_cast<int2*>(c + L.span);
+    w.part = reinterpret_cast<uint32_t*>(c + L.part);
+    return w;
+}
+
 // Optional timing events recorded around the N-sized passes (diagnostics).
 enum Pass { PASS_HIST = 0, PASS_GATHER_WT = 1, PASS_KEYED_GRAD = 2, PASS_GATHER_GRAD = 3,
             PASS_DENSE_ITER = 4, PASS_DENSE_BITER = 5, PASS_PALETTIZE = 6, NPASS = 7 };
@@ -109,8 +175,6 @@ struct PassEvents {
     hipEvent_t stop[NPASS];
 };
 
-size_t workspace_bytes(int max_iter);
-Ws carve_workspace(void* base, int max_iter);
 
 // Launch sequences (all asynchronous on `s`).  Each returns the first HIP error.
 // On failure *where names the launch that failed.

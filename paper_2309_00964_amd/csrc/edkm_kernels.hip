@@ -193,8 +193,11 @@ __device__ __forceinline__ void reduce_tparts2(const float* pa, const float* pb,
 
 // Matrix of an N-pass workgroup, and its slice [beg, end).
 __device__ __forceinline__ int np_matrix(const BatchArgs& b) {
+    // wg_begin ascends with the matrix: count the matrices starting at or
+    // before this workgroup, with independent loads of every start
     int m = 0;
-    while (m + 1 < b.count && blockIdx.x >= b.m[m + 1].wg_begin) ++m;
+#pragma unroll
+    for (int i = 1; i < MAXB; ++i) m += (i < b.count && blockIdx.x >= b.m[i].wg_begin) ? 1 : 0;
     return m;
 }
 
@@ -326,10 +329,11 @@ __device__ __forceinline__ void st_u2(void* p, uint2 x) { *reinterpret_cast<uint
 
 __global__ void __launch_bounds__(T_THREADS) k_init_zero(BatchArgs b) {
     const MatArgs& M = b.m[blockIdx.y];
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
     for (int u = blockIdx.x * T_THREADS + threadIdx.x; u < NKEYS; u += gridDim.x * T_THREADS)
-        M.ws.counts[u] = 0u;
+        ws.counts[u] = 0u;
     if (blockIdx.x == 0 && threadIdx.x == 0) {
-        DevState* st = M.ws.st;
+        DevState* st = ws.st;
         st->teff = 0;
         st->conv = 0;
         st->nonfinite = 0u;
@@ -347,12 +351,13 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
     __shared__ int red[2];
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const uint32_t wl = blockIdx.x - M.wg_begin;
     for (int i = threadIdx.x; i < 2 * W4; i += NP_THREADS) h[i] = 0u;
     if (threadIdx.x == 0) { red[0] = W4; red[1] = 0; }
     __syncthreads();
     const uint16_t* keys = M.keys;
-    uint32_t* gcounts = M.ws.counts;
+    uint32_t* gcounts = ws.counts;
     auto add = [&](uint32_t key) {
         const uint32_t mag = key & 0x7FFFu;
         if (mag < (uint32_t)W4) atomicAdd(&h[(key >> 15) * W4 + mag], 1u);
@@ -382,7 +387,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
     hi = (red[1] + 1) & ~1;
     if (hi <= lo) { lo = 0; hi = 0; }
     const int half = (hi - lo) >> 1;
-    uint32_t* row = M.ws.part + (size_t)wl * ROW4;
+    uint32_t* row = ws.part + (size_t)wl * ROW4;
     for (int p = threadIdx.x; p < 2 * half; p += NP_THREADS) {
         const int s = p >= half;
         const int mag = lo + 2 * (p - s * half);
@@ -391,7 +396,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
         if (c1 > 0xFFFFu) { atomicAdd(&gcounts[(s << 15) | (mag + 1)], c1); c1 = 0u; }
         row[p] = c0 | (c1 << 16);
     }
-    if (threadIdx.x == 0) M.ws.span[wl] = make_int2(lo, hi);
+    if (threadIdx.x == 0) ws.span[wl] = make_int2(lo, hi);
 }
 
 // Partial-row merges.  Thread = one bin (or bin pair), blockIdx.y = a chunk of
@@ -406,6 +411,7 @@ constexpr int MERGE_THREADS = 256;
 // Grid (W4 / MERGE_THREADS, NP_MAX_WG / MERGE_ROWS, count).
 __global__ void __launch_bounds__(MERGE_THREADS) k_hist_merge(BatchArgs b) {
     const MatArgs& M = b.m[blockIdx.z];
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const int r0 = blockIdx.y * MERGE_ROWS;
     const int r1 = min((int)M.wg_count, r0 + MERGE_ROWS);
     if (r0 >= r1) return;
@@ -413,14 +419,14 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_hist_merge(BatchArgs b) {
     const int s = q >= W4 / 2;
     const int mag = 2 * (q - s * (W4 / 2));
     uint32_t s0 = 0u, s1 = 0u;
-    const uint32_t* part = M.ws.part;
+    const uint32_t* part = ws.part;
     uint32_t x[MERGE_ROWS];                    // every row's word in flight at once
 #pragma unroll
     for (int q2 = 0; q2 < MERGE_ROWS; ++q2) {
         const int r = r0 + q2;
         x[q2] = 0u;
         if (r < r1) {
-            const int2 lh = M.ws.span[r];
+            const int2 lh = ws.span[r];
             if (mag >= lh.x && mag < lh.y)
                 x[q2] = part[(size_t)r * ROW4 + s * ((lh.y - lh.x) >> 1) + ((mag - lh.x) >> 1)];
         }
@@ -430,7 +436,7 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_hist_merge(BatchArgs b) {
         s0 += x[q2] & 0xFFFFu;
         s1 += x[q2] >> 16;
     }
-    uint32_t* c = M.ws.counts + (s << 15) + mag;
+    uint32_t* c = ws.counts + (s << 15) + mag;
     if (s0) atomicAdd(c, s0);
     if (s1) atomicAdd(c + 1, s1);
 }
@@ -439,14 +445,15 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_hist_merge(BatchArgs b) {
 // into G.  Grid (2 * W4 / MERGE_THREADS, NP_MAX_WG / MERGE_ROWS, count).
 __global__ void __launch_bounds__(MERGE_THREADS) k_grad_merge(BatchArgs b) {
     const MatArgs& M = b.m[blockIdx.z];
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const int r0 = blockIdx.y * MERGE_ROWS;
     const int r1 = min((int)M.wg_count, r0 + MERGE_ROWS);
-    const DevState* st = M.ws.st;
+    const DevState* st = ws.st;
     const bool wide = st->kmode == KEYED_U64;
     const int w = wide ? st->w8 : st->w4, lo = wide ? st->lo8 : st->lo4;
     const int i = blockIdx.x * MERGE_THREADS + threadIdx.x;
     if (r0 >= r1 || i >= 2 * w) return;
-    const float* part = reinterpret_cast<const float*>(M.ws.part) + i;
+    const float* part = reinterpret_cast<const float*>(ws.part) + i;
     float x[MERGE_ROWS];                       // every row's value in flight at once
 #pragma unroll
     for (int q = 0; q < MERGE_ROWS; ++q) x[q] = r0 + q < r1 ? part[(size_t)(r0 + q) * ROW4] : 0.f;
@@ -456,7 +463,7 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_grad_merge(BatchArgs b) {
         for (int q = 0; q < h; ++q) x[q] += x[q + h];
     const float sum = x[0];
     const int sg = i >= w;
-    if (sum != 0.f) atomicAdd(&M.ws.G[(sg << 15) | (lo + i - sg * w)], sum);
+    if (sum != 0.f) atomicAdd(&ws.G[(sg << 15) | (lo + i - sg * w)], sum);
 }
 
 // Block-wide exclusive scan of one uint32 per thread (1024 threads).
@@ -495,6 +502,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
     __shared__ int red[4];                // lo, hi, occupied patterns, non-finite
     __shared__ unsigned long long sqsum, best[2];
     const MatArgs& M = b.m[blockIdx.y];
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const int fin = fin_mags(M.fmt);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int mw = wave * SPAN + 4 * lane;   // this lane's first magnitude; chunk j adds 256 j
@@ -504,8 +512,8 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
     }
     uint4 p[NCH], q[NCH];
     {
-        const uint4* p4 = reinterpret_cast<const uint4*>(M.ws.counts + mw);
-        const uint4* q4 = reinterpret_cast<const uint4*>(M.ws.counts + MAGS + mw);
+        const uint4* p4 = reinterpret_cast<const uint4*>(ws.counts + mw);
+        const uint4* q4 = reinterpret_cast<const uint4*>(ws.counts + MAGS + mw);
 #pragma unroll
         for (int j = 0; j < NCH; ++j) { p[j] = p4[64 * j]; q[j] = q4[64 * j]; }
     }
@@ -595,7 +603,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
         const uint32_t total = woff[NW];
         // expected number of other lanes sharing an address in a 64-lane keyed atomic
         const double e = total ? 2016.0 * (double)sqsum / ((double)total * (double)total) : 0.0;
-        DevState* st = M.ws.st;
+        DevState* st = ws.st;
         st->num_unique = (uint32_t)red[2];
         st->nonfinite = (uint32_t)red[3];
         st->mlo = mlo;
@@ -627,34 +635,35 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
     __shared__ float csh[K];
     __shared__ int stop;
     const MatArgs& M = b.m[blockIdx.y];
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const int t = b.t;
     if (t > M.max_iter) return;
     // pattern counts do not depend on the centroids: issue their loads first
     uint32_t n4[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) n4[r] = M.ws.counts[table_key(r)];
-    DevState* st = M.ws.st;
+    for (int r = 0; r < 4; ++r) n4[r] = ws.counts[table_key(r)];
+    DevState* st = ws.st;
     const bool lead = blockIdx.x == 0;
     if (t == 1) {
         if (threadIdx.x < K) {
             const float c = M.c_in[threadIdx.x];
             csh[threadIdx.x] = c;
-            if (lead) { M.ws.chist[threadIdx.x] = c; M.ws.shist[threadIdx.x] = 0.f; }
+            if (lead) { ws.chist[threadIdx.x] = c; ws.shist[threadIdx.x] = 0.f; }
         }
         if (lead && threadIdx.x == 0) { st->conv = 0; st->teff = 0; }
         __syncthreads();
     } else {
         if (st->conv) return;
-        reduce_tparts(M.ws.tpart + (size_t)(t - 1) * T_WG * PSTRIDE, 0, 2 * K, tot);
+        reduce_tparts(ws.tpart + (size_t)(t - 1) * T_WG * PSTRIDE, 0, 2 * K, tot);
         if (threadIdx.x == 0) stop = 0;
         __syncthreads();
         if (threadIdx.x < K) {
             const int j = threadIdx.x;
             const float S = tot[j], P = tot[K + j];
-            const float cprev = M.ws.chist[(t - 2) * KMAX + j];
+            const float cprev = ws.chist[(t - 2) * KMAX + j];
             const float cn = S > 0.f ? P / S : cprev;
             csh[j] = cn;
-            if (lead) { M.ws.chist[(t - 1) * KMAX + j] = cn; M.ws.shist[(t - 1) * KMAX + j] = S; }
+            if (lead) { ws.chist[(t - 1) * KMAX + j] = cn; ws.shist[(t - 1) * KMAX + j] = S; }
             if (b.eps > 0.f && !(fabsf(cn - cprev) <= b.eps)) atomicOr(&stop, 1);
         }
         __syncthreads();
@@ -687,7 +696,7 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
     }
     block_sum<2 * K, T_THREADS>(acc, scratch, tot);
     if (threadIdx.x < 2 * K)
-        M.ws.tpart[((size_t)t * T_WG + blockIdx.x) * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
+        ws.tpart[((size_t)t * T_WG + blockIdx.x) * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
 }
 
 // After the last iteration: C^(T), c_out, T; per occupied pattern the W~ value
@@ -699,30 +708,31 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
     __shared__ float tot[2 * K];
     __shared__ float cT[K], cP[K];
     const MatArgs& M = b.m[blockIdx.y];
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
     uint32_t n4[4];   // independent of the centroids: loaded first
 #pragma unroll
-    for (int r = 0; r < 4; ++r) n4[r] = M.ws.counts[table_key(r)];
-    DevState* st = M.ws.st;
+    for (int r = 0; r < 4; ++r) n4[r] = ws.counts[table_key(r)];
+    DevState* st = ws.st;
     const bool lead = blockIdx.x == 0;
     int T;
     if (st->conv) {
         T = st->teff;
         if (threadIdx.x < K) {
-            cT[threadIdx.x] = M.ws.chist[T * KMAX + threadIdx.x];
-            cP[threadIdx.x] = M.ws.chist[(T - 1) * KMAX + threadIdx.x];
+            cT[threadIdx.x] = ws.chist[T * KMAX + threadIdx.x];
+            cP[threadIdx.x] = ws.chist[(T - 1) * KMAX + threadIdx.x];
         }
         __syncthreads();
     } else {
         T = M.max_iter;
-        reduce_tparts(M.ws.tpart + (size_t)T * T_WG * PSTRIDE, 0, 2 * K, tot);
+        reduce_tparts(ws.tpart + (size_t)T * T_WG * PSTRIDE, 0, 2 * K, tot);
         if (threadIdx.x < K) {
             const int j = threadIdx.x;
             const float S = tot[j], P = tot[K + j];
-            const float cprev = M.ws.chist[(T - 1) * KMAX + j];
+            const float cprev = ws.chist[(T - 1) * KMAX + j];
             const float cn = S > 0.f ? P / S : cprev;
             cT[j] = cn;
             cP[j] = cprev;
-            if (lead) { M.ws.chist[T * KMAX + j] = cn; M.ws.shist[T * KMAX + j] = S; }
+            if (lead) { ws.chist[T * KMAX + j] = cn; ws.shist[T * KMAX + j] = S; }
         }
         if (lead && threadIdx.x == 0) st->teff = T;
         __syncthreads();
@@ -737,10 +747,10 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int u = table_key(r);
-        M.ws.G[u] = 0.f;
+        ws.G[u] = 0.f;
         const uint32_t n = n4[r];
         if (n == 0u) continue;
-        if (!key_finite(u, M.fmt)) { M.ws.tab[u] = __builtin_nanf(""); M.ws.H[u] = __builtin_nanf(""); continue; }
+        if (!key_finite(u, M.fmt)) { ws.tab[u] = __builtin_nanf(""); ws.H[u] = __builtin_nanf(""); continue; }
         const float v = key_value(u, M.fmt);
         float a[K], d[K], c1m;
         attn_row_sel<K>(v, c0, b.s2, a, c1, c1m);
@@ -748,8 +758,8 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
         float h = 0.f;
 #pragma unroll
         for (int j = 0; j < K; ++j) h = fmaf(a[j] * d[j], sgnf(v - c0[j]), h);
-        M.ws.tab[u] = tv;
-        M.ws.H[u] = -h * b.inv_tau;
+        ws.tab[u] = tv;
+        ws.H[u] = -h * b.inv_tau;
     }
 }
 
@@ -761,9 +771,10 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
     __shared__ float tw[2 * W4];
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const uint32_t wl = blockIdx.x - M.wg_begin;
-    const int lo = M.ws.st->lo4, w = M.ws.st->w4;
-    const float* tab = M.ws.tab;
+    const int lo = ws.st->lo4, w = ws.st->w4;
+    const float* tab = ws.tab;
     for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) {
         const int s = i >= w;
         tw[i] = tab[(s << 15) | (lo + i - s * w)];
@@ -846,8 +857,9 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
     static_assert(2 * W4 * sizeof(int) <= sizeof(lds), "32-bit window fits the LDS buffer");
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const uint32_t wl = blockIdx.x - M.wg_begin;
-    const DevState* st = M.ws.st;
+    const DevState* st = ws.st;
     const bool wide = st->kmode == KEYED_U64;
     const int lo = wide ? st->lo8 : st->lo4, w = wide ? st->w8 : st->w4;
     const uint16_t* keys = M.keys;
@@ -879,7 +891,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
         }
     }
     __syncthreads();
-    float* G = M.ws.G;
+    float* G = ws.G;
     auto stream = [&](auto add) {
         for_slice<4, 4>(M, wl,
             [&](uint64_t i) { return KeysG4{ld_u2_nt(keys + i), ld_f4_nt(g + i)}; },
@@ -891,7 +903,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
             [&](uint64_t, Nothing) {},
             [&](uint64_t i) { add(keys[i], g[i]); });
     };
-    float* row = reinterpret_cast<float*>(M.ws.part) + (size_t)wl * ROW4;
+    float* row = reinterpret_cast<float*>(ws.part) + (size_t)wl * ROW4;
     if (wide) {
         const int bn = 64 - __clzll((unsigned long long)Slice<4, 4>(M).bound(M) - 1);   // 2^bn >= weights added here
         const int emax = emax_sh;
@@ -973,22 +985,23 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
     __shared__ float2 hw[2 * W8];
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const uint32_t wl = blockIdx.x - M.wg_begin;
-    const DevState* st = M.ws.st;
+    const DevState* st = ws.st;
     const int lo = st->lo8, w = st->w8;
-    const float2* HR = M.ws.HR;
+    const float2* HR = ws.HR;
     if (wl == 0 && threadIdx.x < 64) {
         // dL/dC^(0) = (1/tau) sum of the t = 1 partials + the terms that bypass the softmax
         const int T = st->teff, k = M.k;
-        const float* p1 = M.ws.bpart + (size_t)1 * T_WG * PSTRIDE;
-        const float* p0 = M.ws.bpart;
+        const float* p1 = ws.bpart + (size_t)1 * T_WG * PSTRIDE;
+        const float* p0 = ws.bpart;
         for (int j = 0; j < k; ++j) {
             const float x = wave_sum(p1[threadIdx.x * PSTRIDE + j]);
             const float e = wave_sum(p0[threadIdx.x * PSTRIDE + k + j]);
             if (threadIdx.x == 0) {
                 float gc = x * b.inv_tau;
                 if (T == 1) gc += e * b.inv_tau;
-                if (!(M.ws.shist[KMAX + j] > 0.f)) gc += M.ws.ghist[KMAX + j];
+                if (!(ws.shist[KMAX + j] > 0.f)) gc += ws.ghist[KMAX + j];
                 M.gc[j] = gc;
             }
         }
@@ -996,7 +1009,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
     {
         const uint32_t per = (NKEYS + M.wg_count - 1) / M.wg_count;
         const uint32_t u0 = wl * per, u1 = min((uint32_t)NKEYS, u0 + per);
-        for (uint32_t u = u0 + threadIdx.x; u < u1; u += NP_THREADS) M.ws.G[u] = 0.f;
+        for (uint32_t u = u0 + threadIdx.x; u < u1; u += NP_THREADS) ws.G[u] = 0.f;
     }
     for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) {
         const int s = i >= w;
@@ -1037,6 +1050,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
 __global__ void __launch_bounds__(256) k_pal_table(BatchArgs b) {
     __shared__ float lut[KMAX];
     const MatArgs& M = b.m[blockIdx.y];
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
     if (threadIdx.x < M.k) lut[threadIdx.x] = M.c_in[threadIdx.x];
     __syncthreads();
     const uint32_t u = blockIdx.x * 256 + threadIdx.x;
@@ -1049,7 +1063,7 @@ __global__ void __launch_bounds__(256) k_pal_table(BatchArgs b) {
             if (d < bd) { bd = d; best = (uint32_t)j; }
         }
     }
-    M.ws.pidx[u] = (uint8_t)best;
+    ws.pidx[u] = (uint8_t)best;
 }
 
 // Packed indices: index i occupies bits [B i, B i + B) of a little-endian bit
@@ -1062,8 +1076,9 @@ template <int B>
 __global__ void __launch_bounds__(1024) k_palettize(BatchArgs b) {
     __shared__ uint4 tbl4[NKEYS / 16];
     const MatArgs& M = b.m[np_matrix(b)];
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const uint32_t wl = blockIdx.x - M.wg_begin;
-    const uint4* src = reinterpret_cast<const uint4*>(M.ws.pidx);
+    const uint4* src = reinterpret_cast<const uint4*>(ws.pidx);
     for (int i = threadIdx.x; i < NKEYS / 16; i += blockDim.x) tbl4[i] = src[i];
     __syncthreads();
     const uint8_t* tbl = reinterpret_cast<const uint8_t*>(tbl4);
@@ -1123,19 +1138,20 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_top(BatchArgs b) {
     __shared__ float scratch[T_THREADS / 64 * 2 * K];
     __shared__ float c1sh[K], c0sh[K];
     const MatArgs& M = b.m[blockIdx.y];
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
     uint32_t n4[4];   // per-pattern inputs first: they do not depend on the centroids
     float G4[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int u = table_key(r);
-        n4[r] = M.ws.counts[u];
-        G4[r] = M.ws.G[u];
+        n4[r] = ws.counts[u];
+        G4[r] = ws.G[u];
     }
-    const DevState* st = M.ws.st;
+    const DevState* st = ws.st;
     const int T = st->teff;
     if (threadIdx.x < K) {
-        c1sh[threadIdx.x] = M.ws.chist[T * KMAX + threadIdx.x];
-        c0sh[threadIdx.x] = M.ws.chist[(T - 1) * KMAX + threadIdx.x];
+        c1sh[threadIdx.x] = ws.chist[T * KMAX + threadIdx.x];
+        c0sh[threadIdx.x] = ws.chist[(T - 1) * KMAX + threadIdx.x];
     }
     __syncthreads();
     float c1[K], c0[K];
@@ -1162,7 +1178,7 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_top(BatchArgs b) {
     }
     block_sum<2 * K, T_THREADS>(acc, scratch, tot);
     if (threadIdx.x < 2 * K)
-        M.ws.bpart[(size_t)blockIdx.x * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
+        ws.bpart[(size_t)blockIdx.x * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
 }
 
 // Iteration t = T..1 of the backward: gamma = dL/dC^(t), then per occupied
@@ -1178,7 +1194,8 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
     __shared__ float scratch[T_THREADS / 64 * K];
     __shared__ float gsh[K], gSsh[K], c1sh[K], c0sh[K];
     const MatArgs& M = b.m[blockIdx.y];
-    const DevState* st = M.ws.st;
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
+    const DevState* st = ws.st;
     const int T = st->teff;
     const int t = b.t;
     if (t > T) return;
@@ -1187,35 +1204,35 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int u = table_key(r);
-        n4[r] = M.ws.counts[u];
-        R4[r] = t != T ? M.ws.R[u] : 0.f;
-        H4[r] = t == 1 ? M.ws.H[u] : 0.f;
+        n4[r] = ws.counts[u];
+        R4[r] = t != T ? ws.R[u] : 0.f;
+        H4[r] = t == 1 ? ws.H[u] : 0.f;
     }
     const bool lead = blockIdx.x == 0;
     if (t == T) {
-        reduce_tparts(M.ws.bpart, 0, K, tot);
+        reduce_tparts(ws.bpart, 0, K, tot);
         if (threadIdx.x < K) gsh[threadIdx.x] = tot[threadIdx.x];
     } else {
-        reduce_tparts2(M.ws.bpart + (size_t)(t + 1) * T_WG * PSTRIDE, M.ws.bpart, K, tot);
+        reduce_tparts2(ws.bpart + (size_t)(t + 1) * T_WG * PSTRIDE, ws.bpart, K, tot);
         if (threadIdx.x < K) {
             const int j = threadIdx.x;
             float gm = tot[j] * b.inv_tau;
             if (t + 1 == T) gm += tot[K + j] * b.inv_tau;
-            if (!(M.ws.shist[(t + 1) * KMAX + j] > 0.f)) gm += M.ws.ghist[(t + 1) * KMAX + j];
+            if (!(ws.shist[(t + 1) * KMAX + j] > 0.f)) gm += ws.ghist[(t + 1) * KMAX + j];
             gsh[j] = gm;
         }
     }
     if (threadIdx.x < K) {
         const int j = threadIdx.x;
-        c1sh[j] = M.ws.chist[t * KMAX + j];
-        c0sh[j] = M.ws.chist[(t - 1) * KMAX + j];
+        c1sh[j] = ws.chist[t * KMAX + j];
+        c0sh[j] = ws.chist[(t - 1) * KMAX + j];
     }
     __syncthreads();
     if (threadIdx.x < K) {
         const int j = threadIdx.x;
-        const float S = M.ws.shist[t * KMAX + j];
+        const float S = ws.shist[t * KMAX + j];
         gSsh[j] = S > 0.f ? gsh[j] / S : 0.f;
-        if (lead) M.ws.ghist[t * KMAX + j] = gsh[j];
+        if (lead) ws.ghist[t * KMAX + j] = gsh[j];
     }
     __syncthreads();
     float c1[K], c0[K], gS[K];
@@ -1230,7 +1247,7 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
         const uint32_t n = n4[r];
         if (n == 0u) continue;
         if (!key_finite(u, M.fmt)) {
-            if (t == 1) M.ws.HR[u] = make_float2(__builtin_nanf(""), __builtin_nanf(""));
+            if (t == 1) ws.HR[u] = make_float2(__builtin_nanf(""), __builtin_nanf(""));
             continue;
         }
         const float v = key_value(u, M.fmt);
@@ -1246,12 +1263,12 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
             acc[j] = fmaf(nf, dl, acc[j]);
         }
         const float Ru = fmaf(-r_, b.inv_tau, direct) + R4[r];
-        if (t == 1) M.ws.HR[u] = make_float2(H4[r], Ru);
-        else M.ws.R[u] = Ru;
+        if (t == 1) ws.HR[u] = make_float2(H4[r], Ru);
+        else ws.R[u] = Ru;
     }
     block_sum<K, T_THREADS>(acc, scratch, tot);
     if (threadIdx.x < K)
-        M.ws.bpart[((size_t)t * T_WG + blockIdx.x) * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
+        ws.bpart[((size_t)t * T_WG + blockIdx.x) * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
 }
 
 // ----------------------------------------------------------------------------
@@ -1288,9 +1305,10 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_iter(BatchArgs b) {
     __shared__ float scratch[D_THREADS / 64 * 2 * K];
     __shared__ float csh[K];
     const MatArgs& M = b.m[0];
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const int t = b.t;
-    if (t > 1 && M.ws.st->conv) return;
-    if (threadIdx.x < K) csh[threadIdx.x] = t == 1 ? M.c_in[threadIdx.x] : M.ws.chist[(t - 1) * KMAX + threadIdx.x];
+    if (t > 1 && ws.st->conv) return;
+    if (threadIdx.x < K) csh[threadIdx.x] = t == 1 ? M.c_in[threadIdx.x] : ws.chist[(t - 1) * KMAX + threadIdx.x];
     __syncthreads();
     float c[K];
 #pragma unroll
@@ -1313,7 +1331,7 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_iter(BatchArgs b) {
         }
     }
     block_sum<2 * K, D_THREADS>(acc, scratch, tot);
-    if (threadIdx.x < 2 * K) M.ws.dpart[(size_t)blockIdx.x * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
+    if (threadIdx.x < 2 * K) ws.dpart[(size_t)blockIdx.x * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
 }
 
 // One block: C^(t) from the dense partials, history, early stop.
@@ -1323,20 +1341,21 @@ __global__ void __launch_bounds__(1024) k_dense_fin(BatchArgs b, int nrow) {
     __shared__ float tot[2 * K];
     __shared__ int stop;
     const MatArgs& M = b.m[0];
-    DevState* st = M.ws.st;
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
+    DevState* st = ws.st;
     const int t = b.t;
     if (t > 1 && st->conv) return;
-    reduce_dparts(M.ws.dpart, nrow, 0, 2 * K, scratch, tot);
+    reduce_dparts(ws.dpart, nrow, 0, 2 * K, scratch, tot);
     if (threadIdx.x == 0) stop = 0;
     __syncthreads();
     if (threadIdx.x < K) {
         const int j = threadIdx.x;
-        const float cprev = t == 1 ? M.c_in[j] : M.ws.chist[(t - 1) * KMAX + j];
-        if (t == 1) { M.ws.chist[j] = cprev; M.ws.shist[j] = 0.f; }
+        const float cprev = t == 1 ? M.c_in[j] : ws.chist[(t - 1) * KMAX + j];
+        if (t == 1) { ws.chist[j] = cprev; ws.shist[j] = 0.f; }
         const float S = tot[j], P = tot[K + j];
         const float cn = S > 0.f ? P / S : cprev;
-        M.ws.chist[t * KMAX + j] = cn;
-        M.ws.shist[t * KMAX + j] = S;
+        ws.chist[t * KMAX + j] = cn;
+        ws.shist[t * KMAX + j] = S;
         if (!(fabsf(cn - cprev) <= b.eps)) atomicOr(&stop, 1);
     }
     __syncthreads();
@@ -1349,18 +1368,19 @@ __global__ void __launch_bounds__(1024) k_dense_fin(BatchArgs b, int nrow) {
 template <int K>
 __global__ void __launch_bounds__(D_THREADS) k_dense_out(BatchArgs b) {
     const MatArgs& M = b.m[0];
-    const int T = M.ws.st->teff;
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
+    const int T = ws.st->teff;
     __shared__ float c1sh[K], c0sh[K];
     if (threadIdx.x < K) {
-        c1sh[threadIdx.x] = M.ws.chist[T * KMAX + threadIdx.x];
-        c0sh[threadIdx.x] = M.ws.chist[(T - 1) * KMAX + threadIdx.x];
+        c1sh[threadIdx.x] = ws.chist[T * KMAX + threadIdx.x];
+        c0sh[threadIdx.x] = ws.chist[(T - 1) * KMAX + threadIdx.x];
     }
     __syncthreads();
     float c1[K], c0[K];
 #pragma unroll
     for (int j = 0; j < K; ++j) { c1[j] = c1sh[j]; c0[j] = c0sh[j]; }
     if (blockIdx.x == 0) {
-        if (threadIdx.x < K) M.c_out[threadIdx.x] = M.ws.chist[T * KMAX + threadIdx.x];
+        if (threadIdx.x < K) M.c_out[threadIdx.x] = ws.chist[T * KMAX + threadIdx.x];
         if (threadIdx.x == 0 && M.iters_out) *M.iters_out = T;
     }
     uint64_t beg, end;
@@ -1395,11 +1415,12 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_btop(BatchArgs b) {
     __shared__ float tot[2 * K];
     __shared__ float scratch[D_THREADS / 64 * 2 * K];
     const MatArgs& M = b.m[0];
-    const int T = M.ws.st->teff;
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
+    const int T = ws.st->teff;
     __shared__ float c1sh[K], c0sh[K];
     if (threadIdx.x < K) {
-        c1sh[threadIdx.x] = M.ws.chist[T * KMAX + threadIdx.x];
-        c0sh[threadIdx.x] = M.ws.chist[(T - 1) * KMAX + threadIdx.x];
+        c1sh[threadIdx.x] = ws.chist[T * KMAX + threadIdx.x];
+        c0sh[threadIdx.x] = ws.chist[(T - 1) * KMAX + threadIdx.x];
     }
     __syncthreads();
     float c1[K], c0[K];
@@ -1429,7 +1450,7 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_btop(BatchArgs b) {
         M.gw[i] = -g * h * b.inv_tau;
     }
     block_sum<2 * K, D_THREADS>(acc, scratch, tot);
-    if (threadIdx.x < 2 * K) M.ws.dpart[(size_t)blockIdx.x * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
+    if (threadIdx.x < 2 * K) ws.dpart[(size_t)blockIdx.x * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
 }
 
 // Dense backward iteration t (reads gamma^(t) from ghist).
@@ -1439,15 +1460,16 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_biter(BatchArgs b) {
     __shared__ float scratch[D_THREADS / 64 * K];
     __shared__ float c1sh[K], c0sh[K], gSsh[K];
     const MatArgs& M = b.m[0];
-    const int T = M.ws.st->teff;
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
+    const int T = ws.st->teff;
     const int t = b.t;
     if (t > T) return;
     if (threadIdx.x < K) {
         const int j = threadIdx.x;
-        c1sh[j] = M.ws.chist[t * KMAX + j];
-        c0sh[j] = M.ws.chist[(t - 1) * KMAX + j];
-        const float S = M.ws.shist[t * KMAX + j];
-        gSsh[j] = S > 0.f ? M.ws.ghist[t * KMAX + j] / S : 0.f;
+        c1sh[j] = ws.chist[t * KMAX + j];
+        c0sh[j] = ws.chist[(t - 1) * KMAX + j];
+        const float S = ws.shist[t * KMAX + j];
+        gSsh[j] = S > 0.f ? ws.ghist[t * KMAX + j] / S : 0.f;
     }
     __syncthreads();
     float c1[K], c0[K], gS[K];
@@ -1475,7 +1497,7 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_biter(BatchArgs b) {
         M.gw[i] += fmaf(-r, b.inv_tau, direct);
     }
     block_sum<K, D_THREADS>(acc, scratch, tot);
-    if (threadIdx.x < K) M.ws.dpart[(size_t)blockIdx.x * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
+    if (threadIdx.x < K) ws.dpart[(size_t)blockIdx.x * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
 }
 
 // One block.  b.t = 0 (after btop): gamma^(T) = dL/dC^(T) and E.  b.t = t in
@@ -1485,24 +1507,25 @@ __global__ void __launch_bounds__(1024) k_dense_bfin(BatchArgs b, int nrow) {
     __shared__ float scratch[16 * PSTRIDE];
     __shared__ float tot[2 * K];
     const MatArgs& M = b.m[0];
-    const int T = M.ws.st->teff;
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
+    const int T = ws.st->teff;
     const int t = b.t;
     if (t == 0) {
-        reduce_dparts(M.ws.dpart, nrow, 0, 2 * K, scratch, tot);
+        reduce_dparts(ws.dpart, nrow, 0, 2 * K, scratch, tot);
         if (threadIdx.x < K) {
-            M.ws.ghist[T * KMAX + threadIdx.x] = tot[threadIdx.x];
-            M.ws.ehist[threadIdx.x] = tot[K + threadIdx.x] * b.inv_tau;
+            ws.ghist[T * KMAX + threadIdx.x] = tot[threadIdx.x];
+            ws.ehist[threadIdx.x] = tot[K + threadIdx.x] * b.inv_tau;
         }
         return;
     }
     if (t > T) return;
-    reduce_dparts(M.ws.dpart, nrow, 0, K, scratch, tot);
+    reduce_dparts(ws.dpart, nrow, 0, K, scratch, tot);
     if (threadIdx.x < K) {
         const int j = threadIdx.x;
         float gm = tot[j] * b.inv_tau;
-        if (t == T) gm += M.ws.ehist[j];
-        if (!(M.ws.shist[t * KMAX + j] > 0.f)) gm += M.ws.ghist[t * KMAX + j];
-        M.ws.ghist[(t - 1) * KMAX + j] = gm;
+        if (t == T) gm += ws.ehist[j];
+        if (!(ws.shist[t * KMAX + j] > 0.f)) gm += ws.ghist[t * KMAX + j];
+        ws.ghist[(t - 1) * KMAX + j] = gm;
         if (t == 1) M.gc[j] = gm;
     }
 }

@@ -51,6 +51,7 @@ NKEYS = 65536
 PASS_HIST, PASS_GATHER_WT, PASS_KEYED_GRAD, PASS_GATHER_GRAD = 0, 1, 2, 3
 PASS_DENSE_ITER, PASS_DENSE_BITER, PASS_PALETTIZE = 4, 5, 6
 KEYS_FP16, KEYS_BF16 = 0, 1
+LAUNCH_GROUP = 28          # EDKM_LAUNCH_GROUP: matrices per launch in the batched calls
 KEYED_AUTO, KEYED_I32, KEYED_U64 = -1, 0, 1
 KEY_FORMATS = {"fp16": KEYS_FP16, "bf16": KEYS_BF16}
 
@@ -296,7 +297,7 @@ def backward_batch(plans, w_bits, grad_w_tilde, grad_w, grad_c, stream=None) -> 
 
 def palettize_batch(plans, w_bits, lut, indices_out, stream=None) -> None:
     """palettize over a batch: one table launch and one packing launch per
-    launch group (up to 8 matrices with the same bit width and format)."""
+    launch group (up to LAUNCH_GROUP matrices with the same bit width and format)."""
     _same_len("palettize_batch", plans, w_bits=w_bits, lut=lut, indices_out=indices_out)
     for p, o in zip(plans, indices_out):
         need = (p.n * p.bits + 7) // 8

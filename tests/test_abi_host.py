@@ -155,6 +155,11 @@ def test_batch_bindings_reject_lists_of_other_lengths():
         edkm.palettize_batch(plans, two, two, [object(), object(), object()])
 
 
+def test_launch_group_size_matches_header():
+    text = open(HEADER).read()
+    assert int(re.search(r"#define EDKM_LAUNCH_GROUP (\d+)", text).group(1)) == edkm.LAUNCH_GROUP
+
+
 def test_status_strings():
     for s in (0, -1, -2, -3, -4, -5):
         assert edkm.status_str(s) and edkm.status_str(s) != "unknown status"

@@ -153,11 +153,12 @@ def gpu_palettize_batch(keys_list, luts, bits_list, fmt, offsets=None):
 
 @pytest.mark.parametrize("fmt", ["fp16", "bf16"])
 def test_palettize_batch_bit_exact(fmt):
-    """Eleven matrices: two launch groups cut by size (8 + 3) and by bit width,
-    ragged sizes, one matrix off alignment (its scalar path beside vectorised
-    neighbours)."""
-    sizes = [1, 31, 65537, 1_000_003, 33, 300_007, 16, 2_000_001, 999, 70_000, 8]
-    bits = [3, 3, 3, 3, 3, 3, 3, 3, 2, 2, 4]
+    """Thirty-two matrices in four launch groups: 28 + 2 at 3 bits (cut by
+    size), then one each at 2 and 4 bits (cut by bit width); ragged sizes, one
+    matrix off alignment (its scalar path beside vectorised neighbours)."""
+    sizes = [1, 31, 65537, 1_000_003, 33, 300_007, 16, 2_000_001] + [999 + 4099 * i for i in range(22)] + [70_000, 8]
+    bits = [3] * 30 + [2, 4]
+    assert edkm.LAUNCH_GROUP == 28
     offsets = [(0, 0)] * len(sizes)
     offsets[5] = (1, 1)
     keys = [inputs.weights(n, 220 + i, i % 2 == 1, fmt) for i, n in enumerate(sizes)]

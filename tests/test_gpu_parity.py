@@ -401,6 +401,38 @@ def test_batch_equals_single_calls():
         check(res, oracle(ks[i], c0s[i], gs[i]), what="batch %d" % i)
 
 
+def test_batch_spanning_launch_groups():
+    """31 matrices: one full launch group of LAUNCH_GROUP matrices and one of 3
+    (cut by size).  Every matrix equals its single-matrix call (forward
+    bitwise) and the oracle."""
+    assert edkm.LAUNCH_GROUP == 28
+    sizes = [4096 + 1531 * i for i in range(31)]
+    ks = [inputs.fp16_weights(n, 400 + i, outliers=(i % 5 == 2)) for i, n in enumerate(sizes)]
+    c0s = [inputs.quantile_init(k, 8) for k in ks]
+    gs = [inputs.upstream_grad(n, 440 + i) for i, n in enumerate(sizes)]
+    say("batch over two launch groups")
+    plans = [edkm.Plan(n, 3, ITERS) for n in sizes]
+    kd = [dkeys(k) for k in ks]
+    ci = [torch.from_numpy(c).to(DEV) for c in c0s]
+    co = [torch.empty(8, device=DEV) for _ in sizes]
+    wt = [torch.empty(n, device=DEV) for n in sizes]
+    it = [torch.zeros(1, dtype=torch.int32, device=DEV) for _ in sizes]
+    gd = [torch.from_numpy(g).to(DEV) for g in gs]
+    gw = [torch.empty(n, device=DEV) for n in sizes]
+    gc = [torch.empty(8, device=DEV) for _ in sizes]
+    edkm.init_unique_batch(plans, kd)
+    edkm.forward_batch(plans, kd, TAU, 0.0, ci, co, wt, False, it)
+    edkm.backward_batch(plans, kd, gd, gw, gc)
+    torch.cuda.synchronize()
+    for i in range(len(sizes)):
+        single = gpu(ks[i], c0s[i], 3, g=gs[i])
+        assert np.array_equal(co[i].cpu().numpy(), single["c_out"]), i
+        assert np.array_equal(wt[i].cpu().numpy(), single["w_tilde"]), i
+        res = dict(iters=it[i].cpu().numpy(), c_out=co[i].cpu().numpy(), w_tilde=wt[i].cpu().numpy(),
+                   grad_w=gw[i].cpu().numpy(), grad_c=gc[i].cpu().numpy())
+        check(res, oracle(ks[i], c0s[i], gs[i]), what="group batch %d" % i)
+
+
 def test_call_order_and_key_buffer_checks():
     keys = inputs.fp16_weights(4096, 141)
     c0 = torch.from_numpy(inputs.quantile_init(keys, 8)).to(DEV)
