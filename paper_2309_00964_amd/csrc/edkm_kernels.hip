@@ -15,8 +15,9 @@
 //     bitwise repeatable;
 //   * the dense comparison path (the same mathematics per weight over the
 //     N x k map) and the palettization export (packed nearest-entry indices).
-// Every launch carries up to MAXB matrices (blockIdx.y or a workgroup range per
-// matrix), so a whole decoder layer pays each launch latency once.
+// Every launch carries up to MAXB = 28 matrices (blockIdx.y or a workgroup
+// range per matrix), so a decoder layer, or four of them, pays each launch
+// latency once.
 //
 // Nothing here uses MFMA: k <= 16 centroids is not a dense contraction.
 
