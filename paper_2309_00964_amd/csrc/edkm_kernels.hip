@@ -1114,7 +1114,7 @@ __global__ void __launch_bounds__(1024) k_palettize(BatchArgs b) {
                 }
             }
 #pragma unroll
-            for (int q2 = 0; q2 < B; ++q2) out32[gi * B + q2] = w[q2];
+            for (int q2 = 0; q2 < B; ++q2) __builtin_nontemporal_store(w[q2], out32 + gi * B + q2);
         } else {
 #pragma unroll
             for (int t = 0; t < 32; ++t)
