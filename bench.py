@@ -183,11 +183,11 @@ def timed(step, plan, pass_ids, steps, warmup):
     return max(wall, gpu_s), avg
 
 
-def hbm_roofline(avg_ms, total):
+def hbm_roofline(avg_ms, total, out_half=False):
     """Roofline of the dominant N-sized pass (HBM-bound) plus all passes."""
     passes = {}
     for p, ms in avg_ms.items():
-        nbytes = PASS_BYTES[p] * total
+        nbytes = (4 if out_half and p == "k_gather_wt" else PASS_BYTES[p]) * total
         passes[p] = {"avg_us": ms * 1000.0, "bytes": nbytes, "GBps": nbytes / (ms * 1e-3) / 1e9}
     dom = max(passes, key=lambda p: passes[p]["avg_us"])
     traffic = None
@@ -223,7 +223,8 @@ class Matrices:
     """Device inputs and outputs of a list of (name, rows, cols) matrices, each
     with its own plan and centroids."""
 
-    def __init__(self, config, mats, bits, outliers=False, on_device=False, keep_host=(), fmt="fp16"):
+    def __init__(self, config, mats, bits, outliers=False, on_device=False, keep_host=(), fmt="fp16",
+                 out_half=False):
         import numpy as np
         import torch
         from paper_2309_00964_amd import edkm, inputs
@@ -256,19 +257,20 @@ class Matrices:
             self.keys.append(kt)
             self.c_in.append(c0)
             self.c_out.append(torch.empty(k, device=dev))
-            self.wt.append(torch.empty(n, device=dev))
+            self.wt.append(torch.empty(n, dtype=torch.int16 if out_half else torch.float32, device=dev))
             self.iters.append(torch.zeros(1, dtype=torch.int32, device=dev))
             self.grads.append(gt)
             self.gw.append(torch.empty(n, device=dev))
             self.gc.append(torch.empty(k, device=dev))
         self.fmt = fmt
+        self.out_half = out_half
         torch.cuda.synchronize()
 
     def step(self):
         from paper_2309_00964_amd import edkm, inputs
         edkm.init_unique_batch(self.plans, self.keys)
         edkm.forward_batch(self.plans, self.keys, inputs.TAU, 0.0, self.c_in, self.c_out, self.wt,
-                           False, self.iters)
+                           self.out_half, self.iters)
         edkm.backward_batch(self.plans, self.keys, self.grads, self.gw, self.gc)
 
     def dense_step(self):
@@ -312,10 +314,12 @@ def bench_decoder_layer(args):
     from paper_2309_00964_amd import inputs
     bits = 3
     keep = () if args.no_cpu_baseline else tuple(args.cpu_sample)
-    m = Matrices(4, inputs.WORKLOADS[4]["mats"], bits, keep_host=keep, fmt=args.key_format)
+    half = args.w_tilde == "half"
+    m = Matrices(4, inputs.WORKLOADS[4]["mats"], bits, keep_host=keep, fmt=args.key_format, out_half=half)
     elapsed, avg = timed(m.step, m.plans[0], PASS_IDS, args.steps, args.warmup)
-    out = result_line(args, "llama7b_decoder_layer_3bit" + _fmt_tag(args), m, bits, elapsed,
-                      hbm_roofline(avg, m.total))
+    out = result_line(args, "llama7b_decoder_layer_3bit" + _fmt_tag(args) + ("_half_wtilde" if half else ""),
+                      m, bits, elapsed, hbm_roofline(avg, m.total, half),
+                      {"w_tilde": m.fmt if half else "fp32"})
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(m.host, 1 << bits, fmt=m.fmt)
     return out
@@ -468,6 +472,9 @@ def main():
                          "palettize: 1-4 (default 3)")
     ap.add_argument("--key-format", choices=("fp16", "bf16"), default="fp16",
                     help="weight format (default fp16, the metric's; bf16 is the paper's training format)")
+    ap.add_argument("--w-tilde", choices=("fp32", "half"), default="fp32",
+                    help="decoder_layer: W~ output as fp32 (default, 24 B per weight) or in the "
+                         "16-bit weight format (22 B per weight)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", nargs="+", default=[m[0] for m in LLAMA7B_LAYER],
                     help="matrices of the layer the CPU oracle is timed on (default: all seven)")

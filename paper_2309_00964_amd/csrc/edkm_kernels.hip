@@ -302,9 +302,9 @@ typedef float v4f_t __attribute__((ext_vector_type(4)));
 // non-temporal (nt) loads help the read-only passes (histogram, keyed sum) and
 // the gradient gather; the W~ gather keeps plain loads, which leave the keys
 // in the caches for the keyed sum when a backward follows.  The gathers'
-// float4 outputs use nt stores (gradient gather 404 -> 381 us on the decoder
-// layer, and the kernel after the W~ gather no longer inherits its dirty
-// lines).
+// outputs use nt stores, float4 or (16-bit W~) uint2: gradient gather 404 ->
+// 381 us on the decoder layer, 16-bit W~ gather 168 -> 162 us, and the kernel
+// after the W~ gather no longer inherits its dirty lines.
 __device__ __forceinline__ uint4 ld_u4(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 __device__ __forceinline__ uint2 ld_u2(const void* p) { return *reinterpret_cast<const uint2*>(p); }
 __device__ __forceinline__ float4 ld_f4(const float* p) { return *reinterpret_cast<const float4*>(p); }
@@ -323,7 +323,9 @@ __device__ __forceinline__ float4 ld_f4_nt(const float* p) {
 __device__ __forceinline__ void st_f4_nt(float* p, float4 x) {
     __builtin_nontemporal_store(v4f_t{x.x, x.y, x.z, x.w}, reinterpret_cast<v4f_t*>(p));
 }
-__device__ __forceinline__ void st_u2(void* p, uint2 x) { *reinterpret_cast<uint2*>(p) = x; }
+__device__ __forceinline__ void st_u2_nt(void* p, uint2 x) {
+    __builtin_nontemporal_store(v2u_t{x.x, x.y}, reinterpret_cast<v2u_t*>(p));
+}
 
 // ----------------------------------------------------------------------------
 // init_unique: zero, histogram, partial merge, window selection
@@ -809,7 +811,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
                 const float4 v = look4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16);
                 return make_uint2(h2(v.x, v.y), h2(v.z, v.w));
             },
-            [&](uint64_t i, uint2 o) { st_u2(out + i, o); },
+            [&](uint64_t i, uint2 o) { st_u2_nt(out + i, o); },
             [&](uint64_t i) { out[i] = (uint16_t)to_half_bits(look(keys[i]), M.fmt); });
     } else {
         float* out = reinterpret_cast<float*>(M.wt);
