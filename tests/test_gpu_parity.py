@@ -433,6 +433,80 @@ def test_batch_spanning_launch_groups():
         check(res, oracle(ks[i], c0s[i], gs[i]), what="group batch %d" % i)
 
 
+class _Mats:
+    """Device buffers of a list of (n, bits) matrices for the batched calls."""
+
+    def __init__(self, spec, seed):
+        self.spec = spec
+        self.ks = [inputs.fp16_weights(n, seed + i, outliers=(i % 3 == 1)) for i, (n, _) in enumerate(spec)]
+        self.c0s = [inputs.quantile_init(k, 1 << b) for k, (_, b) in zip(self.ks, spec)]
+        self.gs = [inputs.upstream_grad(n, seed + 40 + i) for i, (n, _) in enumerate(spec)]
+        self.plans = [edkm.Plan(n, b, ITERS) for n, b in spec]
+        self.kd = [dkeys(k) for k in self.ks]
+        self.ci = [torch.from_numpy(c).to(DEV) for c in self.c0s]
+        self.co = [torch.empty(1 << b, device=DEV) for _, b in spec]
+        self.wt = [torch.empty(n, device=DEV) for n, _ in spec]
+        self.it = [torch.zeros(1, dtype=torch.int32, device=DEV) for _ in spec]
+        self.gd = [torch.from_numpy(g).to(DEV) for g in self.gs]
+        self.gw = [torch.empty(n, device=DEV) for n, _ in spec]
+        self.gc = [torch.empty(1 << b, device=DEV) for _, b in spec]
+
+    def sub(self, name, idx):
+        return [getattr(self, name)[i] for i in idx]
+
+    def result(self, i):
+        return dict(iters=self.it[i].cpu().numpy(), c_out=self.co[i].cpu().numpy(),
+                    w_tilde=self.wt[i].cpu().numpy(), grad_w=self.gw[i].cpu().numpy(),
+                    grad_c=self.gc[i].cpu().numpy())
+
+
+def test_batch_mixed_bit_widths():
+    """Matrices of 1 to 4 bits in one batched step: launch groups are cut where
+    the bit width changes.  Each matrix equals its single call (forward
+    bitwise) and the oracle."""
+    spec = [(70_001, 3), (65536, 1), (100_003, 4), (30_000, 4), (5000, 2), (90_000, 3)]
+    m = _Mats(spec, 470)
+    say("batch, mixed bit widths")
+    edkm.init_unique_batch(m.plans, m.kd)
+    edkm.forward_batch(m.plans, m.kd, TAU, 0.0, m.ci, m.co, m.wt, False, m.it)
+    edkm.backward_batch(m.plans, m.kd, m.gd, m.gw, m.gc)
+    torch.cuda.synchronize()
+    for i, (n, b) in enumerate(spec):
+        single = gpu(m.ks[i], m.c0s[i], b, g=m.gs[i])
+        assert np.array_equal(m.co[i].cpu().numpy(), single["c_out"]), i
+        assert np.array_equal(m.wt[i].cpu().numpy(), single["w_tilde"]), i
+        check(m.result(i), oracle(m.ks[i], m.c0s[i], m.gs[i]), what="mixed bits %d" % i)
+
+
+def test_backward_batch_over_forwards_with_different_tau():
+    """Two forward_batch calls with different tau, then one backward_batch over
+    all plans: the backward splits its launch groups where tau changes, and each
+    matrix's gradients match the oracle at its own tau."""
+    spec = [(65536, 3), (100_003, 3), (70_001, 3), (30_000, 3)]
+    taus = [TAU, TAU, 5e-3, 5e-3]
+    m = _Mats(spec, 480)
+    say("backward batch, two taus")
+    edkm.init_unique_batch(m.plans, m.kd)
+    for idx, tau in (([0, 1], TAU), ([2, 3], 5e-3)):
+        edkm.forward_batch(m.sub("plans", idx), m.sub("kd", idx), tau, 0.0, m.sub("ci", idx), m.sub("co", idx),
+                           m.sub("wt", idx), False, m.sub("it", idx))
+    edkm.backward_batch(m.plans, m.kd, m.gd, m.gw, m.gc)
+    torch.cuda.synchronize()
+    for i in range(len(spec)):
+        check(m.result(i), oracle(m.ks[i], m.c0s[i], m.gs[i], tau=taus[i]), what="tau %g matrix %d" % (taus[i], i))
+
+
+@pytest.mark.parametrize("tau", [2e-4, 5e-2])
+def test_unique_path_at_other_temperatures(tau):
+    """Near-hard assignment (tau = 2e-4, a tenth of the workload's) and a soft
+    one (tau = 5e-2, most weights spread over several centroids)."""
+    keys = inputs.fp16_weights(300_007, 490, outliers=True)
+    c0 = inputs.quantile_init(keys, 8)
+    g = inputs.upstream_grad(keys.size, 491)
+    say("tau", tau)
+    check(gpu(keys, c0, 3, g=g, tau=tau), oracle(keys, c0, g, tau=tau), what="tau %g" % tau)
+
+
 def test_call_order_and_key_buffer_checks():
     keys = inputs.fp16_weights(4096, 141)
     c0 = torch.from_numpy(inputs.quantile_init(keys, 8)).to(DEV)
