@@ -6,8 +6,11 @@ functions keep the C names without the ``edkm_`` prefix.  Importing this module
 loads the library and raises ``ImportError`` if it has not been built (run
 ``__graft_entry__.build()``); there is no fallback.
 
-Weights are passed as fp16 bit patterns: any contiguous 2-byte device tensor
-(``torch.float16`` weights themselves, or ``int16`` / ``uint16`` views).
+Weights are passed as 16-bit patterns of the plan's format (fp16 or bf16): any
+contiguous 2-byte device tensor (the weights themselves, or ``int16`` views).
+Every tensor is checked here to be a contiguous device tensor with the element
+size and at least the element count the kernels access through it (the C ABI
+takes raw pointers and cannot check sizes).
 """
 from __future__ import annotations
 
@@ -125,8 +128,9 @@ def _check(status: int, where: str, plans=()) -> None:
         raise EdkmError(status, where, detail)
 
 
-def _ptr(t, nbytes_elem=None, name="tensor"):
-    """Device pointer of a contiguous tensor (None -> NULL)."""
+def _ptr(t, nbytes_elem=None, name="tensor", count=None):
+    """Device pointer of a contiguous tensor (None -> NULL) holding at least
+    `count` elements: the kernels read and write that many through it."""
     if t is None:
         return None
     if isinstance(t, int):
@@ -137,6 +141,8 @@ def _ptr(t, nbytes_elem=None, name="tensor"):
         raise ValueError("%s must be contiguous" % name)
     if nbytes_elem is not None and t.element_size() != nbytes_elem:
         raise ValueError("%s must have %d-byte elements" % (name, nbytes_elem))
+    if count is not None and t.numel() < count:
+        raise ValueError("%s has %d elements, %d needed" % (name, t.numel(), count))
     return t.data_ptr()
 
 
@@ -185,7 +191,8 @@ def palettize(plan: Plan, w_bits, lut, indices_out, stream=None) -> None:
     need = (plan.n * plan.bits + 7) // 8
     if indices_out.numel() * indices_out.element_size() < need:
         raise EdkmError(ERR_ARG, "palettize", "indices_out needs %d bytes" % need)
-    _check(_lib.edkm_palettize(plan.ref, _ptr(w_bits, 2, "w_bits"), _ptr(lut, 4), _ptr(indices_out, 1),
+    _check(_lib.edkm_palettize(plan.ref, _ptr(w_bits, 2, "w_bits", plan.n), _ptr(lut, 4, "lut", plan.k),
+                               _ptr(indices_out, 1),
                                _stream(stream)), "palettize", (plan,))
 
 
@@ -205,42 +212,53 @@ def plan_init(n: int, bits: int, max_iter: int, device="cuda") -> Plan:
 
 def init_unique(plan: Plan, w_bits, counts_out=None, num_unique_out=None, check_finite=False,
                 stream=None) -> None:
-    _check(_lib.edkm_init_unique(plan.ref, _ptr(w_bits, 2, "w_bits"), _ptr(counts_out, 4),
-                                 _ptr(num_unique_out, 4), int(bool(check_finite)), _stream(stream)),
+    _check(_lib.edkm_init_unique(plan.ref, _ptr(w_bits, 2, "w_bits", plan.n),
+                                 _ptr(counts_out, 4, "counts_out", NKEYS),
+                                 _ptr(num_unique_out, 4, "num_unique_out", 1), int(bool(check_finite)),
+                                 _stream(stream)),
            "init_unique", (plan,))
 
 
 def forward(plan: Plan, w_bits, tau: float, eps: float, c_in, c_out, w_tilde, out_half=False,
             iters_out=None, stream=None) -> None:
-    _check(_lib.edkm_forward(plan.ref, _ptr(w_bits, 2, "w_bits"), float(tau), float(eps),
-                             _ptr(c_in, 4), _ptr(c_out, 4), _ptr(w_tilde, 2 if out_half else 4),
-                             int(bool(out_half)), _ptr(iters_out, 4), _stream(stream)),
+    _check(_lib.edkm_forward(plan.ref, _ptr(w_bits, 2, "w_bits", plan.n), float(tau), float(eps),
+                             _ptr(c_in, 4, "c_in", plan.k), _ptr(c_out, 4, "c_out", plan.k),
+                             _ptr(w_tilde, 2 if out_half else 4, "w_tilde", plan.n),
+                             int(bool(out_half)), _ptr(iters_out, 4, "iters_out", 1), _stream(stream)),
            "forward", (plan,))
 
 
 def backward(plan: Plan, w_bits, grad_w_tilde, grad_w, grad_c, stream=None) -> None:
-    _check(_lib.edkm_backward(plan.ref, _ptr(w_bits, 2, "w_bits"), _ptr(grad_w_tilde, 4),
-                              _ptr(grad_w, 4), _ptr(grad_c, 4), _stream(stream)),
+    _check(_lib.edkm_backward(plan.ref, _ptr(w_bits, 2, "w_bits", plan.n),
+                              _ptr(grad_w_tilde, 4, "grad_w_tilde", plan.n),
+                              _ptr(grad_w, 4, "grad_w", plan.n), _ptr(grad_c, 4, "grad_c", plan.k),
+                              _stream(stream)),
            "backward", (plan,))
 
 
 def forward_dense(plan: Plan, w_bits, tau: float, eps: float, c_in, c_out, w_tilde,
                   out_half=False, iters_out=None, attn_out=None, stream=None) -> None:
-    _check(_lib.edkm_forward_dense(plan.ref, _ptr(w_bits, 2, "w_bits"), float(tau), float(eps),
-                                   _ptr(c_in, 4), _ptr(c_out, 4),
-                                   _ptr(w_tilde, 2 if out_half else 4), int(bool(out_half)),
-                                   _ptr(iters_out, 4), _ptr(attn_out, 4), _stream(stream)),
+    _check(_lib.edkm_forward_dense(plan.ref, _ptr(w_bits, 2, "w_bits", plan.n), float(tau), float(eps),
+                                   _ptr(c_in, 4, "c_in", plan.k), _ptr(c_out, 4, "c_out", plan.k),
+                                   _ptr(w_tilde, 2 if out_half else 4, "w_tilde", plan.n),
+                                   int(bool(out_half)), _ptr(iters_out, 4, "iters_out", 1),
+                                   _ptr(attn_out, 4, "attn_out", plan.n * plan.k), _stream(stream)),
            "forward_dense", (plan,))
 
 
 def backward_dense(plan: Plan, w_bits, grad_w_tilde, grad_w, grad_c, stream=None) -> None:
-    _check(_lib.edkm_backward_dense(plan.ref, _ptr(w_bits, 2, "w_bits"), _ptr(grad_w_tilde, 4),
-                                    _ptr(grad_w, 4), _ptr(grad_c, 4), _stream(stream)),
+    _check(_lib.edkm_backward_dense(plan.ref, _ptr(w_bits, 2, "w_bits", plan.n),
+                                    _ptr(grad_w_tilde, 4, "grad_w_tilde", plan.n),
+                                    _ptr(grad_w, 4, "grad_w", plan.n), _ptr(grad_c, 4, "grad_c", plan.k),
+                                    _stream(stream)),
            "backward_dense", (plan,))
 
 
-def _parr(items, esize=None):
-    arr = (ctypes.c_void_p * len(items))(*[_ptr(t, esize) for t in items])
+def _parr(items, esize=None, name="tensor", counts=None):
+    """Host array of device pointers; counts[i] = elements items[i] must hold."""
+    counts = counts or [None] * len(items)
+    arr = (ctypes.c_void_p * len(items))(*[_ptr(t, esize, "%s[%d]" % (name, i), c)
+                                             for i, (t, c) in enumerate(zip(items, counts))])
     return ctypes.cast(arr, _PP), arr
 
 
@@ -262,9 +280,10 @@ def init_unique_batch(plans, w_bits, counts_out=None, num_unique_out=None, check
     _same_len("init_unique_batch", plans, w_bits=w_bits, counts_out=counts_out, num_unique_out=num_unique_out)
     n = len(plans)
     pp, _a = _plans(plans)
-    kk, _b = _parr(w_bits, 2)
-    co, _c = _parr(counts_out, 4) if counts_out is not None else (None, None)
-    nu, _d = _parr(num_unique_out, 4) if num_unique_out is not None else (None, None)
+    ns, ks = [p.n for p in plans], [p.k for p in plans]
+    kk, _b = _parr(w_bits, 2, "w_bits", ns)
+    co, _c = _parr(counts_out, 4, "counts_out", [NKEYS] * n) if counts_out is not None else (None, None)
+    nu, _d = _parr(num_unique_out, 4, "num_unique_out", [1] * n) if num_unique_out is not None else (None, None)
     _check(_lib.edkm_init_unique_batch(n, pp, kk, co, nu, int(bool(check_finite)), _stream(stream)),
            "init_unique_batch", plans)
 
@@ -274,11 +293,12 @@ def forward_batch(plans, w_bits, tau, eps, c_in, c_out, w_tilde, out_half=False,
     _same_len("forward_batch", plans, w_bits=w_bits, c_in=c_in, c_out=c_out, w_tilde=w_tilde, iters_out=iters_out)
     n = len(plans)
     pp, _a = _plans(plans)
-    kk, _b = _parr(w_bits, 2)
-    ci, _c = _parr(c_in, 4)
-    co, _d = _parr(c_out, 4)
-    wt, _e = _parr(w_tilde, 2 if out_half else 4)
-    it, _f = _parr(iters_out, 4) if iters_out is not None else (None, None)
+    ns, ks = [p.n for p in plans], [p.k for p in plans]
+    kk, _b = _parr(w_bits, 2, "w_bits", ns)
+    ci, _c = _parr(c_in, 4, "c_in", ks)
+    co, _d = _parr(c_out, 4, "c_out", ks)
+    wt, _e = _parr(w_tilde, 2 if out_half else 4, "w_tilde", ns)
+    it, _f = _parr(iters_out, 4, "iters_out", [1] * n) if iters_out is not None else (None, None)
     _check(_lib.edkm_forward_batch(n, pp, kk, float(tau), float(eps), ci, co, wt,
                                    int(bool(out_half)), it, _stream(stream)),
            "forward_batch", plans)
@@ -288,10 +308,11 @@ def backward_batch(plans, w_bits, grad_w_tilde, grad_w, grad_c, stream=None) -> 
     _same_len("backward_batch", plans, w_bits=w_bits, grad_w_tilde=grad_w_tilde, grad_w=grad_w, grad_c=grad_c)
     n = len(plans)
     pp, _a = _plans(plans)
-    kk, _b = _parr(w_bits, 2)
-    g, _c = _parr(grad_w_tilde, 4)
-    gw, _d = _parr(grad_w, 4)
-    gc, _e = _parr(grad_c, 4)
+    ns, ks = [p.n for p in plans], [p.k for p in plans]
+    kk, _b = _parr(w_bits, 2, "w_bits", ns)
+    g, _c = _parr(grad_w_tilde, 4, "grad_w_tilde", ns)
+    gw, _d = _parr(grad_w, 4, "grad_w", ns)
+    gc, _e = _parr(grad_c, 4, "grad_c", ks)
     _check(_lib.edkm_backward_batch(n, pp, kk, g, gw, gc, _stream(stream)), "backward_batch", plans)
 
 
@@ -305,7 +326,7 @@ def palettize_batch(plans, w_bits, lut, indices_out, stream=None) -> None:
             raise EdkmError(ERR_ARG, "palettize_batch", "indices_out needs %d bytes" % need)
     n = len(plans)
     pp, _a = _plans(plans)
-    kk, _b = _parr(w_bits, 2)
-    lt, _c = _parr(lut, 4)
-    oo, _d = _parr(indices_out, 1)
+    kk, _b = _parr(w_bits, 2, "w_bits", [p.n for p in plans])
+    lt, _c = _parr(lut, 4, "lut", [p.k for p in plans])
+    oo, _d = _parr(indices_out, 1, "indices_out", [(p.n * p.bits + 7) // 8 for p in plans])
     _check(_lib.edkm_palettize_batch(n, pp, kk, lt, oo, _stream(stream)), "palettize_batch", plans)

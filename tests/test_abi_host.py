@@ -160,6 +160,60 @@ def test_launch_group_size_matches_header():
     assert int(re.search(r"#define EDKM_LAUNCH_GROUP (\d+)", text).group(1)) == edkm.LAUNCH_GROUP
 
 
+class _FakeDeviceTensor:
+    """Just enough of a tensor for the binding's checks (no GPU here).  Its
+    address is never dereferenced: an undersized one must be refused while the
+    arguments are marshalled, and should a check be missing, the stub plan (a
+    NULL record) makes the library reject the call on the host, which the
+    test's match on the argument name reports."""
+
+    def __init__(self, numel, esize):
+        self._n, self._e = numel, esize
+        self.is_cuda = True
+
+    def is_contiguous(self):
+        return True
+
+    def element_size(self):
+        return self._e
+
+    def numel(self):
+        return self._n
+
+    def data_ptr(self):
+        return 1 << 40
+
+
+def test_binding_refuses_undersized_tensors():
+    from types import SimpleNamespace
+    plan = SimpleNamespace(n=1000, bits=3, k=8, ref=None, plan=edkm.edkm_plan())   # a zeroed record: rejected on the host
+    f = _FakeDeviceTensor
+    keys, short_keys = f(1000, 2), f(999, 2)
+    c, short_c = f(8, 4), f(7, 4)
+    vec, short_vec = f(1000, 4), f(999, 4)
+    cases = [
+        (lambda: edkm.init_unique(plan, short_keys), "w_bits"),
+        (lambda: edkm.init_unique(plan, keys, counts_out=f(65535, 4)), "counts_out"),
+        (lambda: edkm.forward(plan, keys, 2e-3, 0.0, short_c, c, vec), "c_in"),
+        (lambda: edkm.forward(plan, keys, 2e-3, 0.0, c, short_c, vec), "c_out"),
+        (lambda: edkm.forward(plan, keys, 2e-3, 0.0, c, c, short_vec), "w_tilde"),
+        (lambda: edkm.forward(plan, keys, 2e-3, 0.0, c, c, f(999, 2), out_half=True), "w_tilde"),
+        (lambda: edkm.backward(plan, keys, short_vec, vec, c), "grad_w_tilde"),
+        (lambda: edkm.backward(plan, keys, vec, short_vec, c), "grad_w"),
+        (lambda: edkm.backward(plan, keys, vec, vec, short_c), "grad_c"),
+        (lambda: edkm.forward_dense(plan, keys, 2e-3, 0.0, c, c, vec, attn_out=f(7999, 4)), "attn_out"),
+        (lambda: edkm.backward_dense(plan, short_keys, vec, vec, c), "w_bits"),
+        (lambda: edkm.palettize(plan, keys, short_c, f(375, 1)), "lut"),
+        (lambda: edkm.forward_batch([plan, plan], [keys, keys], 2e-3, 0.0, [c, c], [c, c], [vec, short_vec]),
+         r"w_tilde\[1\]"),
+        (lambda: edkm.backward_batch([plan], [keys], [vec], [vec], [short_c]), r"grad_c\[0\]"),
+        (lambda: edkm.palettize_batch([plan], [keys], [c], [f(374, 1)]), "indices_out"),
+    ]
+    for call, what in cases:
+        with pytest.raises((ValueError, edkm.EdkmError), match=what):
+            call()
+
+
 def test_status_strings():
     for s in (0, -1, -2, -3, -4, -5):
         assert edkm.status_str(s) and edkm.status_str(s) != "unknown status"
