@@ -99,6 +99,44 @@ __device__ __forceinline__ void attn_row(float v, const float (&c)[K], float s2,
     attn_row_sel<K>(v, c, s2, a, c, unused);
 }
 
+// Attention row of the dense comparison path.  The exponent is formed from
+// plain fp32 distances, -(|v - c_j| - x) with x = min_i |v - c_i|, at about a
+// third of attn_row_sel's instructions.  Each distance carries a rounding
+// error of at most 2^-24 of itself, so for every a_j >= 2^-24 the exponent is
+// off by at most about (x s2 + 24) 2^-24 (in units of log2).  The row is used
+// while x s2 <= DENSE_FAST_X (error below 6e-6 relative); a weight farther
+// than that from every centroid (an outlier) takes attn_row_sel.  e and em as
+// in attn_row_sel (nearest centroid, first on ties).
+constexpr float DENSE_FAST_X = 64.f;
+
+template <int K>
+__device__ __forceinline__ void attn_row_dense(float v, const float (&c)[K], float s2, float (&a)[K],
+                                               const float (&e)[K], float& em) {
+    float d[K];
+    d[0] = fabsf(v - c[0]);
+    float xm = d[0];
+    em = e[0];
+#pragma unroll
+    for (int j = 1; j < K; ++j) {
+        d[j] = fabsf(v - c[j]);
+        if (d[j] < xm) { xm = d[j]; em = e[j]; }
+    }
+    const float off = xm * s2;
+    if (off <= DENSE_FAST_X) {
+        float sum = 0.f;
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            a[j] = __builtin_amdgcn_exp2f(fmaf(-d[j], s2, off));
+            sum += a[j];
+        }
+        const float r = 1.0f / sum;
+#pragma unroll
+        for (int j = 0; j < K; ++j) a[j] *= r;
+    } else {
+        attn_row_sel<K>(v, c, s2, a, e, em);
+    }
+}
+
 // Deviations d_j = C^(T)_j - W~ of one map row a, W~ = sum_j a_j C^(T)_j,
 // written around c1m = C^(T)_m of the nearest centroid m:
 //   d_j = (C_j - c1m) - sum_i a_i (C_i - c1m),   W~ = c1m + sum_i a_i (C_i - c1m).
@@ -1326,7 +1364,8 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_iter(BatchArgs b) {
         if (!key_finite(key, M.fmt)) continue;
         const float v = key_value(key, M.fmt);
         float a[K];
-        attn_row<K>(v, c, b.s2, a);
+        float unused;
+        attn_row_dense<K>(v, c, b.s2, a, c, unused);
 #pragma unroll
         for (int j = 0; j < K; ++j) {
             acc[j] += a[j];
@@ -1394,7 +1433,8 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_out(BatchArgs b) {
         float a[K];
         if (key_finite(key, M.fmt)) {
             const float v = key_value(key, M.fmt);
-            attn_row<K>(v, c0, b.s2, a);
+            float unused;
+            attn_row_dense<K>(v, c0, b.s2, a, c0, unused);
             wv = 0.f;
 #pragma unroll
             for (int j = 0; j < K; ++j) wv = fmaf(a[j], c1[j], wv);
@@ -1440,7 +1480,7 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_btop(BatchArgs b) {
         const float v = key_value(key, M.fmt);
         const float g = M.g[i];
         float a[K], d[K], c1m;
-        attn_row_sel<K>(v, c0, b.s2, a, c1, c1m);
+        attn_row_dense<K>(v, c0, b.s2, a, c1, c1m);
         centroid_dev<K>(a, c1, c1m, d);
         float h = 0.f;
 #pragma unroll
@@ -1488,7 +1528,7 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_biter(BatchArgs b) {
         if (!key_finite(key, M.fmt)) continue;
         const float v = key_value(key, M.fmt);
         float a[K], dev[K], cm;
-        attn_row_sel<K>(v, c0, b.s2, a, c1, cm);
+        attn_row_dense<K>(v, c0, b.s2, a, c1, cm);
         const float direct = softmax_dev<K>(v, a, gS, c1, cm, dev);
         float r = 0.f;
 #pragma unroll
