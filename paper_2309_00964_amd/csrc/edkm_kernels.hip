@@ -104,14 +104,16 @@ __device__ __forceinline__ void attn_row(float v, const float (&c)[K], float s2,
 // third of attn_row_sel's instructions.  Each distance carries a rounding
 // error of at most 2^-24 of itself, so for every a_j >= 2^-24 the exponent is
 // off by at most about (x s2 + 24) 2^-24 (in units of log2).  The row is used
-// while x s2 <= DENSE_FAST_X (error below 6e-6 relative); a weight farther
-// than that from every centroid (an outlier) takes attn_row_sel.  e and em as
-// in attn_row_sel (nearest centroid, first on ties).
-constexpr float DENSE_FAST_X = 64.f;
+// while x s2 <= DENSE_FAST_X (a_j within 1.2e-5 relative); a weight farther
+// than that from every centroid (a far outlier) takes attn_row_sel.  e and em
+// as in attn_row_sel (nearest centroid, first on ties).
+constexpr float DENSE_FAST_X = 256.f;
 
+// Unnormalised form: a_j up to the factor r it returns (r = 1 after the
+// careful row, which normalises itself).
 template <int K>
-__device__ __forceinline__ void attn_row_dense(float v, const float (&c)[K], float s2, float (&a)[K],
-                                               const float (&e)[K], float& em) {
+__device__ __forceinline__ float attn_row_dense_un(float v, const float (&c)[K], float s2, float (&a)[K],
+                                                   const float (&e)[K], float& em) {
     float d[K];
     d[0] = fabsf(v - c[0]);
     float xm = d[0];
@@ -129,12 +131,18 @@ __device__ __forceinline__ void attn_row_dense(float v, const float (&c)[K], flo
             a[j] = __builtin_amdgcn_exp2f(fmaf(-d[j], s2, off));
             sum += a[j];
         }
-        const float r = 1.0f / sum;
-#pragma unroll
-        for (int j = 0; j < K; ++j) a[j] *= r;
-    } else {
-        attn_row_sel<K>(v, c, s2, a, e, em);
+        return 1.0f / sum;
     }
+    attn_row_sel<K>(v, c, s2, a, e, em);
+    return 1.0f;
+}
+
+template <int K>
+__device__ __forceinline__ void attn_row_dense(float v, const float (&c)[K], float s2, float (&a)[K],
+                                               const float (&e)[K], float& em) {
+    const float r = attn_row_dense_un<K>(v, c, s2, a, e, em);
+#pragma unroll
+    for (int j = 0; j < K; ++j) a[j] *= r;
 }
 
 // Deviations d_j = C^(T)_j - W~ of one map row a, W~ = sum_j a_j C^(T)_j,
@@ -1365,11 +1373,12 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_iter(BatchArgs b) {
         const float v = key_value(key, M.fmt);
         float a[K];
         float unused;
-        attn_row_dense<K>(v, c, b.s2, a, c, unused);
+        const float r = attn_row_dense_un<K>(v, c, b.s2, a, c, unused);   // normalised below
+        const float rv = r * v;
 #pragma unroll
         for (int j = 0; j < K; ++j) {
-            acc[j] += a[j];
-            acc[K + j] = fmaf(a[j], v, acc[K + j]);
+            acc[j] = fmaf(a[j], r, acc[j]);
+            acc[K + j] = fmaf(a[j], rv, acc[K + j]);
         }
     }
     block_sum<2 * K, D_THREADS>(acc, scratch, tot);
