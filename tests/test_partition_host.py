@@ -58,12 +58,14 @@ def split(tmp_path_factory):
 
 LAYER = [r * c for _, r, c in inputs.LLAMA7B_LAYER]
 STACK = [r * c for _, r, c in inputs.WORKLOADS[5]["mats"]]
+GROUP = 28   # EDKM_LAUNCH_GROUP: the stack runs as 8 launch groups of 28 matrices
 MIXES = [LAYER, STACK[:8], STACK[8:16], STACK[16:24], [65536], [4096 * 4096], [11008 * 4096],
          [1], [7, 9, 1], [65536 + 37, 300007, 8], [16384 * 3 + 1, 10 ** 9], [2 ** 32 - 1] * 8,
-         [1] * 8, [16384] * 8]
+         [1] * 8, [16384] * 8, STACK[:GROUP], STACK[GROUP * 7:], [1] * GROUP,
+         [4096 * 4096] * (GROUP - 1) + [7]]
 
 
-@pytest.mark.parametrize("budget", [256, 255, 80, 32, 8, 1])
+@pytest.mark.parametrize("budget", [512, 256, 255, 80, 32, 8, 1])
 @pytest.mark.parametrize("mix", range(len(MIXES)))
 def test_split_covers_every_weight_within_budget(split, mix, budget):
     sizes = MIXES[mix]
@@ -90,6 +92,21 @@ def test_split_is_proportional(split, mix):
     total = sum(sizes)
     for n, (_, cnt, _) in zip(sizes, parts):
         assert abs(cnt - 256 * n / total) <= 1.0
+
+
+@pytest.mark.parametrize("mix", [14, 15])
+@pytest.mark.parametrize("budget", [256, 512])
+def test_full_launch_group_is_proportional(split, mix, budget):
+    """A launch group of 28 matrices (four layers of the stack) under the
+    one-per-CU budget of the training passes and the two-per-CU budget of the
+    palettization export."""
+    sizes = MIXES[mix]
+    assert len(sizes) == GROUP
+    grid, parts = split(sizes, budget)
+    assert budget - GROUP <= grid <= budget
+    total = sum(sizes)
+    for n, (_, cnt, _) in zip(sizes, parts):
+        assert abs(cnt - budget * n / total) <= 1.0
 
 
 def test_first_stack_group_fits_one_wave(split):
