@@ -112,6 +112,38 @@ def test_counts_single_pattern_overflow_path():
     assert np.allclose(res["w_tilde"], v, rtol=1e-6)
 
 
+@pytest.mark.parametrize("case", ["constant", "signed_zeros", "on_centroids"])
+def test_degenerate_inputs_match_oracle(case):
+    """Inputs where the method degenerates: one repeated value (every quantile
+    centroid equals it, so rows are uniform and C never moves), a random mix of
+    +0 and -0 (two keys, one value, every distance 0), and two values sitting
+    exactly on their starting centroids (d|x|/dx at 0 taken as 0).  Counts are
+    bit-exact and C, W~ and dL/dw are held to the usual tolerances.  dL/dC^(0)
+    is zero or underflow-sized in fp64 here (the centroids settle onto isolated
+    values, so C^(T) hardly depends on C^(0)); it is held to an absolute bound,
+    1e-6 of sum |g|, the scale a centroid gradient could take."""
+    n = 50_003
+    rng = np.random.default_rng(490)
+    if case == "constant":
+        keys = np.full(n, np.float16(0.01).view(np.uint16), dtype=np.uint16)
+        c0 = inputs.quantile_init(keys, 4)
+    elif case == "signed_zeros":
+        keys = np.where(rng.random(n) < 0.5, 0x0000, 0x8000).astype(np.uint16)
+        c0 = inputs.quantile_init(keys, 4)
+    else:
+        a, b = np.float16(-0.02), np.float16(0.03)
+        keys = np.where(rng.random(n) < 0.3, a.view(np.uint16), b.view(np.uint16)).astype(np.uint16)
+        c0 = np.array([float(a), float(b), 0.0, 0.05], np.float32)
+    g = inputs.upstream_grad(n, 491)
+    say("degenerate", case)
+    res = gpu(keys, c0, 2, g=g, want_counts=True)
+    assert np.array_equal(res["counts"].view(np.uint32), table.histogram(keys))
+    ref = oracle(keys, c0, g)
+    check(res, ref, g=False, what=case)
+    assert_close(res["grad_w"], ref["gw"], TOL_BWD, case + " grad_w")
+    assert np.all(np.abs(res["grad_c"] - ref["gc"]) <= 1e-6 * float(np.abs(g).sum())), case
+
+
 # ------------------------------------------------------------------ forward / backward
 
 CASES = [
