@@ -344,6 +344,52 @@ def test_early_stop_matches_oracle():
         check(res, oracle(keys, c0, g, iters=12, eps=eps), what="eps dense=%s" % dense_path)
 
 
+def test_batch_early_stop_at_different_iterations():
+    """One eps for a batch whose matrices converge at different speeds: each
+    stops at its own iteration, the backward unrolls its own T, and every matrix
+    equals its single call and the oracle.  eps is chosen so that no matrix has
+    a step size within 5% of it (no fp32-versus-fp64 ambiguity)."""
+    spec = [(65536, 90, False), (100_003, 91, True), (70_001, 92, False)]
+    ks = [inputs.fp16_weights(n, seed, outliers=o) for n, seed, o in spec]
+    c0s = [inputs.quantile_init(k, 8) for k in ks]
+    gs = [inputs.upstream_grad(n, seed + 10) for n, seed, _ in spec]
+    steps = []
+    for k, c0 in zip(ks, c0s):
+        h = dense.forward(k, c0.astype(np.float64), TAU, 12)["c_hist"]
+        steps.append(np.max(np.abs(np.diff(h, axis=0)), axis=1))
+    eps, ts = None, None
+    for cand in np.geomspace(1e-4, 1e-2, 400):
+        if any(np.any(np.abs(np.log(st / cand)) < np.log(1.05)) for st in steps):
+            continue
+        t = [int(np.argmax(st <= cand)) + 1 if np.any(st <= cand) else 12 for st in steps]
+        if len(set(t)) > 1:
+            eps, ts = float(cand), t
+            break
+    assert eps is not None, "no eps separates the matrices' stopping points"
+    say("batch early stop", eps, ts)
+    plans = [edkm.Plan(n, 3, 12) for n, _, _ in spec]
+    kd = [dkeys(k) for k in ks]
+    ci = [torch.from_numpy(c).to(DEV) for c in c0s]
+    co = [torch.empty(8, device=DEV) for _ in spec]
+    wt = [torch.empty(n, device=DEV) for n, _, _ in spec]
+    it = [torch.zeros(1, dtype=torch.int32, device=DEV) for _ in spec]
+    gd = [torch.from_numpy(g).to(DEV) for g in gs]
+    gw = [torch.empty(n, device=DEV) for n, _, _ in spec]
+    gc = [torch.empty(8, device=DEV) for _ in spec]
+    edkm.init_unique_batch(plans, kd)
+    edkm.forward_batch(plans, kd, TAU, eps, ci, co, wt, False, it)
+    edkm.backward_batch(plans, kd, gd, gw, gc)
+    torch.cuda.synchronize()
+    for i in range(len(spec)):
+        single = gpu(ks[i], c0s[i], 3, g=gs[i], iters=12, eps=eps)
+        assert int(it[i].item()) == int(single["iters"][0]), i
+        assert np.array_equal(co[i].cpu().numpy(), single["c_out"]), i
+        res = dict(iters=it[i].cpu().numpy(), c_out=co[i].cpu().numpy(), w_tilde=wt[i].cpu().numpy(),
+                   grad_w=gw[i].cpu().numpy(), grad_c=gc[i].cpu().numpy())
+        check(res, oracle(ks[i], c0s[i], gs[i], iters=12, eps=eps), what="batch eps %d" % i)
+    assert len({int(t.item()) for t in it}) > 1
+
+
 def test_empty_cluster_keeps_centroid():
     keys = inputs.fp16_weights(30_000, 91)
     c0 = np.append(inputs.quantile_init(keys, 7), np.float32(2.0))   # fp64 underflows too
