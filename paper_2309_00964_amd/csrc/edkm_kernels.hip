@@ -185,13 +185,92 @@ __device__ __forceinline__ float softmax_dev(float v, const float (&a)[K], const
     return gbar;
 }
 
-// Butterfly sum over the 64 lanes; lane 0's value is the one used, so the
-// association order is fixed.
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
-    return x;
+// DPP lane moves: a VALU operand read from another lane of the same row of 16
+// lanes or, for the two broadcasts, from lane 15 of the row below / lane 31.
+// Lanes outside row_mask keep `old`.  (__shfl_xor compiles to LDS-crossbar
+// reads, one round trip per butterfly level: about 40% of a table kernel's
+// time went there.)
+constexpr int DPP_XOR1 = 0xB1;          // quad_perm [1,0,3,2]
+constexpr int DPP_XOR2 = 0x4E;          // quad_perm [2,3,0,1]
+constexpr int DPP_HALF_MIRROR = 0x141;  // lane i <- lane 7 - i within each 8
+constexpr int DPP_MIRROR = 0x140;       // lane i <- lane 15 - i within each row
+constexpr int DPP_BCAST15 = 0x142;      // row r <- lane 15 of row r - 1
+constexpr int DPP_BCAST31 = 0x143;      // rows 2, 3 <- lane 31
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ float dpp_f(float old, float x) {
+    return __int_as_float(
+        __builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(x), CTRL, ROW_MASK, 0xF, false));
 }
+
+// Sum over the 64 lanes of a wave (all active), in a fixed association
+// order: pairs, quads, eights and rows of 16 by DPP, then row 1 += row 0,
+// row 3 += row 2, row 3 += rows 0-1; the total is lane 63's, returned to
+// every lane.
+__device__ __forceinline__ float wave_sum(float x) {
+    x += dpp_f<DPP_XOR1>(x, x);
+    x += dpp_f<DPP_XOR2>(x, x);
+    x += dpp_f<DPP_HALF_MIRROR>(x, x);
+    x += dpp_f<DPP_MIRROR>(x, x);
+    x += dpp_f<DPP_BCAST15, 0xA>(0.f, x);
+    x += dpp_f<DPP_BCAST31, 0xC>(0.f, x);
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
+}
+
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ int dpp_i(int old, int x) {
+    return __builtin_amdgcn_update_dpp(old, x, CTRL, ROW_MASK, 0xF, false);
+}
+constexpr int DPP_SHR1 = 0x111, DPP_SHR2 = 0x112, DPP_SHR4 = 0x114, DPP_SHR8 = 0x118;   // lane i <- i - n in its row
+
+// Inclusive prefix sum over the 64 lanes (all active): within rows of 16 by
+// shifts of 1, 2, 4, 8 (lanes without a source add 0), then the row totals.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+    int v = (int)x;
+    v += dpp_i<DPP_SHR1>(0, v);
+    v += dpp_i<DPP_SHR2>(0, v);
+    v += dpp_i<DPP_SHR4>(0, v);
+    v += dpp_i<DPP_SHR8>(0, v);
+    v += dpp_i<DPP_BCAST15, 0xA>(0, v);
+    v += dpp_i<DPP_BCAST31, 0xC>(0, v);
+    return (uint32_t)v;
+}
+
+// Reduction of a 32-bit integer over the 64 lanes (all active) by an
+// associative, commutative op with identity id; every lane gets the result.
+template <class Op>
+__device__ __forceinline__ int wave_reduce(int x, int id, Op op) {
+    x = op(x, dpp_i<DPP_XOR1>(x, x));
+    x = op(x, dpp_i<DPP_XOR2>(x, x));
+    x = op(x, dpp_i<DPP_HALF_MIRROR>(x, x));
+    x = op(x, dpp_i<DPP_MIRROR>(x, x));
+    x = op(x, dpp_i<DPP_BCAST15, 0xA>(id, x));
+    x = op(x, dpp_i<DPP_BCAST31, 0xC>(id, x));
+    return __builtin_amdgcn_readlane(x, 63);
+}
+
+// Sum of a 64-bit integer over the 64 lanes (all active); both halves move
+// with the same lane pattern.
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ unsigned long long dpp_u64(unsigned long long old, unsigned long long x) {
+    const uint32_t lo = (uint32_t)dpp_i<CTRL, ROW_MASK>((int)(uint32_t)old, (int)(uint32_t)x);
+    const uint32_t hi = (uint32_t)dpp_i<CTRL, ROW_MASK>((int)(uint32_t)(old >> 32), (int)(uint32_t)(x >> 32));
+    return ((unsigned long long)hi << 32) | lo;
+}
+__device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long x) {
+    x += dpp_u64<DPP_XOR1>(x, x);
+    x += dpp_u64<DPP_XOR2>(x, x);
+    x += dpp_u64<DPP_HALF_MIRROR>(x, x);
+    x += dpp_u64<DPP_MIRROR>(x, x);
+    x += dpp_u64<DPP_BCAST15, 0xA>(0ull, x);
+    x += dpp_u64<DPP_BCAST31, 0xC>(0ull, x);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), 63);
+    return ((unsigned long long)hi << 32) | lo;
+}
+__device__ __forceinline__ int op_min(int a, int b) { return min(a, b); }
+__device__ __forceinline__ int op_max(int a, int b) { return max(a, b); }
+__device__ __forceinline__ int op_add(int a, int b) { return a + b; }
+__device__ __forceinline__ int op_or(int a, int b) { return a | b; }
 
 // Sum NV per-thread values over a block of NT threads into out[0..NV) (LDS),
 // in a fixed order.  `scratch` holds NT/64 * NV floats.
@@ -515,23 +594,6 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_grad_merge(BatchArgs b) {
     if (sum != 0.f) atomicAdd(&ws.G[(sg << 15) | (lo + i - sg * w)], sum);
 }
 
-// Block-wide exclusive scan of one uint32 per thread (1024 threads).
-__device__ __forceinline__ uint32_t block_excl_scan(uint32_t x, uint32_t* tmp /*16*/) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    uint32_t inc = x;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        uint32_t y = __shfl_up(inc, o, 64);
-        if (lane >= o) inc += y;
-    }
-    if (lane == 63) tmp[wave] = inc;
-    __syncthreads();
-    uint32_t base = 0;
-    for (int w = 0; w < wave; ++w) base += tmp[w];
-    __syncthreads();
-    return base + inc - x;
-}
-
 // Window selection: one block per matrix, grid (1, count).  Wave w owns the
 // SPAN = 2048 magnitudes [2048 w, 2048 w + 2048) of both signs, in NCH = 8
 // chunks of 256; lane l holds the 4 consecutive magnitudes 4 l .. 4 l + 3 of
@@ -586,12 +648,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
             s4[e] = run;
         }
         finm |= (f ? 0xFu : 0u) << (4 * j);
-        uint32_t x = run;                      // inclusive scan over the wave's lanes
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const uint32_t y = __shfl_up(x, o, 64);
-            if (lane >= o) x += y;
-        }
+        const uint32_t x = wave_incl_scan(run);   // over the wave's lanes
         const uint32_t base = carry + x - run;
         *reinterpret_cast<uint4*>(pre + mw + 256 * j) =
             make_uint4(base + s4[0], base + s4[1], base + s4[2], base + s4[3]);
@@ -603,14 +660,11 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
     int hi = occ ? bit_mag(31 - __builtin_clz(occ)) : -1;
     int nu = __builtin_popcount(occp) + __builtin_popcount(occn);
     int nf = ((occp | occn) & ~finm) != 0u;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        lo = min(lo, __shfl_xor(lo, o, 64));
-        hi = max(hi, __shfl_xor(hi, o, 64));
-        nu += __shfl_xor(nu, o, 64);
-        nf |= __shfl_xor(nf, o, 64);
-        sq += __shfl_xor(sq, o, 64);
-    }
+    lo = wave_reduce(lo, 0x7FFFFFFF, op_min);
+    hi = wave_reduce(hi, -0x7FFFFFFF - 1, op_max);
+    nu = wave_reduce(nu, 0, op_add);
+    nf = wave_reduce(nf, 0, op_or);
+    sq = wave_sum_u64(sq);
     if (lane == 0) {
         woff[wave + 1] = carry;
         atomicMin(&red[0], lo);
@@ -927,12 +981,9 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
         const int e = (int)((__float_as_uint(g[i]) >> 23) & 0xFFu);
         const bool use = e != 0 && e != 0xFF;
         int smax = use ? e : 0, ssum = smax, scnt = use ? 1 : 0;
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-            smax = max(smax, __shfl_xor(smax, o, 64));
-            ssum += __shfl_xor(ssum, o, 64);
-            scnt += __shfl_xor(scnt, o, 64);
-        }
+        smax = wave_reduce(smax, 0, op_max);
+        ssum = wave_reduce(ssum, 0, op_add);
+        scnt = wave_reduce(scnt, 0, op_add);
         if ((threadIdx.x & 63) == 0) {
             atomicMax(&emax_sh, smax);
             atomicAdd(&esum_sh, ssum);
