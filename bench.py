@@ -403,6 +403,11 @@ def copy_calibration():
     print(json.dumps({"copy_bytes": COPY_BYTES}), flush=True)
 
 
+def kernel_base_name(name):
+    """'edkm::k_hist(edkm::BatchArgs)' -> 'k_hist'; 'void edkm::k_fwd_iter<8>(...)' -> 'k_fwd_iter'."""
+    return name.split("(")[0].split("<")[0].split("::")[-1].split(" ")[-1]
+
+
 def _pmc_rows(d, prefix):
     import csv
     files = glob.glob(os.path.join(d, "**", prefix + "*counter_collection.csv"), recursive=True)
@@ -430,8 +435,8 @@ def pmc_summary(fetch_dir, write_dir):
     def passes(d, counter):
         out = {}
         for (_, _, name), v in per_dispatch(d, "bench", counter).items():
-            p = next((p for p in PASS_IDS if p in name), None)
-            if p:
+            p = kernel_base_name(name)   # exact: k_hist is not k_hist_merge
+            if p in PASS_IDS:
                 out.setdefault(p, []).append(v)
         return {p: sum(v) / len(v) for p, v in out.items()}
 

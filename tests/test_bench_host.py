@@ -61,9 +61,14 @@ def test_pmc_summary_scales_by_the_copy_calibration(tmp_path, monkeypatch):
         dict(Dispatch_Id=1, Kernel_Name="__amd_rocclr_copyBuffer", Counter_Name="WRITE_SIZE", Counter_Value=gib)])
     _write_counters(fetch / "bench_counter_collection.csv", [
         dict(Dispatch_Id=5, Kernel_Name="edkm::k_gather_grad(edkm::BatchArgs)", Counter_Name="FETCH_SIZE", Counter_Value=100.0),
-        dict(Dispatch_Id=9, Kernel_Name="edkm::k_gather_grad(edkm::BatchArgs)", Counter_Name="FETCH_SIZE", Counter_Value=300.0)])
+        dict(Dispatch_Id=9, Kernel_Name="edkm::k_gather_grad(edkm::BatchArgs)", Counter_Name="FETCH_SIZE", Counter_Value=300.0),
+        # the merge kernel's name starts with the histogram's: it must not count as k_hist
+        dict(Dispatch_Id=3, Kernel_Name="edkm::k_hist(edkm::BatchArgs)", Counter_Name="FETCH_SIZE", Counter_Value=1000.0),
+        dict(Dispatch_Id=4, Kernel_Name="edkm::k_hist_merge(edkm::BatchArgs)", Counter_Name="FETCH_SIZE", Counter_Value=10.0)])
     _write_counters(write / "bench_counter_collection.csv", [
-        dict(Dispatch_Id=5, Kernel_Name="edkm::k_gather_grad(edkm::BatchArgs)", Counter_Name="WRITE_SIZE", Counter_Value=50.0)])
+        dict(Dispatch_Id=5, Kernel_Name="edkm::k_gather_grad(edkm::BatchArgs)", Counter_Name="WRITE_SIZE", Counter_Value=50.0),
+        dict(Dispatch_Id=3, Kernel_Name="edkm::k_hist(edkm::BatchArgs)", Counter_Name="WRITE_SIZE", Counter_Value=4.0),
+        dict(Dispatch_Id=4, Kernel_Name="edkm::k_hist_merge(edkm::BatchArgs)", Counter_Name="WRITE_SIZE", Counter_Value=8.0)])
     out = tmp_path / "traffic.json"
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(out))
     bench.pmc_summary(str(fetch), str(write))
@@ -72,7 +77,16 @@ def test_pmc_summary_scales_by_the_copy_calibration(tmp_path, monkeypatch):
     kg = res["kernels"]["k_gather_grad"]
     assert kg["fetch_bytes"] == pytest.approx(200.0 * 1024 * 2)
     assert kg["write_bytes"] == pytest.approx(50.0 * 1024)
+    kh = res["kernels"]["k_hist"]
+    assert kh["fetch_bytes"] == pytest.approx(1000.0 * 1024 * 2) and kh["write_bytes"] == pytest.approx(4.0 * 1024)
     assert res["source_hash"] == bench.source_hash()
+
+
+def test_kernel_base_name():
+    assert bench.kernel_base_name("edkm::k_hist(edkm::BatchArgs)") == "k_hist"
+    assert bench.kernel_base_name("edkm::k_hist_merge(edkm::BatchArgs)") == "k_hist_merge"
+    assert bench.kernel_base_name("void edkm::k_fwd_iter<8>(edkm::BatchArgs)") == "k_fwd_iter"
+    assert bench.kernel_base_name("__amd_rocclr_copyBuffer") == "__amd_rocclr_copyBuffer"
 
 
 def test_cpu_baseline_record():
