@@ -21,6 +21,8 @@ Other workloads (--workload; one JSON line each, same fields):
                               drawn on the GPU), one step over every matrix
   palettize [--bits 1..4]     export of the decoder layer after a clustering step:
                               packed b-bit nearest-centroid indices per weight
+  unique_inverse              the decoder layer's distinct patterns and 16-bit inverse
+                              index per weight (the uniquification's lists)
 
 Other modes (measurement helpers):
   --copy-calibration          run a plain 1 GiB device copy (HBM counter calibration)
@@ -372,6 +374,33 @@ def bench_palettize(args):
                        bits, elapsed, roof, {"w_tilde": None, "output": "packed %d-bit indices" % bits})
 
 
+def bench_unique_inverse(args):
+    """The uniquification's lists for the decoder layer (edkm_unique_inverse_batch
+    after one init_unique): the sorted distinct patterns and the 16-bit inverse
+    index of every weight, one ranking launch and one N-sized launch for the
+    seven matrices.  Pass events time the inverse-index kernel; the roofline is
+    its 2 + 2 bytes per weight."""
+    import torch
+    from paper_2309_00964_amd import edkm, inputs
+    bits = args.bits or 3
+    m = Matrices(4, inputs.WORKLOADS[4]["mats"], bits, fmt=args.key_format)
+    m.step()
+    uniq = [torch.empty(edkm.NKEYS, dtype=torch.int16, device="cuda") for _ in m.plans]
+    inv = [torch.empty(p.n, dtype=torch.int16, device="cuda") for p in m.plans]
+
+    def step():
+        edkm.unique_inverse_batch(m.plans, m.keys, uniq, inv)
+    elapsed, avg = timed(step, m.plans[0], {"k_inverse": edkm.PASS_INVERSE}, args.steps, args.warmup)
+    per_w = 4.0
+    kern_s = avg["k_inverse"] / 1000.0
+    achieved = per_w * m.total / kern_s / 1e9
+    roof = {"bound": "hbm", "kernel": "k_inverse", "achieved": achieved, "peak": PEAK_HBM_GBS,
+            "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS, "traffic": None,
+            "bytes_per_weight": per_w, "kernel_us_per_step": kern_s * 1e6}
+    return result_line(args, "llama7b_decoder_layer_unique_inverse%s" % _fmt_tag(args), m,
+                       bits, elapsed, roof, {"w_tilde": None, "output": "distinct patterns + 16-bit inverse index"})
+
+
 def bench_stack(args):
     """A 32-layer stack of decoder-layer shapes (224 matrices, 6.48e9 weights),
     drawn on the device; one step clusters every matrix forward and backward."""
@@ -470,7 +499,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", choices=("decoder_layer", "mlp_outliers", "stack", "palettize"),
+    ap.add_argument("--workload", choices=("decoder_layer", "mlp_outliers", "stack", "palettize",
+                                           "unique_inverse"),
                     default="decoder_layer")
     ap.add_argument("--bits", type=int, choices=(1, 2, 3, 4), default=None,
                     help="mlp_outliers: 3 or 4 (default 4); stack: 2, 3 or 4 (default 3); "
@@ -497,7 +527,8 @@ def main():
     if not torch.cuda.is_available():
         sys.exit("bench.py needs a GPU")
     fn = {"decoder_layer": bench_decoder_layer, "mlp_outliers": bench_mlp_outliers,
-          "stack": bench_stack, "palettize": bench_palettize}[args.workload]
+          "stack": bench_stack, "palettize": bench_palettize,
+          "unique_inverse": bench_unique_inverse}[args.workload]
     if args.workload == "decoder_layer" and args.bits not in (None, 3):
         sys.exit("the decoder-layer workload is 3-bit")
     print(json.dumps(fn(args)), flush=True)

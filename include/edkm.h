@@ -198,7 +198,8 @@ enum {
      * the last one of the call. */
     EDKM_PASS_DENSE_ITER = 4,   /* forward_dense: one centroid iteration, reads 2 B */
     EDKM_PASS_DENSE_BITER = 5,  /* backward_dense: one unrolled iteration, 2 B + 4 B + 4 B */
-    EDKM_PASS_PALETTIZE = 6     /* palettize: packed indices, 2 B + b/8 B */
+    EDKM_PASS_PALETTIZE = 6,    /* palettize: packed indices, 2 B + b/8 B */
+    EDKM_PASS_INVERSE = 7       /* unique_inverse: inverse index, 2 B + 2 B */
 };
 /* When set (non-NULL), later calls on this plan record `start` on the stream
  * right before that pass's launch and `stop` right after it; in a batched call
@@ -232,6 +233,38 @@ edkm_status edkm_palettize(edkm_plan* plan, const uint16_t* w_bits, const float*
 edkm_status edkm_palettize_batch(int count, edkm_plan* const* plans, const uint16_t* const* w_bits,
                                  const float* const* lut, uint8_t* const* indices_out,
                                  hipStream_t stream);
+
+/* The uniquification's two lists (Sec. 2.2): the distinct weight patterns
+ * and, per weight, the index of its pattern among them, in ascending order of
+ * the 16-bit key (the order of numpy.unique on the uint16 view, with
+ * return_inverse).  Every pattern counts, Inf/NaN ones included, and +0 / -0
+ * are distinct.  The forward and backward never need these lists (the key is
+ * the table offset); this is for callers that store or ship the index list.
+ *   w_bits       device, n patterns; must be the buffer given to init_unique
+ *                (the distinct patterns come from its counts)
+ *   unique_out   nullable, device uint16[65536]: entries 0 .. U-1 receive the
+ *                U distinct patterns, ascending (U = num_unique of
+ *                init_unique); later entries are left alone
+ *   inverse_out  nullable, device uint16[n]: inverse_out[i] = the index of
+ *                w_bits[i] in unique_out, so unique_out[inverse_out[i]] =
+ *                w_bits[i]
+ * At least one output must be given (EDKM_ERR_ARG otherwise).  Needs
+ * init_unique on this plan and key buffer (EDKM_ERR_STATE otherwise); may be
+ * called after forward or backward and leaves their state alone (it uses its
+ * own part of the workspace).  Exact (integer).  Cost: one pass over the
+ * 65,536 counts, and with inverse_out one read of the keys and one write of
+ * 2 bytes per weight. */
+edkm_status edkm_unique_inverse(edkm_plan* plan, const uint16_t* w_bits, uint16_t* unique_out,
+                                uint16_t* inverse_out, hipStream_t stream);
+/* Batched form: host arrays of `count` entries (the arrays and their entries
+ * may be NULL where an output is not wanted, but each matrix needs one
+ * output), cut into launch groups of up to EDKM_LAUNCH_GROUP consecutive
+ * matrices; each group is one ranking launch and, if any matrix of the group
+ * wants the inverse index, one N-sized launch.  Equivalent to calling
+ * edkm_unique_inverse on each. */
+edkm_status edkm_unique_inverse_batch(int count, edkm_plan* const* plans,
+                                      const uint16_t* const* w_bits, uint16_t* const* unique_out,
+                                      uint16_t* const* inverse_out, hipStream_t stream);
 
 /* Keyed-gradient accumulators (the backward's keyed reduction).  AUTO, the
  * default, chooses per matrix at init_unique from how concentrated the

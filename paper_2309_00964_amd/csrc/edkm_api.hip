@@ -37,7 +37,9 @@ static_assert(sizeof(PlanImpl) <= sizeof(edkm_plan), "edkm_plan too small");
 static_assert(EDKM_KEYS_FP16 != EDKM_KEYS_BF16, "key formats");
 static_assert(EDKM_KEYED_I32 == KEYED_I32 && EDKM_KEYED_U64 == KEYED_U64, "keyed-sum modes");
 static_assert(EDKM_PASS_HIST == PASS_HIST && EDKM_PASS_GATHER_WT == PASS_GATHER_WT &&
-                  EDKM_PASS_KEYED_GRAD == PASS_KEYED_GRAD && EDKM_PASS_GATHER_GRAD == PASS_GATHER_GRAD,
+                  EDKM_PASS_KEYED_GRAD == PASS_KEYED_GRAD && EDKM_PASS_GATHER_GRAD == PASS_GATHER_GRAD &&
+                  EDKM_PASS_DENSE_ITER == PASS_DENSE_ITER && EDKM_PASS_DENSE_BITER == PASS_DENSE_BITER &&
+                  EDKM_PASS_PALETTIZE == PASS_PALETTIZE && EDKM_PASS_INVERSE == PASS_INVERSE,
               "pass ids");
 
 inline PlanImpl* impl(edkm_plan* p) { return reinterpret_cast<PlanImpl*>(p); }
@@ -452,6 +454,48 @@ edkm_status edkm_palettize_batch(int count, edkm_plan* const* plans, const uint1
         const uint32_t grid = partition(b, 2 * np_budget());
         const char* where = "";
         const hipError_t e = launch_palettize(b, grid, stream, &where, &impl(plans[first])->ev);
+        if (e != hipSuccess) return hip_fail(plans, first, cnt, e, where);
+        return EDKM_OK;
+    });
+}
+
+edkm_status edkm_unique_inverse(edkm_plan* plan, const uint16_t* w_bits, uint16_t* unique_out,
+                                uint16_t* inverse_out, hipStream_t stream) {
+    return edkm_unique_inverse_batch(1, &plan, &w_bits, &unique_out, &inverse_out, stream);
+}
+
+edkm_status edkm_unique_inverse_batch(int count, edkm_plan* const* plans,
+                                      const uint16_t* const* w_bits, uint16_t* const* unique_out,
+                                      uint16_t* const* inverse_out, hipStream_t stream) {
+    edkm_status st = check_batch(count, plans, w_bits);
+    if (st != EDKM_OK) return st;
+    auto uniq = [&](int i) { return unique_out ? unique_out[i] : nullptr; };
+    auto inv = [&](int i) { return inverse_out ? inverse_out[i] : nullptr; };
+    for (int i = 0; i < count; ++i)
+        if (!uniq(i) && !inv(i)) return EDKM_ERR_ARG;
+    for (int i = 0; i < count; ++i) {
+        const PlanImpl* P = impl(plans[i]);
+        if ((P->stage != COUNTED && P->stage != FORWARD) || P->keys != w_bits[i]) return EDKM_ERR_STATE;
+    }
+    return for_groups(count, plans, [&](int first, int cnt) -> edkm_status {
+        BatchArgs b;
+        std::memset(&b, 0, sizeof(b));
+        b.count = cnt;
+        bool vec = true, any_inv = false;
+        for (int i = 0; i < cnt; ++i) {
+            const int q = first + i;
+            MatArgs& M = b.m[i];
+            fill_mat(M, impl(plans[q]), w_bits[q]);
+            M.uniq = uniq(q);
+            M.wt = inv(q);
+            any_inv = any_inv || M.wt;
+            vec = vec && aligned16(w_bits[q]) && (!M.wt || aligned16(M.wt));
+        }
+        for (int i = 0; i < cnt; ++i) b.m[i].vec = vec;
+        const uint32_t grid = partition(b, np_budget());
+        const char* where = "";
+        const hipError_t e =
+            launch_unique_inverse(b, grid, any_inv, stream, &where, &impl(plans[first])->ev);
         if (e != hipSuccess) return hip_fail(plans, first, cnt, e, where);
         return EDKM_OK;
     });

@@ -59,6 +59,7 @@ struct Ws {
     int2* span;         // [NP_MAX_WG]  histogram partial spans
     uint32_t* part;     // [NP_MAX_WG * ROW4]  N-pass partial rows
     uint8_t* pidx;      // [NKEYS]  palettization: nearest lookup-table entry per pattern
+    uint16_t* rank;     // [NKEYS]  occupied patterns below each pattern (unique_inverse)
     DevState* st;
 };
 
@@ -75,13 +76,15 @@ struct MatArgs {
     uint64_t n;
     const float* c_in;
     float* c_out;
-    void* wt;                 // W~ output (float or fp16 bits)
+    void* wt;                 // W~ output (float or 16-bit); packed indices (palettize);
+                              // inverse index (unique_inverse)
     int32_t* iters_out;
     uint32_t* nuniq_out;
     const float* g;           // dL/dW~
     float* gw;                // dL/dw
     float* gc;                // dL/dC^(0)
     float* attn;              // dense map output (nullable)
+    uint16_t* uniq;           // sorted distinct patterns (unique_inverse, nullable)
     void* wsb;                // workspace base (regions: carve_workspace)
     int k;
     int max_iter;
@@ -111,7 +114,7 @@ static_assert(sizeof(BatchArgs) <= 4096, "launch arguments fit the kernel-argume
 // in every kernel (from the workspace base in the launch arguments).
 struct Layout {
     size_t counts, tab, H, R, HR, G, chist, shist, ghist, ehist, tpart, bpart, dpart, span, part, pidx,
-        st, total;
+        rank, st, total;
 };
 
 __host__ __device__ inline Layout layout(int max_iter) {
@@ -137,6 +140,7 @@ __host__ __device__ inline Layout layout(int max_iter) {
     L.span = take(NP_MAX_WG * sizeof(int2));
     L.part = take((size_t)NP_MAX_WG * ROW4 * sizeof(uint32_t));
     L.pidx = take(NKEYS);
+    L.rank = take(NKEYS * sizeof(uint16_t));
     L.total = o;
     return L;
 }
@@ -148,6 +152,7 @@ __host__ __device__ inline Ws carve_workspace(void* base, int max_iter) {
     char* c = static_cast<char*>(base);
     Ws w;
     w.pidx = reinterpret_cast<uint8_t*>(c + L.pidx);
+    w.rank = reinterpret_cast<uint16_t*>(c + L.rank);
     w.st = reinterpret_cast<DevState*>(c + L.st);
     w.counts = reinterpret_cast<uint32_t*>(c + L.counts);
     w.tab = reinterpret_cast<float*>(c + L.tab);
@@ -169,7 +174,8 @@ __host__ __device__ inline Ws carve_workspace(void* base, int max_iter) {
 
 // Optional timing events recorded around the N-sized passes (diagnostics).
 enum Pass { PASS_HIST = 0, PASS_GATHER_WT = 1, PASS_KEYED_GRAD = 2, PASS_GATHER_GRAD = 3,
-            PASS_DENSE_ITER = 4, PASS_DENSE_BITER = 5, PASS_PALETTIZE = 6, NPASS = 7 };
+            PASS_DENSE_ITER = 4, PASS_DENSE_BITER = 5, PASS_PALETTIZE = 6, PASS_INVERSE = 7,
+            NPASS = 8 };
 struct PassEvents {
     hipEvent_t start[NPASS];
     hipEvent_t stop[NPASS];
@@ -186,6 +192,8 @@ hipError_t launch_backward(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_
                               const PassEvents* ev = nullptr);
 hipError_t launch_palettize(BatchArgs& b, uint32_t grid_np, hipStream_t s, const char** where,
                             const PassEvents* ev);
+hipError_t launch_unique_inverse(BatchArgs& b, uint32_t grid_np, bool inverse, hipStream_t s,
+                                 const char** where, const PassEvents* ev);
 hipError_t launch_forward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where,
                                 const PassEvents* ev = nullptr);
 hipError_t launch_backward_dense(BatchArgs& b, uint32_t nwg, hipStream_t s, const char** where,

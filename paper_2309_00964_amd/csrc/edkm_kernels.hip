@@ -451,6 +451,9 @@ __device__ __forceinline__ void st_f4_nt(float* p, float4 x) {
 __device__ __forceinline__ void st_u2_nt(void* p, uint2 x) {
     __builtin_nontemporal_store(v2u_t{x.x, x.y}, reinterpret_cast<v2u_t*>(p));
 }
+__device__ __forceinline__ void st_u4_nt(void* p, uint4 x) {
+    __builtin_nontemporal_store(v4u_t{x.x, x.y, x.z, x.w}, reinterpret_cast<v4u_t*>(p));
+}
 
 // ----------------------------------------------------------------------------
 // init_unique: zero, histogram, partial merge, window selection
@@ -1227,6 +1230,99 @@ __global__ void __launch_bounds__(1024) k_palettize(BatchArgs b) {
 }
 
 // ----------------------------------------------------------------------------
+// Distinct patterns and the inverse index: the unique-value list and the
+// per-weight index list of the uniquification (Sec. 2.2), in ascending order
+// of the 16-bit key (the order np.unique gives)
+
+// rank[u] = number of occupied patterns (count > 0) below u, for every u.  For
+// an occupied u that is its position in the sorted list of distinct patterns,
+// written to M.uniq when given.  One 1024-thread block per matrix, grid
+// (1, count); thread t ranks the patterns [64 t, 64 t + 64).
+__global__ void __launch_bounds__(1024) k_rank(BatchArgs b) {
+    __shared__ unsigned long long occ[NKEYS / 64];   // bit e of word t: pattern 64 t + e occupied
+    __shared__ uint32_t wtot[1024 / 64];
+    const MatArgs& M = b.m[blockIdx.y];
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    // byte m of the bitmap (patterns 8 m .. 8 m + 7) from two 16-byte loads of
+    // counts; m = 1024 i + t keeps every load contiguous across the wave
+    const uint4* c4 = reinterpret_cast<const uint4*>(ws.counts);
+    uint4 q[16];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        q[2 * i] = c4[2 * (1024 * i + t)];
+        q[2 * i + 1] = c4[2 * (1024 * i + t) + 1];
+    }
+    uint8_t* occ8 = reinterpret_cast<uint8_t*>(occ);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const uint4 a = q[2 * i], c = q[2 * i + 1];
+        occ8[1024 * i + t] =
+            (uint8_t)((uint32_t)(a.x != 0u) | (uint32_t)(a.y != 0u) << 1 | (uint32_t)(a.z != 0u) << 2 |
+                      (uint32_t)(a.w != 0u) << 3 | (uint32_t)(c.x != 0u) << 4 | (uint32_t)(c.y != 0u) << 5 |
+                      (uint32_t)(c.z != 0u) << 6 | (uint32_t)(c.w != 0u) << 7);
+    }
+    __syncthreads();
+    const unsigned long long bits = occ[t];
+    const uint32_t pc = (uint32_t)__popcll(bits);
+    const uint32_t incl = wave_incl_scan(pc);
+    if (lane == 63) wtot[wave] = incl;
+    __syncthreads();
+    uint32_t base = incl - pc;   // occupied patterns below 64 t
+    for (int w = 0; w < wave; ++w) base += wtot[w];
+    // the thread's 64 ranks, 8 per 16-byte store (pattern 2 j in the low half
+    // of word j); a rank never exceeds 65,535
+    uint4* rk = reinterpret_cast<uint4*>(ws.rank + 64 * t);
+    uint32_t r = base;
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+        uint32_t h[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int e = 8 * g + 2 * j;
+            const uint32_t r0 = r;
+            r += (uint32_t)(bits >> e) & 1u;
+            h[j] = r0 | (r << 16);
+            r += (uint32_t)(bits >> (e + 1)) & 1u;
+        }
+        rk[g] = make_uint4(h[0], h[1], h[2], h[3]);
+    }
+    if (M.uniq) {
+        unsigned long long x = bits;
+        uint32_t ru = base;
+        while (x) {
+            M.uniq[ru++] = (uint16_t)(64 * t + __builtin_ctzll(x));
+            x &= x - 1;
+        }
+    }
+}
+
+// inverse[i] = rank[bits_i]: the position of w_i's pattern among the distinct
+// patterns.  The whole rank table (128 KiB) is loaded into LDS; no window.
+// Matrices of the launch without an inverse output (M.wt null) skip the pass.
+__global__ void __launch_bounds__(NP_THREADS) k_inverse(BatchArgs b) {
+    __shared__ uint4 rk4[NKEYS * sizeof(uint16_t) / sizeof(uint4)];
+    const int mi = np_matrix(b);
+    const MatArgs& M = b.m[mi];
+    if (!M.wt) return;   // the same for the whole workgroup
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
+    const uint32_t wl = blockIdx.x - M.wg_begin;
+    const uint4* src = reinterpret_cast<const uint4*>(ws.rank);
+    for (int i = threadIdx.x; i < (int)(NKEYS * sizeof(uint16_t) / sizeof(uint4)); i += NP_THREADS)
+        rk4[i] = src[i];
+    __syncthreads();
+    const uint16_t* rk = reinterpret_cast<const uint16_t*>(rk4);
+    const uint16_t* keys = M.keys;
+    uint16_t* out = reinterpret_cast<uint16_t*>(M.wt);
+    auto pair = [&](uint32_t x) { return (uint32_t)rk[x & 0xFFFFu] | ((uint32_t)rk[x >> 16] << 16); };
+    for_slice<8, 8>(M, wl,
+        [&](uint64_t i) { return Keys8{ld_u4_nt(keys + i)}; },
+        [&](const Keys8& r) { return make_uint4(pair(r.q.x), pair(r.q.y), pair(r.q.z), pair(r.q.w)); },
+        [&](uint64_t i, uint4 o) { st_u4_nt(out + i, o); },
+        [&](uint64_t i) { out[i] = rk[keys[i]]; });
+}
+
+// ----------------------------------------------------------------------------
 // backward table phase
 
 // Direct use of A^(T) and C^(T) by W~: with G_u (merged keyed sums), partials of gamma_j = sum_u G_u a^(T)_uj (= dL/dC^(T)_j) and
@@ -1756,6 +1852,14 @@ hipError_t launch_palettize(BatchArgs& b, uint32_t grid_np, hipStream_t s, const
     case 16: EDKM_NPASS(PASS_PALETTIZE, "k_palettize", k_palettize<4>, grid, dim3(1024), b); break;
     default: return hipErrorInvalidValue;
     }
+    return hipSuccess;
+}
+
+hipError_t launch_unique_inverse(BatchArgs& b, uint32_t grid_np, bool inverse, hipStream_t s,
+                                 const char** where, const PassEvents* ev) {
+    (void)hipGetLastError();
+    EDKM_LAUNCH("k_rank", k_rank, dim3(1, b.count), dim3(1024), b);
+    if (inverse) EDKM_NPASS(PASS_INVERSE, "k_inverse", k_inverse, dim3(grid_np), dim3(NP_THREADS), b);
     return hipSuccess;
 }
 

@@ -52,7 +52,7 @@ ERR_STATE = -4
 ERR_HIP = -5
 NKEYS = 65536
 PASS_HIST, PASS_GATHER_WT, PASS_KEYED_GRAD, PASS_GATHER_GRAD = 0, 1, 2, 3
-PASS_DENSE_ITER, PASS_DENSE_BITER, PASS_PALETTIZE = 4, 5, 6
+PASS_DENSE_ITER, PASS_DENSE_BITER, PASS_PALETTIZE, PASS_INVERSE = 4, 5, 6, 7
 KEYS_FP16, KEYS_BF16 = 0, 1
 LAUNCH_GROUP = 28          # EDKM_LAUNCH_GROUP: matrices per launch in the batched calls
 KEYED_AUTO, KEYED_I32, KEYED_U64 = -1, 0, 1
@@ -82,6 +82,8 @@ _SIGS = {
     "edkm_plan_set_keyed_mode": (_i32, [_PLAN, _i32]),
     "edkm_palettize": (_i32, [_PLAN, _P, _P, _P, _P]),
     "edkm_palettize_batch": (_i32, [_i32, _PP, _PP, _PP, _PP, _P]),
+    "edkm_unique_inverse": (_i32, [_PLAN, _P, _P, _P, _P]),
+    "edkm_unique_inverse_batch": (_i32, [_i32, _PP, _PP, _PP, _PP, _P]),
     "edkm_init_unique": (_i32, [_PLAN, _P, _P, _P, _i32, _P]),
     "edkm_forward": (_i32, [_PLAN, _P, _f32, _f32, _P, _P, _P, _i32, _P, _P]),
     "edkm_backward": (_i32, [_PLAN, _P, _P, _P, _P, _P]),
@@ -194,6 +196,18 @@ def palettize(plan: Plan, w_bits, lut, indices_out, stream=None) -> None:
     _check(_lib.edkm_palettize(plan.ref, _ptr(w_bits, 2, "w_bits", plan.n), _ptr(lut, 4, "lut", plan.k),
                                _ptr(indices_out, 1),
                                _stream(stream)), "palettize", (plan,))
+
+
+def unique_inverse(plan: Plan, w_bits, unique_out=None, inverse_out=None, stream=None) -> None:
+    """The uniquification's two lists, ascending by 16-bit key (numpy.unique's
+    order): the distinct patterns into ``unique_out`` (16-bit elements, room
+    for 65,536; the first num_unique are written) and each weight's index
+    among them into ``inverse_out`` (16-bit, n).  After init_unique on the
+    same keys; at least one output."""
+    _check(_lib.edkm_unique_inverse(plan.ref, _ptr(w_bits, 2, "w_bits", plan.n),
+                                    _ptr(unique_out, 2, "unique_out", NKEYS),
+                                    _ptr(inverse_out, 2, "inverse_out", plan.n), _stream(stream)),
+           "unique_inverse", (plan,))
 
 
 def plan_set_keyed_mode(plan: Plan, mode: int) -> None:
@@ -330,3 +344,17 @@ def palettize_batch(plans, w_bits, lut, indices_out, stream=None) -> None:
     lt, _c = _parr(lut, 4, "lut", [p.k for p in plans])
     oo, _d = _parr(indices_out, 1, "indices_out", [(p.n * p.bits + 7) // 8 for p in plans])
     _check(_lib.edkm_palettize_batch(n, pp, kk, lt, oo, _stream(stream)), "palettize_batch", plans)
+
+
+def unique_inverse_batch(plans, w_bits, unique_out=None, inverse_out=None, stream=None) -> None:
+    """unique_inverse over a batch (list entries may be None where that output
+    is not wanted): one ranking launch per launch group, plus one N-sized
+    launch if any matrix of the group wants its inverse index."""
+    _same_len("unique_inverse_batch", plans, w_bits=w_bits, unique_out=unique_out, inverse_out=inverse_out)
+    n = len(plans)
+    pp, _a = _plans(plans)
+    ns = [p.n for p in plans]
+    kk, _b = _parr(w_bits, 2, "w_bits", ns)
+    uo, _c = _parr(unique_out, 2, "unique_out", [NKEYS] * n) if unique_out is not None else (None, None)
+    io, _d = _parr(inverse_out, 2, "inverse_out", ns) if inverse_out is not None else (None, None)
+    _check(_lib.edkm_unique_inverse_batch(n, pp, kk, uo, io, _stream(stream)), "unique_inverse_batch", plans)

@@ -102,6 +102,30 @@ def test_null_pointers_are_argument_errors():
     assert lib.edkm_backward_dense(ctypes.byref(p), keys, None, f, f, None) == edkm.ERR_ARG
 
 
+def test_unique_inverse_argument_and_state_errors():
+    p = _plan()
+    keys, u = 1 << 41, 1 << 42
+    # no output at all
+    assert lib.edkm_unique_inverse(ctypes.byref(p), keys, None, None, None) == edkm.ERR_ARG
+    assert lib.edkm_unique_inverse(ctypes.byref(p), None, u, None, None) == edkm.ERR_ARG
+    # before init_unique: nothing to rank
+    assert lib.edkm_unique_inverse(ctypes.byref(p), keys, u, None, None) == edkm.ERR_STATE
+    assert lib.edkm_unique_inverse(ctypes.byref(p), keys, None, u, None) == edkm.ERR_STATE
+    q = edkm.edkm_plan()
+    assert lib.edkm_unique_inverse(ctypes.byref(q), keys, u, u, None) == edkm.ERR_ARG
+    # batch: one matrix without either output is an argument error
+    p2 = edkm.edkm_plan()
+    ws = edkm.workspace_bytes(1000, 3, 5)
+    assert lib.edkm_plan_init(ctypes.byref(p2), 1000, 3, 5, FAKE_WS + ws + (256 - ws % 256) % 256, ws) == edkm.OK
+    arr = (ctypes.c_void_p * 2)(ctypes.addressof(p), ctypes.addressof(p2))
+    kk = (ctypes.c_void_p * 2)(keys, keys)
+    uo = (ctypes.c_void_p * 2)(u, None)
+    pp, kp, up = (ctypes.cast(x, edkm._PP) for x in (arr, kk, uo))
+    assert lib.edkm_unique_inverse_batch(2, pp, kp, up, None, None) == edkm.ERR_ARG
+    uo[1] = u
+    assert lib.edkm_unique_inverse_batch(2, pp, kp, up, None, None) == edkm.ERR_STATE
+
+
 def test_batch_argument_errors():
     p1, p2 = _plan(), _plan()
     arr = (ctypes.c_void_p * 2)(ctypes.addressof(p1), ctypes.addressof(p1))
