@@ -267,6 +267,19 @@ __device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long x)
     const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), 63);
     return ((unsigned long long)hi << 32) | lo;
 }
+// Maximum of a 64-bit unsigned integer over the 64 lanes (all active).
+__device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long x) {
+    auto mx = [](unsigned long long a, unsigned long long b) { return a > b ? a : b; };
+    x = mx(x, dpp_u64<DPP_XOR1>(x, x));
+    x = mx(x, dpp_u64<DPP_XOR2>(x, x));
+    x = mx(x, dpp_u64<DPP_HALF_MIRROR>(x, x));
+    x = mx(x, dpp_u64<DPP_MIRROR>(x, x));
+    x = mx(x, dpp_u64<DPP_BCAST15, 0xA>(0ull, x));
+    x = mx(x, dpp_u64<DPP_BCAST31, 0xC>(0ull, x));
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), 63);
+    return ((unsigned long long)hi << 32) | lo;
+}
 __device__ __forceinline__ int op_min(int a, int b) { return min(a, b); }
 __device__ __forceinline__ int op_max(int a, int b) { return max(a, b); }
 __device__ __forceinline__ int op_add(int a, int b) { return a + b; }
@@ -511,8 +524,12 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
     for (int mag = threadIdx.x; mag < W4; mag += NP_THREADS) {
         if (h[mag] | h[W4 + mag]) { lo = min(lo, mag); hi = max(hi, mag + 1); }
     }
-    atomicMin(&red[0], lo);
-    atomicMax(&red[1], hi);
+    lo = wave_reduce(lo, 0x7FFFFFFF, op_min);   // one LDS atomic per wave
+    hi = wave_reduce(hi, -0x7FFFFFFF - 1, op_max);
+    if ((threadIdx.x & 63) == 0) {
+        atomicMin(&red[0], lo);
+        atomicMax(&red[1], hi);
+    }
     __syncthreads();
     lo = red[0] & ~1;
     hi = (red[1] + 1) & ~1;
@@ -700,7 +717,8 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
             const unsigned long long key = ((unsigned long long)cov << 32) | (uint32_t)(0x7FFFFFFF - s);
             mine = key > mine ? key : mine;
         }
-        atomicMax(&best[w], mine);
+        mine = wave_max_u64(mine);   // one LDS atomic per wave, not per thread
+        if ((threadIdx.x & 63) == 0) atomicMax(&best[w], mine);
         __syncthreads();
         wl[w] = 0x7FFFFFFF - (int)(uint32_t)(best[w] & 0xFFFFFFFFull);
         ww[w] = W;

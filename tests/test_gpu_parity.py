@@ -425,6 +425,32 @@ def test_forward_repeatable_and_exact_scaling():
             assert_close(s["w_tilde"], 2 * a["w_tilde"].astype(np.float64), 1e-6, "scaled w_tilde")
 
 
+def test_negation_symmetry_on_gpu():
+    """w, C^(0) -> -w, -C^(0): C and W~ negate, dL/dw and dL/dC^(0) are
+    unchanged (the map depends on |w - c| only).  Bitwise for the dense
+    forward, whose sums keep their order; to rounding elsewhere: on the table
+    path negation moves every pattern to the other sign half (key ^ 0x8000),
+    which reorders the fixed-order sums, and the keyed gradient sum uses
+    atomics."""
+    n, bits = 65536 * 3 + 5, 3
+    keys = inputs.fp16_weights(n, 102)
+    c0 = inputs.quantile_init(keys, 1 << bits)
+    g = inputs.upstream_grad(n, 103)
+    kn = keys ^ np.uint16(0x8000)
+    say("negation symmetry")
+    for dense_path in (True, False):
+        a = gpu(keys, c0, bits, g=g, dense=dense_path)
+        b = gpu(kn, -c0, bits, g=g, dense=dense_path)
+        what = "dense" if dense_path else "table"
+        if dense_path:
+            assert np.array_equal(b["c_out"], -a["c_out"]) and np.array_equal(b["w_tilde"], -a["w_tilde"])
+        else:
+            assert_close(b["c_out"], -a["c_out"].astype(np.float64), 1e-6, what + " c_out")
+            assert_close(b["w_tilde"], -a["w_tilde"].astype(np.float64), 1e-6, what + " w_tilde")
+        assert_close(b["grad_w"], a["grad_w"].astype(np.float64), 1e-5, what + " grad_w")
+        assert_close(b["grad_c"], a["grad_c"].astype(np.float64), 1e-4, what + " grad_c")
+
+
 def test_misaligned_buffers_take_the_scalar_path():
     n = 65536 + 11
     keys = inputs.fp16_weights(n + 1, 111)
