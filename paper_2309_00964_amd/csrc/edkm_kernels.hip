@@ -307,7 +307,7 @@ __device__ __forceinline__ void block_sum(const float (&v)[NV], float* scratch, 
 }
 
 // Reduce rows [0, T_WG) of a partial block (T_WG x PSTRIDE floats) for columns
-// [c0, c0 + ncol) into out[0..ncol) (LDS), by wave butterflies.  Called by all
+// [c0, c0 + ncol) into out[0..ncol) (LDS), by wave reductions.  Called by all
 // threads of a T_THREADS block.
 __device__ __forceinline__ void reduce_tparts(const float* part, int c0, int ncol, float* out) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -556,7 +556,7 @@ constexpr int MERGE_ROWS = 16;
 constexpr int MERGE_THREADS = 256;
 
 // Histogram rows (packed 16-bit pairs over per-row spans) into counts.
-// Grid (W4 / MERGE_THREADS, NP_MAX_WG / MERGE_ROWS, count).
+// Grid (W4 / MERGE_THREADS, row chunks, count).
 __global__ void __launch_bounds__(MERGE_THREADS) k_hist_merge(BatchArgs b) {
     const MatArgs& M = b.m[blockIdx.z];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
@@ -590,7 +590,7 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_hist_merge(BatchArgs b) {
 }
 
 // Keyed-gradient rows (fp32 over the window of the matrix's keyed-sum mode)
-// into G.  Grid (2 * W4 / MERGE_THREADS, NP_MAX_WG / MERGE_ROWS, count).
+// into G.  Grid (2 * W4 / MERGE_THREADS, row chunks, count).
 __global__ void __launch_bounds__(MERGE_THREADS) k_grad_merge(BatchArgs b) {
     const MatArgs& M = b.m[blockIdx.z];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
@@ -1768,6 +1768,14 @@ __global__ void __launch_bounds__(1024) k_dense_bfin(BatchArgs b, int nrow) {
         if (e_ != hipSuccess) { *where = name; return e_; }              \
     } while (0)
 
+// Row chunks of the partial-row merges: enough for the matrix of the launch
+// with the most N-pass workgroups (one partial row each).
+static uint32_t merge_chunks(const BatchArgs& b) {
+    uint32_t rows = 1;
+    for (int i = 0; i < b.count; ++i) rows = b.m[i].wg_count > rows ? b.m[i].wg_count : rows;
+    return (rows + MERGE_ROWS - 1) / MERGE_ROWS;
+}
+
 template <int K>
 static hipError_t forward_k(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_t s, const char** where,
                             const PassEvents* ev) {
@@ -1786,8 +1794,7 @@ static hipError_t backward_k(BatchArgs& b, uint32_t grid_np, int max_t, hipStrea
                              const PassEvents* ev) {
     const dim3 tg(T_WG, b.count);
     EDKM_NPASS(PASS_KEYED_GRAD, "k_keyed_grad", k_keyed_grad, dim3(grid_np), dim3(NP_THREADS), b);
-    EDKM_LAUNCH("k_grad_merge", k_grad_merge,
-                dim3(2 * W4 / MERGE_THREADS, NP_MAX_WG / MERGE_ROWS, b.count),
+    EDKM_LAUNCH("k_grad_merge", k_grad_merge, dim3(2 * W4 / MERGE_THREADS, merge_chunks(b), b.count),
                 dim3(MERGE_THREADS), b);
     EDKM_LAUNCH("k_bwd_top", k_bwd_top<K>, tg, dim3(T_THREADS), b);
     for (int t = max_t; t >= 1; --t) {
@@ -1840,7 +1847,7 @@ hipError_t launch_init_unique(BatchArgs& b, uint32_t grid_np, hipStream_t s, con
     (void)hipGetLastError();   // an earlier, unrelated failure is not ours to report
     EDKM_LAUNCH("k_init_zero", k_init_zero, dim3(T_WG, b.count), dim3(T_THREADS), b);
     EDKM_NPASS(PASS_HIST, "k_hist", k_hist, dim3(grid_np), dim3(NP_THREADS), b);
-    EDKM_LAUNCH("k_hist_merge", k_hist_merge, dim3(W4 / MERGE_THREADS, NP_MAX_WG / MERGE_ROWS, b.count),
+    EDKM_LAUNCH("k_hist_merge", k_hist_merge, dim3(W4 / MERGE_THREADS, merge_chunks(b), b.count),
                 dim3(MERGE_THREADS), b);
     EDKM_LAUNCH("k_window", k_window, dim3(1, b.count), dim3(NP_THREADS), b);
     return hipSuccess;
