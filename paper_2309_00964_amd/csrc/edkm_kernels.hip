@@ -267,6 +267,26 @@ __device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long x)
     const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), 63);
     return ((unsigned long long)hi << 32) | lo;
 }
+// Fill an LDS table: dst[i] = src[idx(i)] for i < n (n <= MAXN), by a block of
+// NT threads.  Every load of a thread is issued before its first LDS write;
+// written as a plain loop, each iteration waited for its load, so the copy
+// cost one L2 round trip per iteration.  The caller synchronises the block.
+template <int MAXN, int NT, class T, class Idx>
+__device__ __forceinline__ void fill_lds(T* dst, const T* src, int n, Idx idx) {
+    constexpr int PER = (MAXN + NT - 1) / NT;
+    T v[PER];
+#pragma unroll
+    for (int c = 0; c < PER; ++c) {
+        const int i = threadIdx.x + c * NT;
+        if (i < n) v[c] = src[idx(i)];
+    }
+#pragma unroll
+    for (int c = 0; c < PER; ++c) {
+        const int i = threadIdx.x + c * NT;
+        if (i < n) dst[i] = v[c];
+    }
+}
+
 // Maximum of a 64-bit unsigned integer over the 64 lanes (all active).
 __device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long x) {
     auto mx = [](unsigned long long a, unsigned long long b) { return a > b ? a : b; };
@@ -899,10 +919,10 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
     const uint32_t wl = blockIdx.x - M.wg_begin;
     const int lo = ws.st->lo4, w = ws.st->w4;
     const float* tab = ws.tab;
-    for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) {
+    fill_lds<2 * W4, NP_THREADS>(tw, tab, 2 * w, [&](int i) {
         const int s = i >= w;
-        tw[i] = tab[(s << 15) | (lo + i - s * w)];
-    }
+        return (s << 15) | (lo + i - s * w);
+    });
     __syncthreads();
     // Lookup, written as an LDS read at a clamped index that lanes outside the
     // window overwrite with a global read: the compiler turns this into a
@@ -1132,10 +1152,10 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
         const uint32_t u0 = wl * per, u1 = min((uint32_t)NKEYS, u0 + per);
         for (uint32_t u = u0 + threadIdx.x; u < u1; u += NP_THREADS) ws.G[u] = 0.f;
     }
-    for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) {
+    fill_lds<2 * W8, NP_THREADS>(hw, HR, 2 * w, [&](int i) {
         const int s = i >= w;
-        hw[i] = HR[(s << 15) | (lo + i - s * w)];
-    }
+        return (s << 15) | (lo + i - s * w);
+    });
     __syncthreads();
     auto look = [&](uint32_t key) -> float2 {   // one flat load per lookup, as in k_gather_wt
         const uint32_t d = (key & 0x7FFFu) - (uint32_t)lo;
@@ -1200,7 +1220,7 @@ __global__ void __launch_bounds__(1024) k_palettize(BatchArgs b) {
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const uint32_t wl = blockIdx.x - M.wg_begin;
     const uint4* src = reinterpret_cast<const uint4*>(ws.pidx);
-    for (int i = threadIdx.x; i < NKEYS / 16; i += blockDim.x) tbl4[i] = src[i];
+    fill_lds<NKEYS / 16, 1024>(tbl4, src, NKEYS / 16, [](int i) { return i; });   // blockDim.x = 1024
     __syncthreads();
     const uint8_t* tbl = reinterpret_cast<const uint8_t*>(tbl4);
     const uint16_t* keys = M.keys;
@@ -1326,8 +1346,8 @@ __global__ void __launch_bounds__(NP_THREADS) k_inverse(BatchArgs b) {
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const uint32_t wl = blockIdx.x - M.wg_begin;
     const uint4* src = reinterpret_cast<const uint4*>(ws.rank);
-    for (int i = threadIdx.x; i < (int)(NKEYS * sizeof(uint16_t) / sizeof(uint4)); i += NP_THREADS)
-        rk4[i] = src[i];
+    constexpr int NV = NKEYS * sizeof(uint16_t) / sizeof(uint4);
+    fill_lds<NV, NP_THREADS>(rk4, src, NV, [](int i) { return i; });
     __syncthreads();
     const uint16_t* rk = reinterpret_cast<const uint16_t*>(rk4);
     const uint16_t* keys = M.keys;
