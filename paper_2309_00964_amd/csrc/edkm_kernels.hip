@@ -456,13 +456,17 @@ struct KeysG4 { uint2 q; float4 g; };
 typedef unsigned int v4u_t __attribute__((ext_vector_type(4)));
 typedef unsigned int v2u_t __attribute__((ext_vector_type(2)));
 typedef float v4f_t __attribute__((ext_vector_type(4)));
-// Streaming loads and stores.  Measured with the round-robin tile sweep:
-// non-temporal (nt) loads help the read-only passes (histogram, keyed sum) and
-// the gradient gather; the W~ gather keeps plain loads, which leave the keys
-// in the caches for the keyed sum when a backward follows.  The gathers'
-// outputs use nt stores, float4 or (16-bit W~) uint2: gradient gather 404 ->
-// 381 us on the decoder layer, 16-bit W~ gather 168 -> 162 us, and the kernel
-// after the W~ gather no longer inherits its dirty lines.
+// Streaming loads and stores.  Consecutive N-sized passes sweep in opposite
+// directions (histogram forward, W~ gather backward, keyed sum forward,
+// gradient gather backward), so the last ~256 MB a pass reads with plain
+// (cached) loads are still in the Infinity Cache where the next pass starts.
+// Plain loads: the histogram (for the W~ gather), the W~ gather (keys, for
+// the keyed sum) and g in the keyed sum (for the gradient gather); the rest
+// is non-temporal (nt), which a pass runs a little faster with when nothing
+// after it reads the same data.  The gathers' outputs use nt stores, float4
+// or (16-bit W~) uint2: gradient gather 404 -> 381 us on the decoder layer,
+// 16-bit W~ gather 168 -> 162 us, and the kernel after the W~ gather no
+// longer inherits its dirty lines.
 __device__ __forceinline__ uint4 ld_u4(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 __device__ __forceinline__ uint2 ld_u2(const void* p) { return *reinterpret_cast<const uint2*>(p); }
 __device__ __forceinline__ float4 ld_f4(const float* p) { return *reinterpret_cast<const float4*>(p); }
@@ -527,8 +531,10 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
         if (mag < (uint32_t)W4) atomicAdd(&h[(key >> 15) * W4 + mag], 1u);
         else atomicAdd(&gcounts[key], 1u);
     };
+    // Plain (cached) loads: the tail of this forward sweep stays in the
+    // Infinity Cache, where the W~ gather, sweeping backwards, starts.
     for_slice<4, 8>(M, wl,
-        [&](uint64_t i) { return Keys8{ld_u4_nt(keys + i)}; },
+        [&](uint64_t i) { return Keys8{ld_u4(keys + i)}; },
         [&](const Keys8& r) {
             add(r.q.x & 0xFFFFu); add(r.q.x >> 16);
             add(r.q.y & 0xFFFFu); add(r.q.y >> 16);
@@ -1033,9 +1039,11 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
     }
     __syncthreads();
     float* G = ws.G;
+    // Keys non-temporal, g cached: the tail of g stays in the Infinity Cache
+    // for the gradient gather, which sweeps backwards.
     auto stream = [&](auto add) {
         for_slice<4, 4>(M, wl,
-            [&](uint64_t i) { return KeysG4{ld_u2_nt(keys + i), ld_f4_nt(g + i)}; },
+            [&](uint64_t i) { return KeysG4{ld_u2_nt(keys + i), ld_f4(g + i)}; },
             [&](const KeysG4& r) {
                 add(r.q.x & 0xFFFFu, r.g.x); add(r.q.x >> 16, r.g.y);
                 add(r.q.y & 0xFFFFu, r.g.z); add(r.q.y >> 16, r.g.w);
@@ -1092,7 +1100,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
         };
         struct Pend4 { uint2 keys; int q[4], old[4]; };
         for_slice<3, 4>(M, wl,
-            [&](uint64_t i) { return KeysG4{ld_u2_nt(keys + i), ld_f4_nt(g + i)}; },
+            [&](uint64_t i) { return KeysG4{ld_u2_nt(keys + i), ld_f4(g + i)}; },   // as above
             [&](const KeysG4& r) {
                 Pend4 p;
                 p.keys = r.q;
