@@ -460,10 +460,10 @@ typedef float v4f_t __attribute__((ext_vector_type(4)));
 // directions (histogram forward, W~ gather backward, keyed sum forward,
 // gradient gather backward), so the last ~256 MB a pass reads with plain
 // (cached) loads are still in the Infinity Cache where the next pass starts.
-// Plain loads: the histogram (for the W~ gather), the W~ gather (keys, for
-// the keyed sum) and g in the keyed sum (for the gradient gather); the rest
-// is non-temporal (nt), which a pass runs a little faster with when nothing
-// after it reads the same data.  The gathers' outputs use nt stores, float4
+// Plain loads for the keys in the histogram (for the W~ gather), the W~
+// gather (for the keyed sum) and the keyed sum (for the gradient gather);
+// the rest is non-temporal (nt), which a pass runs a little faster with when
+// nothing after it reads the same data.  The gathers' outputs use nt stores, float4
 // or (16-bit W~) uint2: gradient gather 404 -> 381 us on the decoder layer,
 // 16-bit W~ gather 168 -> 162 us, and the kernel after the W~ gather no
 // longer inherits its dirty lines.
@@ -1039,11 +1039,11 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
     }
     __syncthreads();
     float* G = ws.G;
-    // Keys non-temporal, g cached: the tail of g stays in the Infinity Cache
-    // for the gradient gather, which sweeps backwards.
+    // Keys cached, g non-temporal: the tail of the keys stays in the Infinity
+    // Cache for the gradient gather, which sweeps backwards.
     auto stream = [&](auto add) {
         for_slice<4, 4>(M, wl,
-            [&](uint64_t i) { return KeysG4{ld_u2_nt(keys + i), ld_f4(g + i)}; },
+            [&](uint64_t i) { return KeysG4{ld_u2(keys + i), ld_f4_nt(g + i)}; },
             [&](const KeysG4& r) {
                 add(r.q.x & 0xFFFFu, r.g.x); add(r.q.x >> 16, r.g.y);
                 add(r.q.y & 0xFFFFu, r.g.z); add(r.q.y >> 16, r.g.w);
@@ -1100,7 +1100,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
         };
         struct Pend4 { uint2 keys; int q[4], old[4]; };
         for_slice<3, 4>(M, wl,
-            [&](uint64_t i) { return KeysG4{ld_u2_nt(keys + i), ld_f4(g + i)}; },   // as above
+            [&](uint64_t i) { return KeysG4{ld_u2(keys + i), ld_f4_nt(g + i)}; },   // as above
             [&](const KeysG4& r) {
                 Pend4 p;
                 p.keys = r.q;
