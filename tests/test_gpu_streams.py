@@ -1,6 +1,7 @@
 """Streams and graphs: distinct plans run concurrently on distinct streams, and
 a whole batched step (init_unique + forward + backward) captured in a HIP graph
-replays to the eager results.
+replays to the eager results, as do the export calls (distinct-pattern list,
+inverse index, palettization).
 
 Forward outputs are compared bitwise (fixed-order reductions).  Backward
 outputs within 1e-6 relative: the keyed sum's fp32 fallback and merge atomics
@@ -117,3 +118,55 @@ def test_graph_capture_replays_the_eager_step():
         graph.replay()
         torch.cuda.synchronize()
         same(x.outputs(), ref, "replay %d" % rep)
+
+
+def test_graph_capture_of_the_export_calls():
+    """init_unique, the distinct-pattern list with the inverse index, and the
+    packed palettization indices, captured in one graph: every replay (with
+    the outputs poisoned and other eager work in between) matches the eager
+    results exactly (integer outputs)."""
+    x = Batch([65536, 300_007], 340)
+    other = Batch([50_000], 350)
+    uo = [torch.empty(edkm.NKEYS, dtype=torch.int16, device=DEV) for _ in x.plans]
+    io = [torch.empty(p.n, dtype=torch.int16, device=DEV) for p in x.plans]
+    po = [torch.empty((p.n * p.bits + 7) // 8, dtype=torch.uint8, device=DEV) for p in x.plans]
+
+    def poison():
+        for t in uo + io:
+            t.fill_(0x5A5A)
+        for t in po:
+            t.fill_(0xAB)
+
+    def step():
+        edkm.init_unique_batch(x.plans, x.keys)
+        edkm.unique_inverse_batch(x.plans, x.keys, uo, io)
+        edkm.palettize_batch(x.plans, x.keys, x.c0, po)
+
+    def outs():
+        return [t.cpu().numpy().copy() for t in uo + io + po]
+
+    say("graph export: eager reference")
+    poison()
+    step()
+    torch.cuda.synchronize()
+    ref = outs()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    say("graph export: capture")
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        other.step()
+        poison()
+        torch.cuda.synchronize()
+        say("graph export: replay", rep)
+        graph.replay()
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(zip(outs(), ref)):
+            assert np.array_equal(a, b), "replay %d output %d" % (rep, i)
