@@ -654,35 +654,46 @@ def test_full_size_matrix(cfg, bits, fmt):
     check(res, oracle(keys, c0, g, form="table", fmt=fmt), what="cfg%d bits=%d %s" % (cfg, bits, fmt))
 
 
-def test_decoder_layer_batch_full_size():
+@pytest.mark.parametrize("fmt,out_half", [("fp16", False), ("fp16", True), ("bf16", False)])
+def test_decoder_layer_batch_full_size(fmt, out_half):
     """The seven matrices of one LLaMA-7B decoder layer in one batch (the call the
-    benchmark times), each against the table-form oracle."""
+    benchmark times, also in its 16-bit W~ and bf16-weight modes), each against
+    the table-form oracle.  16-bit W~ is held to one ulp of the oracle value
+    rounded to the weight format."""
     w = inputs.WORKLOADS[4]
-    say("decoder layer")
+    say("decoder layer", fmt, "half W~" if out_half else "fp32 W~")
     plans, kd, ci, co, wt, it, gd, gw, gc, host = [], [], [], [], [], [], [], [], [], []
     for i, (name, r, c) in enumerate(w["mats"]):
         n = r * c
-        keys = inputs.fp16_weights(n, inputs.weight_seed(4, i))
-        c0 = inputs.quantile_init(keys, 8)
+        keys = inputs.weights(n, inputs.weight_seed(4, i), False, fmt)
+        c0 = inputs.quantile_init(keys, 8, fmt)
         g = inputs.upstream_grad(n, inputs.grad_seed(4, i))
         host.append((keys, c0, g))
-        plans.append(edkm.Plan(n, 3, ITERS))
+        plans.append(edkm.Plan(n, 3, ITERS, key_format=fmt))
         kd.append(dkeys(keys))
         ci.append(torch.from_numpy(c0).to(DEV))
         co.append(torch.empty(8, device=DEV))
-        wt.append(torch.empty(n, device=DEV))
+        wt.append(torch.empty(n, dtype=torch.int16 if out_half else torch.float32, device=DEV))
         it.append(torch.zeros(1, dtype=torch.int32, device=DEV))
         gd.append(torch.from_numpy(g).to(DEV))
         gw.append(torch.empty(n, device=DEV))
         gc.append(torch.empty(8, device=DEV))
     edkm.init_unique_batch(plans, kd)
-    edkm.forward_batch(plans, kd, TAU, 0.0, ci, co, wt, False, it)
+    edkm.forward_batch(plans, kd, TAU, 0.0, ci, co, wt, out_half, it)
     edkm.backward_batch(plans, kd, gd, gw, gc)
     torch.cuda.synchronize()
     for i, (keys, c0, g) in enumerate(host):
-        res = dict(iters=it[i].cpu().numpy(), c_out=co[i].cpu().numpy(), w_tilde=wt[i].cpu().numpy(),
-                   grad_w=gw[i].cpu().numpy(), grad_c=gc[i].cpu().numpy())
-        check(res, oracle(keys, c0, g, form="table"), what=w["mats"][i][0])
+        what = "%s %s" % (w["mats"][i][0], fmt)
+        ref = oracle(keys, c0, g, form="table", fmt=fmt)
+        wv = wt[i].cpu().numpy()
+        assert int(it[i].item()) == ref["T"], what
+        assert_close(co[i].cpu().numpy(), ref["c_out"], TOL_FWD, what + " c_out")
+        if out_half:
+            assert_fp16_within_ulp(wv.view(np.uint16), ref["w_tilde"], what + " fp16 W~")
+        else:
+            assert_close(wv, ref["w_tilde"], TOL_FWD, what + " w_tilde")
+        assert_close(gw[i].cpu().numpy(), ref["gw"], TOL_BWD, what + " grad_w")
+        assert_close(gc[i].cpu().numpy(), ref["gc"], TOL_BWD, what + " grad_c")
 
 
 # ------------------------------------------------------------------ bf16 weights
