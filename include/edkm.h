@@ -16,7 +16,9 @@
  *   index list whose entry is the weight's own pattern.  Here every sum over
  *   weights becomes a sum over table rows weighted by per-pattern counts, and
  *   the N-sized work reduces to a histogram, a keyed gradient sum and two
- *   gathers.
+ *   gathers.  edkm_unique_inverse returns the compacted form of the two lists
+ *   (sorted distinct patterns, each weight's position among them) for callers
+ *   that store them; edkm_palettize exports the clustered result.
  *
  * Conventions for every entry point:
  *   - Weights are 16-bit floats, fp16 (IEEE binary16, the default) or bf16
@@ -35,7 +37,9 @@
  *     order init_unique -> forward -> backward (or forward_dense ->
  *     backward_dense) on one stream, with the same key buffer and unchanged
  *     keys; a call out of order returns EDKM_ERR_STATE before touching the
- *     GPU.  Distinct plans with distinct workspaces may be used concurrently.
+ *     GPU.  edkm_unique_inverse may follow init_unique at any point of that
+ *     sequence; edkm_palettize needs no earlier call.  Distinct plans with
+ *     distinct workspaces may be used concurrently.
  *   - Errors are returned, never thrown; argument errors are detected on the
  *     host before any HIP call and leave the plan unchanged.
  *   - Every entry point can be captured in a HIP graph (no allocation, no
