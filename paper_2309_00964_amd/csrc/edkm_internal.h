@@ -20,8 +20,9 @@ constexpr int NP_THREADS = 1024;      // N-pass workgroup size
 constexpr int NP_MAX_WG = 256;        // N-pass workgroups per launch group, at most (one per CU)
 constexpr int NP_MIN_CHUNK = 16384;   // smallest slice of a matrix given to one workgroup
 constexpr int ROW4 = 2 * W4;          // 32-bit words per N-pass partial row
-constexpr int T_WG = 64;              // table-phase workgroups per matrix (= wave size)
+constexpr int T_WG = 64;              // table-phase workgroups per matrix (a multiple of 64)
 constexpr int T_THREADS = 256;
+constexpr int T_KPT = NKEYS / (T_WG * T_THREADS);   // patterns per table-phase thread
 constexpr int KMAX = 16;
 constexpr int PSTRIDE = 32;           // floats per table-phase partial row (2 * KMAX)
 constexpr int MAXB = EDKM_LAUNCH_GROUP;   // matrices per launch

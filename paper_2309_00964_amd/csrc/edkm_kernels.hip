@@ -329,10 +329,19 @@ __device__ __forceinline__ void block_sum(const float (&v)[NV], float* scratch, 
 // Reduce rows [0, T_WG) of a partial block (T_WG x PSTRIDE floats) for columns
 // [c0, c0 + ncol) into out[0..ncol) (LDS), by wave reductions.  Called by all
 // threads of a T_THREADS block.
+// Rows lane, lane + 64, ... of one column, summed in that order (one lane per
+// 64 rows).
+__device__ __forceinline__ float tpart_rows(const float* part, int lane, int col) {
+    float x = part[lane * PSTRIDE + col];
+#pragma unroll
+    for (int q = 1; q < T_WG / 64; ++q) x += part[(lane + 64 * q) * PSTRIDE + col];
+    return x;
+}
+
 __device__ __forceinline__ void reduce_tparts(const float* part, int c0, int ncol, float* out) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     for (int j = wave; j < ncol; j += T_THREADS / 64) {
-        float s = wave_sum(part[lane * PSTRIDE + c0 + j]);
+        float s = wave_sum(tpart_rows(part, lane, c0 + j));
         if (lane == 0) out[j] = s;
     }
     __syncthreads();
@@ -343,7 +352,7 @@ __device__ __forceinline__ void reduce_tparts(const float* part, int c0, int nco
 __device__ __forceinline__ void reduce_tparts2(const float* pa, const float* pb, int ncol, float* out) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     for (int j = wave; j < 2 * ncol; j += T_THREADS / 64) {
-        const float x = j < ncol ? pa[lane * PSTRIDE + j] : pb[lane * PSTRIDE + ncol + (j - ncol)];
+        const float x = j < ncol ? tpart_rows(pa, lane, j) : tpart_rows(pb, lane, ncol + (j - ncol));
         const float s = wave_sum(x);
         if (lane == 0) out[j] = s;
     }
@@ -768,7 +777,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
 // ----------------------------------------------------------------------------
 // forward table phase
 
-// Table keys of a thread: 4 per thread over T_WG blocks x T_THREADS threads
+// Table keys of a thread: T_KPT per thread over T_WG blocks x T_THREADS threads
 // (= 65,536).  Kernels load everything the 4 patterns need first and compute
 // afterwards, so the loads overlap instead of forming a chain.
 __device__ __forceinline__ int table_key(int r) {
@@ -789,9 +798,9 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
     const int t = b.t;
     if (t > M.max_iter) return;
     // pattern counts do not depend on the centroids: issue their loads first
-    uint32_t n4[4];
+    uint32_t n4[T_KPT];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) n4[r] = ws.counts[table_key(r)];
+    for (int r = 0; r < T_KPT; ++r) n4[r] = ws.counts[table_key(r)];
     DevState* st = ws.st;
     const bool lead = blockIdx.x == 0;
     if (t == 1) {
@@ -829,7 +838,7 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
 #pragma unroll
     for (int j = 0; j < 2 * K; ++j) acc[j] = 0.f;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < T_KPT; ++r) {
         const int u = table_key(r);
         const uint32_t n = n4[r];
         if (n == 0u || !key_finite(u, M.fmt)) continue;
@@ -859,9 +868,9 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
     __shared__ float cT[K], cP[K];
     const MatArgs& M = b.m[blockIdx.y];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
-    uint32_t n4[4];   // independent of the centroids: loaded first
+    uint32_t n4[T_KPT];   // independent of the centroids: loaded first
 #pragma unroll
-    for (int r = 0; r < 4; ++r) n4[r] = ws.counts[table_key(r)];
+    for (int r = 0; r < T_KPT; ++r) n4[r] = ws.counts[table_key(r)];
     DevState* st = ws.st;
     const bool lead = blockIdx.x == 0;
     int T;
@@ -895,7 +904,7 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
 #pragma unroll
     for (int j = 0; j < K; ++j) { c1[j] = cT[j]; c0[j] = cP[j]; }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < T_KPT; ++r) {
         const int u = table_key(r);
         ws.G[u] = 0.f;
         const uint32_t n = n4[r];
@@ -1145,8 +1154,8 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
         const float* p1 = ws.bpart + (size_t)1 * T_WG * PSTRIDE;
         const float* p0 = ws.bpart;
         for (int j = 0; j < k; ++j) {
-            const float x = wave_sum(p1[threadIdx.x * PSTRIDE + j]);
-            const float e = wave_sum(p0[threadIdx.x * PSTRIDE + k + j]);
+            const float x = wave_sum(tpart_rows(p1, threadIdx.x, j));
+            const float e = wave_sum(tpart_rows(p0, threadIdx.x, k + j));
             if (threadIdx.x == 0) {
                 float gc = x * b.inv_tau;
                 if (T == 1) gc += e * b.inv_tau;
@@ -1381,10 +1390,10 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_top(BatchArgs b) {
     __shared__ float c1sh[K], c0sh[K];
     const MatArgs& M = b.m[blockIdx.y];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
-    uint32_t n4[4];   // per-pattern inputs first: they do not depend on the centroids
-    float G4[4];
+    uint32_t n4[T_KPT];   // per-pattern inputs first: they do not depend on the centroids
+    float G4[T_KPT];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < T_KPT; ++r) {
         const int u = table_key(r);
         n4[r] = ws.counts[u];
         G4[r] = ws.G[u];
@@ -1403,7 +1412,7 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_top(BatchArgs b) {
 #pragma unroll
     for (int j = 0; j < 2 * K; ++j) acc[j] = 0.f;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < T_KPT; ++r) {
         const int u = table_key(r);
         if (n4[r] == 0u || !key_finite(u, M.fmt)) continue;
         const float G = G4[r];
@@ -1441,10 +1450,10 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
     const int T = st->teff;
     const int t = b.t;
     if (t > T) return;
-    uint32_t n4[4];   // per-pattern inputs first: they do not depend on gamma
-    float R4[4], H4[4];
+    uint32_t n4[T_KPT];   // per-pattern inputs first: they do not depend on gamma
+    float R4[T_KPT], H4[T_KPT];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < T_KPT; ++r) {
         const int u = table_key(r);
         n4[r] = ws.counts[u];
         R4[r] = t != T ? ws.R[u] : 0.f;
@@ -1484,7 +1493,7 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
 #pragma unroll
     for (int j = 0; j < K; ++j) acc[j] = 0.f;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < T_KPT; ++r) {
         const int u = table_key(r);
         const uint32_t n = n4[r];
         if (n == 0u) continue;
@@ -1934,7 +1943,7 @@ static_assert(2 * W4 + 64 <= 2 * W8 * 2, "keyed sum: the 32-bit window and its s
 static_assert(MAGS == (NP_THREADS / 64) * 8 * 256, "window selection: 8 chunks of 256 magnitudes per wave");
 static_assert(fin_mags(FMT_FP16) % 4 == 0 && fin_mags(FMT_BF16) % 4 == 0,
               "window selection: a lane's 4 magnitudes are all finite or all not");
-static_assert(T_WG == 64, "table partial reduction uses one lane per workgroup");
-static_assert(T_WG * T_THREADS * 4 == NKEYS, "table blocks cover every pattern");
+static_assert(T_WG % 64 == 0, "table partial reduction: one lane per 64 workgroups");
+static_assert(T_WG * T_THREADS * T_KPT == NKEYS, "table blocks cover every pattern");
 
 }  // namespace edkm
