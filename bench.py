@@ -13,6 +13,7 @@ N-sized kernel (timed live with HIP events around its launches), and the CPU
 oracle timed on a bounded sample on this host.
 
 Weight format: --key-format fp16 (default) or bf16 (any workload).
+Cold-cache passes: --evict-between-calls (decoder layer; pass times only).
 
 Other workloads (--workload; one JSON line each, same fields):
   mlp_outliers [--bits 3|4]   the 11008x4096 MLP matrix with 0.1% outliers; the
@@ -226,7 +227,7 @@ class Matrices:
     with its own plan and centroids."""
 
     def __init__(self, config, mats, bits, outliers=False, on_device=False, keep_host=(), fmt="fp16",
-                 out_half=False):
+                 out_half=False, evict=False):
         import numpy as np
         import torch
         from paper_2309_00964_amd import edkm, inputs
@@ -266,14 +267,26 @@ class Matrices:
             self.gc.append(torch.empty(k, device=dev))
         self.fmt = fmt
         self.out_half = out_half
+        self.evict_buf = torch.ones(1 << 28, device="cuda") if evict else None
+        self.evict_sink = torch.zeros((), device="cuda")
         torch.cuda.synchronize()
 
     def step(self):
         from paper_2309_00964_amd import edkm, inputs
         edkm.init_unique_batch(self.plans, self.keys)
+        self.evict()
         edkm.forward_batch(self.plans, self.keys, inputs.TAU, 0.0, self.c_in, self.c_out, self.wt,
                            self.out_half, self.iters)
+        self.evict()
         edkm.backward_batch(self.plans, self.keys, self.grads, self.gw, self.gc)
+        self.evict()
+
+    def evict(self):
+        """With an eviction buffer: read 1 GiB between calls, so that no call
+        finds the previous call's data in the 256 MB Infinity Cache (as when a
+        model's own work runs between them)."""
+        if self.evict_buf is not None:
+            self.evict_sink += self.evict_buf.sum()
 
     def dense_step(self):
         from paper_2309_00964_amd import edkm, inputs
@@ -317,11 +330,17 @@ def bench_decoder_layer(args):
     bits = 3
     keep = () if args.no_cpu_baseline else tuple(args.cpu_sample)
     half = args.w_tilde == "half"
-    m = Matrices(4, inputs.WORKLOADS[4]["mats"], bits, keep_host=keep, fmt=args.key_format, out_half=half)
+    m = Matrices(4, inputs.WORKLOADS[4]["mats"], bits, keep_host=keep, fmt=args.key_format, out_half=half,
+                 evict=args.evict_between_calls)
     elapsed, avg = timed(m.step, m.plans[0], PASS_IDS, args.steps, args.warmup)
-    out = result_line(args, "llama7b_decoder_layer_3bit" + _fmt_tag(args) + ("_half_wtilde" if half else ""),
-                      m, bits, elapsed, hbm_roofline(avg, m.total, half),
-                      {"w_tilde": m.fmt if half else "fp32"})
+    extra = {"w_tilde": m.fmt if half else "fp32"}
+    if args.evict_between_calls:
+        # the step time then includes three 1 GiB eviction reads; the pass
+        # times (roofline) are the figures this mode is for
+        extra["evict_between_calls"] = True
+    out = result_line(args, "llama7b_decoder_layer_3bit" + _fmt_tag(args) + ("_half_wtilde" if half else "")
+                      + ("_evicted" if args.evict_between_calls else ""),
+                      m, bits, elapsed, hbm_roofline(avg, m.total, half), extra)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(m.host, 1 << bits, fmt=m.fmt)
     return out
@@ -510,6 +529,9 @@ def main():
     ap.add_argument("--w-tilde", choices=("fp32", "half"), default="fp32",
                     help="decoder_layer: W~ output as fp32 (default, 24 B per weight) or in the "
                          "16-bit weight format (22 B per weight)")
+    ap.add_argument("--evict-between-calls", action="store_true",
+                    help="decoder layer: read 1 GiB between init_unique, forward and backward, so that "
+                         "no call finds its predecessor's data in the Infinity Cache (pass times only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", nargs="+", default=[m[0] for m in LLAMA7B_LAYER],
                     help="matrices of the layer the CPU oracle is timed on (default: all seven)")
