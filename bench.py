@@ -541,7 +541,7 @@ def main():
     if args.pmc_summary:
         return pmc_summary(*args.pmc_summary)
     if args.gpus != 1:
-        sys.exit("bench.py runs on one GPU: this build has no multi-GPU path (--gpus %d asked)"
+        sys.exit("bench.py runs on one GPU: the library has no multi-GPU path (--gpus %d asked)"
                  % args.gpus)
     if args.copy_calibration:
         return copy_calibration()
