@@ -13,11 +13,18 @@ N-sized kernel (timed live with HIP events around its launches), and the CPU
 oracle timed on a bounded sample on this host.
 
 Weight format: --key-format fp16 (default) or bf16 (any workload).
-Cold-cache passes: --evict-between-calls (decoder layer; pass times only).
+Cold-cache passes only: --evict-between-calls (decoder layer; pass times only).
+
+The per-pass times are measured twice: back to back (the line's roofline) and
+with the Infinity Cache evicted between the three calls
+(roofline.evicted_between_calls; --no-evicted-passes skips it).
 
 Other workloads (--workload; one JSON line each, same fields):
-  mlp_outliers [--bits 3|4]   the 11008x4096 MLP matrix with 0.1% outliers; the
-                              dense per-weight-map path is timed beside it ("dense")
+  single_256x256 [--bits]     one 256x256 matrix (65,536 weights; launch-bound)
+  attn_proj_4096x4096 [--bits]  one 4096x4096 attention projection (16.8M weights)
+  mlp_outliers [--bits 3|4]   the 11008x4096 MLP matrix with 0.1% outliers
+                              (single-matrix workloads: the dense per-weight-map
+                              path is timed beside the uniquified one, "dense")
   stack [--bits 2|3|4]        32 decoder layers (224 matrices, 6.48e9 weights,
                               drawn on the GPU), one step over every matrix
   palettize [--bits 1..4]     export of the decoder layer after a clustering step:
@@ -37,6 +44,7 @@ import hashlib
 import json
 import os
 import re
+import statistics
 import sys
 import time
 
@@ -103,48 +111,80 @@ class HipEvents:
         self.lib.hipEventDestroy(e)
 
 
-def cpu_baseline(samples, k, table_names=("q_proj", "gate_proj", "w", "L0.q_proj"), fmt="fp16"):
+def cpu_model():
+    """The host CPU's model name (Linux /proc/cpuinfo), or the platform's."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or platform.machine()
+
+
+def _repeat_until(fn, min_s):
+    """Run fn() at least once and until min_s seconds have passed; (runs, seconds)."""
+    runs = 0
+    t0 = time.perf_counter()
+    while True:
+        fn()
+        runs += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_s:
+            return runs, dt
+
+
+def cpu_baseline(samples, k, table_names=("q_proj", "gate_proj", "w", "L0.q_proj"), fmt="fp16",
+                 min_s=3.0):
     """The fp64 oracles, as they stand, on bounded samples of the workload:
     ``samples`` is a list of (name, keys, c0, g) host arrays.  The headline
-    value is the dense oracle on all host threads over every sample; beside it
-    the same on one thread (first 2^20 weights of the first sample) and the
-    table-form oracle (numpy) on the samples named in ``table_names``."""
+    value is the dense oracle on all host threads over every sample (repeated
+    until ``min_s`` seconds have passed, for samples too small to time once);
+    beside it the same on one thread (first 2^20 weights of the first sample)
+    and the table-form oracle (numpy) on the samples named in ``table_names``."""
     import numpy as np
     from oracle import dense, table
     from paper_2309_00964_amd import inputs
-    n = 0
-    t0 = time.perf_counter()
-    for _, keys, c0, g in samples:
-        f = dense.forward(keys, c0.astype("float64"), inputs.TAU, inputs.ITERS, fmt=fmt)
-        dense.backward(keys, f, g.astype("float64"))
-        n += keys.size
-    dt = time.perf_counter() - t0
+
+    def dense_all():
+        for _, keys, c0, g in samples:
+            f = dense.forward(keys, c0.astype("float64"), inputs.TAU, inputs.ITERS, fmt=fmt)
+            dense.backward(keys, f, g.astype("float64"))
+    n1 = sum(x[1].size for x in samples)
+    runs, dt = _repeat_until(dense_all, min_s)
+    n = n1 * runs
     out = {"value": n / dt, "unit": "weights/s", "cores": dense.threads(), "kind": "oracle",
-           "sample": "fp64 dense DKM forward+backward (%d iterations, k=%d) of %s (%d weights) "
-                     "in %.1f s" % (inputs.ITERS, k, "+".join(s[0] for s in samples), n, dt)}
+           "cpu_model": cpu_model(), "logical_cpus": os.cpu_count(),
+           "sample": "fp64 dense DKM forward+backward (%d iterations, k=%d) of %s (%d weights)%s "
+                     "in %.1f s" % (inputs.ITERS, k, "+".join(s[0] for s in samples), n1,
+                                    " x %d runs" % runs if runs > 1 else "", dt)}
     name, keys, c0, g = samples[0]
     m = min(keys.size, 1 << 20)
     nth = dense.threads()
     dense.set_threads(1)
-    t0 = time.perf_counter()
-    f = dense.forward(keys[:m], c0.astype("float64"), inputs.TAU, inputs.ITERS, fmt=fmt)
-    dense.backward(keys[:m], f, g[:m].astype("float64"))
-    dt1 = time.perf_counter() - t0
+
+    def dense_one():
+        f = dense.forward(keys[:m], c0.astype("float64"), inputs.TAU, inputs.ITERS, fmt=fmt)
+        dense.backward(keys[:m], f, g[:m].astype("float64"))
+    runs1, dt1 = _repeat_until(dense_one, min(min_s, 1.0))
     dense.set_threads(nth)
-    out["single_thread"] = {"value": m / dt1, "unit": "weights/s", "cores": 1,
-                            "sample": "the same oracle on the first %d weights of %s in %.1f s"
-                                      % (m, name, dt1)}
+    out["single_thread"] = {"value": m * runs1 / dt1, "unit": "weights/s", "cores": 1,
+                            "sample": "the same oracle on the first %d weights of %s%s in %.1f s"
+                                      % (m, name, " x %d runs" % runs1 if runs1 > 1 else "", dt1)}
     tab = [x for x in samples if x[0] in table_names] or samples[:1]
-    nt = 0
-    t0 = time.perf_counter()
-    for _, keys, c0, g in tab:
-        f = table.forward(keys, c0.astype(np.float64), inputs.TAU, inputs.ITERS, fmt=fmt)
-        table.backward(keys, f, g.astype(np.float64))
-        nt += keys.size
-    dt2 = time.perf_counter() - t0
-    out["table_form"] = {"value": nt / dt2, "unit": "weights/s", "kind": "oracle (table form, numpy)",
-                         "sample": "fp64 uniquified DKM forward+backward of %s (%d weights) in %.1f s"
-                                   % ("+".join(x[0] for x in tab), nt, dt2)}
+
+    def table_all():
+        for _, keys, c0, g in tab:
+            f = table.forward(keys, c0.astype(np.float64), inputs.TAU, inputs.ITERS, fmt=fmt)
+            table.backward(keys, f, g.astype(np.float64))
+    nt1 = sum(x[1].size for x in tab)
+    runs2, dt2 = _repeat_until(table_all, min(min_s, 1.0))
+    out["table_form"] = {"value": nt1 * runs2 / dt2, "unit": "weights/s", "kind": "oracle (table form, numpy)",
+                         "sample": "fp64 uniquified DKM forward+backward of %s (%d weights)%s in %.1f s"
+                                   % ("+".join(x[0] for x in tab), nt1,
+                                      " x %d runs" % runs2 if runs2 > 1 else "", dt2)}
     return out
 
 
@@ -154,7 +194,8 @@ def timed(step, plan, pass_ids, steps, warmup):
     time), then with the library recording per-pass events on `plan` around
     each timed pass (the per-launch kernel times of the roofline).  The event
     records add a few microseconds per pass, so they stay out of the step time.
-    Returns (seconds for `steps` steps, {pass: average launch ms})."""
+    Returns (seconds for `steps` steps, {pass: average launch ms},
+    {pass: median launch ms})."""
     import torch
     from paper_2309_00964_amd import edkm
     for _ in range(warmup):
@@ -180,18 +221,24 @@ def timed(step, plan, pass_ids, steps, warmup):
     torch.cuda.synchronize()
     for pid in pass_ids.values():
         edkm.plan_set_pass_events(plan, pid, None, None)
-    avg = {p: sum(hip.elapsed_ms(a, b) for a, b in ev[p]) / steps for p in pass_ids}
+    per = {p: [hip.elapsed_ms(a, b) for a, b in ev[p]] for p in pass_ids}
+    avg = {p: sum(v) / steps for p, v in per.items()}
+    med = {p: statistics.median(v) for p, v in per.items()}
     for e in [t_start, t_stop] + [x for p in ev for pair in ev[p] for x in pair]:
         hip.destroy(e)
-    return max(wall, gpu_s), avg
+    return max(wall, gpu_s), avg, med
 
 
-def hbm_roofline(avg_ms, total, out_half=False):
-    """Roofline of the dominant N-sized pass (HBM-bound) plus all passes."""
+def hbm_roofline(avg_ms, total, out_half=False, med_ms=None):
+    """Roofline of the dominant N-sized pass (HBM-bound) plus all passes:
+    achieved from the average launch time (as the kernel trace reports it),
+    the median beside it."""
     passes = {}
     for p, ms in avg_ms.items():
         nbytes = (4 if out_half and p == "k_gather_wt" else PASS_BYTES[p]) * total
         passes[p] = {"avg_us": ms * 1000.0, "bytes": nbytes, "GBps": nbytes / (ms * 1e-3) / 1e9}
+        if med_ms:
+            passes[p]["median_us"] = med_ms[p] * 1000.0
     dom = max(passes, key=lambda p: passes[p]["avg_us"])
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
@@ -204,7 +251,8 @@ def hbm_roofline(avg_ms, total, out_half=False):
             "unit": "GB/s", "frac": passes[dom]["GBps"] / PEAK_HBM_GBS, "traffic": traffic,
             "n_pass_total_GBps": n_bytes_all / t_all / 1e9,
             "n_pass_total_frac": n_bytes_all / t_all / 1e9 / PEAK_HBM_GBS,
-            "passes": {p: {"avg_us": round(v["avg_us"], 2), "GBps": round(v["GBps"], 1)}
+            "passes": {p: dict({"avg_us": round(v["avg_us"], 2), "GBps": round(v["GBps"], 1)},
+                               **({"median_us": round(v["median_us"], 2)} if "median_us" in v else {}))
                        for p, v in passes.items()}}
 
 
@@ -269,6 +317,7 @@ class Matrices:
         self.out_half = out_half
         self.evict_buf = torch.ones(1 << 28, device="cuda") if evict else None
         self.evict_sink = torch.zeros((), device="cuda")
+        self.evicting = evict
         torch.cuda.synchronize()
 
     def step(self):
@@ -285,7 +334,7 @@ class Matrices:
         """With an eviction buffer: read 1 GiB between calls, so that no call
         finds the previous call's data in the 256 MB Infinity Cache (as when a
         model's own work runs between them)."""
-        if self.evict_buf is not None:
+        if self.evict_buf is not None and self.evicting:
             self.evict_sink += self.evict_buf.sum()
 
     def dense_step(self):
@@ -325,39 +374,64 @@ def result_line(args, workload, m, bits, elapsed, roof, extra_cfg=None):
 
 
 def bench_decoder_layer(args):
-    """One LLaMA-7B decoder layer at 3 bits: the seven matrices as batched calls."""
+    """One LLaMA-7B decoder layer at 3 bits: the seven matrices as batched calls.
+
+    The step runs init_unique, forward and backward back to back, so a pass
+    can find the tail of what the previous call read in the Infinity Cache.
+    Unless --no-evicted-passes is given, the per-pass times are measured a
+    second time with 1 GiB read between the three calls (no call then finds
+    its predecessor's data, as when a model's own work runs in between) and
+    reported beside the back-to-back figures in roofline.evicted_between_calls."""
     from paper_2309_00964_amd import inputs
     bits = 3
     keep = () if args.no_cpu_baseline else tuple(args.cpu_sample)
     half = args.w_tilde == "half"
+    want_evicted = args.evict_between_calls or not args.no_evicted_passes
     m = Matrices(4, inputs.WORKLOADS[4]["mats"], bits, keep_host=keep, fmt=args.key_format, out_half=half,
-                 evict=args.evict_between_calls)
-    elapsed, avg = timed(m.step, m.plans[0], PASS_IDS, args.steps, args.warmup)
+                 evict=want_evicted)
+    m.evicting = args.evict_between_calls
+    elapsed, avg, med = timed(m.step, m.plans[0], PASS_IDS, args.steps, args.warmup)
     extra = {"w_tilde": m.fmt if half else "fp32"}
     if args.evict_between_calls:
         # the step time then includes three 1 GiB eviction reads; the pass
         # times (roofline) are the figures this mode is for
         extra["evict_between_calls"] = True
+    roof = hbm_roofline(avg, m.total, half, med)
+    if want_evicted and not args.evict_between_calls:
+        m.evicting = True
+        _, eavg, emed = timed(m.step, m.plans[0], PASS_IDS, args.steps, 1)
+        m.evicting = False
+        ev = hbm_roofline(eavg, m.total, half, emed)
+        roof["evicted_between_calls"] = {
+            "kernel": ev["kernel"], "achieved": ev["achieved"], "frac": ev["frac"],
+            "n_pass_total_GBps": ev["n_pass_total_GBps"], "n_pass_total_frac": ev["n_pass_total_frac"],
+            "passes": ev["passes"],
+            "note": "same passes with 1 GiB read between init_unique, forward and backward "
+                    "(no Infinity Cache reuse across calls); the gradient gather keeps the "
+                    "reuse inside the backward"}
     out = result_line(args, "llama7b_decoder_layer_3bit" + _fmt_tag(args) + ("_half_wtilde" if half else "")
                       + ("_evicted" if args.evict_between_calls else ""),
-                      m, bits, elapsed, hbm_roofline(avg, m.total, half), extra)
+                      m, bits, elapsed, roof, extra)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(m.host, 1 << bits, fmt=m.fmt)
     return out
 
 
-def bench_mlp_outliers(args):
-    """The 11008x4096 MLP matrix with 0.1% outliers: the uniquified path, and the
-    dense (per-weight map) path timed beside it on the same inputs."""
+def bench_single_matrix(args, cfg, default_bits):
+    """One matrix of the synthetic workloads: 256x256 (config 1), 4096x4096
+    (config 2, an attention projection) or 11008x4096 with 0.1% outliers
+    (config 3, an MLP matrix).  The uniquified path is the line; the dense
+    (per-weight map) path is timed beside it on the same inputs."""
     from paper_2309_00964_amd import inputs
-    bits = args.bits or 4
-    w = inputs.WORKLOADS[3]
+    bits = args.bits or default_bits
+    w = inputs.WORKLOADS[cfg]
     keep = () if args.no_cpu_baseline else ("w",)
-    m = Matrices(3, w["mats"], bits, outliers=True, keep_host=keep, fmt=args.key_format)
-    elapsed, avg = timed(m.step, m.plans[0], PASS_IDS, args.steps, args.warmup)
-    out = result_line(args, "llama7b_mlp_11008x4096_outliers_%dbit%s" % (bits, _fmt_tag(args)), m, bits, elapsed,
-                      hbm_roofline(avg, m.total), {"outliers": inputs.OUTLIER_P})
-    d_el, d_avg = timed(m.dense_step, m.plans[0], DENSE_PASS_IDS, args.steps, args.warmup)
+    m = Matrices(cfg, w["mats"], bits, outliers=w["outliers"], keep_host=keep, fmt=args.key_format)
+    elapsed, avg, med = timed(m.step, m.plans[0], PASS_IDS, args.steps, args.warmup)
+    name = "%s_%dbit%s" % (SINGLE_NAMES[cfg], bits, _fmt_tag(args))
+    extra = {"outliers": inputs.OUTLIER_P} if w["outliers"] else {}
+    out = result_line(args, name, m, bits, elapsed, hbm_roofline(avg, m.total, med_ms=med), extra)
+    d_el, d_avg, _ = timed(m.dense_step, m.plans[0], DENSE_PASS_IDS, args.steps, args.warmup)
     out["dense"] = {"value": m.total * args.steps / d_el, "unit": "weights/s",
                     "ms_per_step": d_el * 1000.0 / args.steps,
                     "unique_speedup": d_el / elapsed,
@@ -365,6 +439,14 @@ def bench_mlp_outliers(args):
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(m.host, 1 << bits, fmt=m.fmt)
     return out
+
+
+SINGLE_NAMES = {1: "single_256x256", 2: "attn_proj_4096x4096", 3: "llama7b_mlp_11008x4096_outliers"}
+
+
+def bench_mlp_outliers(args):
+    """The 11008x4096 MLP matrix with 0.1% outliers (4 bits unless --bits 3)."""
+    return bench_single_matrix(args, 3, 4)
 
 
 def bench_palettize(args):
@@ -382,7 +464,7 @@ def bench_palettize(args):
 
     def step():
         edkm.palettize_batch(m.plans, m.keys, m.c_out, outs)
-    elapsed, avg = timed(step, m.plans[0], {"k_palettize": edkm.PASS_PALETTIZE}, args.steps, args.warmup)
+    elapsed, avg, _ = timed(step, m.plans[0], {"k_palettize": edkm.PASS_PALETTIZE}, args.steps, args.warmup)
     per_w = 2.0 + bits / 8.0
     kern_s = avg["k_palettize"] / 1000.0
     achieved = per_w * m.total / kern_s / 1e9
@@ -409,7 +491,7 @@ def bench_unique_inverse(args):
 
     def step():
         edkm.unique_inverse_batch(m.plans, m.keys, uniq, inv)
-    elapsed, avg = timed(step, m.plans[0], {"k_inverse": edkm.PASS_INVERSE}, args.steps, args.warmup)
+    elapsed, avg, _ = timed(step, m.plans[0], {"k_inverse": edkm.PASS_INVERSE}, args.steps, args.warmup)
     per_w = 4.0
     kern_s = avg["k_inverse"] / 1000.0
     achieved = per_w * m.total / kern_s / 1e9
@@ -426,14 +508,15 @@ def bench_stack(args):
     from paper_2309_00964_amd import inputs
     bits = args.bits or 3
     w = inputs.WORKLOADS[5]
-    keep = () if args.no_cpu_baseline else ("L0.q_proj",)
+    # the CPU oracle's rate on two of the 32 layers (14 matrices, 405M weights)
+    keep = () if args.no_cpu_baseline else tuple(n for n, _, _ in w["mats"] if n.split(".")[0] in ("L0", "L1"))
     m = Matrices(5, w["mats"], bits, on_device=True, keep_host=keep, fmt=args.key_format)
-    elapsed, avg = timed(m.step, m.plans[0], PASS_IDS, args.steps, args.warmup)
+    elapsed, avg, med = timed(m.step, m.plans[0], PASS_IDS, args.steps, args.warmup)
     # the pass events bracket the first launch group of each step: its first
     # LAUNCH_GROUP matrices (layers 0-3)
     from paper_2309_00964_amd import edkm
     group = edkm.LAUNCH_GROUP
-    roof = hbm_roofline(avg, sum(r * c for _, r, c in w["mats"][:group]))
+    roof = hbm_roofline(avg, sum(r * c for _, r, c in w["mats"][:group]), med_ms=med)
     roof["note"] = "pass events cover the first launch group (%d matrices) of each step" % group
     out = result_line(args, "llama7b_32_layer_stack_%dbit%s" % (bits, _fmt_tag(args)), m, bits, elapsed, roof)
     if not args.no_cpu_baseline:
@@ -518,8 +601,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", choices=("decoder_layer", "mlp_outliers", "stack", "palettize",
-                                           "unique_inverse"),
+    ap.add_argument("--workload", choices=("decoder_layer", "single_256x256", "attn_proj_4096x4096",
+                                           "mlp_outliers", "stack", "palettize", "unique_inverse"),
                     default="decoder_layer")
     ap.add_argument("--bits", type=int, choices=(1, 2, 3, 4), default=None,
                     help="mlp_outliers: 3 or 4 (default 4); stack: 2, 3 or 4 (default 3); "
@@ -532,6 +615,9 @@ def main():
     ap.add_argument("--evict-between-calls", action="store_true",
                     help="decoder layer: read 1 GiB between init_unique, forward and backward, so that "
                          "no call finds its predecessor's data in the Infinity Cache (pass times only)")
+    ap.add_argument("--no-evicted-passes", action="store_true",
+                    help="decoder layer: skip the second per-pass measurement with the Infinity Cache "
+                         "evicted between the calls")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", nargs="+", default=[m[0] for m in LLAMA7B_LAYER],
                     help="matrices of the layer the CPU oracle is timed on (default: all seven)")
@@ -549,6 +635,8 @@ def main():
     if not torch.cuda.is_available():
         sys.exit("bench.py needs a GPU")
     fn = {"decoder_layer": bench_decoder_layer, "mlp_outliers": bench_mlp_outliers,
+          "single_256x256": lambda a: bench_single_matrix(a, 1, 3),
+          "attn_proj_4096x4096": lambda a: bench_single_matrix(a, 2, 3),
           "stack": bench_stack, "palettize": bench_palettize,
           "unique_inverse": bench_unique_inverse}[args.workload]
     if args.workload == "decoder_layer" and args.bits not in (None, 3):

@@ -52,6 +52,11 @@
 
 #include <stddef.h>
 #include <stdint.h>
+/* The HIP runtime header wants the platform named when a plain C or C++
+ * compiler (not hipcc) includes it; this library exists for AMD GPUs only. */
+#ifndef __HIP_PLATFORM_AMD__
+#define __HIP_PLATFORM_AMD__ 1
+#endif
 #include <hip/hip_runtime_api.h>
 
 #ifdef __cplusplus
@@ -75,7 +80,8 @@ enum {
 };
 
 /* Host-side per-matrix record.  Opaque; the caller owns the memory (stack or
- * heap) and must not copy it between calls. */
+ * heap) and must not copy it between calls: the record knows its own address,
+ * and a copy is refused (EDKM_ERR_ARG) by every call but edkm_plan_init. */
 typedef struct edkm_plan {
     uint64_t opaque[32];
 } edkm_plan;

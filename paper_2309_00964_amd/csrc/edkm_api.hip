@@ -20,6 +20,7 @@ enum Stage : int32_t { PLANNED = 1, COUNTED = 2, FORWARD = 3, DENSE_FORWARD = 4 
 
 struct PlanImpl {
     uint64_t magic;
+    const void* self;        // the record's own address: a copied record is refused
     uint64_t n;
     int32_t bits, k, max_iter, stage;
     int32_t fmt;             // FMT_FP16 or FMT_BF16
@@ -47,7 +48,8 @@ inline PlanImpl* impl(edkm_plan* p) { return reinterpret_cast<PlanImpl*>(p); }
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 bool plan_ok(const edkm_plan* p) {
-    return p && reinterpret_cast<const PlanImpl*>(p)->magic == PLAN_MAGIC;
+    return p && reinterpret_cast<const PlanImpl*>(p)->magic == PLAN_MAGIC &&
+           reinterpret_cast<const PlanImpl*>(p)->self == p;
 }
 
 // Workgroups one N-sized pass may use: one per compute unit of the current
@@ -177,6 +179,7 @@ edkm_status edkm_plan_init_ex(edkm_plan* plan, uint64_t n, int bits, int max_ite
     P->ws = ws;
     P->ws_bytes = ws_bytes;
     P->stage = PLANNED;
+    P->self = plan;
     P->magic = PLAN_MAGIC;
     return EDKM_OK;
 }

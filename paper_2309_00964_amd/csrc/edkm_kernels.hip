@@ -665,17 +665,17 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
     constexpr int NCH = SPAN / 256;
     __shared__ __align__(16) uint32_t pre[MAGS];   // weights with finite magnitude in [2048 w, x], w = x / 2048
     __shared__ uint32_t woff[NW + 1];     // weights with finite magnitude < 2048 w
-    __shared__ int red[4];                // lo, hi, occupied patterns, non-finite
+    __shared__ int wred[4][NW];           // per wave: lo, hi, occupied patterns, non-finite
+    __shared__ unsigned long long wsq[NW];
+    __shared__ int red[4];                // the block's: lo, hi, occupied patterns, non-finite
     __shared__ unsigned long long sqsum, best[2];
     const MatArgs& M = b.m[blockIdx.y];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const int fin = fin_mags(M.fmt);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int mw = wave * SPAN + 4 * lane;   // this lane's first magnitude; chunk j adds 256 j
-    if (threadIdx.x == 0) {
-        red[0] = 1 << 30; red[1] = -1; red[2] = 0; red[3] = 0;
-        sqsum = 0ull; best[0] = 0ull; best[1] = 0ull;
-    }
+    // best[] is first used after two barriers below
+    if (threadIdx.x == 0) { best[0] = 0ull; best[1] = 0ull; }
     uint4 p[NCH], q[NCH];
     {
         const uint4* p4 = reinterpret_cast<const uint4*>(ws.counts + mw);
@@ -720,18 +720,31 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
     nu = wave_reduce(nu, 0, op_add);
     nf = wave_reduce(nf, 0, op_or);
     sq = wave_sum_u64(sq);
+    // each wave's results go to slots of its own; one thread combines them after
+    // the barrier (no LDS word is written by two waves)
     if (lane == 0) {
         woff[wave + 1] = carry;
-        atomicMin(&red[0], lo);
-        atomicMax(&red[1], hi);
-        atomicAdd(&red[2], nu);
-        atomicOr(&red[3], nf);
-        atomicAdd(&sqsum, sq);
+        wred[0][wave] = lo;
+        wred[1][wave] = hi;
+        wred[2][wave] = nu;
+        wred[3][wave] = nf;
+        wsq[wave] = sq;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
         woff[0] = 0u;
-        for (int w = 1; w <= NW; ++w) woff[w] += woff[w - 1];
+        int r0 = 1 << 30, r1 = -1, r2 = 0, r3 = 0;
+        unsigned long long q = 0ull;
+        for (int w = 0; w < NW; ++w) {
+            woff[w + 1] += woff[w];
+            r0 = min(r0, wred[0][w]);
+            r1 = max(r1, wred[1][w]);
+            r2 += wred[2][w];
+            r3 |= wred[3][w];
+            q += wsq[w];
+        }
+        red[0] = r0; red[1] = r1; red[2] = r2; red[3] = r3;
+        sqsum = q;
     }
     __syncthreads();
     const int mlo = red[0], mhi = red[1];

@@ -109,6 +109,18 @@ def quantile_init(keys: np.ndarray, k: int, fmt: str = "fp16") -> np.ndarray:
     return part[ranks].astype(np.float32)
 
 
+def two_cluster_weights(n_bulk: int, n_far: int, far_mean: float, far_sigma: float, seed: int,
+                        bulk_sigma: float = 0.01) -> np.ndarray:
+    """n_bulk fp32 draws from N(0, bulk_sigma^2) followed by n_far draws from
+    N(far_mean, far_sigma^2), rounded to fp16 (raw bit patterns, uint16).  A
+    small far group next to a bulk lets a centroid be empty in one iteration
+    and occupied in the next."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    w = np.concatenate([rng.standard_normal(n_bulk) * bulk_sigma,
+                        far_mean + rng.standard_normal(n_far) * far_sigma])
+    return w.astype(np.float32).astype(np.float16).view(np.uint16)
+
+
 def upstream_grad(n: int, seed: int) -> np.ndarray:
     """dL/dW~ ~ N(0, 1), fp32."""
     rng = np.random.Generator(np.random.PCG64(seed))

@@ -10,6 +10,8 @@ oracle value rounded to fp16.
 """
 import numpy as np
 
+from paper_2309_00964_amd import inputs
+
 TOL_FWD = 1e-4
 TOL_BWD = 1e-3
 
@@ -59,3 +61,21 @@ def assert_bf16_within_ulp(x_bits, ref, what="bf16 W~"):
     x = _bf16_values(x_bits)
     bad = ~(np.abs(x - rv) <= ulp)
     assert not np.any(bad), "%s: %d entries beyond one ulp" % (what, int(bad.sum()))
+
+
+# A centroid that is empty at t = 1 and occupied at t = 2: 2,000 weights near 0
+# and 20 near 1.005, C^(0) = (0.9, 2.0), tau = 1e-3.  At t = 1 every weight is at
+# least 0.89 / tau = 890 e-foldings closer to 0.9 than to 2.0, so the second
+# column of the map underflows to exactly 0 (fp64 and fp32 alike) and C^(1)_2 =
+# C^(0)_2 = 2.0.  C^(1)_1 is then the mean, near 0.01, which puts the midpoint of
+# the two centroids inside the far group: at t = 2 both centroids share it.  The
+# whole gradient dL/dC^(1)_2 reaches C^(0)_2 through the kept value.
+EMPTY_THEN_LIVE = dict(n_bulk=2000, n_far=20, far_mean=1.005, far_sigma=0.004, seed=2,
+                       c0=(0.9, 2.0), tau=1e-3, T=2)
+
+
+def empty_then_live_inputs():
+    e = EMPTY_THEN_LIVE
+    keys = inputs.two_cluster_weights(e["n_bulk"], e["n_far"], e["far_mean"], e["far_sigma"], e["seed"])
+    g = inputs.upstream_grad(keys.size, e["seed"] + 1).astype(np.float64)
+    return keys, np.array(e["c0"], np.float64), g

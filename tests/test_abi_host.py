@@ -277,3 +277,23 @@ def test_plan_init_ex_key_formats():
 def test_plan_record_size_matches_header():
     m = re.search(r"uint64_t\s+opaque\[(\d+)\]", open(HEADER).read())
     assert m and ctypes.sizeof(edkm.edkm_plan) == 8 * int(m.group(1))
+
+
+def test_plain_c_consumer_compiles_and_gets_host_errors(tmp_path):
+    """tests/abi_consumer.c, a plain C program, compiles with gcc against
+    include/edkm.h alone (no platform define on the command line), links the
+    built library and sees the documented host-side errors, a copied plan
+    record included."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not available")
+    libdir = os.path.dirname(os.path.abspath(edkm._lib._name))
+    exe = str(tmp_path / "abi_consumer")
+    subprocess.check_call([gcc, "-std=c99", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"),
+                           "-I", "/opt/rocm/include", os.path.join(ROOT, "tests", "abi_consumer.c"),
+                           "-L", libdir, "-ledkm", "-Wl,-rpath," + libdir, "-o", exe])
+    out = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    assert out.returncode == 0, out.stdout + out.stderr
+    assert out.stdout.strip() == "ok"

@@ -19,8 +19,9 @@ torch = pytest.importorskip("torch")
 from oracle import dense, table                                  # noqa: E402
 from paper_2309_00964_amd import edkm, inputs                     # noqa: E402
 from paper_2309_00964_amd.runner import run                       # noqa: E402
-from parity_util import (TOL_BWD, TOL_FWD, assert_bf16_within_ulp,  # noqa: E402
-                         assert_close, assert_fp16_within_ulp)
+from parity_util import (EMPTY_THEN_LIVE, TOL_BWD, TOL_FWD,  # noqa: E402
+                         assert_bf16_within_ulp, assert_close, assert_fp16_within_ulp,
+                         empty_then_live_inputs)
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -402,6 +403,22 @@ def test_empty_cluster_keeps_centroid():
         check(res, ref, what="empty cluster dense=%s" % dense_path)
 
 
+@pytest.mark.parametrize("dense_path", [False, True])
+def test_empty_then_live_cluster(dense_path):
+    """A centroid that is empty at t = 1 (its attention underflows for every
+    weight, in fp32 as in fp64) and occupied at t = 2: it keeps its value, and
+    dL/dC^(0) for it is the whole gradient that reaches C^(1) through the kept
+    value (about -325 here, where dropping the identity gradient would give 0).
+    Both the uniquified and the dense path against the oracle."""
+    keys, c0, g = empty_then_live_inputs()
+    e = EMPTY_THEN_LIVE
+    say("empty then live", "dense" if dense_path else "unique")
+    res = gpu(keys, c0, 1, g=g, tau=e["tau"], iters=e["T"], dense=dense_path)
+    ref = oracle(keys, c0, g, tau=e["tau"], iters=e["T"])
+    assert ref["s_hist"][1, 1] == 0.0 and ref["s_hist"][2, 1] > 1.0 and abs(ref["gc"][1]) > 100.0
+    check(res, ref, what="empty then live")
+
+
 def test_forward_repeatable_and_exact_scaling():
     """Forward results are bitwise repeatable.  Scaling w, C^(0) and tau by 2 scales
     C and W~ by 2: bitwise on the dense path (same reduction order), and to
@@ -652,6 +669,23 @@ def test_full_size_matrix(cfg, bits, fmt):
     res = gpu(keys, c0, bits, g=g, want_counts=True, key_format=fmt)
     assert np.array_equal(res["counts"].view(np.uint32), table.histogram(keys))
     check(res, oracle(keys, c0, g, form="table", fmt=fmt), what="cfg%d bits=%d %s" % (cfg, bits, fmt))
+
+
+@pytest.mark.parametrize("cfg,bits", [(2, 3), (3, 3), (3, 4)])
+def test_full_size_dense_path(cfg, bits):
+    """The dense comparison path at the sizes the benchmark times it (4096x4096,
+    and 11008x4096 with outliers at 3 and 4 bits): 1,024 workgroups of up to
+    44,032 weights each, every partial row summed by the one-block finishing
+    kernels.  Against the table-form oracle (pinned to the dense one)."""
+    w = inputs.WORKLOADS[cfg]
+    _, r, c = w["mats"][0]
+    n = r * c
+    keys = inputs.fp16_weights(n, inputs.weight_seed(cfg, 0), w["outliers"])
+    c0 = inputs.quantile_init(keys, 1 << bits)
+    g = inputs.upstream_grad(n, inputs.grad_seed(cfg, 0))
+    say("full dense", cfg, bits, n)
+    res = gpu(keys, c0, bits, g=g, dense=True)
+    check(res, oracle(keys, c0, g, form="table"), what="dense cfg%d bits=%d" % (cfg, bits))
 
 
 @pytest.mark.parametrize("fmt,out_half", [("fp16", False), ("fp16", True), ("bf16", False)])

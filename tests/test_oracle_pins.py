@@ -13,6 +13,7 @@ import pytest
 from oracle import dense, table
 from paper_2309_00964_amd import inputs
 from golden_io import read_uniquify_example
+from parity_util import EMPTY_THEN_LIVE, empty_then_live_inputs
 
 
 def rel(a, b):
@@ -410,3 +411,90 @@ def test_bf16_inputs_round_like_torch():
     c0 = inputs.quantile_init(keys, 8, "bf16")
     v = np.sort(inputs.values(keys, "bf16"))
     np.testing.assert_array_equal(c0, v[[((2 * j + 1) * n) // 16 for j in range(8)]])
+
+
+# --------------------------------------------------------------------------- autograd pins
+
+def _torch_dense_grads(v, c0, g, tau, T):
+    """dL/dw and dL/dC^(0) of L = sum_i g_i W~_i by torch's own reverse-mode
+    autograd of a plain dense DKM loop in fp64 on the CPU.  The loop is written
+    with library operations only (softmax over centroids, abs, where), so its
+    conventions are torch's: d|x|/dx at 0 is 0, and a centroid whose cluster
+    mass S_j is 0 keeps its value through torch.where, whose gradient then
+    flows to the previous centroid unchanged.  This is the autograd of the
+    dense map that the uniquified backward must reproduce (Sec. 2.2)."""
+    torch = pytest.importorskip("torch")
+    vt = torch.tensor(np.asarray(v, np.float64), requires_grad=True)
+    ct0 = torch.tensor(np.asarray(c0, np.float64), requires_grad=True)
+    gt = torch.tensor(np.asarray(g, np.float64))
+    c, cprev = ct0, None
+    for _ in range(T):
+        a = torch.softmax(-(vt[:, None] - c[None, :]).abs() / tau, dim=1)
+        S = a.sum(0)
+        P = (a * vt[:, None]).sum(0)
+        live = S > 0
+        cprev, c = c, torch.where(live, P / torch.where(live, S, torch.ones_like(S)), c)
+    a = torch.softmax(-(vt[:, None] - cprev[None, :]).abs() / tau, dim=1)
+    (gt * (a @ c)).sum().backward()
+    return vt.grad.numpy(), ct0.grad.numpy()
+
+
+def _on_a_weight(keys, c0):
+    v = keys.view(np.float16).astype(np.float64)
+    return np.isin(np.asarray(c0, np.float64), v)
+
+
+@pytest.mark.parametrize("case", ["quantile_n64_k4_t3", "quantile_n4096_k8_t5", "empty_then_live"])
+def test_backward_matches_torch_autograd(case):
+    """Both oracles' backward equal torch fp64 autograd of the dense loop.  The
+    quantile cases put every C^(0)_j exactly on a weight, so the d|x|/dx = 0 at
+    x = 0 reading decides terms of the first iteration (sgn(0) = +1 moves dL/dw
+    by ~1e-4 and dL/dC^(0) by ~1e-3 relative there); the empty_then_live case
+    decides the identity gradient of an empty cluster (without it dL/dC^(0)_2
+    would be 0 instead of about -325)."""
+    if case == "empty_then_live":
+        keys, c0, g = empty_then_live_inputs()
+        tau, T = EMPTY_THEN_LIVE["tau"], EMPTY_THEN_LIVE["T"]
+    else:
+        n, k, T = {"quantile_n64_k4_t3": (64, 4, 3), "quantile_n4096_k8_t5": (4096, 8, 5)}[case]
+        keys = inputs.fp16_weights(n, 60 + n)
+        c0 = inputs.quantile_init(keys, k).astype(np.float64)
+        g = inputs.upstream_grad(n, 61 + n).astype(np.float64)
+        tau = 2e-3
+        assert np.all(_on_a_weight(keys, c0))
+    v = keys.view(np.float16).astype(np.float64)
+    tw, tc = _torch_dense_grads(v, c0, g, tau, T)
+    fd_ = dense.forward(keys, c0, tau, T)
+    ft_ = table.forward(keys, c0, tau, T)
+    if case == "empty_then_live":
+        assert fd_["s_hist"][1, 1] == 0.0 and fd_["s_hist"][2, 1] > 1.0
+        assert abs(tc[1]) > 100.0
+    for name, (gw, gc) in (("dense", dense.backward(keys, fd_, g)),
+                           ("table", table.backward(keys, ft_, g)[:2])):
+        assert rel(gw, tw) <= 1e-10, name
+        assert rel(gc, tc) <= 1e-10, name
+
+
+def test_empty_then_live_central_differences():
+    """The empty-then-live case against central differences of the forward on
+    the weights' real values: dL/dC^(0) (the identity path of the empty
+    centroid included) and dL/dw of the far group and of some bulk weights."""
+    keys, c0, g = empty_then_live_inputs()
+    tau, T = EMPTY_THEN_LIVE["tau"], EMPTY_THEN_LIVE["T"]
+    v = keys.view(np.float16).astype(np.float64)
+    f = dense.forward(v, c0, tau, T)
+    gw, gc = dense.backward(v, f, g)
+    h = 1e-7
+    # no kink of |v - C^(t)| within reach: a step of h moves no centroid by more than h
+    assert np.min(np.abs(v[:, None, None] - f["c_hist"][None, :T, :])) > 10 * h
+    fd_c = np.array([(_loss(v, c0 + h * e, g, tau, T) - _loss(v, c0 - h * e, g, tau, T)) / (2 * h)
+                     for e in np.eye(2)])
+    assert abs(fd_c[1]) > 100.0
+    assert rel(gc, fd_c) <= 1e-6
+    idx = np.r_[np.arange(0, 2000, 100), np.arange(2000, 2020)]
+    fd_w = np.empty(idx.size)
+    for q, i in enumerate(idx):
+        e = np.zeros(v.size)
+        e[i] = h
+        fd_w[q] = (_loss(v + e, c0, g, tau, T) - _loss(v - e, c0, g, tau, T)) / (2 * h)
+    assert rel(gw[idx], fd_w) <= 1e-6

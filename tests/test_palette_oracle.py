@@ -49,3 +49,39 @@ def test_ties_take_the_lowest_entry_and_nonfinite_get_zero():
     np.testing.assert_array_equal(palette.indices(keys, lut), [0, 0, 0, 0, 0])
     lut = np.array([0.75, 0.25], np.float32)
     np.testing.assert_array_equal(palette.indices(keys, lut), [0, 1, 0, 0, 0])
+
+
+def test_nearest_final_centroid_versus_largest_final_attention():
+    """The two readings of the export rule (the paper names the artefact, a
+    table of centroids plus an index per weight, but not how a weight picks
+    its entry).  This library takes the entry of the given table nearest to
+    the weight; passing C^(T) as the table gives the nearest final centroid.
+    The other reading, the largest entry of the weight's final attention row
+    A^(T), is the nearest entry of C^(T-1), since A^(T) is built from C^(T-1)
+    and softmax(-|v - c| / tau) decreases with the distance.  The two differ
+    exactly on weights whose nearest centroid changes in the last update:
+    about 3% of the config-1 weights after five iterations."""
+    from oracle import table
+    keys = inputs.fp16_weights(65536, inputs.weight_seed(1, 0))
+    c0 = inputs.quantile_init(keys, 8)
+    f = table.forward(keys, c0, 2e-3, 5)
+    T = f["T"]
+    v = keys.view(np.float16).astype(np.float64)
+    d = -np.abs(v[:, None] - f["c_hist"][T - 1][None, :]) / 2e-3
+    a = np.exp(d - d.max(axis=1, keepdims=True))
+    a /= a.sum(axis=1, keepdims=True)
+    largest = np.argmax(a, axis=1)
+    prev = palette.indices(keys, f["c_hist"][T - 1].astype(np.float32))
+    final = palette.indices(keys, f["c_hist"][T].astype(np.float32))
+    np.testing.assert_array_equal(largest, prev)
+    differ = final != largest
+    assert 0.005 < differ.mean() < 0.1
+    # where they differ, the weight lies between the old and the new midpoint
+    # of two neighbouring centroids
+    for c in (f["c_hist"][T - 1], f["c_hist"][T]):
+        assert np.all(np.diff(c) > 0)
+    m_old = (f["c_hist"][T - 1][1:] + f["c_hist"][T - 1][:-1]) / 2
+    m_new = (f["c_hist"][T][1:] + f["c_hist"][T][:-1]) / 2
+    lo, hi = np.minimum(m_old, m_new), np.maximum(m_old, m_new)
+    between = np.any((v[:, None] >= lo[None, :] - 1e-7) & (v[:, None] <= hi[None, :] + 1e-7), axis=1)
+    assert np.all(between[differ])
