@@ -39,6 +39,7 @@ Other modes (measurement helpers):
 """
 import argparse
 import ctypes
+import gc
 import glob
 import hashlib
 import json
@@ -188,6 +189,9 @@ def cpu_baseline(samples, k, table_names=("q_proj", "gate_proj", "w", "L0.q_proj
     return out
 
 
+LAST_TIMING = {}   # the first timed region of the last timed() call: GPU and host clocks
+
+
 def timed(step, plan, pass_ids, steps, warmup):
     """Warm up, then run `steps` calls of step() twice on the current stream:
     first as the library runs them, timed between two HIP events (the step
@@ -198,6 +202,21 @@ def timed(step, plan, pass_ids, steps, warmup):
     {pass: median launch ms})."""
     import torch
     from paper_2309_00964_amd import edkm
+    # Python's cyclic garbage collector stays off while steps are enqueued (as
+    # timeit does): a full collection of this process's objects stops the
+    # host for ~35 ms, which a 20-step region would count as 1.7 ms per step
+    # of idle GPU.
+    gc.collect()
+    gc_was_on = gc.isenabled()
+    gc.disable()
+    try:
+        return _timed(step, plan, pass_ids, steps, warmup, torch, edkm)
+    finally:
+        if gc_was_on:
+            gc.enable()
+
+
+def _timed(step, plan, pass_ids, steps, warmup, torch, edkm):
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
@@ -210,6 +229,7 @@ def timed(step, plan, pass_ids, steps, warmup):
     for _ in range(steps):
         step()
     hip.record(t_stop, stream)
+    enq = time.perf_counter() - wall0
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     gpu_s = hip.elapsed_ms(t_start, t_stop) / 1000.0
@@ -226,6 +246,8 @@ def timed(step, plan, pass_ids, steps, warmup):
     med = {p: statistics.median(v) for p, v in per.items()}
     for e in [t_start, t_stop] + [x for p in ev for pair in ev[p] for x in pair]:
         hip.destroy(e)
+    LAST_TIMING.update(gpu_ms_per_step=gpu_s * 1000.0 / steps, host_wall_ms_per_step=wall * 1000.0 / steps,
+                       host_enqueue_ms_per_step=enq * 1000.0 / steps)
     return max(wall, gpu_s), avg, med
 
 
@@ -370,6 +392,7 @@ def result_line(args, workload, m, bits, elapsed, roof, extra_cfg=None):
         "data": "synthetic",
         "config": cfg,
         "roofline": roof,
+        "timing": {k: round(v, 4) for k, v in LAST_TIMING.items()},
     }
 
 
@@ -397,6 +420,7 @@ def bench_decoder_layer(args):
         # times (roofline) are the figures this mode is for
         extra["evict_between_calls"] = True
     roof = hbm_roofline(avg, m.total, half, med)
+    line_timing = dict(LAST_TIMING)
     if want_evicted and not args.evict_between_calls:
         m.evicting = True
         _, eavg, emed = timed(m.step, m.plans[0], PASS_IDS, args.steps, 1)
@@ -409,6 +433,8 @@ def bench_decoder_layer(args):
             "note": "same passes with 1 GiB read between init_unique, forward and backward "
                     "(no Infinity Cache reuse across calls); the gradient gather keeps the "
                     "reuse inside the backward"}
+    LAST_TIMING.clear()
+    LAST_TIMING.update(line_timing)
     out = result_line(args, "llama7b_decoder_layer_3bit" + _fmt_tag(args) + ("_half_wtilde" if half else "")
                       + ("_evicted" if args.evict_between_calls else ""),
                       m, bits, elapsed, roof, extra)
