@@ -244,6 +244,26 @@ edkm_status edkm_palettize_batch(int count, edkm_plan* const* plans, const uint1
                                  const float* const* lut, uint8_t* const* indices_out,
                                  hipStream_t stream);
 
+/* Palettization for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * edkm_palettize for one matrix of n weights (1..EDKM_MAX_N), bits in 1..4
+ * and key_format EDKM_KEYS_FP16 or EDKM_KEYS_BF16, with the same inputs,
+ * output and result, but no plan and no workspace.  Its per-pattern index
+ * table lives in a device array of EDKM_NOALLOC_SCRATCH_BYTES that the
+ * library holds on each GPU it runs on until the process ends; the call
+ * allocates nothing (no hipMalloc, no allocating library routine).  The first
+ * call on a device looks up that array's address there (hipGetSymbolAddress;
+ * make one call on each device before capturing a graph if the capture mode
+ * forbids that query).  Every call on one GPU uses the same array and
+ * rewrites all of it, so nothing carries over between calls, but calls that
+ * overlap on one GPU (other streams, other threads) race on it: serialise
+ * them.  Errors: EDKM_ERR_ARG for a null pointer, n = 0 or above EDKM_MAX_N,
+ * bits outside 1..4 or an unknown format (checked before any HIP call);
+ * EDKM_ERR_HIP if the address lookup or a launch fails. */
+#define EDKM_NOALLOC_SCRATCH_BYTES 65536
+edkm_status edkm_palettize_noalloc(const uint16_t* w_bits, uint64_t n, int bits, int key_format,
+                                   const float* lut, uint8_t* indices_out, hipStream_t stream);
+
 /* The uniquification's two lists (Sec. 2.2): the distinct weight patterns
  * and, per weight, the index of its pattern among them, in ascending order of
  * the 16-bit key (the order of numpy.unique on the uint16 view, with

@@ -462,6 +462,32 @@ edkm_status edkm_palettize_batch(int count, edkm_plan* const* plans, const uint1
     });
 }
 
+edkm_status edkm_palettize_noalloc(const uint16_t* w_bits, uint64_t n, int bits, int key_format,
+                                   const float* lut, uint8_t* indices_out, hipStream_t stream) {
+    if (!w_bits || !lut || !indices_out || n < 1 || n > EDKM_MAX_N || bits < 1 ||
+        bits > EDKM_MAX_BITS || (key_format != EDKM_KEYS_FP16 && key_format != EDKM_KEYS_BF16))
+        return EDKM_ERR_ARG;
+    uint8_t* tab = nullptr;
+    if (noalloc_scratch(&tab) != hipSuccess) return EDKM_ERR_HIP;
+    BatchArgs b;
+    std::memset(&b, 0, sizeof(b));
+    b.count = 1;
+    b.pal_tab = tab;   // the library's array on this device: no workspace
+    MatArgs& M = b.m[0];
+    M.keys = w_bits;
+    M.n = n;
+    M.k = 1 << bits;
+    M.max_iter = 1;
+    M.fmt = key_format == EDKM_KEYS_BF16 ? FMT_BF16 : FMT_FP16;
+    M.c_in = lut;
+    M.wt = indices_out;
+    M.vec = aligned16(w_bits) && ((uintptr_t)indices_out & 3u) == 0;
+    // the packing kernel's 64 KiB index table leaves room for two workgroups per CU
+    const uint32_t grid = partition(b, 2 * np_budget());
+    const char* where = "";
+    return launch_palettize(b, grid, stream, &where, nullptr) == hipSuccess ? EDKM_OK : EDKM_ERR_HIP;
+}
+
 edkm_status edkm_unique_inverse(edkm_plan* plan, const uint16_t* w_bits, uint16_t* unique_out,
                                 uint16_t* inverse_out, hipStream_t stream) {
     return edkm_unique_inverse_batch(1, &plan, &w_bits, &unique_out, &inverse_out, stream);

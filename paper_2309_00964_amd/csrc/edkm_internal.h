@@ -104,6 +104,8 @@ struct BatchArgs {
     float s2;                 // log2(e) / tau
     float inv_tau;
     float eps;
+    uint8_t* pal_tab;         // palettization index table of the launch's single matrix
+                              // (allocation-free entry point); null: each matrix's workspace
     MatArgs m[MAXB];
 };
 
@@ -182,6 +184,12 @@ struct PassEvents {
     hipEvent_t stop[NPASS];
 };
 
+
+// The allocation-free palettization keeps its index table (one byte per
+// pattern) in a library-owned device array of this size, one per GPU.
+constexpr size_t NOALLOC_SCRATCH_BYTES = NKEYS;
+// Address of that array on the current device (looked up once per device).
+hipError_t noalloc_scratch(uint8_t** out);
 
 // Launch sequences (all asynchronous on `s`).  Each returns the first HIP error.
 // On failure *where names the launch that failed.

@@ -25,6 +25,7 @@
 
 #include <hip/hip_fp16.h>
 #include <algorithm>
+#include <atomic>
 
 namespace edkm {
 
@@ -1218,10 +1219,16 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
 
 // Nearest lookup-table entry for every pattern: fp32 distance |v - lut_j|,
 // lowest entry on ties; non-finite patterns get 0.  Grid (NKEYS / 256, count).
+// The table of the launch's matrix mi: the allocation-free entry point's array
+// (single-matrix launches), or the matrix's own workspace region.
+__device__ __forceinline__ uint8_t* pal_table(const BatchArgs& b, const MatArgs& M) {
+    return b.pal_tab ? b.pal_tab : carve_workspace(M.wsb, M.max_iter).pidx;
+}
+
 __global__ void __launch_bounds__(256) k_pal_table(BatchArgs b) {
     __shared__ float lut[KMAX];
     const MatArgs& M = b.m[blockIdx.y];
-    const Ws ws = carve_workspace(M.wsb, M.max_iter);
+    uint8_t* const tbl = pal_table(b, M);
     if (threadIdx.x < M.k) lut[threadIdx.x] = M.c_in[threadIdx.x];
     __syncthreads();
     const uint32_t u = blockIdx.x * 256 + threadIdx.x;
@@ -1234,7 +1241,7 @@ __global__ void __launch_bounds__(256) k_pal_table(BatchArgs b) {
             if (d < bd) { bd = d; best = (uint32_t)j; }
         }
     }
-    ws.pidx[u] = (uint8_t)best;
+    tbl[u] = (uint8_t)best;
 }
 
 // Packed indices: index i occupies bits [B i, B i + B) of a little-endian bit
@@ -1247,9 +1254,8 @@ template <int B>
 __global__ void __launch_bounds__(1024) k_palettize(BatchArgs b) {
     __shared__ uint4 tbl4[NKEYS / 16];
     const MatArgs& M = b.m[np_matrix(b)];
-    const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const uint32_t wl = blockIdx.x - M.wg_begin;
-    const uint4* src = reinterpret_cast<const uint4*>(ws.pidx);
+    const uint4* src = reinterpret_cast<const uint4*>(pal_table(b, M));
     fill_lds<NKEYS / 16, 1024>(tbl4, src, NKEYS / 16, [](int i) { return i; });   // blockDim.x = 1024
     __syncthreads();
     const uint8_t* tbl = reinterpret_cast<const uint8_t*>(tbl4);
@@ -1795,6 +1801,34 @@ __global__ void __launch_bounds__(1024) k_dense_bfin(BatchArgs b, int nrow) {
         ws.ghist[(t - 1) * KMAX + j] = gm;
         if (t == 1) M.gc[j] = gm;
     }
+}
+
+// ----------------------------------------------------------------------------
+// Library-owned scratch of the allocation-free palettization: the index table
+// of one matrix, one copy per GPU (held until the process ends).  Host code
+// never passes the array's name to a kernel (on the host it only names the
+// symbol); it uses the device address that hipGetSymbolAddress returns, looked
+// up once per device with that device current.
+
+static __device__ __align__(256) uint8_t scratch[NOALLOC_SCRATCH_BYTES];
+
+hipError_t noalloc_scratch(uint8_t** out) {
+    static std::atomic<uint8_t*> addr[64];
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    uint8_t* p = addr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        void* q = nullptr;
+        e = hipGetSymbolAddress(&q, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!q) return hipErrorInvalidSymbol;
+        p = static_cast<uint8_t*>(q);
+        addr[dev].store(p, std::memory_order_release);
+    }
+    *out = p;
+    return hipSuccess;
 }
 
 // ----------------------------------------------------------------------------

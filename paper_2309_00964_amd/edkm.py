@@ -82,6 +82,7 @@ _SIGS = {
     "edkm_plan_set_keyed_mode": (_i32, [_PLAN, _i32]),
     "edkm_palettize": (_i32, [_PLAN, _P, _P, _P, _P]),
     "edkm_palettize_batch": (_i32, [_i32, _PP, _PP, _PP, _PP, _P]),
+    "edkm_palettize_noalloc": (_i32, [_P, _u64, _i32, _i32, _P, _P, _P]),
     "edkm_unique_inverse": (_i32, [_PLAN, _P, _P, _P, _P]),
     "edkm_unique_inverse_batch": (_i32, [_i32, _PP, _PP, _PP, _PP, _P]),
     "edkm_init_unique": (_i32, [_PLAN, _P, _P, _P, _i32, _P]),
@@ -196,6 +197,22 @@ def palettize(plan: Plan, w_bits, lut, indices_out, stream=None) -> None:
     _check(_lib.edkm_palettize(plan.ref, _ptr(w_bits, 2, "w_bits", plan.n), _ptr(lut, 4, "lut", plan.k),
                                _ptr(indices_out, 1),
                                _stream(stream)), "palettize", (plan,))
+
+
+def palettize_noalloc(w_bits, n: int, bits: int, lut, indices_out, key_format: str = "fp16",
+                      stream=None) -> None:
+    """palettize without a plan or workspace: the library keeps the per-pattern
+    table in its own device array (one per GPU; calls on one GPU must not
+    overlap).  ``indices_out`` holds ceil(n b / 8) bytes."""
+    if key_format not in KEY_FORMATS:
+        raise EdkmError(ERR_ARG, "palettize_noalloc", "key_format must be one of %s" % sorted(KEY_FORMATS))
+    n, bits = int(n), int(bits)
+    if not 1 <= bits <= 4:
+        raise EdkmError(ERR_ARG, "palettize_noalloc", "bits must be 1..4")
+    _check(_lib.edkm_palettize_noalloc(_ptr(w_bits, 2, "w_bits", n), n, bits, KEY_FORMATS[key_format],
+                                       _ptr(lut, 4, "lut", 1 << bits),
+                                       _ptr(indices_out, 1, "indices_out", (n * bits + 7) // 8),
+                                       _stream(stream)), "palettize_noalloc")
 
 
 def unique_inverse(plan: Plan, w_bits, unique_out=None, inverse_out=None, stream=None) -> None:

@@ -297,3 +297,20 @@ def test_plain_c_consumer_compiles_and_gets_host_errors(tmp_path):
     out = subprocess.run([exe], capture_output=True, text=True, timeout=60)
     assert out.returncode == 0, out.stdout + out.stderr
     assert out.stdout.strip() == "ok"
+
+
+def test_palettize_noalloc_argument_errors():
+    """The allocation-free palettization rejects bad arguments on the host,
+    before its device-address lookup or any launch."""
+    keys, lut, out = 1 << 41, 1 << 42, 1 << 43   # never dereferenced
+    f = lib.edkm_palettize_noalloc
+    assert f(None, 100, 3, edkm.KEYS_FP16, lut, out, None) == edkm.ERR_ARG
+    assert f(keys, 100, 3, edkm.KEYS_FP16, None, out, None) == edkm.ERR_ARG
+    assert f(keys, 100, 3, edkm.KEYS_FP16, lut, None, None) == edkm.ERR_ARG
+    assert f(keys, 0, 3, edkm.KEYS_FP16, lut, out, None) == edkm.ERR_ARG
+    assert f(keys, (1 << 32), 3, edkm.KEYS_FP16, lut, out, None) == edkm.ERR_ARG   # above EDKM_MAX_N
+    assert f(keys, 100, 0, edkm.KEYS_FP16, lut, out, None) == edkm.ERR_ARG
+    assert f(keys, 100, 5, edkm.KEYS_FP16, lut, out, None) == edkm.ERR_ARG
+    assert f(keys, 100, 3, 2, lut, out, None) == edkm.ERR_ARG
+    text = open(HEADER).read()
+    assert re.search(r"#define EDKM_NOALLOC_SCRATCH_BYTES 65536\b", text)
