@@ -81,7 +81,7 @@ uint32_t partition(BatchArgs& b, int budget) {
     for (int i = 0; i < b.count; ++i) {
         b.m[i].chunk = chunk[i];
         b.m[i].wg_count = cnt[i];
-        b.m[i].wg_begin = beg[i];
+        b.wg_begin[i] = beg[i];
     }
     return grid;
 }

@@ -366,7 +366,7 @@ __device__ __forceinline__ int np_matrix(const BatchArgs& b) {
     // before this workgroup, with independent loads of every start
     int m = 0;
 #pragma unroll
-    for (int i = 1; i < MAXB; ++i) m += (i < b.count && blockIdx.x >= b.m[i].wg_begin) ? 1 : 0;
+    for (int i = 1; i < MAXB; ++i) m += (i < b.count && blockIdx.x >= b.wg_begin[i]) ? 1 : 0;
     return m;
 }
 
@@ -530,7 +530,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
-    const uint32_t wl = blockIdx.x - M.wg_begin;
+    const uint32_t wl = blockIdx.x - b.wg_begin[mi];
     for (int i = threadIdx.x; i < 2 * W4; i += NP_THREADS) h[i] = 0u;
     if (threadIdx.x == 0) { red[0] = W4; red[1] = 0; }
     __syncthreads();
@@ -578,7 +578,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
         uint32_t c0 = h[s * W4 + mag], c1 = h[s * W4 + mag + 1];
         if (c0 > 0xFFFFu) { atomicAdd(&gcounts[(s << 15) | mag], c0); c0 = 0u; }
         if (c1 > 0xFFFFu) { atomicAdd(&gcounts[(s << 15) | (mag + 1)], c1); c1 = 0u; }
-        row[p] = c0 | (c1 << 16);
+        __builtin_nontemporal_store(c0 | (c1 << 16), row + p);   // read once, by the merge
     }
     if (threadIdx.x == 0) ws.span[wl] = make_int2(lo, hi);
 }
@@ -945,7 +945,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
-    const uint32_t wl = blockIdx.x - M.wg_begin;
+    const uint32_t wl = blockIdx.x - b.wg_begin[mi];
     const int lo = ws.st->lo4, w = ws.st->w4;
     const float* tab = ws.tab;
     fill_lds<2 * W4, NP_THREADS>(tw, tab, 2 * w, [&](int i) {
@@ -1031,7 +1031,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
-    const uint32_t wl = blockIdx.x - M.wg_begin;
+    const uint32_t wl = blockIdx.x - b.wg_begin[mi];
     const DevState* st = ws.st;
     const bool wide = st->kmode == KEYED_U64;
     const int lo = wide ? st->lo8 : st->lo4, w = wide ? st->w8 : st->w4;
@@ -1093,7 +1093,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
         });
         __syncthreads();
         for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS)
-            row[i] = (float)ldexp((double)(long long)lds[i], -S);
+            __builtin_nontemporal_store((float)ldexp((double)(long long)lds[i], -S), row + i);
     } else {
         // Values with exponent <= elim go to LDS: the sample maximum, but at most
         // 2^10 above the mean exponent.  Capped so the wrap value 2^(32 - S)
@@ -1146,7 +1146,8 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
                 settle(key, q, old);
             });
         __syncthreads();
-        for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) row[i] = ldexpf((float)acc32[i], -S);
+        for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS)
+            __builtin_nontemporal_store(ldexpf((float)acc32[i], -S), row + i);
     }
 }
 
@@ -1158,7 +1159,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
-    const uint32_t wl = blockIdx.x - M.wg_begin;
+    const uint32_t wl = blockIdx.x - b.wg_begin[mi];
     const DevState* st = ws.st;
     const int lo = st->lo8, w = st->w8;
     const float2* HR = ws.HR;
@@ -1249,12 +1250,13 @@ __global__ void __launch_bounds__(256) k_pal_table(BatchArgs b) {
 // at byte 4 B g for group g); the per-pattern index table (64 KiB) sits in LDS.
 // The matrix's last, partial group and unaligned buffers are written byte by
 // byte, never past the ceil(n B / 8) output bytes.  A matrix's workgroups
-// [wg_begin, wg_begin + wg_count) take its groups round-robin, 1024 at a time.
+// [b.wg_begin[mi], b.wg_begin[mi] + wg_count) take its groups round-robin, 1024 at a time.
 template <int B>
 __global__ void __launch_bounds__(1024) k_palettize(BatchArgs b) {
     __shared__ uint4 tbl4[NKEYS / 16];
-    const MatArgs& M = b.m[np_matrix(b)];
-    const uint32_t wl = blockIdx.x - M.wg_begin;
+    const int mi = np_matrix(b);
+    const MatArgs& M = b.m[mi];
+    const uint32_t wl = blockIdx.x - b.wg_begin[mi];
     const uint4* src = reinterpret_cast<const uint4*>(pal_table(b, M));
     fill_lds<NKEYS / 16, 1024>(tbl4, src, NKEYS / 16, [](int i) { return i; });   // blockDim.x = 1024
     __syncthreads();
@@ -1380,7 +1382,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_inverse(BatchArgs b) {
     const MatArgs& M = b.m[mi];
     if (!M.wt) return;   // the same for the whole workgroup
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
-    const uint32_t wl = blockIdx.x - M.wg_begin;
+    const uint32_t wl = blockIdx.x - b.wg_begin[mi];
     const uint4* src = reinterpret_cast<const uint4*>(ws.rank);
     constexpr int NV = NKEYS * sizeof(uint16_t) / sizeof(uint4);
     fill_lds<NV, NP_THREADS>(rk4, src, NV, [](int i) { return i; });
