@@ -36,6 +36,8 @@ Other modes (measurement helpers):
   --copy-calibration          run a plain 1 GiB device copy (HBM counter calibration)
   --pmc-summary FETCH WRITE   turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE)
                               into profiles/hbm_traffic.json
+  --dram-summary DIR...       turn rocprofv3 --pmc runs of the DRAM request counters into
+                              profiles/dram_traffic.json (HBM bytes vs Infinity Cache hits)
 """
 import argparse
 import ctypes
@@ -271,6 +273,9 @@ def hbm_roofline(avg_ms, total, out_half=False, med_ms=None):
     t_all = sum(v["avg_us"] for v in passes.values()) * 1e-6
     return {"bound": "hbm", "kernel": dom, "achieved": passes[dom]["GBps"], "peak": PEAK_HBM_GBS,
             "unit": "GB/s", "frac": passes[dom]["GBps"] / PEAK_HBM_GBS, "traffic": traffic,
+            "traffic_kind": "L2-to-fabric bytes per launch (FETCH_SIZE + WRITE_SIZE, scaled by a 1 GiB "
+                            "copy): Infinity Cache hits included; the L2's DRAM-request counters count "
+                            "them too (profiles/dram_traffic.json)",
             "n_pass_total_GBps": n_bytes_all / t_all / 1e9,
             "n_pass_total_frac": n_bytes_all / t_all / 1e9 / PEAK_HBM_GBS,
             "passes": {p: dict({"avg_us": round(v["avg_us"], 2), "GBps": round(v["GBps"], 1)},
@@ -621,6 +626,71 @@ def pmc_summary(fetch_dir, write_dir):
     print(json.dumps(res))
 
 
+DRAM_FILE = os.path.join(ROOT, "profiles", "dram_traffic.json")
+DRAM_COUNTERS = ("TCC_EA0_RDREQ_DRAM_sum", "TCC_EA0_WRREQ_DRAM_sum", "TCC_EA0_RDREQ_sum", "TCC_EA0_WRREQ_sum")
+
+
+def dram_summary(dirs):
+    """Which of the L2's fabric requests the counters see as bound for DRAM.
+    Each directory holds a rocprofv3 --pmc run of the four DRAM_COUNTERS over
+    "bench" (a workload run) and "copy" (--copy-calibration).  Of the read
+    (write) requests the L2 sends to the fabric, TCC_EA0_RDREQ_DRAM
+    (WRREQ_DRAM) counts those addressed to the memory controller.  The
+    summary gives that share per pass and, with the fabric bytes of
+    profiles/hbm_traffic.json (same kernels), the DRAM-addressed bytes.  On
+    MI355X the Infinity Cache sits behind that interface, so its hits are
+    counted as DRAM requests too: the share is 1 for every pass, and the
+    split of HBM bytes from Infinity Cache hits is not observable with these
+    counters (the evicted-between-calls pass times measure the reuse instead)."""
+    def per_pass(d, prefix, counter):
+        acc = {}
+        for r in _pmc_rows(d, prefix):
+            if r.get("Counter_Name") != counter:
+                continue
+            key = (r["_file"], r.get("Dispatch_Id"), r.get("Kernel_Name", ""))
+            acc[key] = acc.get(key, 0.0) + float(r["Counter_Value"])
+        out = {}
+        for (_, _, name), v in acc.items():
+            p = kernel_base_name(name)
+            if p in PASS_IDS or "copyBuffer" in name:
+                out.setdefault("copy" if "copyBuffer" in name else p, []).append(v)
+        return {p: sum(v) / len(v) for p, v in out.items()}
+
+    fabric = json.load(open(TRAFFIC_FILE)) if os.path.exists(TRAFFIC_FILE) else {}
+    same_build = fabric.get("source_hash") == source_hash()
+    res = {"source_hash": source_hash(), "counters": list(DRAM_COUNTERS), "runs": {}}
+    for d in dirs:
+        label = os.path.basename(os.path.normpath(d))
+        rd = per_pass(d, "bench", "TCC_EA0_RDREQ_DRAM_sum")
+        wd = per_pass(d, "bench", "TCC_EA0_WRREQ_DRAM_sum")
+        ra = per_pass(d, "bench", "TCC_EA0_RDREQ_sum")
+        wa = per_pass(d, "bench", "TCC_EA0_WRREQ_sum")
+        cp = {c: per_pass(d, "copy", c).get("copy") for c in DRAM_COUNTERS}
+        run = {"copy_read_dram_share": cp["TCC_EA0_RDREQ_DRAM_sum"] / cp["TCC_EA0_RDREQ_sum"]
+               if cp["TCC_EA0_RDREQ_sum"] else None,
+               "copy_write_dram_share": cp["TCC_EA0_WRREQ_DRAM_sum"] / cp["TCC_EA0_WRREQ_sum"]
+               if cp["TCC_EA0_WRREQ_sum"] else None,
+               "passes": {}}
+        for p in PASS_IDS:
+            if p not in ra:
+                continue
+            q = {"read_requests": ra[p], "read_dram_requests": rd.get(p, 0.0),
+                 "write_requests": wa.get(p, 0.0), "write_dram_requests": wd.get(p, 0.0),
+                 "read_dram_share": rd.get(p, 0.0) / ra[p] if ra[p] else None,
+                 "write_dram_share": wd.get(p, 0.0) / wa[p] if wa.get(p) else None}
+            k = fabric.get("kernels", {}).get(p)
+            if same_build and k:
+                q["fabric_read_bytes"] = k["fetch_bytes"]
+                q["fabric_write_bytes"] = k["write_bytes"]
+                q["dram_addressed_read_bytes"] = k["fetch_bytes"] * q["read_dram_share"]
+                q["dram_addressed_write_bytes"] = k["write_bytes"] * (q["write_dram_share"] or 0.0)
+            run["passes"][p] = q
+        res["runs"][label] = run
+    os.makedirs(os.path.dirname(DRAM_FILE), exist_ok=True)
+    json.dump(res, open(DRAM_FILE, "w"), indent=1)
+    print(json.dumps(res))
+
+
 def main():
     from paper_2309_00964_amd.inputs import LLAMA7B_LAYER
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
@@ -649,9 +719,12 @@ def main():
                     help="matrices of the layer the CPU oracle is timed on (default: all seven)")
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--dram-summary", nargs="+", metavar="DIR")
     args = ap.parse_args()
     if args.pmc_summary:
         return pmc_summary(*args.pmc_summary)
+    if args.dram_summary:
+        return dram_summary(args.dram_summary)
     if args.gpus != 1:
         sys.exit("bench.py runs on one GPU: the library has no multi-GPU path (--gpus %d asked)"
                  % args.gpus)
