@@ -525,13 +525,13 @@ __global__ void __launch_bounds__(T_THREADS) k_init_zero(BatchArgs b) {
 // 16-bit counts (two bins per word); a bin that reached 2^16 in this
 // workgroup is added to the global counts instead.
 __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
-    __shared__ uint32_t h[2 * W4];
+    __shared__ __align__(16) uint32_t h[2 * W4];
     __shared__ int red[2];
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const uint32_t wl = blockIdx.x - b.wg_begin[mi];
-    for (int i = threadIdx.x; i < 2 * W4; i += NP_THREADS) h[i] = 0u;
+    for (int i = threadIdx.x; i < 2 * W4 / 4; i += NP_THREADS) reinterpret_cast<uint4*>(h)[i] = uint4{0u, 0u, 0u, 0u};
     if (threadIdx.x == 0) { red[0] = W4; red[1] = 0; }
     __syncthreads();
     const uint16_t* keys = M.keys;
@@ -555,10 +555,20 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
         [&](uint64_t, Nothing) {},
         [&](uint64_t i) { add(keys[i]); });
     __syncthreads();
-    // occupied span [lo, hi) over both signs, rounded out to even magnitudes
+    // occupied span [lo, hi) over both signs, rounded out to even magnitudes;
+    // a thread's W4 / NP_THREADS magnitudes are read all at once (as a loop
+    // each read waited for the previous one)
     int lo = W4, hi = 0;
-    for (int mag = threadIdx.x; mag < W4; mag += NP_THREADS) {
-        if (h[mag] | h[W4 + mag]) { lo = min(lo, mag); hi = max(hi, mag + 1); }
+    {
+        constexpr int PER = W4 / NP_THREADS;
+        uint32_t x[PER];
+#pragma unroll
+        for (int q = 0; q < PER; ++q) x[q] = h[threadIdx.x + q * NP_THREADS] | h[W4 + threadIdx.x + q * NP_THREADS];
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            const int mag = threadIdx.x + q * NP_THREADS;
+            if (x[q]) { lo = min(lo, mag); hi = max(hi, mag + 1); }
+        }
     }
     lo = wave_reduce(lo, 0x7FFFFFFF, op_min);   // one LDS atomic per wave
     hi = wave_reduce(hi, -0x7FFFFFFF - 1, op_max);
@@ -572,13 +582,29 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
     if (hi <= lo) { lo = 0; hi = 0; }
     const int half = (hi - lo) >> 1;
     uint32_t* row = ws.part + (size_t)wl * ROW4;
-    for (int p = threadIdx.x; p < 2 * half; p += NP_THREADS) {
-        const int s = p >= half;
-        const int mag = lo + 2 * (p - s * half);
-        uint32_t c0 = h[s * W4 + mag], c1 = h[s * W4 + mag + 1];
-        if (c0 > 0xFFFFu) { atomicAdd(&gcounts[(s << 15) | mag], c0); c0 = 0u; }
-        if (c1 > 0xFFFFu) { atomicAdd(&gcounts[(s << 15) | (mag + 1)], c1); c1 = 0u; }
-        __builtin_nontemporal_store(c0 | (c1 << 16), row + p);   // read once, by the merge
+    // four of a thread's pairs per round, every LDS read issued before the
+    // first is used
+    constexpr int RU = 4;
+    for (int p0 = threadIdx.x; p0 < 2 * half; p0 += RU * NP_THREADS) {
+        uint32_t c[RU][2];
+#pragma unroll
+        for (int q = 0; q < RU; ++q) {
+            const int p = p0 + q * NP_THREADS;
+            const int s = p >= half;
+            const int mag = lo + 2 * (p - s * half);
+            if (p < 2 * half) { c[q][0] = h[s * W4 + mag]; c[q][1] = h[s * W4 + mag + 1]; }
+        }
+#pragma unroll
+        for (int q = 0; q < RU; ++q) {
+            const int p = p0 + q * NP_THREADS;
+            if (p >= 2 * half) break;
+            const int s = p >= half;
+            const int mag = lo + 2 * (p - s * half);
+            uint32_t c0 = c[q][0], c1 = c[q][1];
+            if (c0 > 0xFFFFu) { atomicAdd(&gcounts[(s << 15) | mag], c0); c0 = 0u; }
+            if (c1 > 0xFFFFu) { atomicAdd(&gcounts[(s << 15) | (mag + 1)], c1); c1 = 0u; }
+            __builtin_nontemporal_store(c0 | (c1 << 16), row + p);   // read once, by the merge
+        }
     }
     if (threadIdx.x == 0) ws.span[wl] = make_int2(lo, hi);
 }
@@ -1025,7 +1051,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
 // address) the 32-bit mode is 10% faster, with bf16 weights (about 1.8) the
 // 64-bit mode is 30% faster.
 __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
-    __shared__ unsigned long long lds[2 * W8];   // 64-bit sums, or the 32-bit ones
+    __shared__ __align__(16) unsigned long long lds[2 * W8];   // 64-bit sums, or the 32-bit ones
     __shared__ int emax_sh, esum_sh, ecnt_sh;
     static_assert(2 * W4 * sizeof(int) <= sizeof(lds), "32-bit window fits the LDS buffer");
     const int mi = np_matrix(b);
@@ -1038,10 +1064,9 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
     const uint16_t* keys = M.keys;
     const float* g = M.g;
     int* acc32 = reinterpret_cast<int*>(lds);
-    if (wide) {
-        for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) lds[i] = 0ull;
-    } else {
-        for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS) acc32[i] = 0;
+    {   // 16-byte LDS writes over the window (2 w words of 4 or 8 bytes), rounded up
+        const int n16 = wide ? w : (2 * w + 3) / 4;
+        for (int i = threadIdx.x; i < n16; i += NP_THREADS) reinterpret_cast<uint4*>(lds)[i] = uint4{0u, 0u, 0u, 0u};
     }
     if (threadIdx.x == 0) { emax_sh = 0; esum_sh = 0; ecnt_sh = 0; }
     __syncthreads();
@@ -1146,8 +1171,17 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
                 settle(key, q, old);
             });
         __syncthreads();
-        for (int i = threadIdx.x; i < 2 * w; i += NP_THREADS)
-            __builtin_nontemporal_store(ldexpf((float)acc32[i], -S), row + i);
+        constexpr int RU = 4;   // four LDS reads in flight per thread
+        for (int i0 = threadIdx.x; i0 < 2 * w; i0 += RU * NP_THREADS) {
+            int a[RU];
+#pragma unroll
+            for (int q = 0; q < RU; ++q)
+                if (i0 + q * NP_THREADS < 2 * w) a[q] = acc32[i0 + q * NP_THREADS];
+#pragma unroll
+            for (int q = 0; q < RU; ++q)
+                if (i0 + q * NP_THREADS < 2 * w)
+                    __builtin_nontemporal_store(ldexpf((float)a[q], -S), row + i0 + q * NP_THREADS);
+        }
     }
 }
 
