@@ -292,6 +292,12 @@ def alu_roofline(avg_ms, n, k):
     dom = max(kern, key=lambda p: kern[p]["avg_us"])
     return {"bound": "alu", "kernel": dom, "achieved": kern[dom]["TFLOPs"], "peak": PEAK_FP32_TFLOPS,
             "unit": "TFLOP/s", "frac": kern[dom]["TFLOPs"] / PEAK_FP32_TFLOPS, "traffic": None,
+            # the code is built without packed-fp32 instructions, so one lane issues one fp32
+            # operation (two for an FMA) per cycle: half the headline peak
+            "peak_without_packed_fp32": PEAK_FP32_TFLOPS / 2,
+            "frac_without_packed_fp32": kern[dom]["TFLOPs"] / (PEAK_FP32_TFLOPS / 2),
+            "ops_note": "the exponential counts as one operation (one transcendental instruction, "
+                        "issued at a quarter of the FMA rate)",
             "ops_per_entry": DENSE_OPS_PER_ENTRY[dom],
             "kernels": {p: {"avg_us": round(v["avg_us"], 2), "TFLOPs": round(v["TFLOPs"], 2)}
                         for p, v in kern.items()}}
