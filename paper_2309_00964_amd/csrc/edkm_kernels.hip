@@ -1070,9 +1070,13 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
     }
     if (threadIdx.x == 0) { emax_sh = 0; esum_sh = 0; ecnt_sh = 0; }
     __syncthreads();
-    {   // sample: one value per thread, spread over the matrix; exponents of the
-        // normal finite values: largest, sum and count
-        const uint64_t i = (((uint64_t)wl * NP_THREADS + threadIdx.x) * 2654435761ull) % M.n;
+    {   // sample: 64 consecutive values per wave, the waves' runs spread over the
+        // matrix (one value per thread at scattered indices had cost a 128-byte
+        // line per value, 33 MB per decoder layer); exponents of the normal
+        // finite values: largest, sum and count
+        const uint64_t runs = M.n > 64 ? M.n - 63 : 1;
+        const uint64_t run0 = (((uint64_t)wl * (NP_THREADS / 64) + (threadIdx.x >> 6)) * 2654435761ull) % runs;
+        const uint64_t i = min(run0 + (threadIdx.x & 63), M.n - 1);
         const int e = (int)((__float_as_uint(g[i]) >> 23) & 0xFFu);
         const bool use = e != 0 && e != 0xFF;
         int smax = use ? e : 0, ssum = smax, scnt = use ? 1 : 0;
