@@ -36,6 +36,8 @@ struct PlanImpl {
 };
 static_assert(sizeof(PlanImpl) <= sizeof(edkm_plan), "edkm_plan too small");
 static_assert(EDKM_KEYS_FP16 != EDKM_KEYS_BF16, "key formats");
+static_assert(EDKM_NOALLOC_SCRATCH_BYTES == NOALLOC_SCRATCH_BYTES,
+              "the header states the allocation-free palettization's device array size");
 static_assert(EDKM_KEYED_I32 == KEYED_I32 && EDKM_KEYED_U64 == KEYED_U64, "keyed-sum modes");
 static_assert(EDKM_PASS_HIST == PASS_HIST && EDKM_PASS_GATHER_WT == PASS_GATHER_WT &&
                   EDKM_PASS_KEYED_GRAD == PASS_KEYED_GRAD && EDKM_PASS_GATHER_GRAD == PASS_GATHER_GRAD &&
