@@ -153,7 +153,8 @@ edkm_status edkm_forward(edkm_plan* plan, const uint16_t* w_bits, float tau, flo
  *   grad_w        device float[n]
  *   grad_c        device float[k]: dL/dC^(0)
  * d|x|/dx at x = 0 is 0.  The keyed reduction uses float atomics, so results
- * vary in the last bits between runs. */
+ * vary in the last bits between runs.  May be repeated after one forward (with
+ * other gradients); after EDKM_ERR_HIP it needs a new forward first. */
 edkm_status edkm_backward(edkm_plan* plan, const uint16_t* w_bits, const float* grad_w_tilde,
                           float* grad_w, float* grad_c, hipStream_t stream);
 

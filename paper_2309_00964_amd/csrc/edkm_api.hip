@@ -356,6 +356,11 @@ edkm_status edkm_backward_batch(int count, edkm_plan* const* plans, const uint16
         }
         return EDKM_OK;
     });
+    if (st == EDKM_ERR_HIP) {
+        // a backward that did not run to its end may leave its table partials
+        // half-added: the next backward needs a new forward (which clears them)
+        for (int i = 0; i < count; ++i) impl(plans[i])->stage = COUNTED;
+    }
     return st;
 }
 

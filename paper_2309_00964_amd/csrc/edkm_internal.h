@@ -54,6 +54,7 @@ struct Ws {
     float* shist;       // [(max_iter+1) * KMAX]  S^(t)
     float* ghist;       // [(max_iter+1) * KMAX]  dL/dC^(t)
     float* ehist;       // [KMAX]  direct-use term of the dense backward
+    float* cfin;        // [2 * KMAX]  C^(T-1), C^(T) of the last forward (at a fixed place)
     float* tpart;       // [(max_iter+1) * T_WG * PSTRIDE]  forward table partials
     float* bpart;       // [(max_iter+1) * T_WG * PSTRIDE]  backward table partials
     float* dpart;       // [D_WG * PSTRIDE]  dense-path partials
@@ -119,7 +120,7 @@ static_assert(sizeof(BatchArgs) <= 4096, "launch arguments fit the kernel-argume
 // function of max_iter only, evaluated on the host (sizing, plan checks) and
 // in every kernel (from the workspace base in the launch arguments).
 struct Layout {
-    size_t counts, tab, H, R, HR, G, chist, shist, ghist, ehist, tpart, bpart, dpart, span, part, pidx,
+    size_t counts, tab, H, R, HR, G, chist, shist, ghist, ehist, cfin, tpart, bpart, dpart, span, part, pidx,
         rank, st, total;
 };
 
@@ -140,6 +141,7 @@ __host__ __device__ inline Layout layout(int max_iter) {
     L.shist = take(hist);
     L.ghist = take(hist);
     L.ehist = take(KMAX * sizeof(float));
+    L.cfin = take(2 * KMAX * sizeof(float));
     L.tpart = take(tp);
     L.bpart = take(tp);
     L.dpart = take((size_t)D_WG * PSTRIDE * sizeof(float));
@@ -170,6 +172,7 @@ __host__ __device__ inline Ws carve_workspace(void* base, int max_iter) {
     w.shist = reinterpret_cast<float*>(c + L.shist);
     w.ghist = reinterpret_cast<float*>(c + L.ghist);
     w.ehist = reinterpret_cast<float*>(c + L.ehist);
+    w.cfin = reinterpret_cast<float*>(c + L.cfin);
     w.tpart = reinterpret_cast<float*>(c + L.tpart);
     w.bpart = reinterpret_cast<float*>(c + L.bpart);
     w.dpart = reinterpret_cast<float*>(c + L.dpart);

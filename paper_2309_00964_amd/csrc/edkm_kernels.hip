@@ -651,31 +651,6 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_hist_merge(BatchArgs b) {
     if (s1) atomicAdd(c + 1, s1);
 }
 
-// Keyed-gradient rows (fp32 over the window of the matrix's keyed-sum mode)
-// into G.  Grid (2 * W4 / MERGE_THREADS, row chunks, count).
-__global__ void __launch_bounds__(MERGE_THREADS) k_grad_merge(BatchArgs b) {
-    const MatArgs& M = b.m[blockIdx.z];
-    const Ws ws = carve_workspace(M.wsb, M.max_iter);
-    const int r0 = blockIdx.y * MERGE_ROWS;
-    const int r1 = min((int)M.wg_count, r0 + MERGE_ROWS);
-    const DevState* st = ws.st;
-    const bool wide = st->kmode == KEYED_U64;
-    const int w = wide ? st->w8 : st->w4, lo = wide ? st->lo8 : st->lo4;
-    const int i = blockIdx.x * MERGE_THREADS + threadIdx.x;
-    if (r0 >= r1 || i >= 2 * w) return;
-    const float* part = reinterpret_cast<const float*>(ws.part) + i;
-    float x[MERGE_ROWS];                       // every row's value in flight at once
-#pragma unroll
-    for (int q = 0; q < MERGE_ROWS; ++q) x[q] = r0 + q < r1 ? part[(size_t)(r0 + q) * ROW4] : 0.f;
-#pragma unroll
-    for (int h = MERGE_ROWS / 2; h > 0; h /= 2)   // pairwise sum
-#pragma unroll
-        for (int q = 0; q < h; ++q) x[q] += x[q + h];
-    const float sum = x[0];
-    const int sg = i >= w;
-    if (sum != 0.f) atomicAdd(&ws.G[(sg << 15) | (lo + i - sg * w)], sum);
-}
-
 // Window selection: one block per matrix, grid (1, count).  Wave w owns the
 // SPAN = 2048 magnitudes [2048 w, 2048 w + 2048) of both signs, in NCH = 8
 // chunks of 256; lane l holds the 4 consecutive magnitudes 4 l .. 4 l + 3 of
@@ -937,9 +912,15 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
         __syncthreads();
     }
     if (lead) {
-        if (threadIdx.x < K) M.c_out[threadIdx.x] = cT[threadIdx.x];
+        if (threadIdx.x < K) {
+            M.c_out[threadIdx.x] = cT[threadIdx.x];
+            ws.cfin[threadIdx.x] = cP[threadIdx.x];          // for k_grad_top, which does not know T
+            ws.cfin[KMAX + threadIdx.x] = cT[threadIdx.x];
+        }
         if (threadIdx.x == 0 && M.iters_out) *M.iters_out = T;
     }
+    // the backward's first partial block, which k_grad_top adds into
+    if (threadIdx.x < PSTRIDE) ws.bpart[(size_t)blockIdx.x * PSTRIDE + threadIdx.x] = 0.f;
     float c1[K], c0[K];
 #pragma unroll
     for (int j = 0; j < K; ++j) { c1[j] = cT[j]; c0[j] = cP[j]; }
@@ -1216,6 +1197,10 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
                 M.gc[j] = gc;
             }
         }
+        // the first partial block is read: clear it for the next backward's
+        // k_grad_top (a lane clears rows it read itself)
+        for (int r = threadIdx.x; r < T_WG; r += 64)
+            for (int c = 0; c < PSTRIDE; ++c) ws.bpart[(size_t)r * PSTRIDE + c] = 0.f;
     }
     {
         const uint32_t per = (NKEYS + M.wg_count - 1) / M.wg_count;
@@ -1439,56 +1424,96 @@ __global__ void __launch_bounds__(NP_THREADS) k_inverse(BatchArgs b) {
 // ----------------------------------------------------------------------------
 // backward table phase
 
-// Direct use of A^(T) and C^(T) by W~: with G_u (merged keyed sums), partials of gamma_j = sum_u G_u a^(T)_uj (= dL/dC^(T)_j) and
-// E_j = sum_u G_u a^(T)_uj (C^(T)_j - Tab_u) sgn(v_u - C^(T-1)_j).
-// Grid (T_WG, count).
+// The backward's first table quantities, from the keyed-sum partial rows:
+//   gamma_j = sum_u G_u a^(T)_uj                                   (= dL/dC^(T)_j)
+//   E_j     = sum_u G_u a^(T)_uj (C^(T)_j - Tab_u) sgn(v_u - C^(T-1)_j)
+// (a^(T) built from C^(T-1); E without the 1/tau).  Both are linear in the
+// keyed sums G_u, so G_u is never assembled: a thread sums one window
+// pattern's entries over a chunk of GT_ROWS partial rows (blockIdx.y) and
+// adds that partial sum times the pattern's terms.  The last blockIdx.y takes
+// what the keyed-sum pass added to the global G instead (patterns outside the
+// window, values above its fixed-point limit, wrap corrections), over all
+// 65,536 patterns.  Block totals are added with float atomics into the 64 rows
+// of the backward's first partial block, which k_fwd_out clears and
+// k_gather_grad clears again after use.  (Summing the rows into G first, then
+// a table kernel over G, took one launch more.)  Grid (MERGE_X, row chunks +
+// 1, count).
+constexpr int MERGE_X = 2 * W4 / MERGE_THREADS;
+// Rows per chunk here: a pattern's terms are evaluated once per chunk, so
+// larger chunks than the histogram merge's (one for a decoder layer's
+// matrices, of at most 57 rows each).
+constexpr int GT_ROWS = 64;
 template <int K>
-__global__ void __launch_bounds__(T_THREADS) k_bwd_top(BatchArgs b) {
+__global__ void __launch_bounds__(MERGE_THREADS) k_grad_top(BatchArgs b) {
     __shared__ float tot[2 * K];
-    __shared__ float scratch[T_THREADS / 64 * 2 * K];
-    __shared__ float c1sh[K], c0sh[K];
-    const MatArgs& M = b.m[blockIdx.y];
+    __shared__ float scratch[MERGE_THREADS / 64 * 2 * K];
+    constexpr int GPER = (NKEYS + MERGE_X * MERGE_THREADS - 1) / (MERGE_X * MERGE_THREADS);
+    const MatArgs& M = b.m[blockIdx.z];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
-    uint32_t n4[T_KPT];   // per-pattern inputs first: they do not depend on the centroids
-    float G4[T_KPT];
-#pragma unroll
-    for (int r = 0; r < T_KPT; ++r) {
-        const int u = table_key(r);
-        n4[r] = ws.counts[u];
-        G4[r] = ws.G[u];
-    }
     const DevState* st = ws.st;
-    const int T = st->teff;
-    if (threadIdx.x < K) {
-        c1sh[threadIdx.x] = ws.chist[T * KMAX + threadIdx.x];
-        c0sh[threadIdx.x] = ws.chist[(T - 1) * KMAX + threadIdx.x];
-    }
-    __syncthreads();
-    float c1[K], c0[K];
+    // C^(T-1) and C^(T), issued first: independent of everything below
+    float c0[K], c1[K];
 #pragma unroll
-    for (int j = 0; j < K; ++j) { c1[j] = c1sh[j]; c0[j] = c0sh[j]; }
+    for (int j = 0; j < K; ++j) { c0[j] = ws.cfin[j]; c1[j] = ws.cfin[KMAX + j]; }
+    float gv[GPER];
+    uint32_t key[GPER];
+#pragma unroll
+    for (int q = 0; q < GPER; ++q) { gv[q] = 0.f; key[q] = 0u; }
+    if (blockIdx.y == gridDim.y - 1) {
+        // the global G: GPER patterns per thread
+#pragma unroll
+        for (int q = 0; q < GPER; ++q) {
+            const uint32_t u = (q * MERGE_X + blockIdx.x) * MERGE_THREADS + threadIdx.x;
+            key[q] = u;
+            if (u < (uint32_t)NKEYS) gv[q] = ws.G[u];
+        }
+    } else {
+        const bool wide = st->kmode == KEYED_U64;
+        const int w = wide ? st->w8 : st->w4, lo = wide ? st->lo8 : st->lo4;
+        const int r0 = blockIdx.y * GT_ROWS;
+        const int r1 = min((int)M.wg_count, r0 + GT_ROWS);
+        if (r0 >= r1 || (int)(blockIdx.x * MERGE_THREADS) >= 2 * w) return;   // the same for the block
+        const int i = blockIdx.x * MERGE_THREADS + threadIdx.x;
+        if (i < 2 * w) {
+            const float* part = reinterpret_cast<const float*>(ws.part) + i;
+            float x[GT_ROWS];                      // every row's value in flight at once
+#pragma unroll
+            for (int q = 0; q < GT_ROWS; ++q) x[q] = r0 + q < r1 ? part[(size_t)(r0 + q) * ROW4] : 0.f;
+#pragma unroll
+            for (int h = GT_ROWS / 2; h > 0; h /= 2)   // pairwise sum
+#pragma unroll
+                for (int q = 0; q < h; ++q) x[q] += x[q + h];
+            const int sg = i >= w;
+            gv[0] = x[0];
+            key[0] = (uint32_t)((sg << 15) | (lo + i - sg * w));
+        }
+    }
+    int nz = 0;
+#pragma unroll
+    for (int q = 0; q < GPER; ++q) nz |= gv[q] != 0.f;
+    if (!__syncthreads_or(nz)) return;   // nothing to add in this block
     float acc[2 * K];
 #pragma unroll
     for (int j = 0; j < 2 * K; ++j) acc[j] = 0.f;
 #pragma unroll
-    for (int r = 0; r < T_KPT; ++r) {
-        const int u = table_key(r);
-        if (n4[r] == 0u || !key_finite(u, M.fmt)) continue;
-        const float G = G4[r];
-        const float v = key_value(u, M.fmt);
+    for (int q = 0; q < GPER; ++q) {
+        if (gv[q] == 0.f || !key_finite(key[q], M.fmt)) continue;
+        const float v = key_value(key[q], M.fmt);
         float a[K], d[K], c1m;
         attn_row_sel<K>(v, c0, b.s2, a, c1, c1m);
         centroid_dev<K>(a, c1, c1m, d);
 #pragma unroll
         for (int j = 0; j < K; ++j) {
-            const float ga = G * a[j];
+            const float ga = gv[q] * a[j];
             acc[j] += ga;
             acc[K + j] = fmaf(ga * d[j], sgnf(v - c0[j]), acc[K + j]);
         }
     }
-    block_sum<2 * K, T_THREADS>(acc, scratch, tot);
-    if (threadIdx.x < 2 * K)
-        ws.bpart[(size_t)blockIdx.x * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
+    block_sum<2 * K, MERGE_THREADS>(acc, scratch, tot);
+    if (threadIdx.x < 2 * K && tot[threadIdx.x] != 0.f) {
+        const int row = (blockIdx.x + 7 * blockIdx.y) % T_WG;   // spread over the rows
+        atomicAdd(&ws.bpart[(size_t)row * PSTRIDE + threadIdx.x], tot[threadIdx.x]);
+    }
 }
 
 // Iteration t = T..1 of the backward: gamma = dL/dC^(t), then per occupied
@@ -1892,12 +1917,12 @@ hipError_t noalloc_scratch(uint8_t** out) {
         if (e_ != hipSuccess) { *where = name; return e_; }              \
     } while (0)
 
-// Row chunks of the partial-row merges: enough for the matrix of the launch
-// with the most N-pass workgroups (one partial row each).
-static uint32_t merge_chunks(const BatchArgs& b) {
+// Row chunks of `per` rows for a partial-row merge: enough for the matrix of
+// the launch with the most N-pass workgroups (one partial row each).
+static uint32_t merge_chunks(const BatchArgs& b, int per = MERGE_ROWS) {
     uint32_t rows = 1;
     for (int i = 0; i < b.count; ++i) rows = b.m[i].wg_count > rows ? b.m[i].wg_count : rows;
-    return (rows + MERGE_ROWS - 1) / MERGE_ROWS;
+    return (rows + per - 1) / per;
 }
 
 template <int K>
@@ -1918,9 +1943,8 @@ static hipError_t backward_k(BatchArgs& b, uint32_t grid_np, int max_t, hipStrea
                              const PassEvents* ev) {
     const dim3 tg(T_WG, b.count);
     EDKM_NPASS(PASS_KEYED_GRAD, "k_keyed_grad", k_keyed_grad, dim3(grid_np), dim3(NP_THREADS), b);
-    EDKM_LAUNCH("k_grad_merge", k_grad_merge, dim3(2 * W4 / MERGE_THREADS, merge_chunks(b), b.count),
+    EDKM_LAUNCH("k_grad_top", k_grad_top<K>, dim3(MERGE_X, merge_chunks(b, GT_ROWS) + 1, b.count),
                 dim3(MERGE_THREADS), b);
-    EDKM_LAUNCH("k_bwd_top", k_bwd_top<K>, tg, dim3(T_THREADS), b);
     for (int t = max_t; t >= 1; --t) {
         b.t = t;
         EDKM_LAUNCH("k_bwd_iter", k_bwd_iter<K>, tg, dim3(T_THREADS), b);

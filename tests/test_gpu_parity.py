@@ -419,6 +419,39 @@ def test_empty_then_live_cluster(dense_path):
     check(res, ref, what="empty then live")
 
 
+@pytest.mark.parametrize("bits,eps", [(3, 0.0), (2, 1.0)])
+def test_backward_repeated_after_one_forward(bits, eps):
+    """Backward twice after one forward, with different upstream gradients:
+    each matches the oracle (the backward's first table partials are added
+    into a block that the forward clears and each backward clears after use).
+    eps = 1 stops after one iteration, where the gradient gather itself reads
+    that block."""
+    n = 300_007
+    keys = inputs.fp16_weights(n, 131)
+    k = 1 << bits
+    c0 = inputs.quantile_init(keys, k)
+    say("repeated backward", bits, eps)
+    plan = edkm.Plan(n, bits, ITERS)
+    kd = dkeys(keys)
+    c_in = torch.from_numpy(c0).to(DEV)
+    c_out = torch.empty(k, device=DEV)
+    wt = torch.empty(n, device=DEV)
+    it = torch.zeros(1, dtype=torch.int32, device=DEV)
+    edkm.init_unique(plan, kd)
+    edkm.forward(plan, kd, TAU, eps, c_in, c_out, wt, False, it)
+    ref_f = oracle(keys, c0, eps=eps)
+    assert int(it.item()) == ref_f["T"] and (eps == 0.0 or ref_f["T"] == 1)
+    for seed in (132, 133):
+        g = inputs.upstream_grad(n, seed)
+        gw = torch.empty(n, device=DEV)
+        gc = torch.empty(k, device=DEV)
+        edkm.backward(plan, kd, torch.from_numpy(g).to(DEV), gw, gc)
+        torch.cuda.synchronize()
+        ref = oracle(keys, c0, g, eps=eps)
+        assert_close(gw.cpu().numpy(), ref["gw"], TOL_BWD, "grad_w seed %d" % seed)
+        assert_close(gc.cpu().numpy(), ref["gc"], TOL_BWD, "grad_c seed %d" % seed)
+
+
 def test_forward_repeatable_and_exact_scaling():
     """Forward results are bitwise repeatable.  Scaling w, C^(0) and tau by 2 scales
     C and W~ by 2: bitwise on the dense path (same reduction order), and to
