@@ -327,11 +327,8 @@ __device__ __forceinline__ void block_sum(const float (&v)[NV], float* scratch, 
     __syncthreads();
 }
 
-// Reduce rows [0, T_WG) of a partial block (T_WG x PSTRIDE floats) for columns
-// [c0, c0 + ncol) into out[0..ncol) (LDS), by wave reductions.  Called by all
-// threads of a T_THREADS block.
-// Rows lane, lane + 64, ... of one column, summed in that order (one lane per
-// 64 rows).
+// Rows lane, lane + 64, ... of column col of a table partial block (T_WG x
+// PSTRIDE floats), summed in that order (one lane per 64 rows).
 __device__ __forceinline__ float tpart_rows(const float* part, int lane, int col) {
     float x = part[lane * PSTRIDE + col];
 #pragma unroll
@@ -339,25 +336,83 @@ __device__ __forceinline__ float tpart_rows(const float* part, int lane, int col
     return x;
 }
 
-__device__ __forceinline__ void reduce_tparts(const float* part, int c0, int ncol, float* out) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    for (int j = wave; j < ncol; j += T_THREADS / 64) {
-        float s = wave_sum(tpart_rows(part, lane, c0 + j));
-        if (lane == 0) out[j] = s;
-    }
-    __syncthreads();
+// Pairwise (tree-shaped) sum of N values, N a power of two, in a fixed order.
+template <int N>
+__device__ __forceinline__ float tree_sum(float (&x)[N]) {
+    static_assert(N >= 1 && (N & (N - 1)) == 0, "N: a power of two");
+#pragma unroll
+    for (int h = N / 2; h > 0; h /= 2)
+#pragma unroll
+        for (int q = 0; q < h; ++q) x[q] += x[q + h];
+    return x[0];
 }
 
-// As reduce_tparts for columns [0, ncol) of two partial blocks at once:
-// out[0..ncol) from pa, out[ncol..2 ncol) from pb.
-__device__ __forceinline__ void reduce_tparts2(const float* pa, const float* pb, int ncol, float* out) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    for (int j = wave; j < 2 * ncol; j += T_THREADS / 64) {
-        const float x = j < ncol ? tpart_rows(pa, lane, j) : tpart_rows(pb, lane, ncol + (j - ncol));
-        const float s = wave_sum(x);
-        if (lane == 0) out[j] = s;
+// Column totals of a table partial block (T_WG rows, PSTRIDE floats apart), in
+// a fixed tree order and with every load issued up front: virtual column c of
+// NC (a power of two, 4 <= NC <= T_THREADS) is read from src(c), a pointer to
+// its row 0 (null: a column not read).  Thread t holds rows [R s, R s + R) of
+// column c = t % NC, s = t / NC, R = T_WG NC / T_THREADS; stage() sums them
+// pairwise into red[t] (T_THREADS floats of LDS) and synchronises the block;
+// total(red, c) then sums the T_THREADS / NC segment sums of column c
+// pairwise.  (Wave reductions per column had each cost a chain of dependent
+// lane moves, and a kernel read its partial block only after its flags: two
+// round trips to memory and about 2 us per table launch.)
+template <int NC>
+struct PartCols {
+    static_assert(NC >= 4 && NC <= T_THREADS && (NC & (NC - 1)) == 0, "NC: a power of two in [4, T_THREADS]");
+    static constexpr int SEGS = T_THREADS / NC;
+    static constexpr int R = T_WG / SEGS;
+    static_assert(R >= 1, "at least one row per thread");
+    float x[R];
+    template <class Src>
+    __device__ __forceinline__ void load(Src src) {
+        const int c = threadIdx.x % NC, sg = threadIdx.x / NC;
+        const float* p = src(c);
+#pragma unroll
+        for (int r = 0; r < R; ++r) x[r] = p ? p[(size_t)(sg * R + r) * PSTRIDE] : 0.f;
     }
+    __device__ __forceinline__ void stage(float* red) {
+        red[threadIdx.x] = tree_sum<R>(x);
+        __syncthreads();
+    }
+    __device__ __forceinline__ static float total(const float* red, int c) {
+        float y[SEGS];
+#pragma unroll
+        for (int sg = 0; sg < SEGS; ++sg) y[sg] = red[sg * NC + c];
+        return tree_sum<SEGS>(y);
+    }
+};
+
+// Sum of NV per-thread values (NV a power of two dividing T_THREADS) over a
+// T_THREADS block, in a fixed tree order: thread NV s + j sums value j of
+// threads NV s .. NV s + NV - 1 pairwise, then thread j sums the T_THREADS /
+// NV segment sums pairwise.  Returns the total of value threadIdx.x in threads
+// [0, NV).  red: BLOCK_TOTAL_LDS(NV) floats of LDS; every thread
+// calls it.  (One dependent chain of lane moves per value had cost 0.8-2.5 us
+// per table kernel.)
+#define BLOCK_TOTAL_LDS(NV) (T_THREADS * ((NV) + 1) + T_THREADS)
+template <int NV>
+__device__ __forceinline__ float block_total(const float (&v)[NV], float* red) {
+    static_assert(NV <= T_THREADS && T_THREADS % NV == 0, "NV divides the block");
+    constexpr int LD = NV + 1;   // odd pitch: a value's rows fall in different banks
+    float* seg = red + T_THREADS * LD;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) red[threadIdx.x * LD + j] = v[j];
     __syncthreads();
+    const int j = threadIdx.x % NV, sg = threadIdx.x / NV;
+    float a[NV];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) a[i] = red[(sg * NV + i) * LD + j];
+    seg[threadIdx.x] = tree_sum<NV>(a);
+    __syncthreads();
+    float tot = 0.f;
+    if (threadIdx.x < NV) {
+        float y[T_THREADS / NV];
+#pragma unroll
+        for (int q = 0; q < T_THREADS / NV; ++q) y[q] = seg[q * NV + threadIdx.x];
+        tot = tree_sum<T_THREADS / NV>(y);
+    }
+    return tot;
 }
 
 // Matrix of an N-pass workgroup, and its slice [beg, end).
@@ -804,37 +859,43 @@ __device__ __forceinline__ int table_key(int r) {
 // P_j = sum n_u a_uj v_u.  Grid (T_WG, count).
 template <int K>
 __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
-    __shared__ float tot[2 * K];
-    __shared__ float scratch[T_THREADS / 64 * 2 * K];
+    __shared__ float red[BLOCK_TOTAL_LDS(2 * K)];
     __shared__ float csh[K];
     __shared__ int stop;
     const MatArgs& M = b.m[blockIdx.y];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const int t = b.t;
     if (t > M.max_iter) return;
-    // pattern counts do not depend on the centroids: issue their loads first
+    // every load first: the pattern counts, the previous iteration's partial
+    // block and C^(t-2), or c_in
     uint32_t n4[T_KPT];
 #pragma unroll
     for (int r = 0; r < T_KPT; ++r) n4[r] = ws.counts[table_key(r)];
+    PartCols<2 * K> pc;
+    float cprev = 0.f;
+    if (t > 1) {
+        const float* tp = ws.tpart + (size_t)(t - 1) * T_WG * PSTRIDE;
+        pc.load([&](int c) { return tp + c; });
+        if (threadIdx.x < K) cprev = ws.chist[(t - 2) * KMAX + threadIdx.x];
+    } else if (threadIdx.x < K) {
+        cprev = M.c_in[threadIdx.x];
+    }
     DevState* st = ws.st;
     const bool lead = blockIdx.x == 0;
     if (t == 1) {
         if (threadIdx.x < K) {
-            const float c = M.c_in[threadIdx.x];
-            csh[threadIdx.x] = c;
-            if (lead) { ws.chist[threadIdx.x] = c; ws.shist[threadIdx.x] = 0.f; }
+            csh[threadIdx.x] = cprev;
+            if (lead) { ws.chist[threadIdx.x] = cprev; ws.shist[threadIdx.x] = 0.f; }
         }
         if (lead && threadIdx.x == 0) { st->conv = 0; st->teff = 0; }
         __syncthreads();
     } else {
-        if (st->conv) return;
-        reduce_tparts(ws.tpart + (size_t)(t - 1) * T_WG * PSTRIDE, 0, 2 * K, tot);
         if (threadIdx.x == 0) stop = 0;
-        __syncthreads();
+        pc.stage(red);
+        if (st->conv) return;
         if (threadIdx.x < K) {
             const int j = threadIdx.x;
-            const float S = tot[j], P = tot[K + j];
-            const float cprev = ws.chist[(t - 2) * KMAX + j];
+            const float S = PartCols<2 * K>::total(red, j), P = PartCols<2 * K>::total(red, K + j);
             const float cn = S > 0.f ? P / S : cprev;
             csh[j] = cn;
             if (lead) { ws.chist[(t - 1) * KMAX + j] = cn; ws.shist[(t - 1) * KMAX + j] = S; }
@@ -868,9 +929,8 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
             acc[K + j] = fmaf(w, v, acc[K + j]);
         }
     }
-    block_sum<2 * K, T_THREADS>(acc, scratch, tot);
-    if (threadIdx.x < 2 * K)
-        ws.tpart[((size_t)t * T_WG + blockIdx.x) * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
+    const float tot = block_total<2 * K>(acc, red);
+    if (threadIdx.x < 2 * K) ws.tpart[((size_t)t * T_WG + blockIdx.x) * PSTRIDE + threadIdx.x] = tot;
 }
 
 // After the last iteration: C^(T), c_out, T; per occupied pattern the W~ value
@@ -879,15 +939,22 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
 // clears G.  Grid (T_WG, count).
 template <int K>
 __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
-    __shared__ float tot[2 * K];
+    __shared__ float red[T_THREADS];
     __shared__ float cT[K], cP[K];
     const MatArgs& M = b.m[blockIdx.y];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
-    uint32_t n4[T_KPT];   // independent of the centroids: loaded first
+    // every load first (the partial block and C^(T-1) of a run that did all
+    // max_iter iterations; an early stop reads its two rows afterwards)
+    uint32_t n4[T_KPT];
 #pragma unroll
     for (int r = 0; r < T_KPT; ++r) n4[r] = ws.counts[table_key(r)];
+    PartCols<2 * K> pc;
+    const float* tp = ws.tpart + (size_t)M.max_iter * T_WG * PSTRIDE;
+    pc.load([&](int c) { return tp + c; });
+    const float cprev = threadIdx.x < K ? ws.chist[(M.max_iter - 1) * KMAX + threadIdx.x] : 0.f;
     DevState* st = ws.st;
     const bool lead = blockIdx.x == 0;
+    pc.stage(red);
     int T;
     if (st->conv) {
         T = st->teff;
@@ -898,11 +965,9 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
         __syncthreads();
     } else {
         T = M.max_iter;
-        reduce_tparts(ws.tpart + (size_t)T * T_WG * PSTRIDE, 0, 2 * K, tot);
         if (threadIdx.x < K) {
             const int j = threadIdx.x;
-            const float S = tot[j], P = tot[K + j];
-            const float cprev = ws.chist[(T - 1) * KMAX + j];
+            const float S = PartCols<2 * K>::total(red, j), P = PartCols<2 * K>::total(red, K + j);
             const float cn = S > 0.f ? P / S : cprev;
             cT[j] = cn;
             cP[j] = cprev;
@@ -1445,8 +1510,8 @@ constexpr int MERGE_X = 2 * W4 / MERGE_THREADS;
 constexpr int GT_ROWS = 64;
 template <int K>
 __global__ void __launch_bounds__(MERGE_THREADS) k_grad_top(BatchArgs b) {
-    __shared__ float tot[2 * K];
-    __shared__ float scratch[MERGE_THREADS / 64 * 2 * K];
+    static_assert(MERGE_THREADS == T_THREADS, "block_total sums over T_THREADS");
+    __shared__ float red[BLOCK_TOTAL_LDS(2 * K)];
     constexpr int GPER = (NKEYS + MERGE_X * MERGE_THREADS - 1) / (MERGE_X * MERGE_THREADS);
     const MatArgs& M = b.m[blockIdx.z];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
@@ -1509,10 +1574,10 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_grad_top(BatchArgs b) {
             acc[K + j] = fmaf(ga * d[j], sgnf(v - c0[j]), acc[K + j]);
         }
     }
-    block_sum<2 * K, MERGE_THREADS>(acc, scratch, tot);
-    if (threadIdx.x < 2 * K && tot[threadIdx.x] != 0.f) {
+    const float tot = block_total<2 * K>(acc, red);
+    if (threadIdx.x < 2 * K && tot != 0.f) {
         const int row = (blockIdx.x + 7 * blockIdx.y) % T_WG;   // spread over the rows
-        atomicAdd(&ws.bpart[(size_t)row * PSTRIDE + threadIdx.x], tot[threadIdx.x]);
+        atomicAdd(&ws.bpart[(size_t)row * PSTRIDE + threadIdx.x], tot);
     }
 }
 
@@ -1525,49 +1590,57 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_grad_top(BatchArgs b) {
 // make dL/dC^(t-1).  Grid (T_WG, count).
 template <int K>
 __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
-    __shared__ float tot[2 * K];
-    __shared__ float scratch[T_THREADS / 64 * K];
-    __shared__ float gsh[K], gSsh[K], c1sh[K], c0sh[K];
+    __shared__ float red[BLOCK_TOTAL_LDS(K)];
+    __shared__ float gSsh[K], c1sh[K], c0sh[K];
     const MatArgs& M = b.m[blockIdx.y];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const DevState* st = ws.st;
-    const int T = st->teff;
     const int t = b.t;
-    if (t > T) return;
-    uint32_t n4[T_KPT];   // per-pattern inputs first: they do not depend on gamma
+    // Every load first, none waiting for T: the per-pattern inputs, the
+    // partial blocks (columns [0, 2K) of block 0 -- k_grad_top's, used at
+    // t = T and t = T - 1 -- and [0, K) of block t + 1), and the k-vectors of
+    // iterations t - 1, t, t + 1.
+    uint32_t n4[T_KPT];
     float R4[T_KPT], H4[T_KPT];
 #pragma unroll
     for (int r = 0; r < T_KPT; ++r) {
         const int u = table_key(r);
         n4[r] = ws.counts[u];
-        R4[r] = t != T ? ws.R[u] : 0.f;
+        R4[r] = t < M.max_iter ? ws.R[u] : 0.f;
         H4[r] = t == 1 ? ws.H[u] : 0.f;
     }
+    PartCols<4 * K> pc;
+    const float* b0 = ws.bpart;
+    const float* bn = t < M.max_iter ? ws.bpart + (size_t)(t + 1) * T_WG * PSTRIDE : nullptr;
+    pc.load([&](int c) -> const float* {
+        return c < 2 * K ? b0 + c : (c < 3 * K && bn ? bn + (c - 2 * K) : nullptr);
+    });
+    float hc1 = 0.f, hc0 = 0.f, hS = 0.f, hS1 = 0.f, hg1 = 0.f;
+    if (threadIdx.x < K) {
+        const int j = threadIdx.x;
+        hc1 = ws.chist[t * KMAX + j];
+        hc0 = ws.chist[(t - 1) * KMAX + j];
+        hS = ws.shist[t * KMAX + j];
+        if (t < M.max_iter) { hS1 = ws.shist[(t + 1) * KMAX + j]; hg1 = ws.ghist[(t + 1) * KMAX + j]; }
+    }
+    const int T = st->teff;
+    pc.stage(red);
+    if (t > T) return;
     const bool lead = blockIdx.x == 0;
-    if (t == T) {
-        reduce_tparts(ws.bpart, 0, K, tot);
-        if (threadIdx.x < K) gsh[threadIdx.x] = tot[threadIdx.x];
-    } else {
-        reduce_tparts2(ws.bpart + (size_t)(t + 1) * T_WG * PSTRIDE, ws.bpart, K, tot);
-        if (threadIdx.x < K) {
-            const int j = threadIdx.x;
-            float gm = tot[j] * b.inv_tau;
-            if (t + 1 == T) gm += tot[K + j] * b.inv_tau;
-            if (!(ws.shist[(t + 1) * KMAX + j] > 0.f)) gm += ws.ghist[(t + 1) * KMAX + j];
-            gsh[j] = gm;
+    if (threadIdx.x < K) {
+        const int j = threadIdx.x;
+        float gm;
+        if (t == T) {
+            gm = PartCols<4 * K>::total(red, j);
+        } else {
+            gm = PartCols<4 * K>::total(red, 2 * K + j) * b.inv_tau;
+            if (t + 1 == T) gm += PartCols<4 * K>::total(red, K + j) * b.inv_tau;
+            if (!(hS1 > 0.f)) gm += hg1;
         }
-    }
-    if (threadIdx.x < K) {
-        const int j = threadIdx.x;
-        c1sh[j] = ws.chist[t * KMAX + j];
-        c0sh[j] = ws.chist[(t - 1) * KMAX + j];
-    }
-    __syncthreads();
-    if (threadIdx.x < K) {
-        const int j = threadIdx.x;
-        const float S = ws.shist[t * KMAX + j];
-        gSsh[j] = S > 0.f ? gsh[j] / S : 0.f;
-        if (lead) ws.ghist[t * KMAX + j] = gsh[j];
+        c1sh[j] = hc1;
+        c0sh[j] = hc0;
+        gSsh[j] = hS > 0.f ? gm / hS : 0.f;
+        if (lead) ws.ghist[t * KMAX + j] = gm;
     }
     __syncthreads();
     float c1[K], c0[K], gS[K];
@@ -1597,13 +1670,12 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
             r_ += dl;
             acc[j] = fmaf(nf, dl, acc[j]);
         }
-        const float Ru = fmaf(-r_, b.inv_tau, direct) + R4[r];
+        const float Ru = fmaf(-r_, b.inv_tau, direct) + (t != T ? R4[r] : 0.f);
         if (t == 1) ws.HR[u] = make_float2(H4[r], Ru);
         else ws.R[u] = Ru;
     }
-    block_sum<K, T_THREADS>(acc, scratch, tot);
-    if (threadIdx.x < K)
-        ws.bpart[((size_t)t * T_WG + blockIdx.x) * PSTRIDE + threadIdx.x] = tot[threadIdx.x];
+    const float tot = block_total<K>(acc, red);
+    if (threadIdx.x < K) ws.bpart[((size_t)t * T_WG + blockIdx.x) * PSTRIDE + threadIdx.x] = tot;
 }
 
 // ----------------------------------------------------------------------------
