@@ -104,6 +104,7 @@ struct BatchArgs {
     float s2;                 // log2(e) / tau
     float inv_tau;
     float eps;
+    float keep_frac;          // fraction of each sweep read with cached loads (its end)
     uint8_t* pal_tab;         // palettization index table of the launch's single matrix
                               // (allocation-free entry point); null: each matrix's workspace
     // First N-pass workgroup of each matrix, ascending.  Kept together (not in

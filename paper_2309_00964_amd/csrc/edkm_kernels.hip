@@ -459,9 +459,13 @@ struct Slice {
 };
 
 // REV walks the same work in descending order (the rest first, then the rounds
-// from the last), so that the grid sweeps the matrix from its end.
+// from the last), so that the grid sweeps the matrix from its end.  ld(i, c)
+// loads with cached loads when c is std::true_type: for the tiles starting in
+// [c_lo, c_hi), the part of the sweep that the next pass can find in the
+// Infinity Cache; other tiles use non-temporal loads.
 template <int U, int GW, bool REV = false, class Ld, class Cp, class St, class F1>
-__device__ __forceinline__ void for_slice(const MatArgs& M, uint32_t wl, Ld ld, Cp cp, St st, F1 f1) {
+__device__ __forceinline__ void for_slice(const MatArgs& M, uint32_t wl, uint64_t c_lo, uint64_t c_hi, Ld ld,
+                                          Cp cp, St st, F1 f1) {
     const uint64_t n = M.n;
     const uint64_t a = M.wg_count;
     if (!M.vec) {
@@ -470,13 +474,13 @@ __device__ __forceinline__ void for_slice(const MatArgs& M, uint32_t wl, Ld ld, 
     }
     using S = Slice<U, GW>;
     const S sh(M);
-    using R = decltype(ld(0));
-    using O = decltype(cp(ld(0)));
-    auto round = [&](uint64_t q) {         // this workgroup's full tile of round q
-        const uint64_t i0 = ((uint64_t)wl + q * a) * S::TILE + (uint64_t)GW * threadIdx.x;
+    using R = decltype(ld(0, std::true_type{}));
+    using O = decltype(cp(R{}));
+    auto round_c = [&](uint64_t b0, auto cached) {   // a full tile at b0
+        const uint64_t i0 = b0 + (uint64_t)GW * threadIdx.x;
         R r[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) r[u] = ld(i0 + u * S::STEP);
+        for (int u = 0; u < U; ++u) r[u] = ld(i0 + u * S::STEP, cached);
         __builtin_amdgcn_sched_barrier(0);   // all U loads issue before any use
         O o[U];
 #pragma unroll
@@ -484,19 +488,28 @@ __device__ __forceinline__ void for_slice(const MatArgs& M, uint32_t wl, Ld ld, 
 #pragma unroll
         for (int u = 0; u < U; ++u) st(i0 + u * S::STEP, o[u]);
     };
+    auto round = [&](uint64_t q) {         // this workgroup's full tile of round q
+        const uint64_t b0 = ((uint64_t)wl + q * a) * S::TILE;
+        if (b0 >= c_lo && b0 < c_hi) round_c(b0, std::true_type{});
+        else round_c(b0, std::false_type{});
+    };
+    auto rest_c = [&](uint64_t b0, uint64_t s1, auto cached) {
+        const uint64_t i0 = b0 + (uint64_t)GW * threadIdx.x;
+        R r[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (i0 + u * S::STEP < s1) r[u] = ld(i0 + u * S::STEP, cached);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (i0 + u * S::STEP < s1) st(i0 + u * S::STEP, cp(r[u]));
+    };
     auto rest = [&]() {                    // this workgroup's steps of the rest
         const uint64_t s0 = sh.rest0 + (uint64_t)wl * sh.per * S::STEP;
         const uint64_t s1 = min(sh.nvec, s0 + sh.per * S::STEP);
         for (uint64_t b0 = s0; b0 < s1; b0 += S::TILE) {
-            const uint64_t i0 = b0 + (uint64_t)GW * threadIdx.x;
-            R r[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-                if (i0 + u * S::STEP < s1) r[u] = ld(i0 + u * S::STEP);
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-                if (i0 + u * S::STEP < s1) st(i0 + u * S::STEP, cp(r[u]));
+            if (b0 >= c_lo && b0 < c_hi) rest_c(b0, s1, std::true_type{});
+            else rest_c(b0, s1, std::false_type{});
         }
     };
     if (REV) {
@@ -508,6 +521,14 @@ __device__ __forceinline__ void for_slice(const MatArgs& M, uint32_t wl, Ld ld, 
     }
     if (wl == a - 1)
         for (uint64_t j = sh.nvec + threadIdx.x; j < n; j += NP_THREADS) f1(j);
+}
+
+// The cached part of a sweep over n weights: the last keep_frac of it, at the
+// end (top) of the matrix for a forward sweep, at its start for REV.
+__device__ __forceinline__ void cached_range(const BatchArgs& b, uint64_t n, bool rev, uint64_t& lo, uint64_t& hi) {
+    const uint64_t k = (uint64_t)((double)n * (double)b.keep_frac);
+    lo = rev ? 0 : n - k;
+    hi = rev ? k : ~0ull;
 }
 
 struct Nothing {};
@@ -525,10 +546,11 @@ typedef float v4f_t __attribute__((ext_vector_type(4)));
 // directions (histogram forward, W~ gather backward, keyed sum forward,
 // gradient gather backward), so the last ~256 MB a pass reads with plain
 // (cached) loads are still in the Infinity Cache where the next pass starts.
-// Plain loads for the keys in the histogram (for the W~ gather), the W~
-// gather (for the keyed sum) and the keyed sum (for the gradient gather);
-// the rest is non-temporal (nt), which a pass runs a little faster with when
-// nothing after it reads the same data.  The gathers' outputs use nt stores, float4
+// Plain loads for the end of the key sweep in the histogram (for the W~
+// gather), the W~ gather (for the keyed sum) and the keyed sum (for the
+// gradient gather), as much as the cache holds (set_keep_frac); the rest is
+// non-temporal (nt), which a pass runs a little faster with when nothing
+// after it reads the same data.  The gathers' outputs use nt stores, float4
 // or (16-bit W~) uint2: gradient gather 404 -> 381 us on the decoder layer,
 // 16-bit W~ gather 168 -> 162 us, and the kernel after the W~ gather no
 // longer inherits its dirty lines.
@@ -596,10 +618,12 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
         if (mag < (uint32_t)W4) atomicAdd(&h[(key >> 15) * W4 + mag], 1u);
         else atomicAdd(&gcounts[key], 1u);
     };
-    // Plain (cached) loads: the tail of this forward sweep stays in the
-    // Infinity Cache, where the W~ gather, sweeping backwards, starts.
-    for_slice<4, 8>(M, wl,
-        [&](uint64_t i) { return Keys8{ld_u4(keys + i)}; },
+    // Cached loads at the end of this forward sweep: it stays in the Infinity
+    // Cache, where the W~ gather, sweeping backwards, starts.
+    uint64_t c_lo, c_hi;
+    cached_range(b, M.n, false, c_lo, c_hi);
+    for_slice<4, 8>(M, wl, c_lo, c_hi,
+        [&](uint64_t i, auto c) { return Keys8{c ? ld_u4(keys + i) : ld_u4_nt(keys + i)}; },
         [&](const Keys8& r) {
             add(r.q.x & 0xFFFFu); add(r.q.x >> 16);
             add(r.q.y & 0xFFFFu); add(r.q.y >> 16);
@@ -1042,13 +1066,15 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
         return make_float4(look(k0), look(k1), look(k2), look(k3));
     };
     const uint16_t* keys = M.keys;
+    uint64_t c_lo, c_hi;
+    cached_range(b, M.n, true, c_lo, c_hi);
     if (b.out_half) {
         uint16_t* out = reinterpret_cast<uint16_t*>(M.wt);
         auto h2 = [&](float a, float c) -> uint32_t {
             return to_half_bits(a, M.fmt) | (to_half_bits(c, M.fmt) << 16);
         };
-        for_slice<16, 4, true>(M, wl,
-            [&](uint64_t i) { return Keys4{ld_u2(keys + i)}; },
+        for_slice<16, 4, true>(M, wl, c_lo, c_hi,
+            [&](uint64_t i, auto c) { return Keys4{c ? ld_u2(keys + i) : ld_u2_nt(keys + i)}; },
             [&](const Keys4& r) {
                 const float4 v = look4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16);
                 return make_uint2(h2(v.x, v.y), h2(v.z, v.w));
@@ -1057,8 +1083,8 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
             [&](uint64_t i) { out[i] = (uint16_t)to_half_bits(look(keys[i]), M.fmt); });
     } else {
         float* out = reinterpret_cast<float*>(M.wt);
-        for_slice<16, 4, true>(M, wl,
-            [&](uint64_t i) { return Keys4{ld_u2(keys + i)}; },
+        for_slice<16, 4, true>(M, wl, c_lo, c_hi,
+            [&](uint64_t i, auto c) { return Keys4{c ? ld_u2(keys + i) : ld_u2_nt(keys + i)}; },
             [&](const Keys4& r) {
                 return look4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16);
             },
@@ -1137,11 +1163,13 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
     }
     __syncthreads();
     float* G = ws.G;
-    // Keys cached, g non-temporal: the tail of the keys stays in the Infinity
-    // Cache for the gradient gather, which sweeps backwards.
+    uint64_t c_lo, c_hi;
+    cached_range(b, M.n, false, c_lo, c_hi);
+    // The end of the key sweep cached, g non-temporal: those keys stay in the
+    // Infinity Cache for the gradient gather, which sweeps backwards.
     auto stream = [&](auto add) {
-        for_slice<4, 4>(M, wl,
-            [&](uint64_t i) { return KeysG4{ld_u2(keys + i), ld_f4_nt(g + i)}; },
+        for_slice<4, 4>(M, wl, c_lo, c_hi,
+            [&](uint64_t i, auto c) { return KeysG4{c ? ld_u2(keys + i) : ld_u2_nt(keys + i), ld_f4_nt(g + i)}; },
             [&](const KeysG4& r) {
                 add(r.q.x & 0xFFFFu, r.g.x); add(r.q.x >> 16, r.g.y);
                 add(r.q.y & 0xFFFFu, r.g.z); add(r.q.y >> 16, r.g.w);
@@ -1197,8 +1225,8 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
             if (((old ^ sum) & (q ^ sum)) < 0) atomicAdd(&G[key], q > 0 ? wrap : -wrap);
         };
         struct Pend4 { uint2 keys; int q[4], old[4]; };
-        for_slice<3, 4>(M, wl,
-            [&](uint64_t i) { return KeysG4{ld_u2(keys + i), ld_f4_nt(g + i)}; },   // as above
+        for_slice<3, 4>(M, wl, c_lo, c_hi,
+            [&](uint64_t i, auto c) { return KeysG4{c ? ld_u2(keys + i) : ld_u2_nt(keys + i), ld_f4_nt(g + i)}; },
             [&](const KeysG4& r) {
                 Pend4 p;
                 p.keys = r.q;
@@ -1296,8 +1324,8 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
         const float2 h = look(key);
         return fmaf(gv, h.x, h.y);
     };
-    for_slice<8, 4, true>(M, wl,
-        [&](uint64_t i) { return KeysG4{ld_u2_nt(keys + i), ld_f4_nt(g + i)}; },
+    for_slice<8, 4, true>(M, wl, 0, 0,
+        [&](uint64_t i, auto) { return KeysG4{ld_u2_nt(keys + i), ld_f4_nt(g + i)}; },
         [&](const KeysG4& r) { return dw4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16, r.g); },
         [&](uint64_t i, float4 o) { st_f4_nt(out + i, o); },
         [&](uint64_t i) { out[i] = dw(keys[i], g[i]); });
@@ -1479,8 +1507,8 @@ __global__ void __launch_bounds__(NP_THREADS) k_inverse(BatchArgs b) {
     const uint16_t* keys = M.keys;
     uint16_t* out = reinterpret_cast<uint16_t*>(M.wt);
     auto pair = [&](uint32_t x) { return (uint32_t)rk[x & 0xFFFFu] | ((uint32_t)rk[x >> 16] << 16); };
-    for_slice<8, 8>(M, wl,
-        [&](uint64_t i) { return Keys8{ld_u4_nt(keys + i)}; },
+    for_slice<8, 8>(M, wl, 0, 0,
+        [&](uint64_t i, auto) { return Keys8{ld_u4_nt(keys + i)}; },
         [&](const Keys8& r) { return make_uint4(pair(r.q.x), pair(r.q.y), pair(r.q.z), pair(r.q.w)); },
         [&](uint64_t i, uint4 o) { st_u4_nt(out + i, o); },
         [&](uint64_t i) { out[i] = rk[keys[i]]; });
@@ -2053,6 +2081,19 @@ static hipError_t backward_dense_k(BatchArgs& b, uint32_t nwg, hipStream_t s, co
     return hipSuccess;
 }
 
+// Cached loads for the last IC_KEEP_KEYS keys of a pass's sweeps (spread over
+// the launch's matrices in proportion), non-temporal loads before: only the
+// end of a sweep, as many keys as fill the 256 MB Infinity Cache, can still be
+// there when the next pass starts, and non-temporal loads stream faster
+// (histogram of the decoder layer's 202M keys: 74 us all non-temporal, 78 us
+// all cached).
+constexpr double IC_KEEP_KEYS = 134217728.0;   // 256 MB of 16-bit keys
+static void set_keep_frac(BatchArgs& b) {
+    double n = 0.0;
+    for (int i = 0; i < b.count; ++i) n += (double)b.m[i].n;
+    b.keep_frac = n <= IC_KEEP_KEYS ? 1.0f : (float)(IC_KEEP_KEYS / n);
+}
+
 #define EDKM_DISPATCH_K(k, fn, ...)            \
     switch (k) {                               \
     case 2: return fn<2>(__VA_ARGS__);         \
@@ -2065,6 +2106,7 @@ static hipError_t backward_dense_k(BatchArgs& b, uint32_t nwg, hipStream_t s, co
 hipError_t launch_init_unique(BatchArgs& b, uint32_t grid_np, hipStream_t s, const char** where,
                               const PassEvents* ev) {
     (void)hipGetLastError();   // an earlier, unrelated failure is not ours to report
+    set_keep_frac(b);
     EDKM_LAUNCH("k_init_zero", k_init_zero, dim3(T_WG, b.count), dim3(T_THREADS), b);
     EDKM_NPASS(PASS_HIST, "k_hist", k_hist, dim3(grid_np), dim3(NP_THREADS), b);
     EDKM_LAUNCH("k_hist_merge", k_hist_merge, dim3(W4 / MERGE_THREADS, merge_chunks(b), b.count),
@@ -2076,12 +2118,14 @@ hipError_t launch_init_unique(BatchArgs& b, uint32_t grid_np, hipStream_t s, con
 hipError_t launch_forward(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_t s, const char** where,
                           const PassEvents* ev) {
     (void)hipGetLastError();
+    set_keep_frac(b);
     EDKM_DISPATCH_K(b.m[0].k, forward_k, b, grid_np, max_t, s, where, ev);
 }
 
 hipError_t launch_backward(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_t s, const char** where,
                            const PassEvents* ev) {
     (void)hipGetLastError();
+    set_keep_frac(b);
     EDKM_DISPATCH_K(b.m[0].k, backward_k, b, grid_np, max_t, s, where, ev);
 }
 
