@@ -336,14 +336,16 @@ __device__ __forceinline__ float tpart_rows(const float* part, int lane, int col
     return x;
 }
 
-// Pairwise (tree-shaped) sum of N values, N a power of two, in a fixed order.
+// Pairwise (tree-shaped) sum of N values, N a power of two: neighbours first,
+// (0 1) (2 3) ..., then (0..1 2..3) ..., so that sums taken level by level
+// over the bits of an index, low bits first, form one binary tree over it.
 template <int N>
 __device__ __forceinline__ float tree_sum(float (&x)[N]) {
     static_assert(N >= 1 && (N & (N - 1)) == 0, "N: a power of two");
 #pragma unroll
-    for (int h = N / 2; h > 0; h /= 2)
+    for (int h = 1; h < N; h *= 2)
 #pragma unroll
-        for (int q = 0; q < h; ++q) x[q] += x[q + h];
+        for (int q = 0; q < N; q += 2 * h) x[q] += x[q + h];
     return x[0];
 }
 
@@ -1008,8 +1010,6 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
         }
         if (threadIdx.x == 0 && M.iters_out) *M.iters_out = T;
     }
-    // the backward's first partial block, which k_grad_top adds into
-    if (threadIdx.x < PSTRIDE) ws.bpart[(size_t)blockIdx.x * PSTRIDE + threadIdx.x] = 0.f;
     float c1[K], c0[K];
 #pragma unroll
     for (int j = 0; j < K; ++j) { c1[j] = cT[j]; c0[j] = cP[j]; }
@@ -1141,6 +1141,10 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
         for (int i = threadIdx.x; i < n16; i += NP_THREADS) reinterpret_cast<uint4*>(lds)[i] = uint4{0u, 0u, 0u, 0u};
     }
     if (threadIdx.x == 0) { emax_sh = 0; esum_sh = 0; ecnt_sh = 0; }
+    // Clear the backward's first partial block, which k_grad_top adds into
+    // next; the previous backward's reads of it are over.
+    for (uint32_t i = wl * NP_THREADS + threadIdx.x; i < (uint32_t)(T_WG * PSTRIDE); i += M.wg_count * NP_THREADS)
+        ws.bpart[i] = 0.f;
     __syncthreads();
     {   // sample: 64 consecutive values per wave, the waves' runs spread over the
         // matrix (one value per thread at scattered indices had cost a 128-byte
@@ -1275,25 +1279,21 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
     const DevState* st = ws.st;
     const int lo = st->lo8, w = st->w8;
     const float2* HR = ws.HR;
-    if (wl == 0 && threadIdx.x < 64) {
-        // dL/dC^(0) = (1/tau) sum of the t = 1 partials + the terms that bypass the softmax
-        const int T = st->teff, k = M.k;
+    if (wl == 0 && (int)(threadIdx.x >> 6) < M.k) {
+        // dL/dC^(0) = (1/tau) sum of the t = 1 partials + the terms that bypass
+        // the softmax; wave j takes centroid j (one wave doing all k had held
+        // this workgroup back by about 3 us, and with it the whole pass)
+        const int T = st->teff, k = M.k, j = threadIdx.x >> 6, lane = threadIdx.x & 63;
         const float* p1 = ws.bpart + (size_t)1 * T_WG * PSTRIDE;
         const float* p0 = ws.bpart;
-        for (int j = 0; j < k; ++j) {
-            const float x = wave_sum(tpart_rows(p1, threadIdx.x, j));
-            const float e = wave_sum(tpart_rows(p0, threadIdx.x, k + j));
-            if (threadIdx.x == 0) {
-                float gc = x * b.inv_tau;
-                if (T == 1) gc += e * b.inv_tau;
-                if (!(ws.shist[KMAX + j] > 0.f)) gc += ws.ghist[KMAX + j];
-                M.gc[j] = gc;
-            }
+        const float x = wave_sum(tpart_rows(p1, lane, j));
+        const float e = wave_sum(tpart_rows(p0, lane, k + j));
+        if (lane == 0) {
+            float gc = x * b.inv_tau;
+            if (T == 1) gc += e * b.inv_tau;
+            if (!(ws.shist[KMAX + j] > 0.f)) gc += ws.ghist[KMAX + j];
+            M.gc[j] = gc;
         }
-        // the first partial block is read: clear it for the next backward's
-        // k_grad_top (a lane clears rows it read itself)
-        for (int r = threadIdx.x; r < T_WG; r += 64)
-            for (int c = 0; c < PSTRIDE; ++c) ws.bpart[(size_t)r * PSTRIDE + c] = 0.f;
     }
     {
         const uint32_t per = (NKEYS + M.wg_count - 1) / M.wg_count;
@@ -1527,8 +1527,8 @@ __global__ void __launch_bounds__(NP_THREADS) k_inverse(BatchArgs b) {
 // what the keyed-sum pass added to the global G instead (patterns outside the
 // window, values above its fixed-point limit, wrap corrections), over all
 // 65,536 patterns.  Block totals are added with float atomics into the 64 rows
-// of the backward's first partial block, which k_fwd_out clears and
-// k_gather_grad clears again after use.  (Summing the rows into G first, then
+// of the backward's first partial block, which k_keyed_grad clears.
+// (Summing the rows into G first, then
 // a table kernel over G, took one launch more.)  Grid (MERGE_X, row chunks +
 // 1, count).
 constexpr int MERGE_X = 2 * W4 / MERGE_THREADS;

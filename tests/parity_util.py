@@ -32,6 +32,58 @@ def assert_close(x, ref, tol, what=""):
     assert l2 <= tol and worst <= tol, "%s: rel_l2=%.3e worst=%.3e tol=%.1e" % (what, l2, worst, tol)
 
 
+# fp32 rounding of one iterate moves it by at most half an ulp; the GPU's
+# iterates are tree sums over the 65,536 patterns (16 levels) and a quotient,
+# so they may sit several ulps from the fp64 ones.
+COND_ULPS = 16.0
+
+
+def iterate_sensitivity(keys, c0, g, tau, iters, reps=3, seed=0, fmt="fp16"):
+    """How far the fp64 oracle's results move when every iterate C^(t), t >= 1,
+    is moved up or down by one fp32 ulp at random (reps draws, largest change
+    per element): the conditioning of the case at fp32 resolution of the
+    iterates.  Each step is the oracle's own iteration (table form, one
+    iteration from the moved iterate); c0 is an fp32 input and stays exact.
+    Returns (dW~, dgrad_w, dgrad_c) per element."""
+    from oracle import table
+    c0 = np.asarray(c0, np.float64)
+    g = np.asarray(g, np.float64)
+    f = table.forward(keys, c0, tau, iters, fmt=fmt)
+    gw, gc, _ = table.backward(keys, f, g)
+    dwt, dgw, dgc = (np.zeros_like(f["w_tilde"]), np.zeros_like(gw), np.zeros_like(gc))
+    rng = np.random.default_rng(seed)
+    for _ in range(reps):
+        ch, sh = [c0], [np.zeros_like(c0)]
+        last = None
+        for _t in range(iters):
+            last = table.forward(keys, ch[-1], tau, 1, counts=f["counts"], fmt=fmt)
+            c = last["c_hist"][1]
+            ch.append(c * (1.0 + rng.choice([-1.0, 1.0], c.size) * 2.0 ** -24))
+            sh.append(last["s_hist"][1])
+        fp = dict(f, c_hist=np.array(ch), s_hist=np.array(sh))
+        gwp, gcp, _ = table.backward(keys, fp, g)
+        dwt = np.maximum(dwt, np.abs(last["w_tilde"] - f["w_tilde"]))
+        dgw = np.maximum(dgw, np.abs(gwp - gw))
+        dgc = np.maximum(dgc, np.abs(gcp - gc))
+    return dwt, dgw, dgc
+
+
+def assert_close_conditioned(x, ref, sens, tol, what=""):
+    """assert_close with each element also allowed COND_ULPS times its
+    iterate sensitivity (iterate_sensitivity): rel-L2 <= tol as always, and
+    |x_i - ref_i| <= tol (|ref_i| + med|ref|) + COND_ULPS sens_i.  For a
+    well-conditioned element sens_i is orders below the first term."""
+    assert np.all(np.isfinite(np.asarray(x))), "%s has non-finite entries" % what
+    x = np.asarray(x, np.float64).ravel()
+    ref = np.asarray(ref, np.float64).ravel()
+    sens = np.asarray(sens, np.float64).ravel()
+    l2, _ = rel_errors(x, ref)
+    floor = float(np.median(np.abs(ref)))
+    excess = np.abs(x - ref) - tol * (np.abs(ref) + floor) - COND_ULPS * sens
+    assert l2 <= tol and np.all(excess <= 0), "%s: rel_l2=%.3e, %d entries beyond tol + conditioning" % (
+        what, l2, int((excess > 0).sum()))
+
+
 def assert_fp16_within_ulp(x_bits, ref, what="fp16 W~"):
     """x_bits: uint16 patterns; ref: fp64 oracle values."""
     x = np.asarray(x_bits, np.uint16).view(np.float16).astype(np.float64)

@@ -20,8 +20,8 @@ from oracle import dense, table                                  # noqa: E402
 from paper_2309_00964_amd import edkm, inputs                     # noqa: E402
 from paper_2309_00964_amd.runner import run                       # noqa: E402
 from parity_util import (EMPTY_THEN_LIVE, TOL_BWD, TOL_FWD,  # noqa: E402
-                         assert_bf16_within_ulp, assert_close, assert_fp16_within_ulp,
-                         empty_then_live_inputs)
+                         assert_bf16_within_ulp, assert_close, assert_close_conditioned,
+                         assert_fp16_within_ulp, empty_then_live_inputs, iterate_sensitivity)
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -222,7 +222,13 @@ def test_special_values_and_wide_range():
 
 def test_wide_magnitude_span_exceeds_windows():
     """Occupied magnitudes spanning more than the LDS windows: the densest part
-    is windowed, the rest is read through the global table."""
+    is windowed, the rest is read through the global table.  With centroids out
+    to 3.7e4 and tau = 2e-3, one fp32 ulp of an iterate shifts the softmax
+    boundaries by up to ulp(C)/tau: patterns near a boundary have gradients
+    that move by up to about 1e-3 of their size when the iterates are rounded
+    (fp64 oracle, see iterate_sensitivity).  Elementwise, each output is
+    compared within the tolerance plus that conditioning; rel-L2 and the counts
+    are held to the usual bars."""
     rng = np.random.default_rng(61)
     n = 150_000
     logs = rng.uniform(-24, 15.9, n)
@@ -234,7 +240,13 @@ def test_wide_magnitude_span_exceeds_windows():
     say("wide span")
     res = gpu(keys, c0, 3, g=g, want_counts=True)
     assert np.array_equal(res["counts"].view(np.uint32), table.histogram(keys))
-    check(res, oracle(keys, c0, g), what="wide span")
+    ref = oracle(keys, c0, g)
+    dwt, dgw, dgc = iterate_sensitivity(keys, c0, g, TAU, ITERS)
+    assert int(res["iters"][0]) == ref["T"]
+    assert_close(res["c_out"], ref["c_out"], TOL_FWD, "wide span c_out")
+    assert_close_conditioned(res["w_tilde"], ref["w_tilde"], dwt, TOL_FWD, "wide span w_tilde")
+    assert_close_conditioned(res["grad_w"], ref["gw"], dgw, TOL_BWD, "wide span grad_w")
+    assert_close_conditioned(res["grad_c"], ref["gc"], dgc, TOL_BWD, "wide span grad_c")
 
 
 def test_nonfinite_weights():
