@@ -803,7 +803,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
     nu = wave_reduce(nu, 0, op_add);
     nf = wave_reduce(nf, 0, op_or);
     sq = wave_sum_u64(sq);
-    // each wave's results go to slots of its own; one thread combines them after
+    // each wave's results go to slots of its own; wave 0 combines them after
     // the barrier (no LDS word is written by two waves)
     if (lane == 0) {
         woff[wave + 1] = carry;
@@ -814,20 +814,23 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
         wsq[wave] = sq;
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-        woff[0] = 0u;
-        int r0 = 1 << 30, r1 = -1, r2 = 0, r3 = 0;
-        unsigned long long q = 0ull;
-        for (int w = 0; w < NW; ++w) {
-            woff[w + 1] += woff[w];
-            r0 = min(r0, wred[0][w]);
-            r1 = max(r1, wred[1][w]);
-            r2 += wred[2][w];
-            r3 |= wred[3][w];
-            q += wsq[w];
+    if (wave == 0) {
+        // wave 0 combines the NW slots, lane w taking wave w's (a serial loop
+        // over them in one thread, each step waiting on the previous LDS
+        // write, had taken 4 of this kernel's 7.5 us)
+        const bool in = lane < NW;
+        const uint32_t x = wave_incl_scan(in ? woff[lane + 1] : 0u);
+        const int r0 = wave_reduce(in ? wred[0][lane] : 0x7FFFFFFF, 0x7FFFFFFF, op_min);
+        const int r1 = wave_reduce(in ? wred[1][lane] : -0x7FFFFFFF - 1, -0x7FFFFFFF - 1, op_max);
+        const int r2 = wave_reduce(in ? wred[2][lane] : 0, 0, op_add);
+        const int r3 = wave_reduce(in ? wred[3][lane] : 0, 0, op_or);
+        const unsigned long long q = wave_sum_u64(in ? wsq[lane] : 0ull);
+        if (in) woff[lane + 1] = x;
+        if (lane == 0) {
+            woff[0] = 0u;
+            red[0] = r0; red[1] = r1; red[2] = r2; red[3] = r3;
+            sqsum = q;
         }
-        red[0] = r0; red[1] = r1; red[2] = r2; red[3] = r3;
-        sqsum = q;
     }
     __syncthreads();
     const int mlo = red[0], mhi = red[1];
