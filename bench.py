@@ -38,6 +38,10 @@ Other modes (measurement helpers):
                               into profiles/hbm_traffic.json
   --dram-summary DIR...       turn rocprofv3 --pmc runs of the DRAM request counters into
                               profiles/dram_traffic.json (HBM bytes vs Infinity Cache hits)
+  --block-timeline OUT.md     run the workload (decoder_layer, attn_proj_4096x4096,
+                              mlp_outliers, single_256x256) on the diagnostics build
+                              libedkm_stamps.so and write each launch's block timeline
+                              of one step (start, span, gap, phases, per-XCC ends)
 """
 import argparse
 import ctypes
@@ -697,6 +701,155 @@ def dram_summary(dirs):
     print(json.dumps(res))
 
 
+# record shape of the diagnostics build (EDKM_STAMP_* of include/edkm_stamps.h)
+STAMP_LAUNCHES, STAMP_BLOCKS, STAMP_WORDS = 96, 4096, 8
+TIMELINE_PHASES = {   # phase marks (record words 2..5) of the instrumented kernels
+    "k_hist": ("keys streamed", "span found"),
+    "k_window": ("wave 0 scanned", "block totals combined", "windows chosen"),
+    "k_fwd_iter": ("loads issued", "partials summed, C formed", "patterns done", "block summed"),
+    "k_bwd_iter": ("loads issued", "partials summed, gamma formed", "patterns done", "block summed"),
+}
+
+
+def block_timeline(args):
+    """Per-block wall-clock stamps of one step, from the diagnostics build
+    (libedkm_stamps.so: the product sources compiled with EDKM_BLOCK_STAMPS),
+    summarised per launch: when its first block started and its last block
+    ended relative to the step's first block, the gap after the previous
+    launch, block durations, the phase marks of the instrumented kernels and,
+    for the kernels with one block per CU or more, when the blocks of each XCC
+    had finished.  Medians over `reps` steps after `warmup` untimed ones."""
+    import numpy as np
+    import torch
+    from paper_2309_00964_amd import build, edkm, inputs
+    if os.path.abspath(edkm.LIB_PATH) != os.path.abspath(build.OUT_STAMPS):
+        sys.exit("--block-timeline: %s is loaded, not the diagnostics build %s"
+                 % (edkm.LIB_PATH, build.OUT_STAMPS))
+    lib = edkm._lib
+    lib.edkm_stamps_dump.argtypes = [ctypes.c_void_p, ctypes.c_char_p]
+    L, B, W = STAMP_LAUNCHES, STAMP_BLOCKS, STAMP_WORDS
+    work = {"decoder_layer": (4, 3, False), "attn_proj_4096x4096": (2, 3, False),
+            "mlp_outliers": (3, 4, True), "single_256x256": (1, 3, False)}
+    if args.workload not in work:
+        sys.exit("--block-timeline: workload %s has no timeline" % args.workload)
+    cfg, bits, outl = work[args.workload]
+    bits = args.bits or bits
+    m = Matrices(cfg, inputs.WORKLOADS[cfg]["mats"], bits, outliers=outl, fmt=args.key_format)
+    for _ in range(args.warmup):
+        m.step()
+    torch.cuda.synchronize()
+    rate = lib.edkm_stamps_clock_khz() * 1e3
+    if rate <= 0:
+        sys.exit("--block-timeline: no stamp clock rate")
+    reps = 7
+    raw = []
+    for _ in range(reps):
+        if lib.edkm_stamps_reset() != 0:
+            sys.exit("--block-timeline: edkm_stamps_reset failed")
+        m.step()
+        torch.cuda.synchronize()
+        buf = np.zeros(L * B * W, np.uint64)
+        names = ctypes.create_string_buffer(L * 32)
+        n = lib.edkm_stamps_dump(buf.ctypes.data, names)
+        if n < 0 or n > L:
+            sys.exit("--block-timeline: %d launches (record holds %d)" % (n, L))
+        nm = [names.raw[i * 32:(i + 1) * 32].split(b"\0")[0].decode() for i in range(n)]
+        raw.append((nm, buf.reshape(L, B, W)[:n]))
+    cmd = "python bench.py --workload %s%s --block-timeline %s" % (
+        args.workload, "" if args.key_format == "fp16" else " --key-format " + args.key_format,
+        args.block_timeline)
+    title = "%s (%d weights, %d-bit, %s)" % (args.workload, m.total, bits, m.fmt)
+    text = timeline_report(raw, rate, title, cmd, args.warmup)
+    with open(args.block_timeline, "w") as f:
+        f.write(text)
+    print(text, flush=True)
+    return None
+
+
+def timeline_report(raw, rate, title, cmd, warmup):
+    """Markdown summary of stamp records: raw = [(launch names, uint64 array
+    [launches, blocks, STAMP_WORDS]) per step], rate = stamp clock in Hz."""
+    import numpy as np
+    W = STAMP_WORDS
+    reps = len(raw)
+    names0 = raw[0][0]
+    if any(r[0] != names0 for r in raw):
+        raise ValueError("the launch sequence changed between steps")
+    scale = np.where(np.arange(W) < 7, 1e6 / rate, 1.0)
+    steps = []
+    for _, ts in raw:
+        recs = [ts[q][ts[q][:, 0] > 0].astype(np.float64) for q in range(len(names0))]
+        if any(len(r) == 0 for r in recs):
+            raise ValueError("a launch has no block records")
+        t0 = min(r[:, 0].min() for r in recs)
+        # words 0..6 to microseconds from the step's first block start (a phase
+        # mark that was not reached becomes negative); word 7 (XCC id) as is
+        steps.append([(r - np.where(np.arange(W) < 7, t0, 0.0)) * scale for r in recs])
+    med = lambda xs: float(np.median(xs))
+    rows = []
+    for q, name in enumerate(names0):
+        start = med([s_[q][:, 0].min() for s_ in steps])
+        end = med([s_[q][:, 1].max() for s_ in steps])
+        gap = med([s_[q][:, 0].min() - s_[q - 1][:, 1].max() for s_ in steps]) if q else 0.0
+        dur = med([med(s_[q][:, 1] - s_[q][:, 0]) for s_ in steps])
+        dmax = med([(s_[q][:, 1] - s_[q][:, 0]).max() for s_ in steps])
+        rows.append((name, len(steps[0][q]), start, end - start, gap, dur, dmax))
+    span = med([max(r_[:, 1].max() for r_ in s_) for s_ in steps])
+    out = ["# Block timeline of one step: " + title,
+           "", "```", cmd, "```", "",
+           "Diagnostics build libedkm_stamps.so (the product sources with EDKM_BLOCK_STAMPS): every block "
+           "stamps the GPU wall clock (%.0f MHz) at entry and exit and its XCC id.  Medians over %d steps "
+           "after %d warm-up steps; times in microseconds from the step's first block start.  A launch's "
+           "span runs from its first block start to its last block end; its gap from the previous launch's "
+           "last block end to its first block start." % (rate / 1e6, reps, warmup), "",
+           "| # | Kernel | Blocks | Start | Span | Gap before | Block median | Block max |",
+           "|---|---|---|---|---|---|---|---|"]
+    for q, r in enumerate(rows):
+        out.append("| %d | %s | %d | %.1f | %.1f | %.1f | %.1f | %.1f |" % ((q,) + r))
+    tot = {}
+    for r in rows:
+        t = tot.setdefault(r[0], [0, 0.0, 0.0])
+        t[0] += 1
+        t[1] += r[3]
+        t[2] += r[4]
+    out += ["", "Step %.1f us: launch spans %.1f us, gaps %.1f us." % (
+        span, sum(r[3] for r in rows), sum(r[4] for r in rows)), "",
+        "| Kernel | Launches | Spans | Gaps before |", "|---|---|---|---|"]
+    for k_, (c, sp, gp) in sorted(tot.items(), key=lambda kv: -kv[1][1]):
+        out.append("| %s | %d | %.1f | %.1f |" % (k_, c, sp, gp))
+    mid = steps[reps // 2]
+    ph = []
+    for q, name in enumerate(names0):
+        labels = TIMELINE_PHASES.get(name)
+        v = mid[q]
+        if not labels or not (v[:, 2] > 0).any():
+            continue
+        cols = [0] + [2 + i for i in range(len(labels)) if (v[:, 2 + i] > 0).all()] + [1]
+        lab = lambda c: "entry" if c == 0 else "end" if c == 1 else labels[c - 2]
+        seg = ["%s -> %s %.2f" % (lab(a), lab(b_), med(v[:, b_] - v[:, a])) for a, b_ in zip(cols[:-1], cols[1:])]
+        ph.append("| %d | %s | %s |" % (q, name, "; ".join(seg)))
+    if ph:
+        out += ["", "Phases (block medians of the middle step, us):", "", "| # | Kernel | Phases |",
+                "|---|---|---|"] + ph
+    xr = []
+    for q, name in enumerate(names0):
+        v = mid[q]
+        if len(v) < 64:
+            continue
+        x = v[:, 7].astype(np.int64) & 0xF
+        s0 = v[:, 0].min()
+        ends = {c: v[x == c, 1].max() - s0 for c in range(16) if (x == c).any()}
+        blocks = {c: int((x == c).sum()) for c in ends}
+        xr.append("| %d | %s | %s | %.1f |" % (q, name, " ".join("%d:%d/%.1f" % (c, blocks[c], ends[c])
+                                                                    for c in ends),
+                                            max(ends.values()) - min(ends.values())))
+    if xr:
+        out += ["", "Per-XCC finish of the launches with 64 blocks or more (middle step): XCC:blocks/last block "
+                "end from the launch's first block start (us), and the spread between the first and last XCC "
+                "to finish.", "", "| # | Kernel | XCC:blocks/end | Spread |", "|---|---|---|---|"] + xr
+    return "\n".join(out) + "\n"
+
+
 def main():
     from paper_2309_00964_amd.inputs import LLAMA7B_LAYER
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
@@ -726,7 +879,12 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     ap.add_argument("--dram-summary", nargs="+", metavar="DIR")
+    ap.add_argument("--block-timeline", metavar="OUT_MD")
     args = ap.parse_args()
+    if args.block_timeline:
+        # the diagnostics build, loaded in place of the product library
+        from paper_2309_00964_amd import build
+        os.environ["EDKM_LIBRARY"] = build.OUT_STAMPS
     if args.pmc_summary:
         return pmc_summary(*args.pmc_summary)
     if args.dram_summary:
@@ -746,6 +904,8 @@ def main():
           "unique_inverse": bench_unique_inverse}[args.workload]
     if args.workload == "decoder_layer" and args.bits not in (None, 3):
         sys.exit("the decoder-layer workload is 3-bit")
+    if args.block_timeline:
+        return block_timeline(args)
     print(json.dumps(fn(args)), flush=True)
 
 

@@ -105,6 +105,9 @@ struct BatchArgs {
     float inv_tau;
     float eps;
     float keep_frac;          // fraction of each sweep read with cached loads (its end)
+#ifdef EDKM_BLOCK_STAMPS
+    int stamp_slot;           // launch index in the stamp record (diagnostics build)
+#endif
     uint8_t* pal_tab;         // palettization index table of the launch's single matrix
                               // (allocation-free entry point); null: each matrix's workspace
     // First N-pass workgroup of each matrix, ascending.  Kept together (not in

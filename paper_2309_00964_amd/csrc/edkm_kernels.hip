@@ -22,12 +22,70 @@
 // Nothing here uses MFMA: k <= 16 centroids is not a dense contraction.
 
 #include "edkm_internal.h"
+#ifdef EDKM_BLOCK_STAMPS
+#include "edkm_stamps.h"
+#endif
 
 #include <hip/hip_fp16.h>
 #include <algorithm>
 #include <atomic>
 
 namespace edkm {
+
+// ----------------------------------------------------------------------------
+// Block timeline (diagnostics build only, -DEDKM_BLOCK_STAMPS): thread 0 of
+// every block records the wall clock (s_memrealtime, 100 MHz) at entry and the
+// block's XCC id, each wave's lane 0 raises the block's end stamp as it
+// leaves, and a few kernels stamp the phases of their block
+// (EDKM_STAMP_MARK).  Launches are numbered in enqueue order from the last
+// edkm_stamps_reset(); the first STAMP_LAUNCHES launches and STAMP_BLOCKS
+// blocks of each are kept.  The product build compiles none of this.
+#ifdef EDKM_BLOCK_STAMPS
+constexpr int STAMP_LAUNCHES = EDKM_STAMP_LAUNCHES, STAMP_BLOCKS = EDKM_STAMP_BLOCKS,
+              STAMP_WORDS = EDKM_STAMP_WORDS;
+__device__ unsigned long long stamp_ts[STAMP_LAUNCHES * STAMP_BLOCKS * STAMP_WORDS];
+__device__ __forceinline__ unsigned long long* stamp_row(int slot) {
+    const unsigned lin = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+    if (slot < 0 || slot >= STAMP_LAUNCHES || lin >= STAMP_BLOCKS) return nullptr;
+    return stamp_ts + ((size_t)slot * STAMP_BLOCKS + lin) * STAMP_WORDS;
+}
+struct StampScope {   // words: 0 entry, 1 end, 2..6 phase marks, 7 XCC id
+    int slot;
+    __device__ explicit StampScope(int s) : slot(s) {
+        unsigned long long* r = stamp_row(slot);
+        if (r && threadIdx.x == 0) {
+            r[0] = wall_clock64();
+            unsigned x;
+            asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+            r[7] = x;
+        }
+    }
+    __device__ ~StampScope() {
+        unsigned long long* r = stamp_row(slot);
+        if (r && (threadIdx.x & 63) == 0) atomicMax(r + 1, wall_clock64());
+    }
+};
+#define EDKM_STAMP_ENTRY(b) StampScope stamp_scope_((b).stamp_slot)
+#define EDKM_STAMP_MARK(b, i)                                                         \
+    do {                                                                              \
+        unsigned long long* r_ = stamp_row((b).stamp_slot);                           \
+        if (r_ && threadIdx.x == 0) r_[i] = wall_clock64();                           \
+    } while (0)
+static int g_stamp_seq = 0;
+static char g_stamp_names[STAMP_LAUNCHES][32];
+static int stamp_next(const char* name) {
+    const int q = g_stamp_seq++;
+    if (q >= STAMP_LAUNCHES) return -1;
+    for (int i = 0; i < 31; ++i) { g_stamp_names[q][i] = name[i]; if (!name[i]) break; }
+    g_stamp_names[q][31] = 0;
+    return q;
+}
+#define EDKM_STAMP_SLOT(b, name) ((b).stamp_slot = stamp_next(name))
+#else
+#define EDKM_STAMP_ENTRY(b) ((void)0)
+#define EDKM_STAMP_MARK(b, i) ((void)0)
+#define EDKM_STAMP_SLOT(b, name) ((void)0)
+#endif
 
 // ----------------------------------------------------------------------------
 // small device helpers
@@ -585,6 +643,7 @@ __device__ __forceinline__ void st_u4_nt(void* p, uint4 x) {
 // init_unique: zero, histogram, partial merge, window selection
 
 __global__ void __launch_bounds__(T_THREADS) k_init_zero(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     const MatArgs& M = b.m[blockIdx.y];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     for (int u = blockIdx.x * T_THREADS + threadIdx.x; u < NKEYS; u += gridDim.x * T_THREADS)
@@ -604,6 +663,7 @@ __global__ void __launch_bounds__(T_THREADS) k_init_zero(BatchArgs b) {
 // 16-bit counts (two bins per word); a bin that reached 2^16 in this
 // workgroup is added to the global counts instead.
 __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     __shared__ __align__(16) uint32_t h[2 * W4];
     __shared__ int red[2];
     const int mi = np_matrix(b);
@@ -636,6 +696,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
         [&](uint64_t, Nothing) {},
         [&](uint64_t i) { add(keys[i]); });
     __syncthreads();
+    EDKM_STAMP_MARK(b, 2);   // keys streamed
     // occupied span [lo, hi) over both signs, rounded out to even magnitudes;
     // a thread's W4 / NP_THREADS magnitudes are read all at once (as a loop
     // each read waited for the previous one)
@@ -658,6 +719,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
         atomicMax(&red[1], hi);
     }
     __syncthreads();
+    EDKM_STAMP_MARK(b, 3);   // span found
     lo = red[0] & ~1;
     hi = (red[1] + 1) & ~1;
     if (hi <= lo) { lo = 0; hi = 0; }
@@ -701,6 +763,7 @@ constexpr int MERGE_THREADS = 256;
 // Histogram rows (packed 16-bit pairs over per-row spans) into counts.
 // Grid (W4 / MERGE_THREADS, row chunks, count).
 __global__ void __launch_bounds__(MERGE_THREADS) k_hist_merge(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     const MatArgs& M = b.m[blockIdx.z];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const int r0 = blockIdx.y * MERGE_ROWS;
@@ -743,6 +806,7 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_hist_merge(BatchArgs b) {
 // width W covers the whole occupied range when it fits, else the W consecutive
 // magnitudes holding the most weights (lowest start on ties).
 __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     constexpr int NW = NP_THREADS / 64;
     constexpr int SPAN = MAGS / NW;
     constexpr int NCH = SPAN / 256;
@@ -792,6 +856,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
             make_uint4(base + s4[0], base + s4[1], base + s4[2], base + s4[3]);
         carry += (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
     }
+    EDKM_STAMP_MARK(b, 2);   // wave 0's share of the counts scanned
     const uint32_t occ = (occp | occn) & finm;
     auto bit_mag = [&](int bit) { return mw + 256 * (bit >> 2) + (bit & 3); };
     int lo = occ ? bit_mag(__builtin_ctz(occ)) : 1 << 30;
@@ -833,6 +898,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
         }
     }
     __syncthreads();
+    EDKM_STAMP_MARK(b, 3);   // block totals combined
     const int mlo = red[0], mhi = red[1];
     auto P = [&](int x) -> uint32_t {   // weights with finite magnitude < x
         return x == 0 ? 0u : pre[x - 1] + woff[(x - 1) / SPAN];
@@ -858,6 +924,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_window(BatchArgs b) {
         ww[w] = W;
     }
     if (threadIdx.x == 0) {
+        EDKM_STAMP_MARK(b, 4);   // windows chosen
         const uint32_t total = woff[NW];
         // expected number of other lanes sharing an address in a 64-lane keyed atomic
         const double e = total ? 2016.0 * (double)sqsum / ((double)total * (double)total) : 0.0;
@@ -888,6 +955,7 @@ __device__ __forceinline__ int table_key(int r) {
 // P_j = sum n_u a_uj v_u.  Grid (T_WG, count).
 template <int K>
 __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     __shared__ float red[BLOCK_TOTAL_LDS(2 * K)];
     __shared__ float csh[K];
     __shared__ int stop;
@@ -909,6 +977,7 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
     } else if (threadIdx.x < K) {
         cprev = M.c_in[threadIdx.x];
     }
+    EDKM_STAMP_MARK(b, 2);   // loads issued
     DevState* st = ws.st;
     const bool lead = blockIdx.x == 0;
     if (t == 1) {
@@ -936,6 +1005,7 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
             return;
         }
     }
+    EDKM_STAMP_MARK(b, 3);   // partial block summed, C formed
     float c[K];
 #pragma unroll
     for (int j = 0; j < K; ++j) c[j] = csh[j];
@@ -958,7 +1028,9 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
             acc[K + j] = fmaf(w, v, acc[K + j]);
         }
     }
+    EDKM_STAMP_MARK(b, 4);   // patterns done
     const float tot = block_total<2 * K>(acc, red);
+    EDKM_STAMP_MARK(b, 5);   // block summed
     if (threadIdx.x < 2 * K) ws.tpart[((size_t)t * T_WG + blockIdx.x) * PSTRIDE + threadIdx.x] = tot;
 }
 
@@ -968,6 +1040,7 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
 // clears G.  Grid (T_WG, count).
 template <int K>
 __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     __shared__ float red[T_THREADS];
     __shared__ float cT[K], cP[K];
     const MatArgs& M = b.m[blockIdx.y];
@@ -1040,6 +1113,7 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
 
 // W~_i = Tab[bits_i]; the window [lo4, lo4 + w4) of the table sits in LDS.
 __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     __shared__ float tw[2 * W4];
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
@@ -1126,6 +1200,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
 // address) the 32-bit mode is 10% faster, with bf16 weights (about 1.8) the
 // 64-bit mode is 30% faster.
 __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     __shared__ __align__(16) unsigned long long lds[2 * W8];   // 64-bit sums, or the 32-bit ones
     __shared__ int emax_sh, esum_sh, ecnt_sh;
     static_assert(2 * W4 * sizeof(int) <= sizeof(lds), "32-bit window fits the LDS buffer");
@@ -1274,6 +1349,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
 // in LDS.  The first workgroup of each matrix also finishes dL/dC^(0); every
 // workgroup clears a slice of G for the next backward.
 __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     __shared__ float2 hw[2 * W8];
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
@@ -1346,6 +1422,7 @@ __device__ __forceinline__ uint8_t* pal_table(const BatchArgs& b, const MatArgs&
 }
 
 __global__ void __launch_bounds__(256) k_pal_table(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     __shared__ float lut[KMAX];
     const MatArgs& M = b.m[blockIdx.y];
     uint8_t* const tbl = pal_table(b, M);
@@ -1372,6 +1449,7 @@ __global__ void __launch_bounds__(256) k_pal_table(BatchArgs b) {
 // [b.wg_begin[mi], b.wg_begin[mi] + wg_count) take its groups round-robin, 1024 at a time.
 template <int B>
 __global__ void __launch_bounds__(1024) k_palettize(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     __shared__ uint4 tbl4[NKEYS / 16];
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
@@ -1434,6 +1512,7 @@ __global__ void __launch_bounds__(1024) k_palettize(BatchArgs b) {
 // written to M.uniq when given.  One 1024-thread block per matrix, grid
 // (1, count); thread t ranks the patterns [64 t, 64 t + 64).
 __global__ void __launch_bounds__(1024) k_rank(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     __shared__ unsigned long long occ[NKEYS / 64];   // bit e of word t: pattern 64 t + e occupied
     __shared__ uint32_t wtot[1024 / 64];
     const MatArgs& M = b.m[blockIdx.y];
@@ -1496,6 +1575,7 @@ __global__ void __launch_bounds__(1024) k_rank(BatchArgs b) {
 // patterns.  The whole rank table (128 KiB) is loaded into LDS; no window.
 // Matrices of the launch without an inverse output (M.wt null) skip the pass.
 __global__ void __launch_bounds__(NP_THREADS) k_inverse(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     __shared__ uint4 rk4[NKEYS * sizeof(uint16_t) / sizeof(uint4)];
     const int mi = np_matrix(b);
     const MatArgs& M = b.m[mi];
@@ -1541,6 +1621,7 @@ constexpr int MERGE_X = 2 * W4 / MERGE_THREADS;
 constexpr int GT_ROWS = 64;
 template <int K>
 __global__ void __launch_bounds__(MERGE_THREADS) k_grad_top(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     static_assert(MERGE_THREADS == T_THREADS, "block_total sums over T_THREADS");
     __shared__ float red[BLOCK_TOTAL_LDS(2 * K)];
     constexpr int GPER = (NKEYS + MERGE_X * MERGE_THREADS - 1) / (MERGE_X * MERGE_THREADS);
@@ -1621,6 +1702,7 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_grad_top(BatchArgs b) {
 // make dL/dC^(t-1).  Grid (T_WG, count).
 template <int K>
 __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     __shared__ float red[BLOCK_TOTAL_LDS(K)];
     __shared__ float gSsh[K], c1sh[K], c0sh[K];
     const MatArgs& M = b.m[blockIdx.y];
@@ -1654,6 +1736,7 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
         hS = ws.shist[t * KMAX + j];
         if (t < M.max_iter) { hS1 = ws.shist[(t + 1) * KMAX + j]; hg1 = ws.ghist[(t + 1) * KMAX + j]; }
     }
+    EDKM_STAMP_MARK(b, 2);   // loads issued
     const int T = st->teff;
     pc.stage(red);
     if (t > T) return;
@@ -1674,6 +1757,7 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
         if (lead) ws.ghist[t * KMAX + j] = gm;
     }
     __syncthreads();
+    EDKM_STAMP_MARK(b, 3);   // partial blocks summed, gamma formed
     float c1[K], c0[K], gS[K];
 #pragma unroll
     for (int j = 0; j < K; ++j) { c1[j] = c1sh[j]; c0[j] = c0sh[j]; gS[j] = gSsh[j]; }
@@ -1705,7 +1789,9 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
         if (t == 1) ws.HR[u] = make_float2(H4[r], Ru);
         else ws.R[u] = Ru;
     }
+    EDKM_STAMP_MARK(b, 4);   // patterns done
     const float tot = block_total<K>(acc, red);
+    EDKM_STAMP_MARK(b, 5);   // block summed
     if (threadIdx.x < K) ws.bpart[((size_t)t * T_WG + blockIdx.x) * PSTRIDE + threadIdx.x] = tot;
 }
 
@@ -1739,6 +1825,7 @@ __device__ __forceinline__ void reduce_dparts(const float* part, int nrow, int c
 
 template <int K>
 __global__ void __launch_bounds__(D_THREADS) k_dense_iter(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     __shared__ float tot[2 * K];
     __shared__ float scratch[D_THREADS / 64 * 2 * K];
     __shared__ float csh[K];
@@ -1777,6 +1864,7 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_iter(BatchArgs b) {
 // One block: C^(t) from the dense partials, history, early stop.
 template <int K>
 __global__ void __launch_bounds__(1024) k_dense_fin(BatchArgs b, int nrow) {
+    EDKM_STAMP_ENTRY(b);
     __shared__ float scratch[16 * PSTRIDE];
     __shared__ float tot[2 * K];
     __shared__ int stop;
@@ -1807,6 +1895,7 @@ __global__ void __launch_bounds__(1024) k_dense_fin(BatchArgs b, int nrow) {
 
 template <int K>
 __global__ void __launch_bounds__(D_THREADS) k_dense_out(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     const MatArgs& M = b.m[0];
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const int T = ws.st->teff;
@@ -1853,6 +1942,7 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_out(BatchArgs b) {
 // Dense backward, direct use of A^(T): dL/dw_i = g_i H_i, and partials of gamma and E.
 template <int K>
 __global__ void __launch_bounds__(D_THREADS) k_dense_btop(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     __shared__ float tot[2 * K];
     __shared__ float scratch[D_THREADS / 64 * 2 * K];
     const MatArgs& M = b.m[0];
@@ -1897,6 +1987,7 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_btop(BatchArgs b) {
 // Dense backward iteration t (reads gamma^(t) from ghist).
 template <int K>
 __global__ void __launch_bounds__(D_THREADS) k_dense_biter(BatchArgs b) {
+    EDKM_STAMP_ENTRY(b);
     __shared__ float tot[K];
     __shared__ float scratch[D_THREADS / 64 * K];
     __shared__ float c1sh[K], c0sh[K], gSsh[K];
@@ -1945,6 +2036,7 @@ __global__ void __launch_bounds__(D_THREADS) k_dense_biter(BatchArgs b) {
 // T..1 (after biter t): gamma^(t-1) = dL/dC^(t-1); at t = 1 also dL/dC^(0).
 template <int K>
 __global__ void __launch_bounds__(1024) k_dense_bfin(BatchArgs b, int nrow) {
+    EDKM_STAMP_ENTRY(b);
     __shared__ float scratch[16 * PSTRIDE];
     __shared__ float tot[2 * K];
     const MatArgs& M = b.m[0];
@@ -2015,6 +2107,7 @@ hipError_t noalloc_scratch(uint8_t** out) {
 
 #define EDKM_LAUNCH(name, kern, grid, block, ...)                       \
     do {                                                                  \
+        EDKM_STAMP_SLOT(b, name);                                         \
         hipLaunchKernelGGL(kern, grid, block, 0, s, __VA_ARGS__);         \
         hipError_t e_ = hipGetLastError();                                \
         if (e_ != hipSuccess) { *where = name; return e_; }              \
@@ -2177,3 +2270,26 @@ static_assert(T_WG % 64 == 0, "table partial reduction: one lane per 64 workgrou
 static_assert(T_WG * T_THREADS * T_KPT == NKEYS, "table blocks cover every pattern");
 
 }  // namespace edkm
+
+#ifdef EDKM_BLOCK_STAMPS
+extern "C" int edkm_stamps_reset(void) {
+    edkm::g_stamp_seq = 0;
+    void* q = nullptr;
+    hipError_t e = hipGetSymbolAddress(&q, HIP_SYMBOL(edkm::stamp_ts));
+    if (e == hipSuccess) e = hipMemset(q, 0, sizeof(edkm::stamp_ts));
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    return (int)e;
+}
+extern "C" int edkm_stamps_dump(unsigned long long* stamps, char* names) {
+    if (hipDeviceSynchronize() != hipSuccess) return -1;
+    if (hipMemcpyFromSymbol(stamps, HIP_SYMBOL(edkm::stamp_ts), sizeof(edkm::stamp_ts)) != hipSuccess) return -1;
+    for (int i = 0; i < edkm::STAMP_LAUNCHES * 32; ++i) names[i] = (&edkm::g_stamp_names[0][0])[i];
+    return edkm::g_stamp_seq;
+}
+extern "C" int edkm_stamps_clock_khz(void) {
+    int dev = 0, r = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&r, hipDeviceAttributeWallClockRate, dev) != hipSuccess) return 0;
+    return r;
+}
+#endif

@@ -18,10 +18,12 @@ import ctypes
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libedkm.so")
+# EDKM_LIBRARY may name another build of the same sources (the block-timeline
+# diagnostics build, libedkm_stamps.so); by default the product library.
+LIB_PATH = os.environ.get("EDKM_LIBRARY") or os.path.join(_HERE, "libedkm.so")
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError("libedkm.so is not built at %s; run __graft_entry__.build()" % LIB_PATH)
+    raise ImportError("%s is not built; run __graft_entry__.build()" % LIB_PATH)
 
 # torch brings its own HIP runtime (SONAME libamdhip64.so.7, loaded under the
 # name libamdhip64.so).  It must be in the process before libedkm.so is loaded,
