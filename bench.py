@@ -76,13 +76,17 @@ COPY_BYTES = 1 << 30
 
 
 def source_hash():
-    """Hash of the kernel sources' code: comments and blank lines are left out,
-    so the counters stay tied to what is compiled, not to its commentary."""
+    """Hash of the product build's kernel code: comments, blank lines and the
+    block-timeline instrumentation (the EDKM_BLOCK_STAMPS sections and the
+    EDKM_STAMP_* statements, which the product build compiles to nothing) are
+    left out, so the counters stay tied to what the product compiles."""
     h = hashlib.sha256()
     for f in sorted(glob.glob(os.path.join(ROOT, "paper_2309_00964_amd", "csrc", "*"))):
         text = open(f).read()
         text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
         text = re.sub(r"//[^\n]*", "", text)
+        text = re.sub(r"#ifdef EDKM_BLOCK_STAMPS\n.*?#endif", "", text, flags=re.S)
+        text = re.sub(r"(?m)^\s*EDKM_STAMP_\w+\([^;]*\);\s*\\?$", "", text)
         h.update("\n".join(l.rstrip() for l in text.splitlines() if l.strip()).encode())
     return h.hexdigest()[:16]
 
@@ -706,6 +710,8 @@ STAMP_LAUNCHES, STAMP_BLOCKS, STAMP_WORDS = 96, 4096, 8
 TIMELINE_PHASES = {   # phase marks (record words 2..5) of the instrumented kernels
     "k_hist": ("keys streamed", "span found"),
     "k_window": ("wave 0 scanned", "block totals combined", "windows chosen"),
+    "k_hist_merge": ("rows summed",),
+    "k_grad_top": ("rows summed (G loaded)", "patterns done", "block summed"),
     "k_fwd_iter": ("loads issued", "partials summed, C formed", "patterns done", "block summed"),
     "k_bwd_iter": ("loads issued", "partials summed, gamma formed", "patterns done", "block summed"),
 }
@@ -776,9 +782,10 @@ def timeline_report(raw, rate, title, cmd, warmup):
     if any(r[0] != names0 for r in raw):
         raise ValueError("the launch sequence changed between steps")
     scale = np.where(np.arange(W) < 7, 1e6 / rate, 1.0)
-    steps = []
+    steps, blocks = [], []
     for _, ts in raw:
         recs = [ts[q][ts[q][:, 0] > 0].astype(np.float64) for q in range(len(names0))]
+        blocks.append([np.nonzero(ts[q][:, 0] > 0)[0] for q in range(len(names0))])
         if any(len(r) == 0 for r in recs):
             raise ValueError("a launch has no block records")
         t0 = min(r[:, 0].min() for r in recs)
@@ -818,24 +825,29 @@ def timeline_report(raw, rate, title, cmd, warmup):
     for k_, (c, sp, gp) in sorted(tot.items(), key=lambda kv: -kv[1][1]):
         out.append("| %s | %d | %.1f | %.1f |" % (k_, c, sp, gp))
     mid = steps[reps // 2]
+    mid_blocks = blocks[reps // 2]
     ph = []
     for q, name in enumerate(names0):
         labels = TIMELINE_PHASES.get(name)
-        v = mid[q]
-        if not labels or not (v[:, 2] > 0).any():
+        if not labels:
             continue
-        cols = [0] + [2 + i for i in range(len(labels)) if (v[:, 2 + i] > 0).all()] + [1]
+        v = mid[q]
+        v = v[(v[:, 2:2 + len(labels)] > 0).all(axis=1)]   # blocks that reached every mark
+        if not len(v):
+            continue
+        cols = [0] + [2 + i for i in range(len(labels))] + [1]
         lab = lambda c: "entry" if c == 0 else "end" if c == 1 else labels[c - 2]
         seg = ["%s -> %s %.2f" % (lab(a), lab(b_), med(v[:, b_] - v[:, a])) for a, b_ in zip(cols[:-1], cols[1:])]
-        ph.append("| %d | %s | %s |" % (q, name, "; ".join(seg)))
+        ph.append("| %d | %s | %d | %s |" % (q, name, len(v), "; ".join(seg)))
     if ph:
-        out += ["", "Phases (block medians of the middle step, us):", "", "| # | Kernel | Phases |",
-                "|---|---|---|"] + ph
-    xr = []
+        out += ["", "Phases (medians over the blocks of the middle step that reached every mark, us):", "",
+                "| # | Kernel | Blocks | Phases |", "|---|---|---|---|"] + ph
+    xr, dist = [], []
     for q, name in enumerate(names0):
         v = mid[q]
         if len(v) < 64:
             continue
+        blk = mid_blocks[q]
         x = v[:, 7].astype(np.int64) & 0xF
         s0 = v[:, 0].min()
         ends = {c: v[x == c, 1].max() - s0 for c in range(16) if (x == c).any()}
@@ -843,6 +855,15 @@ def timeline_report(raw, rate, title, cmd, warmup):
         xr.append("| %d | %s | %s | %.1f |" % (q, name, " ".join("%d:%d/%.1f" % (c, blocks[c], ends[c])
                                                                     for c in ends),
                                             max(ends.values()) - min(ends.values())))
+        d = v[:, 1] - v[:, 0]
+        slow = np.argsort(-d)[:6]
+        dist.append("| %d | %s | %.1f | %.1f | %.1f | %.1f | %s |" % (
+            q, name, np.percentile(d, 10), np.median(d), np.percentile(d, 90), d.max(),
+            " ".join("%d:%.1f" % (blk[i], d[i]) for i in slow)))
+    if dist:
+        out += ["", "Block durations of the same launches (us): percentiles, and the six slowest blocks "
+                "(linear block index: duration).", "", "| # | Kernel | p10 | p50 | p90 | Max | Slowest |",
+                "|---|---|---|---|---|---|---|"] + dist
     if xr:
         out += ["", "Per-XCC finish of the launches with 64 blocks or more (middle step): XCC:blocks/last block "
                 "end from the launch's first block start (us), and the spread between the first and last XCC "

@@ -790,6 +790,7 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_hist_merge(BatchArgs b) {
         s0 += x[q2] & 0xFFFFu;
         s1 += x[q2] >> 16;
     }
+    EDKM_STAMP_MARK(b, 2);   // rows summed
     uint32_t* c = ws.counts + (s << 15) + mag;
     if (s0) atomicAdd(c, s0);
     if (s1) atomicAdd(c + 1, s1);
@@ -1665,6 +1666,7 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_grad_top(BatchArgs b) {
             key[0] = (uint32_t)((sg << 15) | (lo + i - sg * w));
         }
     }
+    EDKM_STAMP_MARK(b, 2);   // rows summed (G loaded)
     int nz = 0;
 #pragma unroll
     for (int q = 0; q < GPER; ++q) nz |= gv[q] != 0.f;
@@ -1686,7 +1688,9 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_grad_top(BatchArgs b) {
             acc[K + j] = fmaf(ga * d[j], sgnf(v - c0[j]), acc[K + j]);
         }
     }
+    EDKM_STAMP_MARK(b, 3);   // patterns done
     const float tot = block_total<2 * K>(acc, red);
+    EDKM_STAMP_MARK(b, 4);   // block summed
     if (threadIdx.x < 2 * K && tot != 0.f) {
         const int row = (blockIdx.x + 7 * blockIdx.y) % T_WG;   // spread over the rows
         atomicAdd(&ws.bpart[(size_t)row * PSTRIDE + threadIdx.x], tot);

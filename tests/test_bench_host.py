@@ -112,5 +112,11 @@ def test_source_hash_ignores_comments_only(tmp_path, monkeypatch):
     k = dst / "edkm_kernels.hip"
     k.write_text("// a new comment line\n" + k.read_text().replace("namespace edkm {", "namespace edkm {  /* x */", 1))
     assert bench.source_hash() == base
+    # the block-timeline instrumentation is not product code either
+    body = k.read_text()
+    i = body.index("EDKM_STAMP_ENTRY(b);", body.index("k_hist(BatchArgs b)"))
+    k.write_text(body[:i] + "EDKM_STAMP_MARK(b, 6);\n    " + body[i:] +
+                 "\n#ifdef EDKM_BLOCK_STAMPS\nstatic int stamp_only_value = 2;\n#endif\n")
+    assert bench.source_hash() == base
     k.write_text(k.read_text() + "\nstatic int unused_probe_value = 1;\n")
     assert bench.source_hash() != base

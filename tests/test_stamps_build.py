@@ -49,7 +49,12 @@ def test_bench_reads_the_record_with_the_header_shape():
     text = open(os.path.join(ROOT, "include", "edkm_stamps.h")).read()
     got = {k: int(v) for k, v in re.findall(r"EDKM_STAMP_(LAUNCHES|BLOCKS|WORDS)\s*=\s*(\d+)", text)}
     assert got == {"LAUNCHES": bench.STAMP_LAUNCHES, "BLOCKS": bench.STAMP_BLOCKS, "WORDS": bench.STAMP_WORDS}
-    assert set(bench.TIMELINE_PHASES) <= {"k_hist", "k_window", "k_fwd_iter", "k_bwd_iter"}
+    kernels = open(os.path.join(ROOT, "paper_2309_00964_amd", "csrc", "edkm_kernels.hip")).read()
+    for name, labels in bench.TIMELINE_PHASES.items():   # each kernel stamps as many phases as named
+        body = kernels[kernels.index(" %s(BatchArgs b" % name):]
+        body = body[:body.index("\n}\n")]
+        marks = sorted(set(int(x) for x in re.findall(r"EDKM_STAMP_MARK\(b, (\d)\)", body)))
+        assert marks == list(range(2, 2 + len(labels))), (name, marks)
     assert all(len(v) <= 5 for v in bench.TIMELINE_PHASES.values())   # record words 2..6
 
 
@@ -68,6 +73,7 @@ def test_timeline_report_on_a_synthetic_record():
             ts[0, blk] = [base + 100, base + 100 + 1000 + 100 * x, base + 600, base + 700, 0, 0, 0, x]
         for blk in range(4):                       # k_window: starts 2 us after the last k_hist block
             ts[1, blk] = [base + 2000 + 200, base + 2200 + 300, base + 2210, base + 2220, base + 2230, 0, 0, 0]
+        ts[1, 0, 4] = 0                            # one block never chose a window: left out of the phases
         raw.append((["k_hist", "k_window"], ts))
     text = bench.timeline_report(raw, 100e6, "synthetic", "cmd", 2)
     lines = text.splitlines()
@@ -75,8 +81,8 @@ def test_timeline_report_on_a_synthetic_record():
     assert row(0) == "| 0 | k_hist | 128 | 0.0 | 17.0 | 0.0 | 13.5 | 17.0 |"
     assert row(1) == "| 1 | k_window | 4 | 21.0 | 3.0 | 4.0 | 3.0 | 3.0 |"
     assert "Step 24.0 us: launch spans 20.0 us, gaps 4.0 us." in text
-    assert "entry -> keys streamed 5.00; keys streamed -> span found 1.00; span found -> end" in text
-    assert ("wave 0 scanned -> block totals combined 0.10; block totals combined -> windows chosen 0.10; "
+    assert "| 0 | k_hist | 128 | entry -> keys streamed 5.00; keys streamed -> span found 1.00; span found -> end" in text
+    assert ("| 1 | k_window | 3 | entry -> wave 0 scanned 0.10; wave 0 scanned -> block totals combined 0.10; block totals combined -> windows chosen 0.10; "
             "windows chosen -> end 2.70") in text
     xcc = next(l_ for l_ in lines if "0:16/10.0" in l_)
     assert xcc.endswith("7:16/17.0 | 7.0 |")
