@@ -13,7 +13,7 @@ OUT = os.path.join(HERE, "libedkm.so")
 OUT_STAMPS = os.path.join(HERE, "libedkm_stamps.so")
 
 HIPCC_FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared", "-Werror=uninitialized",
     # no packed-fp32 instructions in generated code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I" + os.path.join(ROOT, "include"),

@@ -85,6 +85,7 @@ uint32_t partition(BatchArgs& b, int budget) {
         b.m[i].wg_count = cnt[i];
         b.wg_begin[i] = beg[i];
     }
+    for (int i = b.count; i < MAXB; ++i) b.wg_begin[i] = 0xFFFFFFFFu;   // no workgroup reaches these
     return grid;
 }
 

@@ -110,9 +110,10 @@ struct BatchArgs {
 #endif
     uint8_t* pal_tab;         // palettization index table of the launch's single matrix
                               // (allocation-free entry point); null: each matrix's workspace
-    // First N-pass workgroup of each matrix, ascending.  Kept together (not in
-    // MatArgs) so that a workgroup finds its matrix from two contiguous
-    // scalar loads instead of 27 scattered ones (about 2 us per launch).
+    // First N-pass workgroup of each matrix, ascending; 0xFFFFFFFF past the
+    // launch's matrices.  Kept together (not in MatArgs) so that a workgroup
+    // finds its matrix from contiguous scalar loads issued together instead
+    // of 27 scattered ones (about 2 us per launch).
     uint32_t wg_begin[MAXB];
     MatArgs m[MAXB];
 };

@@ -431,6 +431,13 @@ struct PartCols {
 #pragma unroll
         for (int r = 0; r < R; ++r) x[r] = p ? p[(size_t)(sg * R + r) * PSTRIDE] : 0.f;
     }
+    // column c of the block at base (no null test, so no branch among the loads)
+    __device__ __forceinline__ void load_block(const float* base) {
+        const int c = threadIdx.x % NC, sg = threadIdx.x / NC;
+        const float* p = base + c;
+#pragma unroll
+        for (int r = 0; r < R; ++r) x[r] = p[(size_t)(sg * R + r) * PSTRIDE];
+    }
     __device__ __forceinline__ void stage(float* red) {
         red[threadIdx.x] = tree_sum<R>(x);
         __syncthreads();
@@ -477,12 +484,29 @@ __device__ __forceinline__ float block_total(const float (&v)[NV], float* red) {
 
 // Matrix of an N-pass workgroup, and its slice [beg, end).
 __device__ __forceinline__ int np_matrix(const BatchArgs& b) {
-    // wg_begin ascends with the matrix: count the matrices starting at or
-    // before this workgroup, with independent loads of every start
+    // wg_begin ascends with the matrix (entries past the launch's matrices hold
+    // 0xFFFFFFFF): count the matrices starting at or before this workgroup.
+    // Every start is loaded before any is compared, so the loads issue
+    // together (a test of b.count in the loop had split them into three
+    // waits).
+    uint32_t w[MAXB];
+#pragma unroll
+    for (int i = 1; i < MAXB; ++i) w[i] = b.wg_begin[i];
     int m = 0;
 #pragma unroll
-    for (int i = 1; i < MAXB; ++i) m += (i < b.count && blockIdx.x >= b.wg_begin[i]) ? 1 : 0;
+    for (int i = 1; i < MAXB; ++i) m += blockIdx.x >= w[i] ? 1 : 0;
     return m;
+}
+
+// The launch arguments of an N-pass workgroup's matrix, read in one round
+// trip.  Read where each is used, the compiler had waited for each group of
+// them in turn: 4-8 round trips of about 0.5 us before a pass streamed.
+__device__ __forceinline__ MatArgs np_args(const BatchArgs& b, int mi) {
+    MatArgs M = b.m[mi];
+    asm volatile("" ::"s"(M.keys), "s"(M.n), "s"(M.wt), "s"(M.g), "s"(M.gw), "s"(M.gc), "s"(M.wsb), "s"(M.k),
+                 "s"(M.max_iter), "s"(M.vec), "s"(M.fmt), "s"(M.kforce), "s"(M.wg_count), "s"(b.keep_frac),
+                 "s"(b.out_half), "s"(b.inv_tau), "s"(b.wg_begin[mi]));
+    return M;
 }
 
 // Stream a workgroup's share of a matrix.  Full rounds: the matrix is cut into
@@ -667,7 +691,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_hist(BatchArgs b) {
     __shared__ __align__(16) uint32_t h[2 * W4];
     __shared__ int red[2];
     const int mi = np_matrix(b);
-    const MatArgs& M = b.m[mi];
+    const MatArgs M = np_args(b, mi);
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const uint32_t wl = blockIdx.x - b.wg_begin[mi];
     for (int i = threadIdx.x; i < 2 * W4 / 4; i += NP_THREADS) reinterpret_cast<uint4*>(h)[i] = uint4{0u, 0u, 0u, 0u};
@@ -765,25 +789,30 @@ constexpr int MERGE_THREADS = 256;
 __global__ void __launch_bounds__(MERGE_THREADS) k_hist_merge(BatchArgs b) {
     EDKM_STAMP_ENTRY(b);
     const MatArgs& M = b.m[blockIdx.z];
+    const int wg_count = (int)M.wg_count;
+    asm volatile("" ::"s"(wg_count), "s"(M.wsb), "s"(M.max_iter));   // the arguments, in one wait
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const int r0 = blockIdx.y * MERGE_ROWS;
-    const int r1 = min((int)M.wg_count, r0 + MERGE_ROWS);
+    const int r1 = min(wg_count, r0 + MERGE_ROWS);
     if (r0 >= r1) return;
     const int q = blockIdx.x * MERGE_THREADS + threadIdx.x;   // < W4 pairs
     const int s = q >= W4 / 2;
     const int mag = 2 * (q - s * (W4 / 2));
     uint32_t s0 = 0u, s1 = 0u;
     const uint32_t* part = ws.part;
-    uint32_t x[MERGE_ROWS];                    // every row's word in flight at once
+    // Every row's span first, then every row's word, all in flight at once.
+    // (Loaded under the row test, each span load -- a scalar load -- had
+    // waited for the previous one: 16 round trips, 8 us per block.)
+    int2 lh[MERGE_ROWS];
+#pragma unroll
+    for (int q2 = 0; q2 < MERGE_ROWS; ++q2) lh[q2] = ws.span[min(r0 + q2, r1 - 1)];
+    uint32_t x[MERGE_ROWS];
 #pragma unroll
     for (int q2 = 0; q2 < MERGE_ROWS; ++q2) {
         const int r = r0 + q2;
         x[q2] = 0u;
-        if (r < r1) {
-            const int2 lh = ws.span[r];
-            if (mag >= lh.x && mag < lh.y)
-                x[q2] = part[(size_t)r * ROW4 + s * ((lh.y - lh.x) >> 1) + ((mag - lh.x) >> 1)];
-        }
+        if (r < r1 && mag >= lh[q2].x && mag < lh[q2].y)
+            x[q2] = part[(size_t)r * ROW4 + s * ((lh[q2].y - lh[q2].x) >> 1) + ((mag - lh[q2].x) >> 1)];
     }
 #pragma unroll
     for (int q2 = 0; q2 < MERGE_ROWS; ++q2) {
@@ -961,25 +990,31 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
     __shared__ float csh[K];
     __shared__ int stop;
     const MatArgs& M = b.m[blockIdx.y];
-    const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const int t = b.t;
-    if (t > M.max_iter) return;
-    // every load first: the pattern counts, the previous iteration's partial
-    // block and C^(t-2), or c_in
+    // Every load first, with no branch in between (a branch or an early
+    // return between them had the compiler wait for each scalar load before
+    // issuing the next, 2-3 round trips): the pattern counts, the previous
+    // iteration's partial block and C^(t-2) (at t = 1: c_in, and partial row 0,
+    // unused), the convergence flag.  Indices are clamped for launches past
+    // this matrix's max_iter, which return below.
+    const float* c_in = M.c_in;
+    const int max_iter = M.max_iter, fmt = M.fmt;
+    const float eps = b.eps, s2 = b.s2;
+    // the arguments, in one wait
+    asm volatile("" ::"s"(c_in), "s"(max_iter), "s"(fmt), "s"(t), "s"(eps), "s"(s2), "s"(M.wsb));
+    const Ws ws = carve_workspace(M.wsb, M.max_iter);
+    const int tl = max(1, min(t, max_iter));
     uint32_t n4[T_KPT];
 #pragma unroll
     for (int r = 0; r < T_KPT; ++r) n4[r] = ws.counts[table_key(r)];
     PartCols<2 * K> pc;
-    float cprev = 0.f;
-    if (t > 1) {
-        const float* tp = ws.tpart + (size_t)(t - 1) * T_WG * PSTRIDE;
-        pc.load([&](int c) { return tp + c; });
-        if (threadIdx.x < K) cprev = ws.chist[(t - 2) * KMAX + threadIdx.x];
-    } else if (threadIdx.x < K) {
-        cprev = M.c_in[threadIdx.x];
-    }
-    EDKM_STAMP_MARK(b, 2);   // loads issued
+    pc.load_block(ws.tpart + (size_t)(tl - 1) * T_WG * PSTRIDE);
+    const float* cp = tl > 1 ? ws.chist + (tl - 2) * KMAX : c_in;
+    const float cprev = cp[threadIdx.x % K];
     DevState* st = ws.st;
+    const int conv = st->conv;
+    EDKM_STAMP_MARK(b, 2);   // loads issued
+    if (t > max_iter) return;
     const bool lead = blockIdx.x == 0;
     if (t == 1) {
         if (threadIdx.x < K) {
@@ -991,17 +1026,17 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
     } else {
         if (threadIdx.x == 0) stop = 0;
         pc.stage(red);
-        if (st->conv) return;
+        if (conv) return;
         if (threadIdx.x < K) {
             const int j = threadIdx.x;
             const float S = PartCols<2 * K>::total(red, j), P = PartCols<2 * K>::total(red, K + j);
             const float cn = S > 0.f ? P / S : cprev;
             csh[j] = cn;
             if (lead) { ws.chist[(t - 1) * KMAX + j] = cn; ws.shist[(t - 1) * KMAX + j] = S; }
-            if (b.eps > 0.f && !(fabsf(cn - cprev) <= b.eps)) atomicOr(&stop, 1);
+            if (eps > 0.f && !(fabsf(cn - cprev) <= eps)) atomicOr(&stop, 1);
         }
         __syncthreads();
-        if (b.eps > 0.f && stop == 0) {   // max_j |C^(t-1) - C^(t-2)| <= eps: T = t - 1
+        if (eps > 0.f && stop == 0) {   // max_j |C^(t-1) - C^(t-2)| <= eps: T = t - 1
             if (lead && threadIdx.x == 0) { st->teff = t - 1; st->conv = 1; }
             return;
         }
@@ -1017,10 +1052,10 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_iter(BatchArgs b) {
     for (int r = 0; r < T_KPT; ++r) {
         const int u = table_key(r);
         const uint32_t n = n4[r];
-        if (n == 0u || !key_finite(u, M.fmt)) continue;
-        const float v = key_value(u, M.fmt);
+        if (n == 0u || !key_finite(u, fmt)) continue;
+        const float v = key_value(u, fmt);
         float a[K];
-        attn_row<K>(v, c, b.s2, a);
+        attn_row<K>(v, c, s2, a);
         const float nf = (float)n;
 #pragma unroll
         for (int j = 0; j < K; ++j) {
@@ -1045,29 +1080,37 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
     __shared__ float red[T_THREADS];
     __shared__ float cT[K], cP[K];
     const MatArgs& M = b.m[blockIdx.y];
+    // the arguments, in one wait (read where they are used, each had cost a
+    // round trip of its own)
+    const int max_iter = M.max_iter, fmt = M.fmt;
+    float* const c_out = M.c_out;
+    int32_t* const iters_out = M.iters_out;
+    const float s2 = b.s2, inv_tau = b.inv_tau;
+    asm volatile("" ::"s"(max_iter), "s"(fmt), "s"(c_out), "s"(iters_out), "s"(s2), "s"(inv_tau), "s"(M.wsb));
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     // every load first (the partial block and C^(T-1) of a run that did all
-    // max_iter iterations; an early stop reads its two rows afterwards)
+    // max_iter iterations, the convergence state; an early stop reads its two
+    // rows afterwards)
+    DevState* st = ws.st;
+    const int conv = st->conv, teff = st->teff;
     uint32_t n4[T_KPT];
 #pragma unroll
     for (int r = 0; r < T_KPT; ++r) n4[r] = ws.counts[table_key(r)];
     PartCols<2 * K> pc;
-    const float* tp = ws.tpart + (size_t)M.max_iter * T_WG * PSTRIDE;
-    pc.load([&](int c) { return tp + c; });
-    const float cprev = threadIdx.x < K ? ws.chist[(M.max_iter - 1) * KMAX + threadIdx.x] : 0.f;
-    DevState* st = ws.st;
+    pc.load_block(ws.tpart + (size_t)max_iter * T_WG * PSTRIDE);
+    const float cprev = ws.chist[(max_iter - 1) * KMAX + threadIdx.x % K];
     const bool lead = blockIdx.x == 0;
     pc.stage(red);
     int T;
-    if (st->conv) {
-        T = st->teff;
+    if (conv) {
+        T = teff;
         if (threadIdx.x < K) {
             cT[threadIdx.x] = ws.chist[T * KMAX + threadIdx.x];
             cP[threadIdx.x] = ws.chist[(T - 1) * KMAX + threadIdx.x];
         }
         __syncthreads();
     } else {
-        T = M.max_iter;
+        T = max_iter;
         if (threadIdx.x < K) {
             const int j = threadIdx.x;
             const float S = PartCols<2 * K>::total(red, j), P = PartCols<2 * K>::total(red, K + j);
@@ -1081,11 +1124,11 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
     }
     if (lead) {
         if (threadIdx.x < K) {
-            M.c_out[threadIdx.x] = cT[threadIdx.x];
+            c_out[threadIdx.x] = cT[threadIdx.x];
             ws.cfin[threadIdx.x] = cP[threadIdx.x];          // for k_grad_top, which does not know T
             ws.cfin[KMAX + threadIdx.x] = cT[threadIdx.x];
         }
-        if (threadIdx.x == 0 && M.iters_out) *M.iters_out = T;
+        if (threadIdx.x == 0 && iters_out) *iters_out = T;
     }
     float c1[K], c0[K];
 #pragma unroll
@@ -1096,16 +1139,16 @@ __global__ void __launch_bounds__(T_THREADS) k_fwd_out(BatchArgs b) {
         ws.G[u] = 0.f;
         const uint32_t n = n4[r];
         if (n == 0u) continue;
-        if (!key_finite(u, M.fmt)) { ws.tab[u] = __builtin_nanf(""); ws.H[u] = __builtin_nanf(""); continue; }
-        const float v = key_value(u, M.fmt);
+        if (!key_finite(u, fmt)) { ws.tab[u] = __builtin_nanf(""); ws.H[u] = __builtin_nanf(""); continue; }
+        const float v = key_value(u, fmt);
         float a[K], d[K], c1m;
-        attn_row_sel<K>(v, c0, b.s2, a, c1, c1m);
+        attn_row_sel<K>(v, c0, s2, a, c1, c1m);
         const float tv = centroid_dev<K>(a, c1, c1m, d);
         float h = 0.f;
 #pragma unroll
         for (int j = 0; j < K; ++j) h = fmaf(a[j] * d[j], sgnf(v - c0[j]), h);
         ws.tab[u] = tv;
-        ws.H[u] = -h * b.inv_tau;
+        ws.H[u] = -h * inv_tau;
     }
 }
 
@@ -1117,7 +1160,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
     EDKM_STAMP_ENTRY(b);
     __shared__ float tw[2 * W4];
     const int mi = np_matrix(b);
-    const MatArgs& M = b.m[mi];
+    const MatArgs M = np_args(b, mi);
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const uint32_t wl = blockIdx.x - b.wg_begin[mi];
     const int lo = ws.st->lo4, w = ws.st->w4;
@@ -1206,7 +1249,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
     __shared__ int emax_sh, esum_sh, ecnt_sh;
     static_assert(2 * W4 * sizeof(int) <= sizeof(lds), "32-bit window fits the LDS buffer");
     const int mi = np_matrix(b);
-    const MatArgs& M = b.m[mi];
+    const MatArgs M = np_args(b, mi);
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const uint32_t wl = blockIdx.x - b.wg_begin[mi];
     const DevState* st = ws.st;
@@ -1353,7 +1396,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
     EDKM_STAMP_ENTRY(b);
     __shared__ float2 hw[2 * W8];
     const int mi = np_matrix(b);
-    const MatArgs& M = b.m[mi];
+    const MatArgs M = np_args(b, mi);
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const uint32_t wl = blockIdx.x - b.wg_begin[mi];
     const DevState* st = ws.st;
@@ -1453,7 +1496,7 @@ __global__ void __launch_bounds__(1024) k_palettize(BatchArgs b) {
     EDKM_STAMP_ENTRY(b);
     __shared__ uint4 tbl4[NKEYS / 16];
     const int mi = np_matrix(b);
-    const MatArgs& M = b.m[mi];
+    const MatArgs M = np_args(b, mi);
     const uint32_t wl = blockIdx.x - b.wg_begin[mi];
     const uint4* src = reinterpret_cast<const uint4*>(pal_table(b, M));
     fill_lds<NKEYS / 16, 1024>(tbl4, src, NKEYS / 16, [](int i) { return i; });   // blockDim.x = 1024
@@ -1579,7 +1622,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_inverse(BatchArgs b) {
     EDKM_STAMP_ENTRY(b);
     __shared__ uint4 rk4[NKEYS * sizeof(uint16_t) / sizeof(uint4)];
     const int mi = np_matrix(b);
-    const MatArgs& M = b.m[mi];
+    const MatArgs M = np_args(b, mi);
     if (!M.wt) return;   // the same for the whole workgroup
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const uint32_t wl = blockIdx.x - b.wg_begin[mi];
@@ -1627,9 +1670,17 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_grad_top(BatchArgs b) {
     __shared__ float red[BLOCK_TOTAL_LDS(2 * K)];
     constexpr int GPER = (NKEYS + MERGE_X * MERGE_THREADS - 1) / (MERGE_X * MERGE_THREADS);
     const MatArgs& M = b.m[blockIdx.z];
+    // the arguments in one wait, then the window and C^(T-1), C^(T) in one
+    // more (read where they are used, they had cost five round trips before
+    // the first row load)
+    const int fmt = M.fmt, wg_count = (int)M.wg_count;
+    const float s2 = b.s2;
+    const uint32_t gy = gridDim.y;
+    asm volatile("" ::"s"(fmt), "s"(wg_count), "s"(s2), "s"(gy), "s"(M.wsb), "s"(M.max_iter));
+    const bool gblock = blockIdx.y == gy - 1;
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const DevState* st = ws.st;
-    // C^(T-1) and C^(T), issued first: independent of everything below
+    const int kmode = st->kmode, w4 = st->w4, lo4 = st->lo4, w8 = st->w8, lo8 = st->lo8;
     float c0[K], c1[K];
 #pragma unroll
     for (int j = 0; j < K; ++j) { c0[j] = ws.cfin[j]; c1[j] = ws.cfin[KMAX + j]; }
@@ -1637,7 +1688,7 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_grad_top(BatchArgs b) {
     uint32_t key[GPER];
 #pragma unroll
     for (int q = 0; q < GPER; ++q) { gv[q] = 0.f; key[q] = 0u; }
-    if (blockIdx.y == gridDim.y - 1) {
+    if (gblock) {
         // the global G: GPER patterns per thread
 #pragma unroll
         for (int q = 0; q < GPER; ++q) {
@@ -1646,10 +1697,10 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_grad_top(BatchArgs b) {
             if (u < (uint32_t)NKEYS) gv[q] = ws.G[u];
         }
     } else {
-        const bool wide = st->kmode == KEYED_U64;
-        const int w = wide ? st->w8 : st->w4, lo = wide ? st->lo8 : st->lo4;
+        const bool wide = kmode == KEYED_U64;
+        const int w = wide ? w8 : w4, lo = wide ? lo8 : lo4;
         const int r0 = blockIdx.y * GT_ROWS;
-        const int r1 = min((int)M.wg_count, r0 + GT_ROWS);
+        const int r1 = min(wg_count, r0 + GT_ROWS);
         if (r0 >= r1 || (int)(blockIdx.x * MERGE_THREADS) >= 2 * w) return;   // the same for the block
         const int i = blockIdx.x * MERGE_THREADS + threadIdx.x;
         if (i < 2 * w) {
@@ -1676,10 +1727,10 @@ __global__ void __launch_bounds__(MERGE_THREADS) k_grad_top(BatchArgs b) {
     for (int j = 0; j < 2 * K; ++j) acc[j] = 0.f;
 #pragma unroll
     for (int q = 0; q < GPER; ++q) {
-        if (gv[q] == 0.f || !key_finite(key[q], M.fmt)) continue;
-        const float v = key_value(key[q], M.fmt);
+        if (gv[q] == 0.f || !key_finite(key[q], fmt)) continue;
+        const float v = key_value(key[q], fmt);
         float a[K], d[K], c1m;
-        attn_row_sel<K>(v, c0, b.s2, a, c1, c1m);
+        attn_row_sel<K>(v, c0, s2, a, c1, c1m);
         centroid_dev<K>(a, c1, c1m, d);
 #pragma unroll
         for (int j = 0; j < K; ++j) {
@@ -1710,9 +1761,15 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
     __shared__ float red[BLOCK_TOTAL_LDS(K)];
     __shared__ float gSsh[K], c1sh[K], c0sh[K];
     const MatArgs& M = b.m[blockIdx.y];
+    const int t = b.t;
+    // the arguments, in one wait (read where they are used, each had cost a
+    // round trip of its own), then the executed iteration count with the loads
+    const int max_iter = M.max_iter, fmt = M.fmt;
+    const float s2 = b.s2, inv_tau = b.inv_tau;
+    asm volatile("" ::"s"(max_iter), "s"(fmt), "s"(t), "s"(s2), "s"(inv_tau), "s"(M.wsb));
     const Ws ws = carve_workspace(M.wsb, M.max_iter);
     const DevState* st = ws.st;
-    const int t = b.t;
+    const int T = st->teff;
     // Every load first, none waiting for T: the per-pattern inputs, the
     // partial blocks (columns [0, 2K) of block 0 -- k_grad_top's, used at
     // t = T and t = T - 1 -- and [0, K) of block t + 1), and the k-vectors of
@@ -1723,12 +1780,12 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
     for (int r = 0; r < T_KPT; ++r) {
         const int u = table_key(r);
         n4[r] = ws.counts[u];
-        R4[r] = t < M.max_iter ? ws.R[u] : 0.f;
+        R4[r] = t < max_iter ? ws.R[u] : 0.f;
         H4[r] = t == 1 ? ws.H[u] : 0.f;
     }
     PartCols<4 * K> pc;
     const float* b0 = ws.bpart;
-    const float* bn = t < M.max_iter ? ws.bpart + (size_t)(t + 1) * T_WG * PSTRIDE : nullptr;
+    const float* bn = t < max_iter ? ws.bpart + (size_t)(t + 1) * T_WG * PSTRIDE : nullptr;
     pc.load([&](int c) -> const float* {
         return c < 2 * K ? b0 + c : (c < 3 * K && bn ? bn + (c - 2 * K) : nullptr);
     });
@@ -1738,10 +1795,9 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
         hc1 = ws.chist[t * KMAX + j];
         hc0 = ws.chist[(t - 1) * KMAX + j];
         hS = ws.shist[t * KMAX + j];
-        if (t < M.max_iter) { hS1 = ws.shist[(t + 1) * KMAX + j]; hg1 = ws.ghist[(t + 1) * KMAX + j]; }
+        if (t < max_iter) { hS1 = ws.shist[(t + 1) * KMAX + j]; hg1 = ws.ghist[(t + 1) * KMAX + j]; }
     }
     EDKM_STAMP_MARK(b, 2);   // loads issued
-    const int T = st->teff;
     pc.stage(red);
     if (t > T) return;
     const bool lead = blockIdx.x == 0;
@@ -1751,8 +1807,8 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
         if (t == T) {
             gm = PartCols<4 * K>::total(red, j);
         } else {
-            gm = PartCols<4 * K>::total(red, 2 * K + j) * b.inv_tau;
-            if (t + 1 == T) gm += PartCols<4 * K>::total(red, K + j) * b.inv_tau;
+            gm = PartCols<4 * K>::total(red, 2 * K + j) * inv_tau;
+            if (t + 1 == T) gm += PartCols<4 * K>::total(red, K + j) * inv_tau;
             if (!(hS1 > 0.f)) gm += hg1;
         }
         c1sh[j] = hc1;
@@ -1773,13 +1829,13 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
         const int u = table_key(r);
         const uint32_t n = n4[r];
         if (n == 0u) continue;
-        if (!key_finite(u, M.fmt)) {
+        if (!key_finite(u, fmt)) {
             if (t == 1) ws.HR[u] = make_float2(__builtin_nanf(""), __builtin_nanf(""));
             continue;
         }
-        const float v = key_value(u, M.fmt);
+        const float v = key_value(u, fmt);
         float a[K], dev[K], cm;
-        attn_row_sel<K>(v, c0, b.s2, a, c1, cm);
+        attn_row_sel<K>(v, c0, s2, a, c1, cm);
         const float direct = softmax_dev<K>(v, a, gS, c1, cm, dev);
         const float nf = (float)n;
         float r_ = 0.f;
@@ -1789,7 +1845,7 @@ __global__ void __launch_bounds__(T_THREADS) k_bwd_iter(BatchArgs b) {
             r_ += dl;
             acc[j] = fmaf(nf, dl, acc[j]);
         }
-        const float Ru = fmaf(-r_, b.inv_tau, direct) + (t != T ? R4[r] : 0.f);
+        const float Ru = fmaf(-r_, inv_tau, direct) + (t != T ? R4[r] : 0.f);
         if (t == 1) ws.HR[u] = make_float2(H4[r], Ru);
         else ws.R[u] = Ru;
     }
