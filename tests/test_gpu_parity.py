@@ -699,6 +699,38 @@ def test_call_order_and_key_buffer_checks():
     assert_close(gw.cpu().numpy(), first.cpu().numpy(), 1e-6, "repeat backward")
 
 
+
+def test_plan_reused_across_weight_distributions():
+    """One plan and its workspace carried through matrices with very different
+    pattern sets in turn: narrow Gaussian, a span wider than the LDS windows,
+    special values, one repeated value, then the narrow one again.  Each must
+    give what a fresh plan gives on the same inputs (counts, occupied-pattern
+    count and forward outputs bitwise; backward within 1e-6 relative, as
+    between any two runs), so nothing one matrix left in the workspace
+    (windows, keyed-sum mode, table entries of patterns the next one lacks, G,
+    partial rows) reaches the next."""
+    n = 150_000
+    rng = np.random.default_rng(401)
+    wide = (np.sign(rng.standard_normal(n)) * np.exp2(rng.uniform(-24, 15.9, n))).astype(np.float16).view(np.uint16)
+    wide[: n // 2] = inputs.fp16_weights(n // 2, 402)
+    narrow = inputs.fp16_weights(n, 400)
+    sets = [("narrow", narrow), ("wide", wide), ("special", special_keys(n, 403)),
+            ("constant", np.full(n, np.float16(0.01).view(np.uint16), dtype=np.uint16)),
+            ("narrow again", narrow)]
+    plan = edkm.Plan(n, 3, ITERS)
+    for i, (name, keys) in enumerate(sets):
+        c0 = inputs.quantile_init(keys, 8)
+        g = inputs.upstream_grad(n, 410 + i)
+        say("plan reuse", name)
+        got = gpu(keys, c0, 3, g=g, want_counts=True, plan=plan)
+        ref = gpu(keys, c0, 3, g=g, want_counts=True)
+        for f in ("counts", "num_unique", "iters", "c_out", "w_tilde"):
+            assert np.array_equal(got[f], ref[f]), (name, f)
+        assert_close(got["grad_w"], ref["grad_w"], 1e-6, name + " grad_w")
+        slack = 1e-6 * np.abs(ref["grad_c"]) + 1e-9 * float(np.abs(g).sum())
+        assert np.all(np.abs(got["grad_c"] - ref["grad_c"]) <= slack), name + " grad_c"
+
+
 # ------------------------------------------------------------------ full workload shapes
 
 @pytest.mark.parametrize("cfg,bits,fmt", [(2, 3, "fp16"), (3, 3, "fp16"), (3, 4, "fp16"),
