@@ -103,15 +103,26 @@ def _bf16_values(b):
     return (np.asarray(b, np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
-def assert_bf16_within_ulp(x_bits, ref, what="bf16 W~"):
+def assert_bf16_within_ulp(x_bits, ref, what="bf16 W~", tol=None):
     """x_bits: bf16 patterns; ref: fp64 oracle values.  Within one bf16 ulp of
     the oracle value rounded to bf16 (through fp32: the double rounding moves
-    it by at most half an ulp)."""
+    it by at most half an ulp).
+
+    With ``tol``, an entry may instead lie within the fp32 bar of
+    assert_close, tol (|ref_i| + med|ref|).  The kernels form W~ in
+    fp32 and round it; near a zero crossing of W~ as a function of the
+    weight, the fp32 value carries an absolute error of about 1e-8 of the
+    largest centroid, while bf16 (which keeps fp32's exponent range) has ulps
+    far below that.  fp16 does not meet this: its subnormal spacing, 6e-8,
+    stays above that error."""
     r = _bf16_bits(np.asarray(ref, np.float64).astype(np.float32))
     rv = _bf16_values(r)
     ulp = np.abs(_bf16_values(r + np.uint16(1)) - rv)
     x = _bf16_values(x_bits)
     bad = ~(np.abs(x - rv) <= ulp)
+    if tol is not None:
+        r64 = np.asarray(ref, np.float64)
+        bad &= ~(np.abs(x - r64) <= tol * (np.abs(r64) + np.median(np.abs(r64))))
     assert not np.any(bad), "%s: %d entries beyond one ulp" % (what, int(bad.sum()))
 
 

@@ -75,3 +75,24 @@ def test_wide_span_is_ill_conditioned_and_planted_errors_still_fail():
         pass
     else:
         raise AssertionError("a 2e-3 relative shift passed")
+
+
+def test_bf16_bar_near_zero_crossing():
+    """The bf16 W~ bar (parity_util.assert_bf16_within_ulp with tol): a value
+    next to a zero crossing of W~ that is off by about 1e-8 of the centroid
+    scale (fp32 arithmetic) passes through the fp32 floor, while an entry of
+    ordinary size two bf16 ulps away still fails, floor or not."""
+    import pytest
+    from parity_util import TOL_FWD, _bf16_bits, _bf16_values, assert_bf16_within_ulp
+    ref = np.array([-3.12000202627e-09, 0.0213, -0.0375, 0.0042])
+    near = ref.copy()
+    near[0] = -3.49245965e-09                 # 3.7e-10 away: many bf16 ulps of 3e-9
+    bits = _bf16_bits(near.astype(np.float32))
+    with pytest.raises(AssertionError):
+        assert_bf16_within_ulp(bits, ref)
+    assert_bf16_within_ulp(bits, ref, tol=TOL_FWD)
+    far = _bf16_bits(ref.astype(np.float32))
+    far[1] += np.uint16(2)                    # two ulps of 0.0213: about 2.4e-4
+    assert abs(_bf16_values(far[1:2])[0] - ref[1]) > TOL_FWD * (abs(ref[1]) + np.median(np.abs(ref)))
+    with pytest.raises(AssertionError):
+        assert_bf16_within_ulp(far, ref, tol=TOL_FWD)

@@ -765,12 +765,14 @@ def test_full_size_dense_path(cfg, bits):
     check(res, oracle(keys, c0, g, form="table"), what="dense cfg%d bits=%d" % (cfg, bits))
 
 
-@pytest.mark.parametrize("fmt,out_half", [("fp16", False), ("fp16", True), ("bf16", False)])
+@pytest.mark.parametrize("fmt,out_half", [("fp16", False), ("fp16", True), ("bf16", False), ("bf16", True)])
 def test_decoder_layer_batch_full_size(fmt, out_half):
     """The seven matrices of one LLaMA-7B decoder layer in one batch (the call the
     benchmark times, also in its 16-bit W~ and bf16-weight modes), each against
-    the table-form oracle.  16-bit W~ is held to one ulp of the oracle value
-    rounded to the weight format."""
+    the table-form oracle.  16-bit W~ (fp16 or bf16, the weights' format) is
+    held to one ulp of the oracle value rounded to that format; bf16 entries
+    near a zero crossing of W~, where one bf16 ulp is below fp32 accuracy, to
+    the fp32 forward bar instead."""
     w = inputs.WORKLOADS[4]
     say("decoder layer", fmt, "half W~" if out_half else "fp32 W~")
     plans, kd, ci, co, wt, it, gd, gw, gc, host = [], [], [], [], [], [], [], [], [], []
@@ -799,7 +801,9 @@ def test_decoder_layer_batch_full_size(fmt, out_half):
         wv = wt[i].cpu().numpy()
         assert int(it[i].item()) == ref["T"], what
         assert_close(co[i].cpu().numpy(), ref["c_out"], TOL_FWD, what + " c_out")
-        if out_half:
+        if out_half and fmt == "bf16":
+            assert_bf16_within_ulp(wv.view(np.uint16), ref["w_tilde"], what + " bf16 W~", tol=TOL_FWD)
+        elif out_half:
             assert_fp16_within_ulp(wv.view(np.uint16), ref["w_tilde"], what + " fp16 W~")
         else:
             assert_close(wv, ref["w_tilde"], TOL_FWD, what + " w_tilde")
