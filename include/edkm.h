@@ -41,7 +41,10 @@
  *     sequence; edkm_palettize needs no earlier call.  Distinct plans with
  *     distinct workspaces may be used concurrently.
  *   - Errors are returned, never thrown; argument errors are detected on the
- *     host before any HIP call and leave the plan unchanged.
+ *     host before any HIP call and leave the plan unchanged.  After
+ *     EDKM_ERR_HIP the workspace may hold a half-done step, so the plan falls
+ *     back: a failed init_unique (or forward_dense) needs a new init_unique,
+ *     a failed forward or backward a new forward.
  *   - Every entry point can be captured in a HIP graph (no allocation, no
  *     memset, no synchronisation), except init_unique with check_finite = 1,
  *     which synchronises.  A replay repeats the device work of the captured
@@ -165,7 +168,8 @@ edkm_status edkm_backward(edkm_plan* plan, const uint16_t* w_bits, const float* 
  * are host arrays of `count` entries (count >= 1, any size: groups are formed
  * by the library); entries of the nullable output arrays may be NULL, and the
  * arrays themselves may be NULL.  Equivalent to calling the single-matrix
- * form on each. */
+ * form on each (with check_finite = 1, a matrix with Inf/NaN weights leaves
+ * only its own plan uncounted; the call then returns EDKM_ERR_NONFINITE). */
 edkm_status edkm_init_unique_batch(int count, edkm_plan* const* plans,
                                    const uint16_t* const* w_bits,
                                    uint32_t* const* counts_out,

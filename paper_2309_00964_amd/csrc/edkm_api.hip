@@ -194,6 +194,12 @@ edkm_status edkm_init_unique_batch(int count, edkm_plan* const* plans,
     edkm_status st = check_batch(count, plans, w_bits);
     if (st != EDKM_OK) return st;
     if (check_finite != 0 && check_finite != 1) return EDKM_ERR_ARG;
+    // From the first launch on, the workspaces hold a partial count of the new
+    // keys: until this call succeeds, every plan of it needs a new init_unique.
+    for (int i = 0; i < count; ++i) {
+        impl(plans[i])->stage = PLANNED;
+        impl(plans[i])->keys = nullptr;
+    }
     st = for_groups(count, plans, [&](int first, int cnt) -> edkm_status {
         BatchArgs b;
         std::memset(&b, 0, sizeof(b));
@@ -221,24 +227,26 @@ edkm_status edkm_init_unique_batch(int count, edkm_plan* const* plans,
             if (e != hipSuccess) return hip_fail(plans, i, 1, e, "hipMemcpyAsync(counts)");
         }
     }
-    bool bad = false;
-    if (check_finite) {
-        for (int i = 0; i < count; ++i) {
+    // As the single-matrix form on each: a matrix with non-finite weights
+    // leaves its own plan uncounted, the others are counted.
+    bool any_bad = false;
+    for (int i = 0; i < count; ++i) {
+        bool bad = false;
+        if (check_finite) {
             Ws w = carve_workspace(impl(plans[i])->ws, impl(plans[i])->max_iter);
             uint32_t flag = 0;
             hipError_t e = hipMemcpyAsync(&flag, &w.st->nonfinite, sizeof(flag),
                                           hipMemcpyDeviceToHost, stream);
             if (e == hipSuccess) e = hipStreamSynchronize(stream);
             if (e != hipSuccess) return hip_fail(plans, i, 1, e, "non-finite check");
-            bad = bad || flag != 0;
+            bad = flag != 0;
         }
-    }
-    for (int i = 0; i < count; ++i) {
         PlanImpl* P = impl(plans[i]);
         P->stage = bad ? PLANNED : COUNTED;
         P->keys = bad ? nullptr : w_bits[i];
+        any_bad = any_bad || bad;
     }
-    return bad ? EDKM_ERR_NONFINITE : EDKM_OK;
+    return any_bad ? EDKM_ERR_NONFINITE : EDKM_OK;
 }
 
 edkm_status edkm_init_unique(edkm_plan* plan, const uint16_t* w_bits, uint32_t* counts_out,
@@ -263,6 +271,9 @@ edkm_status edkm_forward_batch(int count, edkm_plan* const* plans, const uint16_
         if (P->stage < COUNTED || P->stage == DENSE_FORWARD || P->keys != w_bits[i])
             return EDKM_ERR_STATE;
     }
+    // From the first launch on, the table state of an earlier forward is being
+    // overwritten: until this call succeeds, a backward needs a new forward.
+    for (int i = 0; i < count; ++i) impl(plans[i])->stage = COUNTED;
     st = for_groups(count, plans, [&](int first, int cnt) -> edkm_status {
         BatchArgs b;
         std::memset(&b, 0, sizeof(b));
@@ -394,6 +405,10 @@ edkm_status edkm_forward_dense(edkm_plan* plan, const uint16_t* w_bits, float ta
     uint64_t nwg = (P->n + 4095) / 4096;
     if (nwg > (uint64_t)D_WG) nwg = D_WG;
     M.chunk = (P->n + nwg - 1) / nwg;
+    // the dense kernels reuse the workspace's iteration history: whatever
+    // state it held is gone once they launch, whether or not they succeed
+    P->stage = PLANNED;
+    P->keys = nullptr;
     const char* where = "";
     const hipError_t e = launch_forward_dense(b, (uint32_t)nwg, stream, &where, &P->ev);
     if (e != hipSuccess) return hip_fail(&plan, 0, 1, e, where);

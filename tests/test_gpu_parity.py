@@ -272,6 +272,52 @@ def test_nonfinite_weights():
     assert_close(res["grad_c"], ref["gc"], TOL_BWD, "grad_c")
 
 
+def test_batch_nonfinite_check_is_per_matrix():
+    """init_unique_batch with check_finite = 1 on [finite, Inf/NaN, finite]:
+    the call reports EDKM_ERR_NONFINITE, as the single form would for the
+    middle matrix, and, as the single form on each would, leaves only that
+    plan uncounted: the other two go on through forward and backward and
+    equal fresh single calls, while the middle plan's forward is a state
+    error."""
+    sizes = [50_000, 60_001, 70_003]
+    ks = [inputs.fp16_weights(n, 73 + i) for i, n in enumerate(sizes)]
+    ks[1][[3, 999, 60_000]] = [0x7C00, 0xFC00, 0x7E00]
+    c0s = [inputs.quantile_init(k, 8) for k in ks]
+    gs = [inputs.upstream_grad(n, 76 + i) for i, n in enumerate(sizes)]
+    plans = [edkm.Plan(n, 3, ITERS) for n in sizes]
+    kd = [dkeys(k) for k in ks]
+    say("batch non-finite check")
+    with pytest.raises(edkm.EdkmError) as e:
+        edkm.init_unique_batch(plans, kd, check_finite=True)
+    assert e.value.status == edkm.ERR_NONFINITE
+    co = torch.empty(8, device=DEV)
+    wt = torch.empty(sizes[1], device=DEV)
+    with pytest.raises(edkm.EdkmError) as e:
+        edkm.forward(plans[1], kd[1], TAU, 0.0, torch.from_numpy(c0s[1]).to(DEV), co, wt)
+    assert e.value.status == edkm.ERR_STATE
+    good = [0, 2]
+    ci = [torch.from_numpy(c0s[i]).to(DEV) for i in good]
+    co = [torch.empty(8, device=DEV) for _ in good]
+    wt = [torch.empty(sizes[i], device=DEV) for i in good]
+    it = [torch.zeros(1, dtype=torch.int32, device=DEV) for _ in good]
+    gd = [torch.from_numpy(gs[i]).to(DEV) for i in good]
+    gw = [torch.empty(sizes[i], device=DEV) for i in good]
+    gc = [torch.empty(8, device=DEV) for _ in good]
+    pg, kg = [plans[i] for i in good], [kd[i] for i in good]
+    edkm.forward_batch(pg, kg, TAU, 0.0, ci, co, wt, False, it)
+    edkm.backward_batch(pg, kg, gd, gw, gc)
+    torch.cuda.synchronize()
+    for q, i in enumerate(good):
+        ref = gpu(ks[i], c0s[i], 3, g=gs[i])
+        assert int(it[q].item()) == int(ref["iters"][0]), i
+        assert np.array_equal(co[q].cpu().numpy(), ref["c_out"]), i
+        assert np.array_equal(wt[q].cpu().numpy(), ref["w_tilde"]), i
+        # a batch splits the N-sized passes differently from a single call,
+        # so the keyed sums' last bits differ (as in the batch-versus-single tests)
+        assert_close(gw[q].cpu().numpy(), ref["grad_w"], 1e-4, "grad_w %d" % i)
+        assert_close(gc[q].cpu().numpy(), ref["grad_c"], 1e-4, "grad_c %d" % i)
+
+
 def test_keyed_sum_wraps_fixed_point_range():
     """Five patterns repeated over a million weights; dL/dW~ is a small bulk
     (N(0, 1e-3^2)) with 5% of entries +-0.75.  The fixed-point scale follows
