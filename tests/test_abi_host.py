@@ -314,3 +314,14 @@ def test_palettize_noalloc_argument_errors():
     assert f(keys, 100, 3, 2, lut, out, None) == edkm.ERR_ARG
     text = open(HEADER).read()
     assert re.search(r"#define EDKM_NOALLOC_SCRATCH_BYTES 65536\b", text)
+
+
+def test_differentiable_wrapper_argument_errors():
+    """function.dkm checks its arguments on the host before any HIP call."""
+    import torch
+    from paper_2309_00964_amd.function import dkm
+    c8 = torch.zeros(8)
+    with pytest.raises(TypeError):
+        dkm(torch.zeros(16, dtype=torch.float16), c8)           # not on the GPU
+    with pytest.raises(TypeError):
+        dkm(torch.zeros(16, dtype=torch.float32), c8)           # not 16-bit weights
