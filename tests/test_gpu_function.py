@@ -3,7 +3,8 @@ equals the library's calls, autograd's gradients through it equal the
 library's backward (dL/dW in the weights' own type, dL/dC^(0)) for fp16 and
 bf16 weights of a 2-D shape, a retained graph gives the same gradients on a
 second backward, and an in-place change of the weights between forward and
-backward is refused by autograd's version check."""
+backward is refused by autograd's version check.  Its batched form,
+dkm_batch, equals one dkm per tensor."""
 import sys
 
 import numpy as np
@@ -12,7 +13,7 @@ import pytest
 torch = pytest.importorskip("torch")
 
 from paper_2309_00964_amd import inputs                           # noqa: E402
-from paper_2309_00964_amd.function import dkm                     # noqa: E402
+from paper_2309_00964_amd.function import dkm, dkm_batch          # noqa: E402
 from paper_2309_00964_amd.runner import run                       # noqa: E402
 from parity_util import assert_close                              # noqa: E402
 
@@ -90,3 +91,30 @@ def test_in_place_change_before_backward_is_refused():
     with pytest.raises(RuntimeError, match="modified by an inplace operation"):
         wt.sum().backward()
     torch.cuda.synchronize()
+
+
+def test_batch_equals_one_call_per_tensor():
+    """dkm_batch over tensors of different shapes, bit widths and formats
+    equals dkm on each: W~, C^(T) and T bitwise; gradients to the weights'
+    rounding (a batch splits the N-sized passes differently, so the keyed
+    sums' last bits differ)."""
+    spec = [("fp16", 300, 257, 3, 630), ("bf16", 128, 513, 2, 631), ("fp16", 1000, 77, 4, 632)]
+    ws, c0s, gs = [], [], []
+    for fmt, r, c, bits, seed in spec:
+        keys, w = weights(fmt, r, c, seed)
+        ws.append(w.requires_grad_(True))
+        c0s.append(torch.from_numpy(inputs.quantile_init(keys, 1 << bits, fmt)).to(DEV).requires_grad_(True))
+        gs.append(torch.from_numpy(inputs.upstream_grad(keys.size, seed + 10)).to(DEV).view(w.shape))
+    say("autograd batch")
+    wt, c_out, it = dkm_batch(ws, c0s, inputs.TAU, inputs.ITERS)
+    loss = sum((a * g).sum() for a, g in zip(wt, gs))
+    grads = torch.autograd.grad(loss, ws + c0s)
+    for i, (w, c0, g) in enumerate(zip(ws, c0s, gs)):
+        wt1, c1, it1 = dkm(w, c0, inputs.TAU, inputs.ITERS)
+        gw1, gc1 = torch.autograd.grad((wt1 * g).sum(), (w, c0))
+        assert torch.equal(wt[i], wt1) and torch.equal(c_out[i], c1) and torch.equal(it[i], it1), i
+        fmt = spec[i][0]
+        assert grads[i].dtype == w.dtype
+        assert_close(grads[i].float().reshape(-1).cpu().numpy(), gw1.float().reshape(-1).cpu().numpy(),
+                     2 * ROUND[fmt], "dL/dW %d" % i)
+        assert_close(grads[len(ws) + i].cpu().numpy(), gc1.cpu().numpy(), 1e-4, "dL/dC0 %d" % i)
