@@ -13,6 +13,8 @@ N-sized kernel (timed live with HIP events around its launches), and the CPU
 oracle timed on a bounded sample on this host.
 
 Weight format: --key-format fp16 (default) or bf16 (any workload).
+16-bit arrays (decoder layer): --w-tilde half (W~), --grads half (dL/dW~ and
+dL/dw), in the weight format.
 Cold-cache passes only: --evict-between-calls (decoder layer; pass times only).
 
 The per-pass times are measured twice: back to back (the line's roofline) and
@@ -261,13 +263,26 @@ def _timed(step, plan, pass_ids, steps, warmup, torch, edkm):
     return max(wall, gpu_s), avg, med
 
 
-def hbm_roofline(avg_ms, total, out_half=False, med_ms=None):
+def pass_bytes(p, out_half=False, grads_half=False):
+    """Algorithmic bytes per weight of an N-sized pass: 16-bit W~ takes 2 of
+    the W~ gather's 6; 16-bit gradients take 2 of the keyed sum's 6 (dL/dW~)
+    and 4 of the gradient gather's 10 (dL/dW~ and dL/dw)."""
+    if out_half and p == "k_gather_wt":
+        return 4
+    if grads_half and p == "k_keyed_grad":
+        return 4
+    if grads_half and p == "k_gather_grad":
+        return 6
+    return PASS_BYTES[p]
+
+
+def hbm_roofline(avg_ms, total, out_half=False, med_ms=None, grads_half=False):
     """Roofline of the dominant N-sized pass (HBM-bound) plus all passes:
     achieved from the average launch time (as the kernel trace reports it),
     the median beside it."""
     passes = {}
     for p, ms in avg_ms.items():
-        nbytes = (4 if out_half and p == "k_gather_wt" else PASS_BYTES[p]) * total
+        nbytes = pass_bytes(p, out_half, grads_half) * total
         passes[p] = {"avg_us": ms * 1000.0, "bytes": nbytes, "GBps": nbytes / (ms * 1e-3) / 1e9}
         if med_ms:
             passes[p]["median_us"] = med_ms[p] * 1000.0
@@ -316,7 +331,7 @@ class Matrices:
     with its own plan and centroids."""
 
     def __init__(self, config, mats, bits, outliers=False, on_device=False, keep_host=(), fmt="fp16",
-                 out_half=False, evict=False):
+                 out_half=False, evict=False, grads_half=False):
         import numpy as np
         import torch
         from paper_2309_00964_amd import edkm, inputs
@@ -351,8 +366,12 @@ class Matrices:
             self.c_out.append(torch.empty(k, device=dev))
             self.wt.append(torch.empty(n, dtype=torch.int16 if out_half else torch.float32, device=dev))
             self.iters.append(torch.zeros(1, dtype=torch.int32, device=dev))
-            self.grads.append(gt)
-            self.gw.append(torch.empty(n, device=dev))
+            if grads_half:   # dL/dW~ rounded to the weights' format; dL/dw written in it
+                self.grads.append(gt.to(torch.float16 if fmt == "fp16" else torch.bfloat16).view(torch.int16))
+                self.gw.append(torch.empty(n, dtype=torch.int16, device=dev))
+            else:
+                self.grads.append(gt)
+                self.gw.append(torch.empty(n, device=dev))
             self.gc.append(torch.empty(k, device=dev))
         self.fmt = fmt
         self.out_half = out_half
@@ -428,23 +447,26 @@ def bench_decoder_layer(args):
     bits = 3
     keep = () if args.no_cpu_baseline else tuple(args.cpu_sample)
     half = args.w_tilde == "half"
+    ghalf = args.grads == "half"
     want_evicted = args.evict_between_calls or not args.no_evicted_passes
     m = Matrices(4, inputs.WORKLOADS[4]["mats"], bits, keep_host=keep, fmt=args.key_format, out_half=half,
-                 evict=want_evicted)
+                 evict=want_evicted, grads_half=ghalf)
     m.evicting = args.evict_between_calls
     elapsed, avg, med = timed(m.step, m.plans[0], PASS_IDS, args.steps, args.warmup)
     extra = {"w_tilde": m.fmt if half else "fp32"}
+    if ghalf:
+        extra["grads"] = m.fmt
     if args.evict_between_calls:
         # the step time then includes three 1 GiB eviction reads; the pass
         # times (roofline) are the figures this mode is for
         extra["evict_between_calls"] = True
-    roof = hbm_roofline(avg, m.total, half, med)
+    roof = hbm_roofline(avg, m.total, half, med, ghalf)
     line_timing = dict(LAST_TIMING)
     if want_evicted and not args.evict_between_calls:
         m.evicting = True
         _, eavg, emed = timed(m.step, m.plans[0], PASS_IDS, args.steps, 1)
         m.evicting = False
-        ev = hbm_roofline(eavg, m.total, half, emed)
+        ev = hbm_roofline(eavg, m.total, half, emed, ghalf)
         roof["evicted_between_calls"] = {
             "kernel": ev["kernel"], "achieved": ev["achieved"], "frac": ev["frac"],
             "n_pass_total_GBps": ev["n_pass_total_GBps"], "n_pass_total_frac": ev["n_pass_total_frac"],
@@ -455,7 +477,7 @@ def bench_decoder_layer(args):
     LAST_TIMING.clear()
     LAST_TIMING.update(line_timing)
     out = result_line(args, "llama7b_decoder_layer_3bit" + _fmt_tag(args) + ("_half_wtilde" if half else "")
-                      + ("_evicted" if args.evict_between_calls else ""),
+                      + ("_half_grads" if ghalf else "") + ("_evicted" if args.evict_between_calls else ""),
                       m, bits, elapsed, roof, extra)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(m.host, 1 << bits, fmt=m.fmt)
@@ -888,6 +910,10 @@ def main():
     ap.add_argument("--w-tilde", choices=("fp32", "half"), default="fp32",
                     help="decoder_layer: W~ output as fp32 (default, 24 B per weight) or in the "
                          "16-bit weight format (22 B per weight)")
+    ap.add_argument("--grads", choices=("fp32", "half"), default="fp32",
+                    help="decoder_layer: dL/dW~ in and dL/dw out as fp32 (default) or in the 16-bit "
+                         "weight format (18 B per weight; with --w-tilde half, 16 B: "
+                         "a training step in the weights' precision)")
     ap.add_argument("--evict-between-calls", action="store_true",
                     help="decoder layer: read 1 GiB between init_unique, forward and backward, so that "
                          "no call finds its predecessor's data in the Infinity Cache (pass times only)")

@@ -161,6 +161,23 @@ edkm_status edkm_forward(edkm_plan* plan, const uint16_t* w_bits, float tau, flo
 edkm_status edkm_backward(edkm_plan* plan, const uint16_t* w_bits, const float* grad_w_tilde,
                           float* grad_w, float* grad_c, hipStream_t stream);
 
+/* edkm_backward with 16-bit N-sized gradients, for training in the weights'
+ * own precision (the 16-bit W~ of forward with out_half = 1 gets a 16-bit
+ * dL/dW~ from autograd, and dL/dw goes back to fp16 or bf16 weights): flags
+ * is a bitwise or of
+ *   EDKM_GRAD_IN_HALF   grad_w_tilde holds n 16-bit floats of the plan's
+ *                       weight format (fp16 or bf16 bits, uint16), else float;
+ *   EDKM_GRAD_OUT_HALF  grad_w receives n 16-bit floats of that format
+ *                       (rounded to nearest even from the fp32 result), else
+ *                       float.
+ * Each halves the bytes its array moves (the keyed sum reads grad_w_tilde,
+ * the gradient gather reads grad_w_tilde and writes grad_w).  The arithmetic
+ * is the same fp32 as edkm_backward's; with both flags 0 it is edkm_backward.
+ * Other flag bits are EDKM_ERR_ARG. */
+enum { EDKM_GRAD_IN_HALF = 1, EDKM_GRAD_OUT_HALF = 2 };
+edkm_status edkm_backward_ex(edkm_plan* plan, const uint16_t* w_bits, const void* grad_w_tilde,
+                             void* grad_w, float* grad_c, int flags, hipStream_t stream);
+
 /* Batched forms: `count` independent matrices (own plan, keys and outputs;
  * same tau and eps) processed together.  The batch is cut into launch groups
  * of up to EDKM_LAUNCH_GROUP consecutive matrices with the same bit width and
@@ -185,6 +202,11 @@ edkm_status edkm_backward_batch(int count, edkm_plan* const* plans,
                                 const float* const* grad_w_tilde,
                                 float* const* grad_w, float* const* grad_c,
                                 hipStream_t stream);
+edkm_status edkm_backward_batch_ex(int count, edkm_plan* const* plans,
+                                   const uint16_t* const* w_bits,
+                                   const void* const* grad_w_tilde,
+                                   void* const* grad_w, float* const* grad_c,
+                                   int flags, hipStream_t stream);
 
 /* Dense (non-uniquified) DKM for comparison (Sec. 2: the O(|W||C|) map):
  * the same mathematics evaluated per weight over the N x k map, recomputing

@@ -320,11 +320,12 @@ edkm_status edkm_forward(edkm_plan* plan, const uint16_t* w_bits, float tau, flo
                               &iters_out, stream);
 }
 
-edkm_status edkm_backward_batch(int count, edkm_plan* const* plans, const uint16_t* const* w_bits,
-                                const float* const* grad_w_tilde, float* const* grad_w,
-                                float* const* grad_c, hipStream_t stream) {
+edkm_status edkm_backward_batch_ex(int count, edkm_plan* const* plans, const uint16_t* const* w_bits,
+                                   const void* const* grad_w_tilde, void* const* grad_w,
+                                   float* const* grad_c, int flags, hipStream_t stream) {
     edkm_status st = check_batch(count, plans, w_bits);
     if (st != EDKM_OK) return st;
+    if (flags & ~(EDKM_GRAD_IN_HALF | EDKM_GRAD_OUT_HALF)) return EDKM_ERR_ARG;
     if (!grad_w_tilde || !grad_w || !grad_c) return EDKM_ERR_ARG;
     for (int i = 0; i < count; ++i)
         if (!grad_w_tilde[i] || !grad_w[i] || !grad_c[i]) return EDKM_ERR_ARG;
@@ -344,6 +345,8 @@ edkm_status edkm_backward_batch(int count, edkm_plan* const* plans, const uint16
             const float tau = impl(plans[first + i0])->tau;
             b.s2 = tau_s2(tau);
             b.inv_tau = 1.0f / tau;
+            b.g_half = (flags & EDKM_GRAD_IN_HALF) != 0;
+            b.gw_half = (flags & EDKM_GRAD_OUT_HALF) != 0;
             bool vec = true;
             int max_t = 0;
             for (int i = 0; i < b.count; ++i) {
@@ -351,8 +354,8 @@ edkm_status edkm_backward_batch(int count, edkm_plan* const* plans, const uint16
                 const PlanImpl* P = impl(plans[q]);
                 MatArgs& M = b.m[i];
                 fill_mat(M, P, w_bits[q]);
-                M.g = grad_w_tilde[q];
-                M.gw = grad_w[q];
+                M.g = static_cast<const float*>(grad_w_tilde[q]);   // 16-bit patterns with g_half
+                M.gw = static_cast<float*>(grad_w[q]);              // 16-bit patterns with gw_half
                 M.gc = grad_c[q];
                 vec = vec && aligned16(w_bits[q]) && aligned16(grad_w_tilde[q]) &&
                       aligned16(grad_w[q]);
@@ -376,9 +379,21 @@ edkm_status edkm_backward_batch(int count, edkm_plan* const* plans, const uint16
     return st;
 }
 
+edkm_status edkm_backward_batch(int count, edkm_plan* const* plans, const uint16_t* const* w_bits,
+                                const float* const* grad_w_tilde, float* const* grad_w,
+                                float* const* grad_c, hipStream_t stream) {
+    return edkm_backward_batch_ex(count, plans, w_bits, reinterpret_cast<const void* const*>(grad_w_tilde),
+                                  reinterpret_cast<void* const*>(grad_w), grad_c, 0, stream);
+}
+
 edkm_status edkm_backward(edkm_plan* plan, const uint16_t* w_bits, const float* grad_w_tilde,
                           float* grad_w, float* grad_c, hipStream_t stream) {
     return edkm_backward_batch(1, &plan, &w_bits, &grad_w_tilde, &grad_w, &grad_c, stream);
+}
+
+edkm_status edkm_backward_ex(edkm_plan* plan, const uint16_t* w_bits, const void* grad_w_tilde,
+                             void* grad_w, float* grad_c, int flags, hipStream_t stream) {
+    return edkm_backward_batch_ex(1, &plan, &w_bits, &grad_w_tilde, &grad_w, &grad_c, flags, stream);
 }
 
 edkm_status edkm_forward_dense(edkm_plan* plan, const uint16_t* w_bits, float tau, float eps,

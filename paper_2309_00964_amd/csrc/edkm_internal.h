@@ -82,8 +82,8 @@ struct MatArgs {
                               // inverse index (unique_inverse)
     int32_t* iters_out;
     uint32_t* nuniq_out;
-    const float* g;           // dL/dW~
-    float* gw;                // dL/dw
+    const float* g;           // dL/dW~ (16-bit patterns when the launch's g_half is set)
+    float* gw;                // dL/dw (16-bit patterns when the launch's gw_half is set)
     float* gc;                // dL/dC^(0)
     float* attn;              // dense map output (nullable)
     uint16_t* uniq;           // sorted distinct patterns (unique_inverse, nullable)
@@ -101,6 +101,8 @@ struct BatchArgs {
     int count;
     int t;                    // iteration index of a per-iteration launch
     int out_half;             // W~ as 16-bit floats of the weight format
+    int g_half;               // dL/dW~ given as 16-bit floats of the weight format
+    int gw_half;              // dL/dw written as 16-bit floats of the weight format
     float s2;                 // log2(e) / tau
     float inv_tau;
     float eps;

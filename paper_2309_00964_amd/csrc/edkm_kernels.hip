@@ -106,6 +106,13 @@ __device__ __forceinline__ bool key_finite(uint32_t h, int fmt) {
     return (int)(h & 0x7FFFu) < fin_mags(fmt);
 }
 
+// 16-bit gradient value -> fp32, exact, Inf and NaN included (unlike
+// key_value, which only ever sees finite patterns).
+__device__ __forceinline__ float grad_value(uint32_t h, int fmt) {
+    if (fmt == FMT_BF16) return __uint_as_float(h << 16);
+    return __half2float(__ushort_as_half((unsigned short)h));
+}
+
 // fp32 -> 16-bit pattern of the weight format, round to nearest even (NaN
 // stays NaN).
 __device__ __forceinline__ uint32_t to_half_bits(float x, int fmt) {
@@ -622,6 +629,15 @@ struct Keys8 { uint4 q; };
 // ... and of one 4-weight group.
 struct Keys4 { uint2 q; };
 struct KeysG4 { uint2 q; float4 g; };
+// ... with four 16-bit gradients, decoded only when used (after every load of
+// the tile has issued).
+struct KeysH4 { uint2 q; uint2 g; };
+struct KeysH8 { uint4 q; uint4 g; };
+__device__ __forceinline__ float4 g4_of(const KeysG4& r, int) { return r.g; }
+__device__ __forceinline__ float4 g4_of(const KeysH4& r, int fmt) {
+    return make_float4(grad_value(r.g.x & 0xFFFFu, fmt), grad_value(r.g.x >> 16, fmt),
+                       grad_value(r.g.y & 0xFFFFu, fmt), grad_value(r.g.y >> 16, fmt));
+}
 
 typedef unsigned int v4u_t __attribute__((ext_vector_type(4)));
 typedef unsigned int v2u_t __attribute__((ext_vector_type(2)));
@@ -1194,13 +1210,16 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
         auto h2 = [&](float a, float c) -> uint32_t {
             return to_half_bits(a, M.fmt) | (to_half_bits(c, M.fmt) << 16);
         };
-        for_slice<16, 4, true>(M, wl, c_lo, c_hi,
-            [&](uint64_t i, auto c) { return Keys4{c ? ld_u2(keys + i) : ld_u2_nt(keys + i)}; },
-            [&](const Keys4& r) {
+        // 16-byte key loads and stores, 8 weights per lane and group (with
+        // 8-byte ones, 4 weights, this path ran at 5.3 instead of 5.6 TB/s)
+        for_slice<8, 8, true>(M, wl, c_lo, c_hi,
+            [&](uint64_t i, auto c) { return Keys8{c ? ld_u4(keys + i) : ld_u4_nt(keys + i)}; },
+            [&](const Keys8& r) {
                 const float4 v = look4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16);
-                return make_uint2(h2(v.x, v.y), h2(v.z, v.w));
+                const float4 u = look4(r.q.z & 0xFFFFu, r.q.z >> 16, r.q.w & 0xFFFFu, r.q.w >> 16);
+                return make_uint4(h2(v.x, v.y), h2(v.z, v.w), h2(u.x, u.y), h2(u.z, u.w));
             },
-            [&](uint64_t i, uint2 o) { st_u2_nt(out + i, o); },
+            [&](uint64_t i, uint4 o) { st_u4_nt(out + i, o); },
             [&](uint64_t i) { out[i] = (uint16_t)to_half_bits(look(keys[i]), M.fmt); });
     } else {
         float* out = reinterpret_cast<float*>(M.wt);
@@ -1243,6 +1262,9 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_wt(BatchArgs b) {
 // not: with fp16 weights (about 0.23 other lanes per 64-lane atomic share an
 // address) the 32-bit mode is 10% faster, with bf16 weights (about 1.8) the
 // 64-bit mode is 30% faster.
+constexpr int KW16_U = 8, KI16_U = 6;   // keyed sum with 16-bit dL/dW~: 64-bit, 32-bit mode
+constexpr int GG16_U = 6;               // gradient gather with 16-bit dL/dW~ and dL/dw (8-weight groups)
+template <bool G16>
 __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
     EDKM_STAMP_ENTRY(b);
     __shared__ __align__(16) unsigned long long lds[2 * W8];   // 64-bit sums, or the 32-bit ones
@@ -1257,6 +1279,17 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
     const int lo = wide ? st->lo8 : st->lo4, w = wide ? st->w8 : st->w4;
     const uint16_t* keys = M.keys;
     const float* g = M.g;
+    const uint16_t* gh = reinterpret_cast<const uint16_t*>(M.g);   // G16: 16-bit patterns
+    const int fmt = M.fmt;
+    auto g1 = [&](uint64_t i) { return G16 ? grad_value(gh[i], fmt) : g[i]; };
+    auto ldkg = [&](uint64_t i, auto c) {
+        const uint2 k = c ? ld_u2(keys + i) : ld_u2_nt(keys + i);
+        if constexpr (G16) return KeysH4{k, ld_u2_nt(gh + i)};
+        else return KeysG4{k, ld_f4_nt(g + i)};
+    };
+    // tile depths (loads in flight per thread): 16-bit gradients move fewer
+    // bytes per load, so they take deeper tiles
+    constexpr int KW_U = G16 ? KW16_U : 4, KI_U = G16 ? KI16_U : 3;
     int* acc32 = reinterpret_cast<int*>(lds);
     {   // 16-byte LDS writes over the window (2 w words of 4 or 8 bytes), rounded up
         const int n16 = wide ? w : (2 * w + 3) / 4;
@@ -1275,7 +1308,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
         const uint64_t runs = M.n > 64 ? M.n - 63 : 1;
         const uint64_t run0 = (((uint64_t)wl * (NP_THREADS / 64) + (threadIdx.x >> 6)) * 2654435761ull) % runs;
         const uint64_t i = min(run0 + (threadIdx.x & 63), M.n - 1);
-        const int e = (int)((__float_as_uint(g[i]) >> 23) & 0xFFu);
+        const int e = (int)((__float_as_uint(g1(i)) >> 23) & 0xFFu);
         const bool use = e != 0 && e != 0xFF;
         int smax = use ? e : 0, ssum = smax, scnt = use ? 1 : 0;
         smax = wave_reduce(smax, 0, op_max);
@@ -1294,19 +1327,19 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
     // The end of the key sweep cached, g non-temporal: those keys stay in the
     // Infinity Cache for the gradient gather, which sweeps backwards.
     auto stream = [&](auto add) {
-        for_slice<4, 4>(M, wl, c_lo, c_hi,
-            [&](uint64_t i, auto c) { return KeysG4{c ? ld_u2(keys + i) : ld_u2_nt(keys + i), ld_f4_nt(g + i)}; },
-            [&](const KeysG4& r) {
-                add(r.q.x & 0xFFFFu, r.g.x); add(r.q.x >> 16, r.g.y);
-                add(r.q.y & 0xFFFFu, r.g.z); add(r.q.y >> 16, r.g.w);
+        for_slice<KW_U, 4>(M, wl, c_lo, c_hi, ldkg,
+            [&](const auto& r) {
+                const float4 gv = g4_of(r, fmt);
+                add(r.q.x & 0xFFFFu, gv.x); add(r.q.x >> 16, gv.y);
+                add(r.q.y & 0xFFFFu, gv.z); add(r.q.y >> 16, gv.w);
                 return Nothing{};
             },
             [&](uint64_t, Nothing) {},
-            [&](uint64_t i) { add(keys[i], g[i]); });
+            [&](uint64_t i) { add(keys[i], g1(i)); });
     };
     float* row = reinterpret_cast<float*>(ws.part) + (size_t)wl * ROW4;
     if (wide) {
-        const int bn = 64 - __clzll((unsigned long long)Slice<4, 4>(M).bound(M) - 1);   // 2^bn >= weights added here
+        const int bn = 64 - __clzll((unsigned long long)Slice<KW_U, 4>(M).bound(M) - 1);   // 2^bn >= weights added here
         const int emax = emax_sh;
         const int S = 181 - bn - emax;               // 2^(emax-126) * 2^S = 2^(55-bn)
         const uint32_t elim = (uint32_t)min(emax + 6, 0xFE);
@@ -1351,15 +1384,15 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
             if (((old ^ sum) & (q ^ sum)) < 0) atomicAdd(&G[key], q > 0 ? wrap : -wrap);
         };
         struct Pend4 { uint2 keys; int q[4], old[4]; };
-        for_slice<3, 4>(M, wl, c_lo, c_hi,
-            [&](uint64_t i, auto c) { return KeysG4{c ? ld_u2(keys + i) : ld_u2_nt(keys + i), ld_f4_nt(g + i)}; },
-            [&](const KeysG4& r) {
+        for_slice<KI_U, 4>(M, wl, c_lo, c_hi, ldkg,
+            [&](const auto& r) {
+                const float4 gv = g4_of(r, fmt);
                 Pend4 p;
                 p.keys = r.q;
-                issue(r.q.x & 0xFFFFu, r.g.x, p.q[0], p.old[0]);
-                issue(r.q.x >> 16, r.g.y, p.q[1], p.old[1]);
-                issue(r.q.y & 0xFFFFu, r.g.z, p.q[2], p.old[2]);
-                issue(r.q.y >> 16, r.g.w, p.q[3], p.old[3]);
+                issue(r.q.x & 0xFFFFu, gv.x, p.q[0], p.old[0]);
+                issue(r.q.x >> 16, gv.y, p.q[1], p.old[1]);
+                issue(r.q.y & 0xFFFFu, gv.z, p.q[2], p.old[2]);
+                issue(r.q.y >> 16, gv.w, p.q[3], p.old[3]);
                 return p;
             },
             [&](uint64_t, const Pend4& p) {
@@ -1371,7 +1404,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
             [&](uint64_t i) {
                 int q, old;
                 const uint32_t key = keys[i];
-                issue(key, g[i], q, old);
+                issue(key, g1(i), q, old);
                 settle(key, q, old);
             });
         __syncthreads();
@@ -1392,6 +1425,7 @@ __global__ void __launch_bounds__(NP_THREADS) k_keyed_grad(BatchArgs b) {
 // dL/dw_i = g_i H[bits_i] + R[bits_i]; the 8-byte window [lo8, lo8 + w8) of (H, R) sits
 // in LDS.  The first workgroup of each matrix also finishes dL/dC^(0); every
 // workgroup clears a slice of G for the next backward.
+template <bool G16, bool O16>
 __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
     EDKM_STAMP_ENTRY(b);
     __shared__ float2 hw[2 * W8];
@@ -1442,16 +1476,55 @@ __global__ void __launch_bounds__(NP_THREADS) k_gather_grad(BatchArgs b) {
     };
     const uint16_t* keys = M.keys;
     const float* g = M.g;
-    float* out = M.gw;
+    const uint16_t* gh = reinterpret_cast<const uint16_t*>(M.g);   // G16: 16-bit patterns
+    const int fmt = M.fmt;
+    auto g1 = [&](uint64_t i) { return G16 ? grad_value(gh[i], fmt) : g[i]; };
     auto dw = [&](uint32_t key, float gv) {
         const float2 h = look(key);
         return fmaf(gv, h.x, h.y);
     };
+    float* out = M.gw;
+    uint16_t* outh = reinterpret_cast<uint16_t*>(M.gw);           // O16: 16-bit patterns
+    auto packed4 = [&](const KeysH4& r) {   // four 16-bit results from four 16-bit gradients
+        const float4 o = dw4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16, g4_of(r, fmt));
+        return make_uint2(to_half_bits(o.x, fmt) | (to_half_bits(o.y, fmt) << 16),
+                          to_half_bits(o.z, fmt) | (to_half_bits(o.w, fmt) << 16));
+    };
+    if constexpr (G16 && O16) {
+        // 16-byte loads and stores, 8 weights per lane and group: with 8-byte
+        // ones (4 weights) this pass ran at 4.4 TB/s, with these at 5.4 TB/s
+        for_slice<GG16_U, 8, true>(M, wl, 0, 0,
+            [&](uint64_t i, auto) { return KeysH8{ld_u4_nt(keys + i), ld_u4_nt(gh + i)}; },
+            [&](const KeysH8& r) {
+                const uint2 a = packed4(KeysH4{make_uint2(r.q.x, r.q.y), make_uint2(r.g.x, r.g.y)});
+                const uint2 c = packed4(KeysH4{make_uint2(r.q.z, r.q.w), make_uint2(r.g.z, r.g.w)});
+                return make_uint4(a.x, a.y, c.x, c.y);
+            },
+            [&](uint64_t i, uint4 o) { st_u4_nt(outh + i, o); },
+            [&](uint64_t i) { outh[i] = (uint16_t)to_half_bits(dw(keys[i], g1(i)), fmt); });
+        return;
+    }
     for_slice<8, 4, true>(M, wl, 0, 0,
-        [&](uint64_t i, auto) { return KeysG4{ld_u2_nt(keys + i), ld_f4_nt(g + i)}; },
-        [&](const KeysG4& r) { return dw4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16, r.g); },
-        [&](uint64_t i, float4 o) { st_f4_nt(out + i, o); },
-        [&](uint64_t i) { out[i] = dw(keys[i], g[i]); });
+        [&](uint64_t i, auto) {
+            if constexpr (G16) return KeysH4{ld_u2_nt(keys + i), ld_u2_nt(gh + i)};
+            else return KeysG4{ld_u2_nt(keys + i), ld_f4_nt(g + i)};
+        },
+        [&](const auto& r) {   // the stored form: float4, or (O16) four packed 16-bit values
+            const float4 o = dw4(r.q.x & 0xFFFFu, r.q.x >> 16, r.q.y & 0xFFFFu, r.q.y >> 16, g4_of(r, fmt));
+            if constexpr (O16)
+                return make_uint2(to_half_bits(o.x, fmt) | (to_half_bits(o.y, fmt) << 16),
+                                  to_half_bits(o.z, fmt) | (to_half_bits(o.w, fmt) << 16));
+            else return o;
+        },
+        [&](uint64_t i, const auto& o) {
+            if constexpr (O16) st_u2_nt(outh + i, o);
+            else st_f4_nt(out + i, o);
+        },
+        [&](uint64_t i) {
+            const float v = dw(keys[i], g1(i));
+            if constexpr (O16) outh[i] = (uint16_t)to_half_bits(v, fmt);
+            else out[i] = v;
+        });
 }
 
 // ----------------------------------------------------------------------------
@@ -2198,14 +2271,19 @@ template <int K>
 static hipError_t backward_k(BatchArgs& b, uint32_t grid_np, int max_t, hipStream_t s, const char** where,
                              const PassEvents* ev) {
     const dim3 tg(T_WG, b.count);
-    EDKM_NPASS(PASS_KEYED_GRAD, "k_keyed_grad", k_keyed_grad, dim3(grid_np), dim3(NP_THREADS), b);
+    if (b.g_half) EDKM_NPASS(PASS_KEYED_GRAD, "k_keyed_grad", k_keyed_grad<true>, dim3(grid_np), dim3(NP_THREADS), b);
+    else EDKM_NPASS(PASS_KEYED_GRAD, "k_keyed_grad", k_keyed_grad<false>, dim3(grid_np), dim3(NP_THREADS), b);
     EDKM_LAUNCH("k_grad_top", k_grad_top<K>, dim3(MERGE_X, merge_chunks(b, GT_ROWS) + 1, b.count),
                 dim3(MERGE_THREADS), b);
     for (int t = max_t; t >= 1; --t) {
         b.t = t;
         EDKM_LAUNCH("k_bwd_iter", k_bwd_iter<K>, tg, dim3(T_THREADS), b);
     }
-    EDKM_NPASS(PASS_GATHER_GRAD, "k_gather_grad", k_gather_grad, dim3(grid_np), dim3(NP_THREADS), b);
+    const dim3 gg(grid_np), gb(NP_THREADS);
+    if (b.g_half && b.gw_half) EDKM_NPASS(PASS_GATHER_GRAD, "k_gather_grad", (k_gather_grad<true, true>), gg, gb, b);
+    else if (b.g_half) EDKM_NPASS(PASS_GATHER_GRAD, "k_gather_grad", (k_gather_grad<true, false>), gg, gb, b);
+    else if (b.gw_half) EDKM_NPASS(PASS_GATHER_GRAD, "k_gather_grad", (k_gather_grad<false, true>), gg, gb, b);
+    else EDKM_NPASS(PASS_GATHER_GRAD, "k_gather_grad", (k_gather_grad<false, false>), gg, gb, b);
     return hipSuccess;
 }
 

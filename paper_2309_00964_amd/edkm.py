@@ -90,9 +90,11 @@ _SIGS = {
     "edkm_init_unique": (_i32, [_PLAN, _P, _P, _P, _i32, _P]),
     "edkm_forward": (_i32, [_PLAN, _P, _f32, _f32, _P, _P, _P, _i32, _P, _P]),
     "edkm_backward": (_i32, [_PLAN, _P, _P, _P, _P, _P]),
+    "edkm_backward_ex": (_i32, [_PLAN, _P, _P, _P, _P, _i32, _P]),
     "edkm_init_unique_batch": (_i32, [_i32, _PP, _PP, _PP, _PP, _i32, _P]),
     "edkm_forward_batch": (_i32, [_i32, _PP, _PP, _f32, _f32, _PP, _PP, _PP, _i32, _PP, _P]),
     "edkm_backward_batch": (_i32, [_i32, _PP, _PP, _PP, _PP, _PP, _P]),
+    "edkm_backward_batch_ex": (_i32, [_i32, _PP, _PP, _PP, _PP, _PP, _i32, _P]),
     "edkm_forward_dense": (_i32, [_PLAN, _P, _f32, _f32, _P, _P, _P, _i32, _P, _P, _P]),
     "edkm_backward_dense": (_i32, [_PLAN, _P, _P, _P, _P, _P]),
     "edkm_plan_set_pass_events": (_i32, [_PLAN, _i32, _P, _P]),
@@ -261,11 +263,29 @@ def forward(plan: Plan, w_bits, tau: float, eps: float, c_in, c_out, w_tilde, ou
            "forward", (plan,))
 
 
+GRAD_IN_HALF, GRAD_OUT_HALF = 1, 2
+
+
+def _grad_flags(grad_w_tilde, grad_w):
+    """edkm_backward_ex flags from the gradient arrays' element sizes: 2-byte
+    elements are 16-bit floats of the plan's weight format, 4-byte ones float."""
+    f = 0
+    for t, bit, name in ((grad_w_tilde, GRAD_IN_HALF, "grad_w_tilde"), (grad_w, GRAD_OUT_HALF, "grad_w")):
+        if t.element_size() == 2:
+            f |= bit
+        elif t.element_size() != 4:
+            raise ValueError("%s must have 2- or 4-byte elements" % name)
+    return f
+
+
 def backward(plan: Plan, w_bits, grad_w_tilde, grad_w, grad_c, stream=None) -> None:
-    _check(_lib.edkm_backward(plan.ref, _ptr(w_bits, 2, "w_bits", plan.n),
-                              _ptr(grad_w_tilde, 4, "grad_w_tilde", plan.n),
-                              _ptr(grad_w, 4, "grad_w", plan.n), _ptr(grad_c, 4, "grad_c", plan.k),
-                              _stream(stream)),
+    """dL/dw and dL/dC^(0); grad_w_tilde and grad_w may each be float32 or
+    16-bit (the plan's weight format), chosen by their element size."""
+    f = _grad_flags(grad_w_tilde, grad_w)
+    _check(_lib.edkm_backward_ex(plan.ref, _ptr(w_bits, 2, "w_bits", plan.n),
+                                 _ptr(grad_w_tilde, grad_w_tilde.element_size(), "grad_w_tilde", plan.n),
+                                 _ptr(grad_w, grad_w.element_size(), "grad_w", plan.n),
+                                 _ptr(grad_c, 4, "grad_c", plan.k), f, _stream(stream)),
            "backward", (plan,))
 
 
@@ -338,15 +358,21 @@ def forward_batch(plans, w_bits, tau, eps, c_in, c_out, w_tilde, out_half=False,
 
 
 def backward_batch(plans, w_bits, grad_w_tilde, grad_w, grad_c, stream=None) -> None:
+    """backward over lists; the gradient arrays are all float32 or all 16-bit
+    (per list, chosen by element size as in backward)."""
     _same_len("backward_batch", plans, w_bits=w_bits, grad_w_tilde=grad_w_tilde, grad_w=grad_w, grad_c=grad_c)
     n = len(plans)
+    flags = {_grad_flags(a, b) for a, b in zip(grad_w_tilde, grad_w)}
+    if len(flags) != 1:
+        raise ValueError("backward_batch: mixed 16-bit and float gradient arrays")
+    f = flags.pop()
     pp, _a = _plans(plans)
     ns, ks = [p.n for p in plans], [p.k for p in plans]
     kk, _b = _parr(w_bits, 2, "w_bits", ns)
-    g, _c = _parr(grad_w_tilde, 4, "grad_w_tilde", ns)
-    gw, _d = _parr(grad_w, 4, "grad_w", ns)
+    g, _c = _parr(grad_w_tilde, 2 if f & GRAD_IN_HALF else 4, "grad_w_tilde", ns)
+    gw, _d = _parr(grad_w, 2 if f & GRAD_OUT_HALF else 4, "grad_w", ns)
     gc, _e = _parr(grad_c, 4, "grad_c", ks)
-    _check(_lib.edkm_backward_batch(n, pp, kk, g, gw, gc, _stream(stream)), "backward_batch", plans)
+    _check(_lib.edkm_backward_batch_ex(n, pp, kk, g, gw, gc, f, _stream(stream)), "backward_batch", plans)
 
 
 def palettize_batch(plans, w_bits, lut, indices_out, stream=None) -> None:

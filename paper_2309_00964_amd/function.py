@@ -4,6 +4,9 @@ W~ = DKM(W, C^(0)) with the uniquified forward and backward of the library
 (paper Sec. 2.2): the forward runs init_unique + forward, the backward the
 library's analytic backward, so a training step that uses W~ in place of W
 gets dL/dW and dL/dC^(0) as autograd of the dense DKM map would give them.
+dL/dW comes straight from the library in the weights' own type (fp16 or
+bf16), and a 16-bit W~ takes its gradient in that type, so no cast kernels run
+around the library's.
 ``dkm`` clusters one tensor; ``dkm_batch`` clusters a list of them (say the
 seven matrices of a decoder layer) with the batched calls, one launch per step
 for up to 28 matrices.  Argument marshalling only: every step runs in the HIP
@@ -34,6 +37,15 @@ def _prepare(w, c0, max_iter):
     plan = edkm.Plan(keys.numel(), bits, int(max_iter), device=w.device, key_format=_FORMATS[w.dtype])
     c_in = c0.detach().to(device=w.device, dtype=torch.float32).contiguous()
     return keys, plan, c_in
+
+
+def _grad_in(grad_wt, w):
+    """dL/dW~ as the library reads it: in w's 16-bit type (the gradient of a
+    16-bit W~) or as float32."""
+    g = grad_wt.detach()
+    if g.dtype != w.dtype:
+        g = g.to(torch.float32)
+    return g.contiguous().view(-1)
 
 
 def _outputs(w, plan, out_half):
@@ -67,11 +79,11 @@ class DKMFunction(torch.autograd.Function):
     def backward(ctx, grad_wt, grad_c_out, grad_iters):
         (w,) = ctx.saved_tensors
         plan = ctx.plan
-        g = grad_wt.detach().to(torch.float32).contiguous().view(-1)
-        gw = torch.empty(plan.n, dtype=torch.float32, device=g.device)
+        g = _grad_in(grad_wt, w)
+        gw = torch.empty(plan.n, dtype=w.dtype, device=g.device)   # written in w's type by the library
         gc = torch.empty(plan.k, dtype=torch.float32, device=g.device)
         edkm.backward(plan, ctx.keys, g, gw, gc)
-        grad_w = gw.view(w.shape).to(w.dtype) if ctx.needs_input_grad[0] else None
+        grad_w = gw.view(w.shape) if ctx.needs_input_grad[0] else None
         grad_c0 = gc if ctx.needs_input_grad[1] else None
         return grad_w, grad_c0, None, None, None, None
 
@@ -103,12 +115,14 @@ class DKMBatchFunction(torch.autograd.Function):
     def backward(ctx, *grads):
         m, plans = ctx.m, ctx.plans
         ws = ctx.saved_tensors
-        g = [x.detach().to(torch.float32).contiguous().view(-1) for x in grads[:m]]
-        gw = [torch.empty(p.n, dtype=torch.float32, device=x.device) for p, x in zip(plans, g)]
+        g = [_grad_in(x, w) for x, w in zip(grads[:m], ws)]
+        if len({x.element_size() for x in g}) > 1:        # one gradient type per batched call
+            g = [x.to(torch.float32) for x in g]
+        gw = [torch.empty(p.n, dtype=w.dtype, device=x.device) for p, x, w in zip(plans, g, ws)]
         gc = [torch.empty(p.k, dtype=torch.float32, device=x.device) for p, x in zip(plans, g)]
         edkm.backward_batch(plans, ctx.keys, g, gw, gc)
         need = ctx.needs_input_grad
-        grad_w = [a.view(w.shape).to(w.dtype) if need[5 + i] else None for i, (a, w) in enumerate(zip(gw, ws))]
+        grad_w = [a.view(w.shape) if need[5 + i] else None for i, (a, w) in enumerate(zip(gw, ws))]
         grad_c = [a if need[5 + m + i] else None for i, a in enumerate(gc)]
         return (None, None, None, None, None, *grad_w, *grad_c)
 

@@ -74,6 +74,8 @@ def test_calls_out_of_order_are_rejected_before_any_gpu_work():
     assert lib.edkm_forward(ctypes.byref(p), keys, 2e-3, 0.0, f, f, f, 0, None, None) == edkm.ERR_STATE
     assert lib.edkm_backward(ctypes.byref(p), keys, f, f, f, None) == edkm.ERR_STATE
     assert lib.edkm_backward_dense(ctypes.byref(p), keys, f, f, f, None) == edkm.ERR_STATE
+    assert lib.edkm_backward_ex(ctypes.byref(p), keys, f, f, f, 3, None) == edkm.ERR_STATE
+    assert lib.edkm_backward_ex(ctypes.byref(p), keys, f, f, f, 4, None) == edkm.ERR_ARG   # unknown flag
     # an uninitialised plan is an argument error
     q = edkm.edkm_plan()
     assert lib.edkm_init_unique(ctypes.byref(q), keys, None, None, 0, None) == edkm.ERR_ARG

@@ -120,3 +120,15 @@ def test_source_hash_ignores_comments_only(tmp_path, monkeypatch):
     assert bench.source_hash() == base
     k.write_text(k.read_text() + "\nstatic int unused_probe_value = 1;\n")
     assert bench.source_hash() != base
+
+
+def test_pass_bytes_per_weight():
+    """Algorithmic bytes per weight over the four N-sized passes: 24 with
+    fp32 W~ and gradients, 22 with 16-bit W~, 18 with 16-bit gradients (dL/dW~
+    read twice, dL/dw written once), 16 with both (the training step in the
+    weights' own precision)."""
+    import bench
+    passes = ("k_hist", "k_gather_wt", "k_keyed_grad", "k_gather_grad")
+    total = {(h, g): sum(bench.pass_bytes(p, h, g) for p in passes)
+             for h in (False, True) for g in (False, True)}
+    assert total == {(False, False): 24, (True, False): 22, (False, True): 18, (True, True): 16}
