@@ -74,6 +74,9 @@ DENSE_PASS_IDS = {"k_dense_iter": 4, "k_dense_biter": 5}
 DENSE_OPS_PER_ENTRY = {"k_dense_iter": 9, "k_dense_biter": 15}
 PEAK_FP32_TFLOPS = 157.3
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+# the counter runs behind TRAFFIC_FILE time the default decoder-layer step; its
+# figures are attached to that workload's line only
+TRAFFIC_WORKLOAD = "llama7b_decoder_layer_3bit"
 COPY_BYTES = 1 << 30
 
 
@@ -276,10 +279,11 @@ def pass_bytes(p, out_half=False, grads_half=False):
     return PASS_BYTES[p]
 
 
-def hbm_roofline(avg_ms, total, out_half=False, med_ms=None, grads_half=False):
+def hbm_roofline(avg_ms, total, out_half=False, med_ms=None, grads_half=False, workload=None):
     """Roofline of the dominant N-sized pass (HBM-bound) plus all passes:
     achieved from the average launch time (as the kernel trace reports it),
-    the median beside it."""
+    the median beside it.  `traffic` comes from the counter summary only for
+    the workload and build it was taken on."""
     passes = {}
     for p, ms in avg_ms.items():
         nbytes = pass_bytes(p, out_half, grads_half) * total
@@ -290,7 +294,8 @@ def hbm_roofline(avg_ms, total, out_half=False, med_ms=None, grads_half=False):
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         tf = json.load(open(TRAFFIC_FILE))
-        if tf.get("source_hash") == source_hash() and dom in tf.get("kernels", {}):
+        if (tf.get("source_hash") == source_hash() and tf.get("workload") == workload
+                and dom in tf.get("kernels", {})):
             traffic = tf["kernels"][dom]["bytes_per_launch"]
     n_bytes_all = sum(v["bytes"] for v in passes.values())
     t_all = sum(v["avg_us"] for v in passes.values()) * 1e-6
@@ -460,7 +465,9 @@ def bench_decoder_layer(args):
         # the step time then includes three 1 GiB eviction reads; the pass
         # times (roofline) are the figures this mode is for
         extra["evict_between_calls"] = True
-    roof = hbm_roofline(avg, m.total, half, med, ghalf)
+    workload = ("llama7b_decoder_layer_3bit" + _fmt_tag(args) + ("_half_wtilde" if half else "")
+                + ("_half_grads" if ghalf else "") + ("_evicted" if args.evict_between_calls else ""))
+    roof = hbm_roofline(avg, m.total, half, med, ghalf, workload)
     line_timing = dict(LAST_TIMING)
     if want_evicted and not args.evict_between_calls:
         m.evicting = True
@@ -476,9 +483,7 @@ def bench_decoder_layer(args):
                     "reuse inside the backward"}
     LAST_TIMING.clear()
     LAST_TIMING.update(line_timing)
-    out = result_line(args, "llama7b_decoder_layer_3bit" + _fmt_tag(args) + ("_half_wtilde" if half else "")
-                      + ("_half_grads" if ghalf else "") + ("_evicted" if args.evict_between_calls else ""),
-                      m, bits, elapsed, roof, extra)
+    out = result_line(args, workload, m, bits, elapsed, roof, extra)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(m.host, 1 << bits, fmt=m.fmt)
     return out
@@ -648,7 +653,7 @@ def pmc_summary(fetch_dir, write_dir):
     cf, cw = copy(fetch_dir, "FETCH_SIZE"), copy(write_dir, "WRITE_SIZE")
     f_scale = COPY_BYTES / (cf * 1024.0)
     w_scale = COPY_BYTES / (cw * 1024.0)
-    res = {"source_hash": source_hash(), "copy_bytes": COPY_BYTES,
+    res = {"source_hash": source_hash(), "workload": TRAFFIC_WORKLOAD, "copy_bytes": COPY_BYTES,
            "copy_fetch_kib": cf, "copy_write_kib": cw,
            "fetch_scale": f_scale, "write_scale": w_scale, "kernels": {}}
     for p in PASS_IDS:

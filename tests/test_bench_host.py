@@ -80,6 +80,12 @@ def test_pmc_summary_scales_by_the_copy_calibration(tmp_path, monkeypatch):
     kh = res["kernels"]["k_hist"]
     assert kh["fetch_bytes"] == pytest.approx(1000.0 * 1024 * 2) and kh["write_bytes"] == pytest.approx(4.0 * 1024)
     assert res["source_hash"] == bench.source_hash()
+    # the counters belong to the workload they were taken on, and to no other line
+    avg_ms = {"k_hist": 0.001, "k_gather_wt": 0.002, "k_keyed_grad": 0.002, "k_gather_grad": 0.004}
+    r = bench.hbm_roofline(avg_ms, 10, workload=bench.TRAFFIC_WORKLOAD)
+    assert r["traffic"] == pytest.approx(kg["bytes_per_launch"])
+    assert bench.hbm_roofline(avg_ms, 10, workload=bench.TRAFFIC_WORKLOAD + "_half_grads")["traffic"] is None
+    assert bench.hbm_roofline(avg_ms, 10)["traffic"] is None
 
 
 def test_kernel_base_name():
