@@ -327,3 +327,16 @@ def test_differentiable_wrapper_argument_errors():
         dkm(torch.zeros(16, dtype=torch.float16), c8)           # not on the GPU
     with pytest.raises(TypeError):
         dkm(torch.zeros(16, dtype=torch.float32), c8)           # not 16-bit weights
+
+
+def test_backward_gradient_flags_follow_element_sizes():
+    """The binding picks edkm_backward_ex's flags from the gradient arrays:
+    2-byte elements are 16-bit floats of the plan's format, 4-byte ones float."""
+    import torch
+    f32, h = torch.zeros(4), torch.zeros(4, dtype=torch.int16)
+    assert edkm._grad_flags(f32, f32) == 0
+    assert edkm._grad_flags(h, f32) == edkm.GRAD_IN_HALF
+    assert edkm._grad_flags(f32, h) == edkm.GRAD_OUT_HALF
+    assert edkm._grad_flags(h, h) == edkm.GRAD_IN_HALF | edkm.GRAD_OUT_HALF
+    with pytest.raises(ValueError):
+        edkm._grad_flags(torch.zeros(4, dtype=torch.float64), f32)
