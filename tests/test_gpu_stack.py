@@ -1,7 +1,8 @@
 """GPU parity at the largest workload: a 32-layer stack of LLaMA-7B decoder-layer
 shapes (224 matrices, 6,476,005,376 fp16 weights, 12.95 GB of keys resident),
 drawn on the GPU, clustered at 3, 2 and 4 bits by one batched init_unique +
-forward + backward over every matrix (the calls bench.py --workload stack times).
+forward + backward over every matrix (the calls bench.py --workload stack times),
+and at 3 bits once more with W~, dL/dW~ and dL/dw in fp16.
 
 Every matrix, at any size: the iteration count, the bit-exact total of its
 pattern counts, W~ inside the range of its final centroids (each W~_i is a convex
@@ -98,4 +99,66 @@ def test_stack_every_matrix(stack, bits):
         assert_close(gw[i].cpu().numpy(), rgw, TOL_BWD, name + " grad_w")
         assert_close(gc[i].cpu().numpy(), rgc, TOL_BWD, name + " grad_c")
     del plans
+    torch.cuda.empty_cache()
+
+
+def _half_ulp_sum(x16):
+    """Sum over a 16-bit float array of half its ulp at each element: a bound on
+    the total of the rounding errors that made it from fp32."""
+    a = x16.double().abs()
+    e = torch.floor(torch.log2(torch.clamp(a, min=2.0 ** -14)))
+    return float((torch.exp2(e - 10) / 2).sum())
+
+
+def test_stack_in_16_bits(stack):
+    """The stack at 3 bits with every N-sized array in fp16, as a training step
+    in the weights' precision runs it (W~ out, dL/dW~ in -- the fp32 draw
+    rounded -- and dL/dw out): the same properties for every matrix, the
+    translation identity now allowing for the rounding of each dL/dw_i to
+    fp16 (at most half an ulp each), and the sampled matrices against the
+    table-form oracle on the rounded gradient, 16-bit outputs to one ulp (or,
+    where they cancel towards 0, the fp32 bar)."""
+    from parity_util import assert_fp16_within_ulp
+    k = 8
+    keys, grads = stack["keys"], stack["grads"]
+    c0 = [inputs.quantile_init_device(x, k) for x in keys]
+    plans = [edkm.Plan(x.numel(), 3, ITERS) for x in keys]
+    g16 = [g.half() for g in grads]
+    wt16 = [torch.empty(x.numel(), dtype=torch.int16, device=DEV) for x in keys]
+    gw16 = [torch.empty(x.numel(), dtype=torch.int16, device=DEV) for x in keys]
+    co = [torch.empty(k, device=DEV) for _ in keys]
+    gc = [torch.empty(k, device=DEV) for _ in keys]
+    it = [torch.zeros(1, dtype=torch.int32, device=DEV) for _ in keys]
+    torch.cuda.synchronize()
+    say("stack 16-bit: %d matrices, one batched init_unique + forward + backward" % len(keys))
+    edkm.init_unique_batch(plans, keys)
+    edkm.forward_batch(plans, keys, TAU, 0.0, c0, co, wt16, True, it)
+    edkm.backward_batch(plans, keys, [g.view(torch.int16) for g in g16], gw16, gc)
+    torch.cuda.synchronize()
+    say("stack 16-bit: properties of every matrix")
+    for i, (name, r, c) in enumerate(MATS):
+        assert int(it[i].item()) == ITERS, name
+        w = wt16[i].view(torch.float16)
+        cmin, cmax = float(co[i].min()), float(co[i].max())
+        slack = (TOL_FWD + 2.0 ** -11) * max(abs(cmin), abs(cmax))
+        assert float(w.min()) >= cmin - slack and float(w.max()) <= cmax + slack, name
+        dw = gw16[i].view(torch.float16)
+        sdw, sdc = float(dw.double().sum()), float(gc[i].double().sum())
+        sg = float(g16[i].double().sum())
+        scale = abs(sdw) + abs(sdc) + abs(sg)
+        assert abs(sdw + sdc - sg) <= TOL_BWD * scale + _half_ulp_sum(dw), \
+            "%s: sum dw %.4f + sum dc %.4f vs sum g %.4f" % (name, sdw, sdc, sg)
+    for i in SAMPLED:
+        name = MATS[i][0]
+        say("stack 16-bit: %s against the table-form oracle" % name)
+        kh = keys[i].cpu().numpy().view(np.uint16)
+        g = g16[i].float().cpu().numpy()
+        c0h = c0[i].cpu().numpy()
+        f = table.forward(kh, c0h.astype(np.float64), TAU, ITERS)
+        rgw, rgc = table.backward(kh, f, g.astype(np.float64))[:2]
+        assert_close(co[i].cpu().numpy(), f["c_out"], TOL_FWD, name + " c_out")
+        assert_fp16_within_ulp(wt16[i].cpu().numpy().view(np.uint16), f["w_tilde"], name + " W~", tol=TOL_FWD)
+        assert_fp16_within_ulp(gw16[i].cpu().numpy().view(np.uint16), rgw, name + " grad_w", tol=TOL_BWD)
+        assert_close(gc[i].cpu().numpy(), rgc, TOL_BWD, name + " grad_c")
+    del plans, g16, wt16, gw16
     torch.cuda.empty_cache()
