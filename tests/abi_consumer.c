@@ -37,6 +37,7 @@ int main(void)
     CHECK(edkm_forward(&plan, keys, 2e-3f, 0.0f, f, f, f, 0, NULL, NULL) == EDKM_ERR_STATE);
     CHECK(edkm_backward(&plan, keys, f, f, f, NULL) == EDKM_ERR_STATE);
     CHECK(edkm_backward_dense(&plan, keys, f, f, f, NULL) == EDKM_ERR_STATE);
+    CHECK(edkm_backward_ex(&plan, keys, f, f, f, EDKM_GRAD_IN_HALF | EDKM_GRAD_OUT_HALF, NULL) == EDKM_ERR_STATE);
     CHECK(edkm_unique_inverse(&plan, keys, (uint16_t*)f, NULL, NULL) == EDKM_ERR_STATE);
     /* bad arguments */
     CHECK(edkm_forward(&plan, keys, 0.0f, 0.0f, f, f, f, 0, NULL, NULL) == EDKM_ERR_ARG);
@@ -46,6 +47,7 @@ int main(void)
     CHECK(edkm_init_unique(&plan, keys, NULL, NULL, 2, NULL) == EDKM_ERR_ARG);
     CHECK(edkm_palettize(&plan, keys, NULL, (uint8_t*)f, NULL) == EDKM_ERR_ARG);
     CHECK(edkm_plan_set_keyed_mode(&plan, 5) == EDKM_ERR_ARG);
+    CHECK(edkm_backward_ex(&plan, keys, f, f, f, 4, NULL) == EDKM_ERR_ARG);   /* unknown flag */
     CHECK(edkm_plan_set_pass_events(&plan, 99, NULL, NULL) == EDKM_ERR_ARG);
 
     /* a copied record is refused; the original still works */
