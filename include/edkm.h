@@ -162,9 +162,9 @@ edkm_status edkm_backward(edkm_plan* plan, const uint16_t* w_bits, const float* 
                           float* grad_w, float* grad_c, hipStream_t stream);
 
 /* edkm_backward (the same gradient, Sec. 2.2) with 16-bit N-sized gradient
- * arrays, for training in the weights' own precision (the 16-bit W~ of forward with out_half = 1 gets a 16-bit
- * dL/dW~ from autograd, and dL/dw goes back to fp16 or bf16 weights): flags
- * is a bitwise or of
+ * arrays, for training in the weights' own precision (the 16-bit W~ of
+ * forward with out_half = 1 gets a 16-bit dL/dW~ from autograd, and dL/dw
+ * goes back to fp16 or bf16 weights): flags is a bitwise or of
  *   EDKM_GRAD_IN_HALF   grad_w_tilde holds n 16-bit floats of the plan's
  *                       weight format (fp16 or bf16 bits, uint16), else float;
  *   EDKM_GRAD_OUT_HALF  grad_w receives n 16-bit floats of that format
